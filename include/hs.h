@@ -1,0 +1,210 @@
+/*
+ * hs.h -- C ABI of the heterogeneous data-parallel training step on one
+ * MI355X (gfx950).
+ *
+ * The method (arXiv 2110.08941, "Distributed Optimization using Heterogeneous
+ * Compute Systems") trains one model with M synchronous workers of different
+ * speeds.  Each step:
+ *   1. worker m computes g_m, the gradient of its mean loss over its partition
+ *      of n_m samples (Section 1, Eq. (1); Section 3)           hs_worker_grad
+ *   2. the gradients are combined with partition-size weights
+ *      w_m = n_m / sum n (Section 4.2, Enhanced Dynamic
+ *      Partitioning)                                       hs_weighted_average
+ *   3. an SGD step with momentum and weight decay (Section 1 update rule,
+ *      Section 5 hyper-parameters)                                hs_sgd_step
+ *      (2 and 3 fused in one pass over memory:                    hs_wavg_sgd)
+ *   4. per-worker times give compute powers CP_m = n_m / X_m (Section 4,
+ *      Eq. (2)), and the total batch is repartitioned in proportion to them
+ *      (Section 4.1, Algorithm 1)     hs_estimate_cp, hs_repartition,
+ *                                     hs_partitioner_*
+ * All M workers run on one GPU; their gradient buffers are reduced in HBM.
+ *
+ * Conventions for every function:
+ *   - Return value: HS_OK (0) or a negative hs_status; hs_last_error() gives a
+ *     message for the calling thread's last failure.
+ *   - Argument errors are detected before any launch and leave every buffer
+ *     untouched (HS_ERR_INVALID).  A failed launch returns HS_ERR_HIP.
+ *     Device work is asynchronous on `stream` (a hipStream_t, NULL = the
+ *     default stream); faults inside kernels surface at the caller's next
+ *     synchronisation.
+ *   - Device pointers point to device memory owned by the caller, 16-byte
+ *     aligned.  The library never frees or reallocates caller memory.
+ *   - Model and workspace objects are owned by the library (create/destroy).
+ *     All library device memory is allocated in hs_workspace_create; nothing
+ *     is allocated on the step path.
+ *   - A model is read-only after creation and may be shared by threads.  A
+ *     workspace serves one hs_worker_grad at a time: concurrent workers need
+ *     one workspace each.
+ *
+ * Flat parameter vector layout (theta, g_m, momentum, theta_bf16):
+ *   tensors in forward order; conv weights OHWI [c_out][3][3][c_in] (1x1 for
+ *   the ResNet projection); linear weights [out][in]; a layer's bias follows
+ *   its weight; batch-norm stores gamma then beta; inside a residual block the
+ *   order is conv1, bn1, conv2, bn2, projection conv, projection bn.  Every
+ *   tensor starts at a multiple of 64 elements; the gaps are zero in g_m.
+ *   hs_num_params() is the padded length P.
+ */
+#ifndef HS_H
+#define HS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HS_OK = 0,
+  HS_ERR_INVALID = -1,     /* bad argument; nothing was launched */
+  HS_ERR_HIP = -2,         /* a HIP runtime call failed */
+  HS_ERR_OOM = -3,         /* device allocation failed */
+  HS_ERR_UNSUPPORTED = -4  /* valid request this build does not support */
+} hs_status;
+
+typedef enum { HS_MLP = 0, HS_SMALLCNN = 1, HS_RESNET18 = 2, HS_VGG16 = 3 } hs_arch;
+typedef enum { HS_FP32 = 0, HS_BF16 = 1 } hs_dtype;
+typedef enum { HS_KIND_CONV_W = 0, HS_KIND_LIN_W = 1, HS_KIND_BIAS = 2,
+               HS_KIND_BN_GAMMA = 3, HS_KIND_BN_BETA = 4 } hs_tensor_kind;
+
+typedef struct hs_model hs_model;
+typedef struct hs_workspace hs_workspace;
+typedef struct hs_partitioner hs_partitioner;
+
+/* ---------------------------------------------------------------- models -- */
+
+/* Network description (no device memory).  arch: hs_arch; dtype: HS_FP32
+ * (all GEMM operands fp32) or HS_BF16 (GEMM operands bf16 with fp32
+ * accumulation; batch-norm statistics, loss, gradients and master weights
+ * fp32).  The networks are CIFAR-shaped: MLP 784-256-10; small CNN
+ * conv32-conv64-pool-conv128-GAP-FC10; ResNet-18 (3x3 stem, 4 stages of 2
+ * basic blocks, widths 64..512); VGG-16 (13 conv-BN-ReLU, 5 pools, FC512,
+ * FC10).  The paper's experiments use ResNet50 / VGG16 on CIFAR10 (Section 5). */
+hs_status hs_model_create(int32_t arch, int32_t dtype, hs_model** out);
+hs_status hs_model_destroy(hs_model* model);
+
+int64_t hs_num_params(const hs_model* model);       /* padded P, or -1 if NULL */
+int64_t hs_num_true_params(const hs_model* model);  /* without padding */
+int32_t hs_num_param_tensors(const hs_model* model);
+/* Tensor i of the layout: offset and element count in the flat vector, shape
+ * (ndim <= 4, dims[0..ndim-1]), hs_tensor_kind, and a static name string. */
+hs_status hs_param_tensor(const hs_model* model, int32_t i, int64_t* offset, int64_t* numel,
+                          int32_t* ndim, int64_t dims[4], int32_t* kind, const char** name);
+/* Input elements per sample: 784 (MLP) or 3*32*32. */
+int64_t hs_input_numel(const hs_model* model);
+/* Multiply-accumulates of one forward pass of one sample (dense 3x3 taps). */
+int64_t hs_forward_macs(const hs_model* model);
+
+/* Device workspace for one worker of at most max_n samples (activations,
+ * batch-norm statistics, split-K partial sums).  Allocated on the current
+ * device. */
+hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace** out);
+hs_status hs_workspace_destroy(hs_workspace* ws);
+/* Device bytes held by the workspace. */
+int64_t hs_workspace_bytes(const hs_workspace* ws);
+
+/* ------------------------------------------------------- the step itself -- */
+
+/* Worker gradient (Section 1, Eq. (1); Section 3): g_m <- gradient of
+ * f_m = (1/n_m) sum_i CE(net(x_i), y_i) over the worker's n_m samples, with
+ * batch-norm statistics taken over this worker's samples only.
+ *   theta      device fp32 [P]
+ *   theta_bf16 device bf16 [P] (the RNE copy of theta) for HS_BF16 models,
+ *              must be NULL for HS_FP32 models
+ *   x_m        device fp32, NCHW [n_m][3][32][32] (or [n_m][784] for the MLP)
+ *   y_m        device int32 [n_m], labels 0..9
+ *   n_m        1 <= n_m <= max_n of the workspace
+ *   g_m        device fp32 [P], fully overwritten (padding gaps set to 0)
+ *   loss_m     device fp32 scalar receiving f_m, or NULL
+ * Labels outside 0..9 give an undefined loss but no out-of-bounds access. */
+hs_status hs_worker_grad(const hs_model* model, hs_workspace* ws, const float* theta,
+                         const uint16_t* theta_bf16, const float* x_m, const int32_t* y_m,
+                         int32_t n_m, float* g_m, float* loss_m, void* stream);
+
+/* Partition-weighted gradient (Section 4.2):
+ *   g_out[i] = sum_{m<M} w_m g[m][i],  w_m = n[m] / sum_j n[j]  (computed in
+ *   double, applied in fp32, summed in worker order).
+ * g: HOST array of M device pointers to fp32 [P]; n: HOST int32 [M], n[m] >= 0,
+ * sum > 0; 1 <= M <= 16; P >= 0 (P = 0 is a no-op).  g_out may alias none of
+ * the g[m]. */
+hs_status hs_weighted_average(const float* const* g, const int32_t* n, int32_t M, int64_t P,
+                              float* g_out, void* stream);
+
+/* SGD step (Section 1 update; momentum and coupled weight decay of Section 5):
+ *   d = g + wd*theta;  mom = mu*mom + d;  theta -= lr*mom
+ * mom (fp32 [P]) may be NULL only when mu == 0, then theta -= lr*d.  Momentum
+ * starts from zeros (the caller zero-fills it once).  If theta_bf16 is not
+ * NULL it receives the round-to-nearest-even bf16 copy of the new theta. */
+hs_status hs_sgd_step(float* theta, const float* g, float* mom, int64_t P, float lr, float mu,
+                      float wd, uint16_t* theta_bf16, void* stream);
+
+/* hs_weighted_average followed by hs_sgd_step in one pass over memory (the
+ * weighted gradient is never stored).  Same arguments and rules as the two. */
+hs_status hs_wavg_sgd(const float* const* g, const int32_t* n, int32_t M, float* theta,
+                      float* mom, int64_t P, float lr, float mu, float wd,
+                      uint16_t* theta_bf16, void* stream);
+
+/* theta_bf16[i] = RNE bf16 of theta[i]. */
+hs_status hs_params_to_bf16(const float* theta, uint16_t* theta_bf16, int64_t P, void* stream);
+
+/* --------------------------------------------- compute power, repartition -- */
+
+/* Eq. (2), Section 4: cp_out[m] = n[m] / mean_time[m] (host, double).
+ * Requires n[m] >= 1 and mean_time[m] finite and > 0. */
+hs_status hs_estimate_cp(const int32_t* n, const double* mean_time, int32_t M, double* cp_out);
+
+/* Algorithm 1, Section 4.1 (host, pure, thread-safe): normalise the compute
+ * powers and give worker m a partition of CP_m * N samples.  The fractional
+ * sizes are rounded by largest remainder with this exact double arithmetic
+ * (no fused operations):  S = sum of throughput (left to right);
+ * q_m = (throughput[m] / S) * N;  f_m = floor(q_m);  the N - sum f_m workers
+ * with the largest q_m - f_m get one more (ties: lower index); then, while a
+ * worker has none, one sample moves from the largest worker (lowest index on
+ * ties) to the lowest-index empty worker.  The even split of the first epoch
+ * is throughput[m] = 1 for all m.
+ * Requires 1 <= M <= N and every throughput finite and > 0. */
+hs_status hs_repartition(const double* throughput, int32_t M, int32_t N, int32_t* n_out);
+
+/* Dynamic Partitioning state across steps (Section 4.1).  Created with the
+ * even split of Algorithm 1 for epoch 0.  After each step the caller reports
+ * tau[m] (the measured time of worker m's gradient, or n[m] for a model
+ * clock) and speed[m] (the simulated relative speed); the worker's batch time
+ * is X_m = tau[m] / speed[m].  Every `window` steps the mean X over the window
+ * (summed in step order, divided by window) gives CP (Eq. (2)) and the next
+ * partition (hs_repartition); *repartitioned is set to 1 on those steps and
+ * cp_out (if not NULL) receives the CP vector.  window = 0 never
+ * repartitions.  1 <= M <= 1024, M <= N. */
+hs_status hs_partitioner_create(int32_t M, int32_t N, int32_t window, hs_partitioner** out);
+hs_status hs_partitioner_destroy(hs_partitioner* p);
+hs_status hs_partitioner_partition(const hs_partitioner* p, int32_t* n_out);
+hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n);
+hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
+                                 int32_t* repartitioned, double* cp_out);
+
+/* ------------------------------------------------------ layer-level access -- */
+
+/* One contraction of a convolution or linear layer, as hs_worker_grad runs it
+ * (for layer-level tests and benchmarks).  NHWC activations, OHWI weights
+ * [K][R][R][C]; a linear layer is H = W = R = 1, stride 1, pad 0.
+ *   mode 0 (forward):      out[n][Ho][Wo][K] = conv(a = x[n][H][W][C], b = W) (+ bias[K])
+ *                          (ReLU if relu != 0)
+ *   mode 1 (data grad):    out[n][H][W][C]  = gradient w.r.t. x of sum(dy * conv(x, W)),
+ *                          a = dy[n][Ho][Wo][K], b = W
+ *   mode 2 (weight grad):  out[K][R][R][C]  = gradient w.r.t. W, a = dy, b = x; fp32
+ *                          output; split over pixels when scratch (fp32, scratch_floats
+ *                          elements) is given, in one pass otherwise
+ * dtype selects the operand type (HS_FP32: float, HS_BF16: bf16 bits);
+ * out_f32 != 0 stores modes 0/1 as fp32 even for bf16 operands.
+ * Ho = (H + 2 pad - R) / stride + 1.  stride is 1 or 2.  All pointers device,
+ * 16-byte aligned. */
+hs_status hs_layer_gemm(int32_t mode, int32_t dtype, int32_t n, int32_t H, int32_t W, int32_t C,
+                        int32_t K, int32_t R, int32_t stride, int32_t pad, const void* a,
+                        const void* b, void* out, const float* bias, int32_t relu,
+                        int32_t out_f32, float* scratch, int64_t scratch_floats, void* stream);
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char* hs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HS_H */

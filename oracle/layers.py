@@ -15,6 +15,20 @@ import numpy as np
 
 
 # ----------------------------------------------------------------------------
+# bf16 rounding (storage emulation only)
+# ----------------------------------------------------------------------------
+def bf16_round(x):
+    """Nearest bf16 value (8-bit significand), ties to even, of each entry:
+    the value is first rounded to float32, then its low 16 bits are rounded
+    away; returned as float64."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    u = ((u + 0x7FFF + lsb) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
 # convolution
 # ----------------------------------------------------------------------------
 def conv_out_size(h, k, stride, pad):
@@ -34,11 +48,12 @@ def conv_forward(x, w, stride, pad, b=None):
     wo = conv_out_size(wd, kw, stride, pad)
     xp = np.zeros((n, h + 2 * pad, wd + 2 * pad, ci), dtype=np.float64)
     xp[:, pad:pad + h, pad:pad + wd, :] = x
-    y = np.zeros((n, ho, wo, co), dtype=np.float64)
+    y = np.zeros((n * ho * wo, co), dtype=np.float64)
     for r in range(kh):
         for s in range(kw):
             patch = xp[:, r:r + stride * (ho - 1) + 1:stride, s:s + stride * (wo - 1) + 1:stride, :]
-            y += patch @ w[:, r, s, :].T
+            y += np.ascontiguousarray(patch).reshape(-1, ci) @ w[:, r, s, :].T
+    y = y.reshape(n, ho, wo, co)
     if b is not None:
         y += b
     return y
@@ -58,14 +73,14 @@ def conv_backward(x, w, dy, stride, pad):
     xp[:, pad:pad + h, pad:pad + wd, :] = x
     dxp = np.zeros_like(xp)
     dw = np.zeros_like(w, dtype=np.float64)
-    dy2 = dy.reshape(-1, co)
+    dy2 = np.ascontiguousarray(dy).reshape(-1, co)
     for r in range(kh):
         for s in range(kw):
             rs = (slice(None), slice(r, r + stride * (ho - 1) + 1, stride),
                   slice(s, s + stride * (wo - 1) + 1, stride), slice(None))
-            patch = xp[rs]
-            dw[:, r, s, :] = dy2.T @ patch.reshape(-1, ci)
-            dxp[rs] += dy @ w[:, r, s, :]
+            patch = np.ascontiguousarray(xp[rs]).reshape(-1, ci)
+            dw[:, r, s, :] = dy2.T @ patch
+            dxp[rs] += (dy2 @ w[:, r, s, :]).reshape(n, ho, wo, ci)
     dx = dxp[:, pad:pad + h, pad:pad + wd, :]
     db = dy2.sum(axis=0)
     return dx, dw, db

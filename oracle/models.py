@@ -22,12 +22,105 @@ ALIGN = 64
 
 
 # ----------------------------------------------------------------------------
+# storage precision and decision margins
+# ----------------------------------------------------------------------------
+class Ctx:
+    """Evaluation context of one forward/backward.
+
+    storage = "exact": every value is float64 (the definition).
+    storage = "bf16": emulates where a bf16 implementation stores tensors, so
+    that the ReLU masks and max-pool choices -- decisions taken on stored
+    values -- are taken on the same bf16 values as the kernels take them:
+    GEMM weight operands and every stored activation / activation gradient are
+    rounded to bf16 (round to nearest even); products are still summed in
+    float64; statistics, logits, the loss and weight gradients stay float64.
+    Rounding happens where a value is written to memory, so a sum that a kernel
+    forms before storing (a block's residual add, the data gradient of a
+    block's first convolution plus the shortcut gradient, the second
+    batch-norm of a block feeding the residual add) is rounded once, after
+    the sum.
+
+    Every ReLU and max-pool decision records its margin: |pre-activation|
+    (ReLU) or the gap between the two largest window values (max-pool),
+    relative to the largest magnitude of that tensor.  A decision whose margin
+    is within the arithmetic's error is ambiguous: either outcome is correct."""
+
+    def __init__(self, storage="exact", capture=0.0, toggles=()):
+        if storage not in ("exact", "bf16"):
+            raise ValueError(storage)
+        self.storage = storage
+        self.margins = []          # (layer tag, smallest relative margins of the decisions)
+        self.capture = capture     # ReLU decisions with a margin below this are listed
+        self.ambiguous = []        # (ReLU call index, flat index, margin)
+        self.toggles = set(toggles)  # (call index, flat index): backward mask inverted
+        self.calls = 0
+
+    def store(self, x):
+        return L.bf16_round(x) if self.storage == "bf16" else x
+
+    def weight(self, w):
+        return L.bf16_round(w) if self.storage == "bf16" else w
+
+    def record(self, tag, rel):
+        self.margins.append((tag, np.sort(np.asarray(rel, dtype=np.float64).ravel())[:64]))
+
+    def relu_decide(self, x):
+        """Forward ReLU decision on x: records margins, returns (y, call index)."""
+        call = self.calls
+        self.calls += 1
+        rel = relu_margins(x)
+        self.record("relu", rel)
+        if self.capture > 0.0:
+            flat = rel.ravel()
+            for i in np.flatnonzero(flat < self.capture):
+                self.ambiguous.append((call, int(i), float(flat[i])))
+        return L.relu_forward(x), call
+
+    def relu_mask_grad(self, call, y, dy):
+        """Backward of the ReLU of call `call`: dy * [y > 0], with the masks of
+        the toggled decisions inverted (the other outcome of an ambiguous
+        decision; the forward value there is within the margin of zero)."""
+        mask = (y > 0.0)
+        tog = [i for (c, i) in self.toggles if c == call]
+        if tog:
+            mask = mask.copy()
+            flat = mask.reshape(-1)
+            flat[tog] = ~flat[tog]
+        return dy * mask
+
+    def min_margin(self):
+        vals = [m[1][0] for m in self.margins if m[1].size]
+        return min(vals) if vals else float("inf")
+
+    def count_below(self, delta):
+        return int(sum(np.count_nonzero(m[1] < delta) for m in self.margins))
+
+
+def relu_margins(x):
+    """|x| / max|x| over the entries (a ReLU decision is x > 0)."""
+    scale = np.max(np.abs(x))
+    return np.abs(x) / scale if scale > 0 else np.full(x.shape, np.inf)
+
+
+def pool_margins(x):
+    """(largest - second largest) / max|x| of every 2x2 window whose maximum
+    is positive (windows of zeros feed a zero ReLU gradient either way)."""
+    w = np.stack([x[:, i::2, j::2, :] for i in (0, 1) for j in (0, 1)], axis=-1)
+    w = np.sort(w, axis=-1)
+    gap = w[..., 3] - w[..., 2]
+    scale = np.max(np.abs(x))
+    live = w[..., 3] > 0
+    return (gap[live] / scale) if scale > 0 else np.array([np.inf])
+
+
+# ----------------------------------------------------------------------------
 # modules
 # ----------------------------------------------------------------------------
 class Conv:
-    def __init__(self, name, cin, cout, k, stride, pad, bias):
+    def __init__(self, name, cin, cout, k, stride, pad, bias, raw_dx=False):
         self.name, self.cin, self.cout, self.k = name, cin, cout, k
         self.stride, self.pad, self.bias = stride, pad, bias
+        self.raw_dx = raw_dx       # data gradient is summed before it is stored
 
     def params(self):
         out = [(self.name + ".weight", "conv_w", (self.cout, self.k, self.k, self.cin))]
@@ -35,75 +128,86 @@ class Conv:
             out.append((self.name + ".bias", "bias", (self.cout,)))
         return out
 
-    def forward(self, x, p):
+    def forward(self, x, p, ctx):
         b = p[self.name + ".bias"] if self.bias else None
-        return L.conv_forward(x, p[self.name + ".weight"], self.stride, self.pad, b), x
+        w = ctx.weight(p[self.name + ".weight"])
+        return ctx.store(L.conv_forward(x, w, self.stride, self.pad, b)), x
 
-    def backward(self, cache, dy, p, g, need_dx=True):
+    def backward(self, cache, dy, p, g, ctx):
         x = cache
-        dx, dw, db = L.conv_backward(x, p[self.name + ".weight"], dy, self.stride, self.pad)
+        w = ctx.weight(p[self.name + ".weight"])
+        dx, dw, db = L.conv_backward(x, w, dy, self.stride, self.pad)
         g[self.name + ".weight"] += dw
         if self.bias:
             g[self.name + ".bias"] += db
-        return dx
+        return dx if self.raw_dx else ctx.store(dx)
 
 
 class Linear:
-    def __init__(self, name, fin, fout):
+    def __init__(self, name, fin, fout, logits=False):
         self.name, self.fin, self.fout = name, fin, fout
+        self.logits = logits       # output layer: logits are not stored rounded
 
     def params(self):
         return [(self.name + ".weight", "lin_w", (self.fout, self.fin)),
                 (self.name + ".bias", "bias", (self.fout,))]
 
-    def forward(self, x, p):
-        return L.linear_forward(x, p[self.name + ".weight"], p[self.name + ".bias"]), x
+    def forward(self, x, p, ctx):
+        y = L.linear_forward(x, ctx.weight(p[self.name + ".weight"]), p[self.name + ".bias"])
+        return (y if self.logits else ctx.store(y)), x
 
-    def backward(self, cache, dy, p, g, need_dx=True):
-        dx, dw, db = L.linear_backward(cache, p[self.name + ".weight"], dy)
+    def backward(self, cache, dy, p, g, ctx):
+        # the output layer's gradient is stored once (rounded) for the two
+        # products; its bias gradient sums the unrounded values
+        dys = ctx.store(dy) if self.logits else dy
+        dx, dw, _ = L.linear_backward(cache, ctx.weight(p[self.name + ".weight"]), dys)
         g[self.name + ".weight"] += dw
-        g[self.name + ".bias"] += db
-        return dx
+        g[self.name + ".bias"] += dy.sum(axis=0)
+        return ctx.store(dx)
 
 
 class BatchNorm:
-    def __init__(self, name, c):
+    def __init__(self, name, c, raw_out=False):
         self.name, self.c = name, c
+        self.raw_out = raw_out     # output feeds a sum before it is stored
 
     def params(self):
         return [(self.name + ".gamma", "bn_gamma", (self.c,)),
                 (self.name + ".beta", "bn_beta", (self.c,))]
 
-    def forward(self, x, p):
-        return L.bn_forward(x, p[self.name + ".gamma"], p[self.name + ".beta"])
+    def forward(self, x, p, ctx):
+        y, cache = L.bn_forward(x, p[self.name + ".gamma"], p[self.name + ".beta"])
+        return (y if self.raw_out else ctx.store(y)), cache
 
-    def backward(self, cache, dy, p, g, need_dx=True):
+    def backward(self, cache, dy, p, g, ctx):
         dz, dgamma, dbeta = L.bn_backward(dy, p[self.name + ".gamma"], cache)
         g[self.name + ".gamma"] += dgamma
         g[self.name + ".beta"] += dbeta
-        return dz
+        return ctx.store(dz)
 
 
 class ReLU:
     def params(self):
         return []
 
-    def forward(self, x, p):
-        y = L.relu_forward(x)
-        return y, y
+    def forward(self, x, p, ctx):
+        y, call = ctx.relu_decide(x)
+        return y, (y, call)
 
-    def backward(self, cache, dy, p, g, need_dx=True):
-        return L.relu_backward(cache, dy)
+    def backward(self, cache, dy, p, g, ctx):
+        y, call = cache
+        return ctx.relu_mask_grad(call, y, dy)
 
 
 class MaxPool2:
     def params(self):
         return []
 
-    def forward(self, x, p):
+    def forward(self, x, p, ctx):
+        ctx.record("maxpool", pool_margins(x))
         return L.maxpool2_forward(x), x
 
-    def backward(self, cache, dy, p, g, need_dx=True):
+    def backward(self, cache, dy, p, g, ctx):
         return L.maxpool2_backward(cache, dy)
 
 
@@ -111,11 +215,11 @@ class GlobalAvgPool:
     def params(self):
         return []
 
-    def forward(self, x, p):
-        return L.gap_forward(x), x.shape
+    def forward(self, x, p, ctx):
+        return ctx.store(L.gap_forward(x)), x.shape
 
-    def backward(self, cache, dy, p, g, need_dx=True):
-        return L.gap_backward(cache, dy)
+    def backward(self, cache, dy, p, g, ctx):
+        return ctx.store(L.gap_backward(cache, dy))
 
 
 class Flatten:
@@ -125,11 +229,11 @@ class Flatten:
     def params(self):
         return []
 
-    def forward(self, x, p):
+    def forward(self, x, p, ctx):
         assert x.shape[1] == 1 and x.shape[2] == 1
         return x.reshape(x.shape[0], -1), x.shape
 
-    def backward(self, cache, dy, p, g, need_dx=True):
+    def backward(self, cache, dy, p, g, ctx):
         return dy.reshape(cache)
 
 
@@ -143,16 +247,16 @@ class Sequential:
             out += m.params()
         return out
 
-    def forward(self, x, p):
+    def forward(self, x, p, ctx):
         caches = []
         for m in self.mods:
-            x, c = m.forward(x, p)
+            x, c = m.forward(x, p, ctx)
             caches.append(c)
         return x, caches
 
-    def backward(self, caches, dy, p, g, need_dx=True):
+    def backward(self, caches, dy, p, g, ctx):
         for i in range(len(self.mods) - 1, -1, -1):
-            dy = self.mods[i].backward(caches[i], dy, p, g, need_dx=(i > 0 or need_dx))
+            dy = self.mods[i].backward(caches[i], dy, p, g, ctx)
         return dy
 
 
@@ -162,10 +266,10 @@ class BasicBlock:
     stride or the width changes."""
 
     def __init__(self, name, cin, cout, stride):
-        self.main = Sequential([Conv(name + ".conv1", cin, cout, 3, stride, 1, False),
+        self.main = Sequential([Conv(name + ".conv1", cin, cout, 3, stride, 1, False, raw_dx=True),
                                 BatchNorm(name + ".bn1", cout), ReLU(),
                                 Conv(name + ".conv2", cout, cout, 3, 1, 1, False),
-                                BatchNorm(name + ".bn2", cout)])
+                                BatchNorm(name + ".bn2", cout, raw_out=True)])
         self.short = None
         if stride != 1 or cin != cout:
             self.short = Sequential([Conv(name + ".proj", cin, cout, 1, stride, 0, False),
@@ -174,24 +278,25 @@ class BasicBlock:
     def params(self):
         return self.main.params() + (self.short.params() if self.short else [])
 
-    def forward(self, x, p):
-        a, ca = self.main.forward(x, p)
+    def forward(self, x, p, ctx):
+        a, ca = self.main.forward(x, p, ctx)
         if self.short:
-            s, cs = self.short.forward(x, p)
+            s, cs = self.short.forward(x, p, ctx)
         else:
             s, cs = x, None
-        y = L.relu_forward(a + s)
-        return y, (ca, cs, y)
+        y, call = ctx.relu_decide(a + s)
+        y = ctx.store(y)
+        return y, (ca, cs, y, call)
 
-    def backward(self, cache, dy, p, g, need_dx=True):
-        ca, cs, y = cache
-        dpre = L.relu_backward(y, dy)
-        dx = self.main.backward(ca, dpre, p, g)
+    def backward(self, cache, dy, p, g, ctx):
+        ca, cs, y, call = cache
+        dpre = ctx.relu_mask_grad(call, y, dy)
+        dx = self.main.backward(ca, dpre, p, g, ctx)
         if self.short:
-            dx = dx + self.short.backward(cs, dpre, p, g)
+            dx = dx + self.short.backward(cs, dpre, p, g, ctx)
         else:
             dx = dx + dpre
-        return dx
+        return ctx.store(dx)
 
 
 # ----------------------------------------------------------------------------
@@ -203,7 +308,8 @@ VGG16_CFG = (64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M",
 
 def mlp(in_dim=784, hidden=256, classes=10):
     """Linear(in, hidden) + ReLU + Linear(hidden, classes)."""
-    return Sequential([Linear("fc1", in_dim, hidden), ReLU(), Linear("fc2", hidden, classes)])
+    return Sequential([Linear("fc1", in_dim, hidden), ReLU(),
+                       Linear("fc2", hidden, classes, logits=True)])
 
 
 def small_cnn(in_ch=3, widths=(32, 64, 128), classes=10):
@@ -213,7 +319,7 @@ def small_cnn(in_ch=3, widths=(32, 64, 128), classes=10):
     return Sequential([Conv("conv1", in_ch, c1, 3, 1, 1, True), ReLU(),
                        Conv("conv2", c1, c2, 3, 1, 1, True), ReLU(), MaxPool2(),
                        Conv("conv3", c2, c3, 3, 1, 1, True), ReLU(),
-                       GlobalAvgPool(), Linear("fc", c3, classes)])
+                       GlobalAvgPool(), Linear("fc", c3, classes, logits=True)])
 
 
 def resnet18(in_ch=3, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2), classes=10):
@@ -227,7 +333,7 @@ def resnet18(in_ch=3, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2), classes=1
             stride = 2 if (si > 0 and bi == 0) else 1
             mods.append(BasicBlock("layer%d.%d" % (si + 1, bi), cin, w, stride))
             cin = w
-    mods += [GlobalAvgPool(), Linear("fc", cin, classes)]
+    mods += [GlobalAvgPool(), Linear("fc", cin, classes, logits=True)]
     return Sequential(mods)
 
 
@@ -243,7 +349,8 @@ def vgg16(in_ch=3, cfg=VGG16_CFG, fc_hidden=512, classes=10):
             i += 1
             mods += [Conv("conv%d" % i, cin, v, 3, 1, 1, False), BatchNorm("bn%d" % i, v), ReLU()]
             cin = v
-    mods += [Flatten(), Linear("fc1", cin, fc_hidden), ReLU(), Linear("fc2", fc_hidden, classes)]
+    mods += [Flatten(), Linear("fc1", cin, fc_hidden), ReLU(),
+             Linear("fc2", fc_hidden, classes, logits=True)]
     return Sequential(mods)
 
 
@@ -287,27 +394,31 @@ def to_nhwc(x):
     return x.transpose(0, 2, 3, 1) if x.ndim == 4 else x
 
 
-def worker_grad(net, theta, x, y):
+def worker_grad(net, theta, x, y, storage="exact", ctx=None):
     """g_m = gradient of f_m = (1/n_m) sum_i CE(net(x_i), y_i) over the worker's
     n_m samples (Eq. (1) with the expectation taken over the partition).
     Batch-norm statistics are those of this worker's samples.
+    storage: "exact" (float64 throughout) or "bf16" (see Ctx).  Pass a Ctx to
+    read the decision margins afterwards.
     Returns (loss_m, g_m) with g_m a flat float64 vector in the layout above."""
+    ctx = ctx or Ctx(storage)
     table, total = param_table(net)
     th = np.asarray(theta, dtype=np.float64)
     assert th.shape == (total,)
     p = views(th, table)
     g = np.zeros(total, dtype=np.float64)
     gv = views(g, table)
-    logits, caches = net.forward(to_nhwc(x), p)
+    logits, caches = net.forward(ctx.store(to_nhwc(x)), p, ctx)
     loss, dz = L.softmax_ce(logits, np.asarray(y, dtype=np.int64))
-    net.backward(caches, dz, p, gv, need_dx=False)
+    net.backward(caches, dz, p, gv, ctx)
     return loss, g
 
 
-def loss_only(net, theta, x, y):
+def loss_only(net, theta, x, y, storage="exact"):
+    ctx = Ctx(storage)
     table, total = param_table(net)
     p = views(np.asarray(theta, dtype=np.float64), table)
-    logits, _ = net.forward(to_nhwc(x), p)
+    logits, _ = net.forward(ctx.store(to_nhwc(x)), p, ctx)
     loss, _ = L.softmax_ce(logits, np.asarray(y, dtype=np.int64))
     return loss
 

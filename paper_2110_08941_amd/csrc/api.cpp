@@ -1,0 +1,428 @@
+// C ABI of libhs (declared in include/hs.h): argument checking, object
+// lifetime, and the host-side parts of the method (compute-power estimate,
+// repartition, the Dynamic Partitioning window).
+//
+// The repartition arithmetic must not be contracted into fused operations:
+// this file is compiled with -ffp-contract=off.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/hs.h"
+#include "model.h"
+
+using namespace hs;
+
+struct hs_model {
+  Model m;
+};
+
+struct hs_workspace {
+  const hs_model* model;
+  Workspace ws;
+  int device;
+};
+
+struct hs_partitioner {
+  int32_t M, N, window, steps_in_window;
+  std::vector<int32_t> n;
+  std::vector<double> xsum;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+hs_status fail(hs_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+hs_status ok() {
+  g_err.clear();
+  return HS_OK;
+}
+
+hs_status hip_fail(hipError_t e, const char* what) {
+  return fail(HS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* hs_last_error(void) { return g_err.c_str(); }
+
+// ------------------------------------------------------------------ models --
+hs_status hs_model_create(int32_t arch, int32_t dtype, hs_model** out) {
+  if (!out) return fail(HS_ERR_INVALID, "hs_model_create: out is NULL");
+  *out = nullptr;
+  if (arch < HS_MLP || arch > HS_VGG16) return fail(HS_ERR_INVALID, "unknown arch %d", arch);
+  if (dtype != HS_FP32 && dtype != HS_BF16) return fail(HS_ERR_INVALID, "unknown dtype %d", dtype);
+  hs_model* m = new (std::nothrow) hs_model;
+  if (!m) return fail(HS_ERR_OOM, "host allocation failed");
+  if (!build_model(arch, dtype, m->m)) {
+    delete m;
+    return fail(HS_ERR_UNSUPPORTED, "arch %d not supported", arch);
+  }
+  *out = m;
+  return ok();
+}
+
+hs_status hs_model_destroy(hs_model* model) {
+  delete model;
+  return ok();
+}
+
+int64_t hs_num_params(const hs_model* model) { return model ? model->m.P : -1; }
+int64_t hs_num_true_params(const hs_model* model) { return model ? model->m.P_true : -1; }
+int32_t hs_num_param_tensors(const hs_model* model) {
+  return model ? (int32_t)model->m.params.size() : -1;
+}
+int64_t hs_input_numel(const hs_model* model) { return model ? model->m.in_numel : -1; }
+int64_t hs_forward_macs(const hs_model* model) { return model ? model->m.fwd_macs : -1; }
+
+hs_status hs_param_tensor(const hs_model* model, int32_t i, int64_t* offset, int64_t* numel,
+                          int32_t* ndim, int64_t dims[4], int32_t* kind, const char** name) {
+  if (!model) return fail(HS_ERR_INVALID, "hs_param_tensor: model is NULL");
+  if (i < 0 || i >= (int32_t)model->m.params.size())
+    return fail(HS_ERR_INVALID, "hs_param_tensor: index %d out of range", i);
+  const ParamT& p = model->m.params[i];
+  if (offset) *offset = p.off;
+  if (numel) *numel = p.numel;
+  if (ndim) *ndim = (int32_t)p.shape.size();
+  if (dims)
+    for (int d = 0; d < 4; ++d) dims[d] = d < (int)p.shape.size() ? p.shape[d] : 0;
+  if (kind) *kind = p.kind;
+  if (name) *name = p.name.c_str();
+  return ok();
+}
+
+// -------------------------------------------------------------- workspace --
+hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace** out) {
+  if (!out) return fail(HS_ERR_INVALID, "hs_workspace_create: out is NULL");
+  *out = nullptr;
+  if (!model) return fail(HS_ERR_INVALID, "hs_workspace_create: model is NULL");
+  if (max_n < 1 || max_n > 16384)
+    return fail(HS_ERR_INVALID, "hs_workspace_create: max_n %d outside 1..16384", max_n);
+  hs_workspace* w = new (std::nothrow) hs_workspace;
+  if (!w) return fail(HS_ERR_OOM, "host allocation failed");
+  w->model = model;
+  w->ws.model = &model->m;
+  w->ws.max_n = max_n;
+  (void)hipGetDevice(&w->device);
+  const int64_t bytes = plan_workspace(model->m, max_n, &w->ws);
+  hipError_t e = hipMalloc((void**)&w->ws.arena, (size_t)bytes);
+  if (e != hipSuccess) {
+    delete w;
+    return fail(HS_ERR_OOM, "hipMalloc of %lld bytes: %s", (long long)bytes, hipGetErrorString(e));
+  }
+  w->ws.bytes = bytes;
+  plan_workspace(model->m, max_n, &w->ws);
+  const std::vector<int64_t>& gaps = model->m.gaps;
+  if (!gaps.empty()) {
+    e = hipMemcpy(w->ws.gaps, gaps.data(), gaps.size() * sizeof(int64_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(w->ws.arena);
+      delete w;
+      return hip_fail(e, "hs_workspace_create: upload");
+    }
+  }
+  *out = w;
+  return ok();
+}
+
+hs_status hs_workspace_destroy(hs_workspace* ws) {
+  if (!ws) return ok();
+  if (ws->ws.arena) (void)hipFree(ws->ws.arena);
+  delete ws;
+  return ok();
+}
+
+int64_t hs_workspace_bytes(const hs_workspace* ws) { return ws ? ws->ws.bytes : -1; }
+
+// ---------------------------------------------------------------- the step --
+hs_status hs_worker_grad(const hs_model* model, hs_workspace* ws, const float* theta,
+                         const uint16_t* theta_bf16, const float* x_m, const int32_t* y_m,
+                         int32_t n_m, float* g_m, float* loss_m, void* stream) {
+  if (!model || !ws) return fail(HS_ERR_INVALID, "hs_worker_grad: model/workspace is NULL");
+  if (ws->model != model) return fail(HS_ERR_INVALID, "hs_worker_grad: workspace of another model");
+  if (!theta || !x_m || !y_m || !g_m)
+    return fail(HS_ERR_INVALID, "hs_worker_grad: theta, x_m, y_m and g_m must not be NULL");
+  const bool bf = model->m.dtype == HS_BF16;
+  if (bf && !theta_bf16) return fail(HS_ERR_INVALID, "hs_worker_grad: bf16 model needs theta_bf16");
+  if (!bf && theta_bf16)
+    return fail(HS_ERR_INVALID, "hs_worker_grad: theta_bf16 must be NULL for an fp32 model");
+  if (n_m < 1 || n_m > ws->ws.max_n)
+    return fail(HS_ERR_INVALID, "hs_worker_grad: n_m %d outside 1..%d", n_m, ws->ws.max_n);
+  if (!aligned16(theta) || !aligned16(x_m) || !aligned16(g_m) ||
+      (theta_bf16 && !aligned16(theta_bf16)))
+    return fail(HS_ERR_INVALID, "hs_worker_grad: device pointers must be 16-byte aligned");
+  hipError_t e = worker_grad(model->m, ws->ws, theta, theta_bf16, x_m, y_m, n_m, g_m, loss_m,
+                             (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_worker_grad");
+  return ok();
+}
+
+static hs_status check_wavg(const float* const* g, const int32_t* n, int32_t M, int64_t P,
+                            float* w) {
+  if (!g || !n) return fail(HS_ERR_INVALID, "weighted average: g and n must not be NULL");
+  if (M < 1 || M > 16) return fail(HS_ERR_INVALID, "weighted average: M %d outside 1..16", M);
+  if (P < 0) return fail(HS_ERR_INVALID, "weighted average: P < 0");
+  double total = 0.0;
+  for (int m = 0; m < M; ++m) {
+    if (n[m] < 0) return fail(HS_ERR_INVALID, "weighted average: n[%d] < 0", m);
+    if (!g[m] && P > 0) return fail(HS_ERR_INVALID, "weighted average: g[%d] is NULL", m);
+    if (!aligned16(g[m])) return fail(HS_ERR_INVALID, "weighted average: g[%d] not 16-byte aligned", m);
+    total += (double)n[m];
+  }
+  if (!(total > 0.0)) return fail(HS_ERR_INVALID, "weighted average: sum of n must be > 0");
+  for (int m = 0; m < M; ++m) w[m] = (float)((double)n[m] / total);
+  return HS_OK;
+}
+
+hs_status hs_weighted_average(const float* const* g, const int32_t* n, int32_t M, int64_t P,
+                              float* g_out, void* stream) {
+  float w[16];
+  hs_status st = check_wavg(g, n, M, P, w);
+  if (st != HS_OK) return st;
+  if (P == 0) return ok();
+  if (!g_out || !aligned16(g_out))
+    return fail(HS_ERR_INVALID, "hs_weighted_average: g_out NULL or not 16-byte aligned");
+  for (int m = 0; m < M; ++m)
+    if (g[m] == g_out) return fail(HS_ERR_INVALID, "hs_weighted_average: g_out aliases g[%d]", m);
+  hipError_t e = launch_wavg_sgd(g, w, M, nullptr, nullptr, g_out, P, 0.f, 0.f, 0.f, nullptr, 0,
+                                 (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_weighted_average");
+  return ok();
+}
+
+static hs_status check_sgd(float* theta, float* mom, int64_t P, float lr, float mu, float wd,
+                           uint16_t* tbf) {
+  if (P < 0) return fail(HS_ERR_INVALID, "sgd: P < 0");
+  if (P > 0 && !theta) return fail(HS_ERR_INVALID, "sgd: theta is NULL");
+  if (!mom && mu != 0.f) return fail(HS_ERR_INVALID, "sgd: momentum buffer needed when mu != 0");
+  if (!isfinite(lr) || !isfinite(mu) || !isfinite(wd))
+    return fail(HS_ERR_INVALID, "sgd: lr, mu, wd must be finite");
+  if (!aligned16(theta) || !aligned16(mom) || !aligned16(tbf))
+    return fail(HS_ERR_INVALID, "sgd: pointers must be 16-byte aligned");
+  return HS_OK;
+}
+
+hs_status hs_sgd_step(float* theta, const float* g, float* mom, int64_t P, float lr, float mu,
+                      float wd, uint16_t* theta_bf16, void* stream) {
+  hs_status st = check_sgd(theta, mom, P, lr, mu, wd, theta_bf16);
+  if (st != HS_OK) return st;
+  if (P == 0) return ok();
+  if (!g || !aligned16(g)) return fail(HS_ERR_INVALID, "hs_sgd_step: g NULL or not aligned");
+  const float* gs[1] = {g};
+  const float w[1] = {1.f};
+  hipError_t e = launch_wavg_sgd(gs, w, 1, theta, mom, nullptr, P, lr, mu, wd, theta_bf16, 1,
+                                 (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_sgd_step");
+  return ok();
+}
+
+hs_status hs_wavg_sgd(const float* const* g, const int32_t* n, int32_t M, float* theta,
+                      float* mom, int64_t P, float lr, float mu, float wd, uint16_t* theta_bf16,
+                      void* stream) {
+  float w[16];
+  hs_status st = check_wavg(g, n, M, P, w);
+  if (st != HS_OK) return st;
+  st = check_sgd(theta, mom, P, lr, mu, wd, theta_bf16);
+  if (st != HS_OK) return st;
+  if (P == 0) return ok();
+  hipError_t e = launch_wavg_sgd(g, w, M, theta, mom, nullptr, P, lr, mu, wd, theta_bf16, 2,
+                                 (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_wavg_sgd");
+  return ok();
+}
+
+hs_status hs_params_to_bf16(const float* theta, uint16_t* theta_bf16, int64_t P, void* stream) {
+  if (P < 0) return fail(HS_ERR_INVALID, "hs_params_to_bf16: P < 0");
+  if (P == 0) return ok();
+  if (!theta || !theta_bf16) return fail(HS_ERR_INVALID, "hs_params_to_bf16: NULL pointer");
+  hipError_t e = launch_to_bf16(theta, theta_bf16, P, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_params_to_bf16");
+  return ok();
+}
+
+hs_status hs_layer_gemm(int32_t mode, int32_t dtype, int32_t n, int32_t H, int32_t W, int32_t C,
+                        int32_t K, int32_t R, int32_t stride, int32_t pad, const void* a,
+                        const void* b, void* out, const float* bias, int32_t relu,
+                        int32_t out_f32, float* scratch, int64_t scratch_floats, void* stream) {
+  if (mode < 0 || mode > 2) return fail(HS_ERR_INVALID, "hs_layer_gemm: mode %d", mode);
+  if (dtype != HS_FP32 && dtype != HS_BF16) return fail(HS_ERR_INVALID, "hs_layer_gemm: dtype");
+  if (n < 1 || H < 1 || W < 1 || C < 1 || K < 1 || R < 1 || pad < 0 || (stride != 1 && stride != 2))
+    return fail(HS_ERR_INVALID, "hs_layer_gemm: bad geometry");
+  const int Ho = (H + 2 * pad - R) / stride + 1, Wo = (W + 2 * pad - R) / stride + 1;
+  if (Ho < 1 || Wo < 1) return fail(HS_ERR_INVALID, "hs_layer_gemm: empty output");
+  if ((int64_t)n * H * W * C >= (1ll << 31) || (int64_t)n * Ho * Wo * K >= (1ll << 31))
+    return fail(HS_ERR_INVALID, "hs_layer_gemm: tensor too large for 32-bit indexing");
+  if (!a || !b || !out) return fail(HS_ERR_INVALID, "hs_layer_gemm: NULL operand");
+  if (!aligned16(a) || !aligned16(b) || !aligned16(out) || !aligned16(scratch))
+    return fail(HS_ERR_INVALID, "hs_layer_gemm: pointers must be 16-byte aligned");
+  if (mode == 1 && dtype == HS_BF16 && out_f32)
+    return fail(HS_ERR_INVALID, "hs_layer_gemm: data gradient of bf16 operands is stored as bf16");
+  ConvL L{};
+  L.cin = C;
+  L.cout = K;
+  L.k = R;
+  L.stride = stride;
+  L.pad = pad;
+  L.H = H;
+  L.W = W;
+  L.Ho = Ho;
+  L.Wo = Wo;
+  L.relu = relu != 0;
+  hipError_t e = layer_gemm(mode, dtype == HS_BF16, L, n, a, b, out, bias, out_f32 != 0,
+                            scratch, scratch_floats, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_layer_gemm");
+  return ok();
+}
+
+// ---------------------------------------------- compute power, repartition --
+hs_status hs_estimate_cp(const int32_t* n, const double* mean_time, int32_t M, double* cp_out) {
+  if (!n || !mean_time || !cp_out || M < 1)
+    return fail(HS_ERR_INVALID, "hs_estimate_cp: bad arguments");
+  for (int m = 0; m < M; ++m) {
+    if (n[m] < 1) return fail(HS_ERR_INVALID, "hs_estimate_cp: n[%d] < 1", m);
+    if (!isfinite(mean_time[m]) || !(mean_time[m] > 0.0))
+      return fail(HS_ERR_INVALID, "hs_estimate_cp: mean_time[%d] not finite and > 0", m);
+  }
+  for (int m = 0; m < M; ++m) cp_out[m] = (double)n[m] / mean_time[m];
+  return ok();
+}
+
+hs_status hs_repartition(const double* throughput, int32_t M, int32_t N, int32_t* n_out) {
+  if (!throughput || !n_out) return fail(HS_ERR_INVALID, "hs_repartition: NULL pointer");
+  if (M < 1 || N < M) return fail(HS_ERR_INVALID, "hs_repartition: need N >= M >= 1 (M=%d N=%d)", M, N);
+  for (int m = 0; m < M; ++m)
+    if (!isfinite(throughput[m]) || !(throughput[m] > 0.0))
+      return fail(HS_ERR_INVALID, "hs_repartition: throughput[%d] not finite and > 0", m);
+  double S = 0.0;
+  for (int m = 0; m < M; ++m) S = S + throughput[m];
+  std::vector<int64_t> f(M);
+  std::vector<double> r(M);
+  int64_t fsum = 0;
+  for (int m = 0; m < M; ++m) {
+    const double c = throughput[m] / S;
+    const double q = c * (double)N;
+    const double fl = floor(q);
+    f[m] = (int64_t)fl;
+    r[m] = q - fl;
+    fsum += f[m];
+  }
+  const int64_t left = (int64_t)N - fsum;
+  if (left < 0 || left > M) return fail(HS_ERR_INVALID, "hs_repartition: rounding left %lld", (long long)left);
+  std::vector<int> order(M);
+  for (int m = 0; m < M; ++m) order[m] = m;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    if (r[a] != r[b]) return r[a] > r[b];
+    return a < b;
+  });
+  for (int64_t i = 0; i < left; ++i) f[order[i]] += 1;
+  for (;;) {
+    int z = -1;
+    for (int m = 0; m < M; ++m)
+      if (f[m] == 0) {
+        z = m;
+        break;
+      }
+    if (z < 0) break;
+    int big = 0;
+    for (int m = 1; m < M; ++m)
+      if (f[m] > f[big]) big = m;
+    f[big] -= 1;
+    f[z] += 1;
+  }
+  for (int m = 0; m < M; ++m) n_out[m] = (int32_t)f[m];
+  return ok();
+}
+
+hs_status hs_partitioner_create(int32_t M, int32_t N, int32_t window, hs_partitioner** out) {
+  if (!out) return fail(HS_ERR_INVALID, "hs_partitioner_create: out is NULL");
+  *out = nullptr;
+  if (M < 1 || M > 1024 || N < M || window < 0)
+    return fail(HS_ERR_INVALID, "hs_partitioner_create: need 1 <= M <= 1024, M <= N, window >= 0");
+  hs_partitioner* p = new (std::nothrow) hs_partitioner;
+  if (!p) return fail(HS_ERR_OOM, "host allocation failed");
+  p->M = M;
+  p->N = N;
+  p->window = window;
+  p->steps_in_window = 0;
+  p->n.assign(M, 0);
+  p->xsum.assign(M, 0.0);
+  std::vector<double> ones(M, 1.0);  // Algorithm 1, epoch 0: CP_m = 1/M
+  hs_status st = hs_repartition(ones.data(), M, N, p->n.data());
+  if (st != HS_OK) {
+    delete p;
+    return st;
+  }
+  *out = p;
+  return ok();
+}
+
+hs_status hs_partitioner_destroy(hs_partitioner* p) {
+  delete p;
+  return ok();
+}
+
+hs_status hs_partitioner_partition(const hs_partitioner* p, int32_t* n_out) {
+  if (!p || !n_out) return fail(HS_ERR_INVALID, "hs_partitioner_partition: NULL pointer");
+  memcpy(n_out, p->n.data(), sizeof(int32_t) * p->M);
+  return ok();
+}
+
+hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n) {
+  if (!p || !n) return fail(HS_ERR_INVALID, "hs_partitioner_set_partition: NULL pointer");
+  int64_t s = 0;
+  for (int m = 0; m < p->M; ++m) {
+    if (n[m] < 1) return fail(HS_ERR_INVALID, "hs_partitioner_set_partition: n[%d] < 1", m);
+    s += n[m];
+  }
+  if (s != p->N) return fail(HS_ERR_INVALID, "hs_partitioner_set_partition: sum != N");
+  memcpy(p->n.data(), n, sizeof(int32_t) * p->M);
+  return ok();
+}
+
+hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
+                                 int32_t* repartitioned, double* cp_out) {
+  if (!p || !tau || !speed) return fail(HS_ERR_INVALID, "hs_partitioner_observe: NULL pointer");
+  for (int m = 0; m < p->M; ++m) {
+    if (!isfinite(tau[m]) || !(tau[m] > 0.0) || !isfinite(speed[m]) || !(speed[m] > 0.0))
+      return fail(HS_ERR_INVALID, "hs_partitioner_observe: tau/speed[%d] not finite and > 0", m);
+  }
+  if (repartitioned) *repartitioned = 0;
+  for (int m = 0; m < p->M; ++m) p->xsum[m] = p->xsum[m] + tau[m] / speed[m];
+  p->steps_in_window += 1;
+  if (p->window == 0 || p->steps_in_window < p->window) return ok();
+  std::vector<double> xbar(p->M), cp(p->M);
+  for (int m = 0; m < p->M; ++m) xbar[m] = p->xsum[m] / (double)p->window;
+  hs_status st = hs_estimate_cp(p->n.data(), xbar.data(), p->M, cp.data());
+  if (st != HS_OK) return st;
+  std::vector<int32_t> next(p->M);
+  st = hs_repartition(cp.data(), p->M, p->N, next.data());
+  if (st != HS_OK) return st;
+  p->n = next;
+  p->steps_in_window = 0;
+  std::fill(p->xsum.begin(), p->xsum.end(), 0.0);
+  if (repartitioned) *repartitioned = 1;
+  if (cp_out) memcpy(cp_out, cp.data(), sizeof(double) * p->M);
+  return ok();
+}
+
+}  // extern "C"

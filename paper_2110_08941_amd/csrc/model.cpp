@@ -1,0 +1,661 @@
+// Network descriptions, workspace plan and the per-worker forward/backward
+// launch schedule.
+//
+// The worker gradient is g_m = grad of the mean softmax cross-entropy over the
+// worker's samples (Eq. (1) of the paper with the expectation over the
+// worker's partition), batch-norm statistics taken over the worker's own
+// samples.  Every contraction runs on the implicit-GEMM MFMA kernel; the
+// remaining layers are the bandwidth-bound kernels of layers.hip.
+#include "model.h"
+
+#include "../../include/hs.h"
+
+namespace hs {
+
+// ----------------------------------------------------------------------------
+// model construction
+// ----------------------------------------------------------------------------
+namespace {
+
+struct Builder {
+  Model& m;
+  explicit Builder(Model& mm) : m(mm) {}
+
+  int64_t add(const std::string& name, int kind, std::vector<int64_t> shape) {
+    int64_t numel = 1;
+    for (int64_t d : shape) numel *= d;
+    int64_t off = (m.P + 63) / 64 * 64;
+    if (off > m.P) {
+      m.gaps.push_back(m.P);
+      m.gaps.push_back(off);
+    }
+    m.params.push_back({name, kind, shape, off, numel});
+    m.P = off + numel;
+    m.P_true += numel;
+    return off;
+  }
+
+  ConvL conv(const std::string& name, int cin, int cout, int k, int stride, int pad, int H, int W,
+             bool bias, bool relu) {
+    ConvL c;
+    c.cin = cin;
+    c.cout = cout;
+    c.k = k;
+    c.stride = stride;
+    c.pad = pad;
+    c.H = H;
+    c.W = W;
+    c.Ho = (H + 2 * pad - k) / stride + 1;
+    c.Wo = (W + 2 * pad - k) / stride + 1;
+    c.w = add(name + ".weight", HS_KIND_CONV_W, {cout, k, k, cin});
+    c.b = bias ? add(name + ".bias", HS_KIND_BIAS, {cout}) : -1;
+    c.relu = relu;
+    m.fwd_macs += (int64_t)c.Ho * c.Wo * cout * k * k * cin;
+    note_act((int64_t)c.Ho * c.Wo * cout);
+    note_act((int64_t)H * W * cin);
+    return c;
+  }
+
+  ConvL linear(const std::string& name, int fin, int fout, bool relu) {
+    ConvL c;
+    c.cin = fin;
+    c.cout = fout;
+    c.k = 1;
+    c.stride = 1;
+    c.pad = 0;
+    c.H = c.W = c.Ho = c.Wo = 1;
+    c.w = add(name + ".weight", HS_KIND_LIN_W, {fout, fin});
+    c.b = add(name + ".bias", HS_KIND_BIAS, {fout});
+    c.relu = relu;
+    m.fwd_macs += (int64_t)fin * fout;
+    note_act(fin);
+    note_act(fout);
+    return c;
+  }
+
+  BNL bn(const std::string& name, int c) {
+    BNL b;
+    b.c = c;
+    b.g = add(name + ".gamma", HS_KIND_BN_GAMMA, {c});
+    b.b = add(name + ".beta", HS_KIND_BN_BETA, {c});
+    b.stat = m.nbn++;
+    if (c > m.max_c) m.max_c = c;
+    return b;
+  }
+
+  void note_act(int64_t e) {
+    if (e > m.max_act) m.max_act = e;
+  }
+};
+
+}  // namespace
+
+bool build_model(int arch, int dtype, Model& m) {
+  m = Model();
+  m.arch = arch;
+  m.dtype = dtype;
+  Builder b(m);
+  if (arch == HS_MLP) {
+    m.in_numel = 784;
+    m.fc1 = b.linear("fc1", 784, 256, true);
+    m.fc2 = b.linear("fc2", 256, 10, false);
+  } else if (arch == HS_SMALLCNN) {
+    m.in_numel = 3 * 32 * 32;
+    m.c1 = b.conv("conv1", 3, 32, 3, 1, 1, 32, 32, true, true);
+    m.c2 = b.conv("conv2", 32, 64, 3, 1, 1, 32, 32, true, true);
+    m.c3 = b.conv("conv3", 64, 128, 3, 1, 1, 16, 16, true, true);
+    m.fc2 = b.linear("fc", 128, 10, false);
+  } else if (arch == HS_RESNET18) {
+    m.in_numel = 3 * 32 * 32;
+    m.stem = b.conv("stem", 3, 64, 3, 1, 1, 32, 32, false, false);
+    m.stem_bn = b.bn("stem_bn", 64);
+    const int widths[4] = {64, 128, 256, 512};
+    int cin = 64, H = 32;
+    for (int si = 0; si < 4; ++si) {
+      for (int bi = 0; bi < 2; ++bi) {
+        const int stride = (si > 0 && bi == 0) ? 2 : 1;
+        const int w = widths[si];
+        std::string nm = "layer" + std::to_string(si + 1) + "." + std::to_string(bi);
+        BlockL blk{};
+        blk.c1 = b.conv(nm + ".conv1", cin, w, 3, stride, 1, H, H, false, false);
+        blk.b1 = b.bn(nm + ".bn1", w);
+        const int Ho = blk.c1.Ho;
+        blk.c2 = b.conv(nm + ".conv2", w, w, 3, 1, 1, Ho, Ho, false, false);
+        blk.b2 = b.bn(nm + ".bn2", w);
+        blk.proj = (stride != 1 || cin != w);
+        if (blk.proj) {
+          blk.cp = b.conv(nm + ".proj", cin, w, 1, stride, 0, H, H, false, false);
+          blk.bp = b.bn(nm + ".proj_bn", w);
+        }
+        m.blocks.push_back(blk);
+        cin = w;
+        H = Ho;
+      }
+    }
+    m.fc2 = b.linear("fc", 512, 10, false);
+  } else if (arch == HS_VGG16) {
+    m.in_numel = 3 * 32 * 32;
+    const int cfg[18] = {64, 64, -1, 128, 128, -1, 256, 256, 256, -1,
+                         512, 512, 512, -1, 512, 512, 512, -1};
+    int cin = 3, H = 32, idx = 0;
+    for (int i = 0; i < 18; ++i) {
+      if (cfg[i] < 0) {
+        m.vgg.back().pool = true;
+        H /= 2;
+        continue;
+      }
+      ++idx;
+      VggL l{};
+      l.c = b.conv("conv" + std::to_string(idx), cin, cfg[i], 3, 1, 1, H, H, false, false);
+      l.bn = b.bn("bn" + std::to_string(idx), cfg[i]);
+      l.pool = false;
+      m.vgg.push_back(l);
+      cin = cfg[i];
+    }
+    m.fc1 = b.linear("fc1", 512, 512, true);
+    m.fc2 = b.linear("fc2", 512, 10, false);
+  } else {
+    return false;
+  }
+  int64_t end = (m.P + 63) / 64 * 64;
+  if (end > m.P) {
+    m.gaps.push_back(m.P);
+    m.gaps.push_back(end);
+  }
+  m.P = end;
+  if (m.max_c < 16) m.max_c = 16;
+  return true;
+}
+
+// ----------------------------------------------------------------------------
+// workspace plan: the same walk sizes the arena (ws->arena == null) and
+// binds the slots
+// ----------------------------------------------------------------------------
+namespace {
+struct Bump {
+  char* base;
+  int64_t off = 0;
+  void* take(int64_t bytes) {
+    off = (off + 255) / 256 * 256;
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+}  // namespace
+
+int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
+  const int64_t es = m.dtype == HS_BF16 ? 2 : 4;
+  Bump a{ws->arena};
+  ws->slot.clear();
+  auto act = [&](int64_t per_sample) { ws->slot.push_back(a.take(per_sample * max_n * es)); };
+  if (m.arch == HS_MLP) {
+    act(784);    // 0: input in activation type
+    act(256);    // 1: hidden (post ReLU)
+  } else if (m.arch == HS_SMALLCNN) {
+    act(3 * 1024);           // 0: X0 (NHWC)
+    act(32 * 1024);          // 1: A1
+    act(64 * 1024);          // 2: A2
+    act(64 * 256);           // 3: P2
+    act(128 * 256);          // 4: A3
+    act(128);                // 5: F
+  } else if (m.arch == HS_RESNET18) {
+    act(3 * 1024);           // 0: X0
+    act(64 * 1024);          // 1: Zs
+    act(64 * 1024);          // 2: As
+    for (const BlockL& b : m.blocks) {
+      const int64_t e = (int64_t)b.c1.Ho * b.c1.Wo * b.c1.cout;
+      act(e);                // Z1
+      act(e);                // H
+      act(e);                // Z2
+      act(b.proj ? e : 0);   // ZP
+      act(e);                // A_out
+    }
+    act(512);                // F
+  } else {
+    act(3 * 1024);           // 0: X0
+    for (const VggL& l : m.vgg) {
+      const int64_t e = (int64_t)l.c.Ho * l.c.Wo * l.c.cout;
+      act(e);                // Z
+      act(e);                // A
+      act(l.pool ? e / 4 : 0);  // P
+    }
+    act(512);                // Hf (fc1 output)
+  }
+  for (int i = 0; i < 5; ++i) ws->grad[i] = a.take(m.max_act * max_n * es);
+  ws->logits = (float*)a.take((int64_t)max_n * 10 * 4);
+  ws->dz32 = (float*)a.take((int64_t)max_n * 10 * 4);
+  ws->dzt = a.take((int64_t)max_n * 10 * es);
+  ws->stats = (float*)a.take((int64_t)(m.nbn > 0 ? m.nbn : 1) * 2 * m.max_c * 4);
+  ws->partial = (double*)a.take((int64_t)1024 * 2 * (m.max_c > 512 ? m.max_c : 512) * 8);
+  ws->splitk_floats = (int64_t)16 << 20;
+  ws->splitk = (float*)a.take(ws->splitk_floats * 4);
+  ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
+  return a.off;
+}
+
+// ----------------------------------------------------------------------------
+// launch helpers
+// ----------------------------------------------------------------------------
+namespace {
+
+#define HS_TRY(expr)                    \
+  do {                                  \
+    hipError_t e_ = (expr);             \
+    if (e_ != hipSuccess) return e_;    \
+  } while (0)
+
+struct Ctx {
+  const Model& m;
+  Workspace& ws;
+  const float* theta;
+  const bf16_t* tbf;
+  float* g;
+  int n;
+  hipStream_t s;
+  bool bf;
+  int V;  // elements per 16 bytes
+  const void* W(int64_t off) const {
+    return bf ? (const void*)(tbf + off) : (const void*)(theta + off);
+  }
+  float* mean(const BNL& b) const { return ws.stats + (int64_t)b.stat * 2 * m.max_c; }
+  float* rstd(const BNL& b) const { return mean(b) + m.max_c; }
+};
+
+ConvGeom geom(const ConvL& c, int n) {
+  ConvGeom g;
+  g.n = n;
+  g.H = c.H;
+  g.W = c.W;
+  g.C = c.cin;
+  g.Ho = c.Ho;
+  g.Wo = c.Wo;
+  g.K = c.cout;
+  g.R = c.k;
+  g.S = c.k;
+  g.stride = c.stride;
+  g.pad = c.pad;
+  g.HWo = make_fastdiv((uint32_t)(c.Ho * c.Wo));
+  g.Wo_ = make_fastdiv((uint32_t)c.Wo);
+  g.HWi = make_fastdiv((uint32_t)(c.H * c.W));
+  g.Wi_ = make_fastdiv((uint32_t)c.W);
+  g.Cdiv = make_fastdiv((uint32_t)c.cin);
+  g.Kdiv = make_fastdiv((uint32_t)c.cout);
+  g.Sdiv = make_fastdiv((uint32_t)c.k);
+  return g;
+}
+
+GemmParams base_params(const ConvL& c, int n) {
+  GemmParams p{};
+  p.g = geom(c, n);
+  return p;
+}
+
+void pick_tiles(int M, int N, int& bm, int& bn) {
+  const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+  for (int i = 0; i < 4; ++i) {
+    if (N <= 64 && cand[i][1] == 128) continue;
+    if (M <= 64 && cand[i][0] == 128) continue;
+    int64_t tiles = (int64_t)ceil_div(M, cand[i][0]) * ceil_div(N, cand[i][1]);
+    if (tiles >= 512) {
+      bm = cand[i][0];
+      bn = cand[i][1];
+      return;
+    }
+  }
+  bm = 64;
+  bn = 64;
+}
+
+// y = conv(x) (+ bias, ReLU); out_f32 forces an fp32 output
+hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32) {
+  GemmParams p = base_params(L, c.n);
+  p.a = x;
+  p.b = c.W(L.w);
+  p.out = y;
+  p.bias = L.b >= 0 ? c.theta + L.b : nullptr;
+  p.relu = L.relu ? 1 : 0;
+  p.out_f32 = (out_f32 || !c.bf) ? 1 : 0;
+  p.M = c.n * L.Ho * L.Wo;
+  p.N = L.cout;
+  p.K = L.k * L.k * L.cin;
+  const bool vec = (L.cin % c.V) == 0;
+  int bm, bn;
+  pick_tiles(p.M, p.N, bm, bn);
+  return launch_igemm(MODE_FWD, c.bf, p, vec, vec, bm, bn, 1, c.s);
+}
+
+// dx = dgrad(dy) (+ addend) (* [mask > 0])
+hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, const void* addend,
+                      const void* mask) {
+  GemmParams p = base_params(L, c.n);
+  p.a = dy;
+  p.b = c.W(L.w);
+  p.out = dx;
+  p.addend = addend;
+  p.mask = mask;
+  p.out_f32 = c.bf ? 0 : 1;
+  p.M = c.n * L.H * L.W;
+  p.N = L.cin;
+  p.K = L.k * L.k * L.cout;
+  const bool veca = (L.cout % c.V) == 0;
+  const bool vecb = (L.cin % c.V) == 0;
+  int bm, bn;
+  pick_tiles(p.M, p.N, bm, bn);
+  return launch_igemm(MODE_DGRAD, c.bf, p, veca, vecb, bm, bn, 1, c.s);
+}
+
+// g[L.w] = wgrad(dy, x); split-K over pixels when the tile grid is small
+hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* x) {
+  GemmParams p = base_params(L, c.n);
+  p.a = dy;
+  p.b = x;
+  p.M = L.cout;
+  p.N = L.k * L.k * L.cin;
+  p.K = c.n * L.Ho * L.Wo;
+  const bool veca = (L.cout % c.V) == 0;
+  const bool vecb = (L.cin % c.V) == 0;
+  const int bm = p.M <= 64 ? 64 : 128, bn = 128;
+  const int tiles = ceil_div(p.M, bm) * ceil_div(p.N, bn);
+  const int bke = 128 / (c.bf ? 2 : 4);
+  const int ktiles = ceil_div(p.K, bke);
+  int splits = ceil_div(1024, tiles);
+  if (splits > ktiles / 4) splits = ktiles / 4;
+  const int64_t mn = (int64_t)p.M * p.N;
+  if (splits > c.ws.splitk_floats / mn) splits = (int)(c.ws.splitk_floats / mn);
+  if (splits < 1) splits = 1;
+  if (splits > 1) {
+    const int per = ceil_div(ktiles, splits);
+    splits = ceil_div(ktiles, per);
+  }
+  float* dst = c.g + L.w;
+  if (splits == 1) {
+    p.out = dst;
+    p.split_stride = 0;
+    return launch_igemm(MODE_WGRAD, c.bf, p, veca, vecb, bm, bn, 1, c.s);
+  }
+  p.out = c.ws.splitk;
+  p.split_stride = mn;
+  HS_TRY(launch_igemm(MODE_WGRAD, c.bf, p, veca, vecb, bm, bn, splits, c.s));
+  return launch_splitk_reduce(c.ws.splitk, splits, mn, mn, dst, c.s);
+}
+
+// g[bias] = sum over rows of dy (dy in activation type unless f32)
+hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64_t rows, int C) {
+  HS_TRY(launch_chan_partials(2, f32 ? false : c.bf, dy, dy, nullptr, nullptr, nullptr, rows, C,
+                              c.ws.partial, c.s));
+  return launch_chan_reduce(c.ws.partial, chan_blocks(rows, C), C, c.g + boff, nullptr, c.s);
+}
+
+hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rows) {
+  HS_TRY(launch_chan_partials(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, rows, b.c,
+                              c.ws.partial, c.s));
+  return launch_bn_finalize(c.ws.partial, chan_blocks(rows, b.c), b.c, rows, 1e-5f, c.mean(b),
+                            c.rstd(b), c.s);
+}
+
+// dz = batch-norm backward of dy (masked by [act > 0] if act); writes
+// dbeta, dgamma into g
+hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
+                  int64_t rows, void* dz) {
+  HS_TRY(launch_chan_partials(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), rows, b.c, c.ws.partial,
+                              c.s));
+  HS_TRY(launch_chan_reduce(c.ws.partial, chan_blocks(rows, b.c), b.c, c.g + b.b, c.g + b.g,
+                            c.s));
+  return launch_bn_backward(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.theta + b.g, c.g + b.b,
+                            c.g + b.g, rows, b.c, dz, c.s);
+}
+
+// softmax cross-entropy on the logits; returns the operand for the last
+// layer's backward (fp32 or bf16 copy of dz)
+hipError_t loss_grad(const Ctx& c, const int32_t* y, float* loss, const void** dzop) {
+  HS_TRY(launch_softmax_ce(c.ws.logits, y, c.n, 10, loss, c.ws.dz32, c.bf ? c.ws.dzt : nullptr,
+                           c.bf, c.s));
+  *dzop = c.bf ? c.ws.dzt : (const void*)c.ws.dz32;
+  return hipSuccess;
+}
+
+// ---------------------------------------------------------------- MLP ----
+hipError_t mlp(const Ctx& c, const float* x, const int32_t* y, float* loss) {
+  const Model& m = c.m;
+  const void* X = x;
+  if (c.bf) {
+    HS_TRY(launch_cast_input(x, c.ws.slot[0], (int64_t)c.n * 784, true, c.s));
+    X = c.ws.slot[0];
+  }
+  void* Hh = c.ws.slot[1];
+  HS_TRY(conv_fwd(c, m.fc1, X, Hh, false));
+  HS_TRY(conv_fwd(c, m.fc2, Hh, c.ws.logits, true));
+  const void* dz;
+  HS_TRY(loss_grad(c, y, loss, &dz));
+  HS_TRY(conv_wgrad(c, m.fc2, dz, Hh));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, c.n, 10));
+  void* dH = c.ws.grad[0];
+  HS_TRY(conv_dgrad(c, m.fc2, dz, dH, nullptr, Hh));
+  HS_TRY(bias_grad(c, m.fc1.b, dH, false, c.n, 256));
+  return conv_wgrad(c, m.fc1, dH, X);
+}
+
+// ----------------------------------------------------------- small CNN ----
+hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss) {
+  const Model& m = c.m;
+  void **S = c.ws.slot.data(), **G = c.ws.grad;
+  const int n = c.n;
+  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
+  HS_TRY(conv_fwd(c, m.c1, S[0], S[1], false));
+  HS_TRY(conv_fwd(c, m.c2, S[1], S[2], false));
+  HS_TRY(launch_maxpool_fwd(c.bf, S[2], n, 32, 32, 64, S[3], c.s));
+  HS_TRY(conv_fwd(c, m.c3, S[3], S[4], false));
+  HS_TRY(launch_gap_fwd(c.bf, S[4], n, 256, 128, S[5], c.s));
+  HS_TRY(conv_fwd(c, m.fc2, S[5], c.ws.logits, true));
+  const void* dz;
+  HS_TRY(loss_grad(c, y, loss, &dz));
+  HS_TRY(conv_wgrad(c, m.fc2, dz, S[5]));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
+  HS_TRY(launch_gap_bwd(c.bf, G[0], S[4], n, 256, 128, G[1], c.s));    // dA3 * [A3 > 0]
+  HS_TRY(bias_grad(c, m.c3.b, G[1], false, (int64_t)n * 256, 128));
+  HS_TRY(conv_wgrad(c, m.c3, G[1], S[3]));
+  HS_TRY(conv_dgrad(c, m.c3, G[1], G[0], nullptr, nullptr));          // dP2
+  HS_TRY(launch_maxpool_bwd(c.bf, S[2], G[0], n, 32, 32, 64, 1, G[2], c.s));  // dA2 * [A2 > 0]
+  HS_TRY(bias_grad(c, m.c2.b, G[2], false, (int64_t)n * 1024, 64));
+  HS_TRY(conv_wgrad(c, m.c2, G[2], S[1]));
+  HS_TRY(conv_dgrad(c, m.c2, G[2], G[0], nullptr, S[1]));             // dA1 * [A1 > 0]
+  HS_TRY(bias_grad(c, m.c1.b, G[0], false, (int64_t)n * 1024, 32));
+  return conv_wgrad(c, m.c1, G[0], S[0]);
+}
+
+// ---------------------------------------------------------- ResNet-18 ----
+hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
+  const Model& m = c.m;
+  void** S = c.ws.slot.data();
+  void** G = c.ws.grad;
+  const int n = c.n;
+  const int64_t rows0 = (int64_t)n * 1024;
+  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
+  HS_TRY(conv_fwd(c, m.stem, S[0], S[1], false));
+  HS_TRY(bn_stats(c, m.stem_bn, S[1], rows0));
+  HS_TRY(launch_bn_apply(c.bf, S[1], c.mean(m.stem_bn), c.rstd(m.stem_bn), c.theta + m.stem_bn.g,
+                         c.theta + m.stem_bn.b, nullptr, 1, rows0, 64, S[2], c.s));
+  const void* cur = S[2];
+  int si = 3;
+  for (const BlockL& b : m.blocks) {
+    void *Z1 = S[si], *Hh = S[si + 1], *Z2 = S[si + 2], *ZP = S[si + 3], *A = S[si + 4];
+    si += 5;
+    const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
+    HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
+    HS_TRY(bn_stats(c, b.b1, Z1, rows));
+    HS_TRY(launch_bn_apply(c.bf, Z1, c.mean(b.b1), c.rstd(b.b1), c.theta + b.b1.g,
+                           c.theta + b.b1.b, nullptr, 1, rows, b.b1.c, Hh, c.s));
+    HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
+    HS_TRY(bn_stats(c, b.b2, Z2, rows));
+    const void* res = cur;
+    if (b.proj) {
+      HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
+      HS_TRY(bn_stats(c, b.bp, ZP, rows));
+      HS_TRY(launch_bn_apply(c.bf, ZP, c.mean(b.bp), c.rstd(b.bp), c.theta + b.bp.g,
+                             c.theta + b.bp.b, nullptr, 0, rows, b.bp.c, G[0], c.s));
+      res = G[0];
+    }
+    HS_TRY(launch_bn_apply(c.bf, Z2, c.mean(b.b2), c.rstd(b.b2), c.theta + b.b2.g,
+                           c.theta + b.b2.b, res, 1, rows, b.b2.c, A, c.s));
+    cur = A;
+  }
+  void* F = S[si];
+  HS_TRY(launch_gap_fwd(c.bf, cur, n, 16, 512, F, c.s));
+  HS_TRY(conv_fwd(c, m.fc2, F, c.ws.logits, true));
+  // ---- backward
+  const void* dz;
+  HS_TRY(loss_grad(c, y, loss, &dz));
+  HS_TRY(conv_wgrad(c, m.fc2, dz, F));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
+  HS_TRY(launch_gap_bwd(c.bf, G[0], nullptr, n, 16, 512, G[1], c.s));
+  int gi = 1;  // buffer holding the gradient of the current block output
+  for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
+    const BlockL& b = m.blocks[bi];
+    const int base = 3 + 5 * bi;
+    void *Z1 = S[base], *Hh = S[base + 1], *Z2 = S[base + 2], *ZP = S[base + 3],
+         *A = S[base + 4];
+    const void* in = bi == 0 ? S[2] : S[3 + 5 * (bi - 1) + 4];
+    int fr[4], k = 0;
+    for (int i = 0; i < 5; ++i)
+      if (i != gi) fr[k++] = i;
+    void *dA = G[gi], *P1 = G[fr[0]], *P2 = G[fr[1]], *P3 = G[fr[2]], *P4 = G[fr[3]];
+    const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
+    HS_TRY(launch_relu_mask(c.bf, dA, A, rows * b.c2.cout, P1, c.s));        // dPre
+    HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rows, P2));                     // dZ2
+    HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
+    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, nullptr));                  // dH
+    HS_TRY(bn_bwd(c, b.b1, P3, Hh, Z1, rows, P2));                          // dZ1
+    HS_TRY(conv_wgrad(c, b.c1, P2, in));
+    if (b.proj) {
+      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rows, P3));                   // dZP
+      HS_TRY(conv_wgrad(c, b.cp, P3, in));
+      HS_TRY(conv_dgrad(c, b.cp, P3, dA, nullptr, nullptr));                // shortcut grad
+      HS_TRY(conv_dgrad(c, b.c1, P2, P4, dA, nullptr));                     // dIn
+      gi = fr[3];
+    } else {
+      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, nullptr));                     // dIn
+      gi = fr[2];
+    }
+  }
+  // stem
+  void* dZs = G[gi == 0 ? 1 : 0];
+  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], S[2], S[1], rows0, dZs));
+  return conv_wgrad(c, m.stem, dZs, S[0]);
+}
+
+// -------------------------------------------------------------- VGG-16 ----
+hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
+  const Model& m = c.m;
+  void** S = c.ws.slot.data();
+  void** G = c.ws.grad;
+  const int n = c.n;
+  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
+  const void* cur = S[0];
+  const int L = (int)m.vgg.size();
+  for (int i = 0; i < L; ++i) {
+    const VggL& l = m.vgg[i];
+    void *Z = S[1 + 3 * i], *A = S[2 + 3 * i], *P = S[3 + 3 * i];
+    const int64_t rows = (int64_t)n * l.c.Ho * l.c.Wo;
+    HS_TRY(conv_fwd(c, l.c, cur, Z, false));
+    HS_TRY(bn_stats(c, l.bn, Z, rows));
+    HS_TRY(launch_bn_apply(c.bf, Z, c.mean(l.bn), c.rstd(l.bn), c.theta + l.bn.g,
+                           c.theta + l.bn.b, nullptr, 1, rows, l.bn.c, A, c.s));
+    cur = A;
+    if (l.pool) {
+      HS_TRY(launch_maxpool_fwd(c.bf, A, n, l.c.Ho, l.c.Wo, l.c.cout, P, c.s));
+      cur = P;
+    }
+  }
+  const void* F = cur;  // [n][1][1][512]
+  void* Hf = S[1 + 3 * L];
+  HS_TRY(conv_fwd(c, m.fc1, F, Hf, false));
+  HS_TRY(conv_fwd(c, m.fc2, Hf, c.ws.logits, true));
+  const void* dz;
+  HS_TRY(loss_grad(c, y, loss, &dz));
+  HS_TRY(conv_wgrad(c, m.fc2, dz, Hf));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, Hf));                // dHf * [Hf > 0]
+  HS_TRY(bias_grad(c, m.fc1.b, G[0], false, n, 512));
+  HS_TRY(conv_wgrad(c, m.fc1, G[0], F));
+  HS_TRY(conv_dgrad(c, m.fc1, G[0], G[1], nullptr, nullptr));         // dF
+  int gi = 1;
+  for (int i = L - 1; i >= 0; --i) {
+    const VggL& l = m.vgg[i];
+    void *Z = S[1 + 3 * i], *A = S[2 + 3 * i];
+    const void* in = i == 0 ? S[0] : (m.vgg[i - 1].pool ? S[3 + 3 * (i - 1)] : S[2 + 3 * (i - 1)]);
+    const int64_t rows = (int64_t)n * l.c.Ho * l.c.Wo;
+    const int a = (gi + 1) % 3, b2 = (gi + 2) % 3;
+    int dAi = gi;
+    if (l.pool) {
+      HS_TRY(launch_maxpool_bwd(c.bf, A, G[gi], n, l.c.Ho, l.c.Wo, l.c.cout, 0, G[a], c.s));
+      dAi = a;
+    }
+    const int dZi = dAi == a ? b2 : a;
+    HS_TRY(bn_bwd(c, l.bn, G[dAi], A, Z, rows, G[dZi]));
+    HS_TRY(conv_wgrad(c, l.c, G[dZi], in));
+    if (i > 0) {
+      const int out = (dZi + 1) % 3 == dAi ? (dZi + 2) % 3 : (dZi + 1) % 3;
+      HS_TRY(conv_dgrad(c, l.c, G[dZi], G[out], nullptr, nullptr));
+      gi = out;
+    }
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a, const void* b,
+                      void* out, const float* bias, bool out_f32, float* scratch,
+                      int64_t scratch_floats, hipStream_t s) {
+  Model m;
+  m.dtype = bf16 ? HS_BF16 : HS_FP32;
+  Workspace ws;
+  ws.splitk = scratch;
+  ws.splitk_floats = scratch ? scratch_floats : 0;
+  // weights are addressed at offset 0 of the given operand
+  const float* th = bf16 ? nullptr : (const float*)b;
+  const bf16_t* tb = bf16 ? (const bf16_t*)b : nullptr;
+  ConvL l = L;
+  l.w = 0;
+  l.b = -1;
+  if (mode == MODE_FWD) {
+    Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};
+    GemmParams p = base_params(l, n);
+    p.a = a;
+    p.b = b;
+    p.out = out;
+    p.bias = bias;
+    p.relu = l.relu ? 1 : 0;
+    p.out_f32 = (out_f32 || !bf16) ? 1 : 0;
+    p.M = n * l.Ho * l.Wo;
+    p.N = l.cout;
+    p.K = l.k * l.k * l.cin;
+    const bool vec = (l.cin % c.V) == 0;
+    int bm, bn;
+    pick_tiles(p.M, p.N, bm, bn);
+    return launch_igemm(MODE_FWD, bf16, p, vec, vec, bm, bn, 1, s);
+  }
+  if (mode == MODE_DGRAD) {
+    Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};
+    if (out_f32 && bf16) return hipErrorInvalidValue;
+    return conv_dgrad(c, l, a, out, nullptr, nullptr);
+  }
+  Ctx c{m, ws, nullptr, nullptr, (float*)out, n, s, bf16, bf16 ? 8 : 4};
+  return conv_wgrad(c, l, a, b);
+}
+
+hipError_t worker_grad(const Model& m, Workspace& ws, const float* theta, const bf16_t* theta_bf16,
+                       const float* x, const int32_t* y, int n, float* g, float* loss,
+                       hipStream_t s) {
+  Ctx c{m, ws, theta, theta_bf16, g, n, s, m.dtype == HS_BF16, m.dtype == HS_BF16 ? 8 : 4};
+  HS_TRY(launch_zero_ranges(g, ws.gaps, (int)(m.gaps.size() / 2), s));
+  if (m.arch == HS_MLP) return mlp(c, x, y, loss);
+  if (m.arch == HS_SMALLCNN) return small_cnn(c, x, y, loss);
+  if (m.arch == HS_RESNET18) return resnet(c, x, y, loss);
+  return vgg(c, x, y, loss);
+}
+
+}  // namespace hs

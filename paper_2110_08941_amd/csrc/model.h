@@ -1,0 +1,92 @@
+// Network descriptions and the per-worker forward/backward schedule (host).
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace hs {
+
+struct ParamT {
+  std::string name;
+  int kind;                    // hs_tensor_kind
+  std::vector<int64_t> shape;
+  int64_t off, numel;
+};
+
+// A convolution or a linear layer (k = 1 on a 1x1 image).  w/b are offsets
+// into the flat parameter vector (b = -1: no bias).
+struct ConvL {
+  int cin, cout, k, stride, pad, H, W, Ho, Wo;
+  int64_t w, b;
+  bool relu;                   // bias + ReLU fused into the forward epilogue
+};
+
+struct BNL {
+  int c;
+  int64_t g, b;                // gamma, beta offsets
+  int stat;                    // index of this layer's mean/rstd in the workspace
+};
+
+struct BlockL {
+  ConvL c1, c2, cp;
+  BNL b1, b2, bp;
+  bool proj;
+};
+
+struct VggL {
+  ConvL c;
+  BNL bn;
+  bool pool;                   // 2x2 max-pool after the ReLU
+};
+
+struct Model {
+  int arch, dtype;
+  std::vector<ParamT> params;
+  int64_t P = 0, P_true = 0;
+  std::vector<int64_t> gaps;   // [begin, end) pairs of the padding gaps
+  int64_t in_numel = 0, fwd_macs = 0;
+  int nbn = 0, max_c = 0;
+  int64_t max_act = 0;         // largest activation, elements per sample
+  // MLP: fc1, fc2.  Small CNN: c1..c3, fc2.  ResNet: stem, stem_bn, blocks,
+  // fc2.  VGG: vgg, fc1, fc2.
+  ConvL fc1{}, fc2{}, c1{}, c2{}, c3{}, stem{};
+  BNL stem_bn{};
+  std::vector<BlockL> blocks;
+  std::vector<VggL> vgg;
+};
+
+bool build_model(int arch, int dtype, Model& m);
+
+// Device workspace of one worker.
+struct Workspace {
+  const Model* model = nullptr;
+  int max_n = 0;
+  char* arena = nullptr;
+  int64_t bytes = 0;
+  std::vector<void*> slot;     // forward activations, in plan order
+  void* grad[5] = {};          // gradient scratch buffers
+  float* logits = nullptr;
+  float* dz32 = nullptr;
+  void* dzt = nullptr;
+  float* stats = nullptr;      // per batch-norm: mean[max_c], rstd[max_c]
+  double* partial = nullptr;   // per-channel partial sums
+  float* splitk = nullptr;     // split-K partial outputs
+  int64_t splitk_floats = 0;
+  int64_t* gaps = nullptr;     // device copy of the padding ranges
+};
+
+int64_t plan_workspace(const Model& m, int max_n, Workspace* ws);  // ws->arena set => bind
+
+hipError_t worker_grad(const Model& m, Workspace& ws, const float* theta, const bf16_t* theta_bf16,
+                       const float* x, const int32_t* y, int n, float* g, float* loss,
+                       hipStream_t s);
+
+// One layer contraction (mode 0 forward, 1 data gradient, 2 weight gradient)
+// with the schedule hs_worker_grad uses.
+hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a, const void* b,
+                      void* out, const float* bias, bool out_f32, float* scratch,
+                      int64_t scratch_floats, hipStream_t s);
+
+}  // namespace hs

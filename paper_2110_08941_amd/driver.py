@@ -1,0 +1,135 @@
+"""Multi-step driver of the heterogeneous data-parallel step on one GPU.
+
+Each step (all device work through libhs):
+  * worker m gets rows [o_m, o_m + n_m) of the step's batch and runs
+    hs_worker_grad on its own HIP stream, bracketed by timing events;
+  * the main stream waits for every worker, then hs_wavg_sgd forms the
+    partition-weighted gradient and applies the SGD step in one pass;
+  * the workers' times tau_m feed the Dynamic Partitioning state
+    (hs_partitioner_observe), which divides them by the simulated speeds
+    s_m, and at the end of every window repartitions the batch in proportion
+    to the estimated compute powers (Eq. (2), Algorithm 1).
+With clock="model" the time of worker m is n_m (X_m = n_m / s_m), which
+makes the partition sequence independent of the hardware.
+PyTorch is used for device memory, streams and events only.
+"""
+import numpy as np
+import torch
+
+from . import hs, synth
+from .configs import WORKLOADS, Workload
+
+
+class Trainer:
+    def __init__(self, workload, seed=0, clock="measured", device="cuda:0", n_batches=4,
+                 max_n=None, steps=None, theta0=None):
+        self.wl = wl = WORKLOADS[workload] if isinstance(workload, str) else workload
+        assert isinstance(wl, Workload)
+        if clock not in ("measured", "model"):
+            raise ValueError("clock must be 'measured' or 'model'")
+        self.clock = clock
+        self.dev = torch.device(device)
+        self.M, self.N = wl.workers, wl.total
+        self.steps = steps if steps is not None else wl.steps
+        self.model = hs.model_create(wl.arch, wl.dtype)
+        self.P = hs.num_params(self.model)
+        self.table = hs.param_table(self.model)
+        self.bf16 = wl.dtype == "bf16"
+        th = synth.he_normal(self.table, self.P, seed) if theta0 is None else theta0
+        self.theta = torch.tensor(np.asarray(th, dtype=np.float32), device=self.dev)
+        self.theta_bf16 = torch.empty(self.P, dtype=torch.int16, device=self.dev) if self.bf16 else None
+        if self.bf16:
+            hs.params_to_bf16(self.theta.data_ptr(), self.theta_bf16.data_ptr(), self.P)
+        self.mom = torch.zeros(self.P, device=self.dev) if wl.mu != 0.0 else None
+        self.grads = [torch.empty(self.P, device=self.dev) for _ in range(self.M)]
+        self.losses = torch.zeros(self.M, device=self.dev)
+        self.streams = [torch.cuda.Stream(device=self.dev) for _ in range(self.M)]
+        self.max_n = max_n or self.N
+        self.ws = [hs.workspace_create(self.model, self.max_n) for _ in range(self.M)]
+        self.part = hs.Partitioner(self.M, self.N, wl.window)
+        if not wl.start_even:                       # fixed split in proportion to the speeds
+            self.part.set_partition(hs.repartition(list(wl.speeds), self.N))
+        self.speeds = synth.speed_schedule(wl.speeds, max(self.steps, 1), seed, wl.drift_sigma)
+        self.in_numel = hs.input_numel(self.model)
+        self.batches = []
+        for b in range(n_batches):
+            x, y = synth.batch(wl.in_shape, self.N, seed, b)
+            self.batches.append((torch.from_numpy(x).to(self.dev), torch.from_numpy(y).to(self.dev)))
+        self.t = 0
+        self.pending = []       # (step, partition, [(e0, e1)] or None) awaiting observation
+        self.log = []           # per step: partition, tau, cp (if a window closed)
+
+    # ------------------------------------------------------------------ step
+    def batch(self, t):
+        return self.batches[t % len(self.batches)]
+
+    def launch_workers(self, n, x, y, timed=True):
+        """Worker gradients on their streams; the main stream waits for all."""
+        main = torch.cuda.current_stream(self.dev)
+        ready = torch.cuda.Event()
+        ready.record(main)
+        events, o = [], 0
+        ew = x.element_size() * self.in_numel
+        for m in range(self.M):
+            s = self.streams[m]
+            s.wait_event(ready)
+            e0 = e1 = None
+            if timed:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+            hs.worker_grad(self.model, self.ws[m], self.theta.data_ptr(),
+                           self.theta_bf16.data_ptr() if self.bf16 else 0,
+                           x.data_ptr() + o * ew, y.data_ptr() + o * 4, n[m],
+                           self.grads[m].data_ptr(), self.losses.data_ptr() + 4 * m,
+                           s.cuda_stream)
+            if timed:
+                e1.record(s)
+            else:
+                e1 = torch.cuda.Event()
+                e1.record(s)
+            events.append((e0, e1))
+            o += n[m]
+        for _, e1 in events:
+            main.wait_event(e1)
+        return events
+
+    def step(self):
+        """One synchronous step; returns the partition it used."""
+        wl, t = self.wl, self.t
+        n = self.part.partition()
+        x, y = self.batch(t)
+        events = self.launch_workers(n, x, y, timed=(self.clock == "measured"))
+        main = torch.cuda.current_stream(self.dev)
+        hs.wavg_sgd([g.data_ptr() for g in self.grads], n, self.theta.data_ptr(),
+                    self.mom.data_ptr() if self.mom is not None else 0, self.P, wl.lr, wl.mu,
+                    wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)
+        self.pending.append((t, n, events))
+        self.t += 1
+        if wl.window > 0 and len(self.pending) >= wl.window:
+            self.flush()
+        return n
+
+    def flush(self):
+        """Report the pending steps' times to the partitioner, in step order."""
+        for t, n, events in self.pending:
+            if self.clock == "measured":
+                tau = [float(e0.elapsed_time(e1)) for e0, e1 in events]
+            else:
+                tau = [float(v) for v in n]
+            speed = self.speeds[min(t, len(self.speeds) - 1)]
+            cp = self.part.observe(tau, speed) if self.wl.window > 0 else None
+            self.log.append({"step": t, "n": list(n), "tau": tau, "speed": list(speed), "cp": cp})
+        self.pending = []
+
+    def run(self, steps=None):
+        for _ in range(steps if steps is not None else self.steps):
+            self.step()
+        self.flush()
+
+    def close(self):
+        for w in self.ws:
+            hs.workspace_destroy(w)
+        self.ws = []
+        self.part.close()
+        hs.model_destroy(self.model)
+        self.model = None

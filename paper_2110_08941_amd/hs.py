@@ -1,0 +1,251 @@
+"""ctypes binding of libhs (the C ABI in include/hs.h).
+
+Argument marshalling only: every function forwards to the library of the
+same name.  Device pointers are passed as integers (e.g. a torch tensor's
+data_ptr()), streams as the integer handle of a hipStream_t (0 = default).
+The library must have been built (``python -m paper_2110_08941_amd.build``);
+importing this module without it raises immediately -- there is no fallback.
+"""
+import ctypes
+import os
+import re
+
+# The process must hold ONE HIP runtime.  PyTorch ships its own copy of
+# libamdhip64 (same soname as the system one); loading torch first makes the
+# library's dependency resolve to that copy instead of mapping a second one.
+import torch  # noqa: F401
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhs.so")
+
+HS_OK, HS_ERR_INVALID, HS_ERR_HIP, HS_ERR_OOM, HS_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
+ARCH = {"mlp": 0, "small_cnn": 1, "resnet18": 2, "vgg16": 3}
+DTYPE = {"fp32": 0, "bf16": 1}
+KIND = {0: "conv_w", 1: "lin_w", 2: "bias", 3: "bn_gamma", 4: "bn_beta"}
+
+
+class HSError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("libhs status %d: %s" % (status, msg))
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libhs.so not built at %s (python -m paper_2110_08941_amd.build)" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, D, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_float
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    PI32 = ctypes.POINTER(ctypes.c_int32)
+    PI64 = ctypes.POINTER(ctypes.c_int64)
+    PD = ctypes.POINTER(ctypes.c_double)
+    sigs = {
+        "hs_model_create": (I32, [I32, I32, PP]),
+        "hs_model_destroy": (I32, [P]),
+        "hs_num_params": (I64, [P]),
+        "hs_num_true_params": (I64, [P]),
+        "hs_num_param_tensors": (I32, [P]),
+        "hs_param_tensor": (I32, [P, I32, PI64, PI64, PI32, PI64, PI32,
+                                  ctypes.POINTER(ctypes.c_char_p)]),
+        "hs_input_numel": (I64, [P]),
+        "hs_forward_macs": (I64, [P]),
+        "hs_workspace_create": (I32, [P, I32, PP]),
+        "hs_workspace_destroy": (I32, [P]),
+        "hs_workspace_bytes": (I64, [P]),
+        "hs_worker_grad": (I32, [P, P, P, P, P, P, I32, P, P, P]),
+        "hs_weighted_average": (I32, [PP, PI32, I32, I64, P, P]),
+        "hs_sgd_step": (I32, [P, P, P, I64, F, F, F, P, P]),
+        "hs_wavg_sgd": (I32, [PP, PI32, I32, P, P, I64, F, F, F, P, P]),
+        "hs_params_to_bf16": (I32, [P, P, I64, P]),
+        "hs_estimate_cp": (I32, [PI32, PD, I32, PD]),
+        "hs_repartition": (I32, [PD, I32, I32, PI32]),
+        "hs_partitioner_create": (I32, [I32, I32, I32, PP]),
+        "hs_partitioner_destroy": (I32, [P]),
+        "hs_partitioner_partition": (I32, [P, PI32]),
+        "hs_partitioner_set_partition": (I32, [P, PI32]),
+        "hs_partitioner_observe": (I32, [P, PD, PD, PI32, PD]),
+        "hs_layer_gemm": (I32, [I32, I32, I32, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, I32,
+                                I32, P, I64, P]),
+        "hs_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    try:
+        maps = open("/proc/self/maps").read()
+    except OSError:
+        maps = ""
+    runtimes = set(re.findall(r"(/\S*libamdhip64[^/\s]*)", maps))
+    if len(runtimes) > 1:
+        raise ImportError("two HIP runtimes are mapped in this process: %s" % sorted(runtimes))
+    return lib
+
+
+_lib = _load()
+EXPORTED = (
+    "hs_model_create", "hs_model_destroy", "hs_num_params", "hs_num_true_params",
+    "hs_num_param_tensors", "hs_param_tensor", "hs_input_numel", "hs_forward_macs",
+    "hs_workspace_create", "hs_workspace_destroy", "hs_workspace_bytes", "hs_worker_grad",
+    "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
+    "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
+    "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
+    "hs_layer_gemm", "hs_last_error")
+
+
+def lib():
+    return _lib
+
+
+def last_error():
+    return _lib.hs_last_error().decode()
+
+
+def _check(st):
+    if st != HS_OK:
+        raise HSError(st, last_error())
+
+
+def _ptrs(seq):
+    return (ctypes.c_void_p * len(seq))(*[int(p) for p in seq])
+
+
+def _i32(seq):
+    return (ctypes.c_int32 * len(seq))(*[int(v) for v in seq])
+
+
+def _f64(seq):
+    return (ctypes.c_double * len(seq))(*[float(v) for v in seq])
+
+
+# ---------------------------------------------------------------- models --
+def model_create(arch, dtype):
+    h = ctypes.c_void_p()
+    _check(_lib.hs_model_create(ARCH.get(arch, arch), DTYPE.get(dtype, dtype), ctypes.byref(h)))
+    return h.value
+
+
+def model_destroy(model):
+    _check(_lib.hs_model_destroy(model))
+
+
+def num_params(model):
+    return int(_lib.hs_num_params(model))
+
+
+def num_true_params(model):
+    return int(_lib.hs_num_true_params(model))
+
+
+def input_numel(model):
+    return int(_lib.hs_input_numel(model))
+
+
+def forward_macs(model):
+    return int(_lib.hs_forward_macs(model))
+
+
+def param_table(model):
+    """[(name, kind, shape, offset)] in layout order."""
+    out = []
+    for i in range(_lib.hs_num_param_tensors(model)):
+        off, numel, ndim, kind = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        dims = (ctypes.c_int64 * 4)()
+        name = ctypes.c_char_p()
+        _check(_lib.hs_param_tensor(model, i, ctypes.byref(off), ctypes.byref(numel),
+                                    ctypes.byref(ndim), dims, ctypes.byref(kind), ctypes.byref(name)))
+        out.append((name.value.decode(), KIND[kind.value], tuple(dims[:ndim.value]), off.value))
+    return out
+
+
+def workspace_create(model, max_n):
+    h = ctypes.c_void_p()
+    _check(_lib.hs_workspace_create(model, int(max_n), ctypes.byref(h)))
+    return h.value
+
+
+def workspace_destroy(ws):
+    _check(_lib.hs_workspace_destroy(ws))
+
+
+def workspace_bytes(ws):
+    return int(_lib.hs_workspace_bytes(ws))
+
+
+# ---------------------------------------------------------------- step --
+def worker_grad(model, ws, theta, theta_bf16, x_m, y_m, n_m, g_m, loss_m=0, stream=0):
+    _check(_lib.hs_worker_grad(model, ws, theta, theta_bf16 or None, x_m, y_m, int(n_m), g_m,
+                               loss_m or None, stream or None))
+
+
+def weighted_average(g, n, P, g_out, stream=0):
+    _check(_lib.hs_weighted_average(_ptrs(g), _i32(n), len(g), int(P), g_out, stream or None))
+
+
+def sgd_step(theta, g, mom, P, lr, mu, wd, theta_bf16=0, stream=0):
+    _check(_lib.hs_sgd_step(theta, g, mom or None, int(P), lr, mu, wd, theta_bf16 or None,
+                            stream or None))
+
+
+def wavg_sgd(g, n, theta, mom, P, lr, mu, wd, theta_bf16=0, stream=0):
+    _check(_lib.hs_wavg_sgd(_ptrs(g), _i32(n), len(g), theta, mom or None, int(P), lr, mu, wd,
+                            theta_bf16 or None, stream or None))
+
+
+def params_to_bf16(theta, theta_bf16, P, stream=0):
+    _check(_lib.hs_params_to_bf16(theta, theta_bf16, int(P), stream or None))
+
+
+def layer_gemm(mode, dtype, n, H, W, C, K, R, stride, pad, a, b, out, bias=0, relu=False,
+               out_f32=False, scratch=0, scratch_floats=0, stream=0):
+    _check(_lib.hs_layer_gemm(int(mode), DTYPE.get(dtype, dtype), n, H, W, C, K, R, stride, pad,
+                              a, b, out, bias or None, int(bool(relu)), int(bool(out_f32)),
+                              scratch or None, int(scratch_floats), stream or None))
+
+
+# ------------------------------------------------- compute power, partition --
+def estimate_cp(n, mean_time):
+    out = (ctypes.c_double * len(n))()
+    _check(_lib.hs_estimate_cp(_i32(n), _f64(mean_time), len(n), out))
+    return list(out)
+
+
+def repartition(throughput, N):
+    out = (ctypes.c_int32 * len(throughput))()
+    _check(_lib.hs_repartition(_f64(throughput), len(throughput), int(N), out))
+    return list(out)
+
+
+class Partitioner:
+    """Dynamic Partitioning state (hs_partitioner_*)."""
+
+    def __init__(self, M, N, window):
+        h = ctypes.c_void_p()
+        _check(_lib.hs_partitioner_create(int(M), int(N), int(window), ctypes.byref(h)))
+        self.h, self.M = h.value, int(M)
+
+    def partition(self):
+        out = (ctypes.c_int32 * self.M)()
+        _check(_lib.hs_partitioner_partition(self.h, out))
+        return list(out)
+
+    def set_partition(self, n):
+        _check(_lib.hs_partitioner_set_partition(self.h, _i32(n)))
+
+    def observe(self, tau, speed):
+        """Returns the CP vector if this step closed a window, else None."""
+        rep = ctypes.c_int32()
+        cp = (ctypes.c_double * self.M)()
+        _check(_lib.hs_partitioner_observe(self.h, _f64(tau), _f64(speed), ctypes.byref(rep), cp))
+        return list(cp) if rep.value else None
+
+    def close(self):
+        if self.h:
+            _lib.hs_partitioner_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

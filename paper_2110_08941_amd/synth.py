@@ -52,6 +52,29 @@ def he_normal(table, total, seed):
     return theta
 
 
+def separate_decisions(table, theta, seed, gamma=0.5, shift=3.0):
+    """Batch-norm parameters that keep every ReLU decision far from its
+    threshold (for exact comparisons of deep ReLU/BN networks): gamma = 0.5
+    and beta = +shift on every channel of a batch-norm that feeds a residual
+    sum (names containing "bn2" or "proj_bn"), and beta = +shift or -shift on
+    a random half of the channels of every other batch-norm.  With |xhat|
+    below shift / gamma, every pre-activation is then >= shift - gamma |xhat|
+    away from zero.  Returns a modified copy of theta."""
+    th = np.array(theta, dtype=np.float32, copy=True)
+    g = _rng(seed, 19)
+    for name, kind, shape, off in table:
+        numel = int(np.prod(shape))
+        if kind == "bn_gamma":
+            th[off:off + numel] = gamma
+        elif kind == "bn_beta":
+            if "bn2" in name or "proj_bn" in name:
+                th[off:off + numel] = shift
+            else:
+                sign = np.where(g.random(numel) < 0.5, -1.0, 1.0)
+                th[off:off + numel] = (sign * shift).astype(np.float32)
+    return th
+
+
 def speed_schedule(base, steps, seed, drift_sigma=0.0):
     """Per-step worker speeds s_m(t), t = 0..steps-1, as float64 [steps, M].
 

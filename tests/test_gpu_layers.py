@@ -1,0 +1,74 @@
+"""Layer-level GPU parity: each implicit-GEMM contraction (forward, data
+gradient, weight gradient) of hs_layer_gemm against the oracle's convolution
+definition, over the shapes the networks use plus ragged edge cases."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import layers as L
+from tests.gpu_util import require_gpu, normwise, rne_bf16_bits, bf16_bits_to_f32, log
+
+pytestmark = pytest.mark.gpu
+
+# (n, H, W, C, K, R, stride, pad)
+SHAPES = [
+    (2, 32, 32, 3, 64, 3, 1, 1),      # stem (C = 3)
+    (2, 32, 32, 64, 64, 3, 1, 1),
+    (3, 32, 32, 32, 64, 3, 1, 1),     # K slice spans two taps (bf16)
+    (2, 16, 16, 64, 128, 3, 2, 1),    # strided 3x3
+    (2, 16, 16, 64, 128, 1, 2, 0),    # 1x1 projection
+    (5, 4, 4, 512, 512, 3, 1, 1),
+    (3, 2, 2, 512, 512, 3, 1, 1),
+    (9, 1, 1, 256, 10, 1, 1, 0),      # linear 256 -> 10
+    (9, 1, 1, 784, 256, 1, 1, 0),     # linear 784 -> 256
+    (7, 1, 1, 512, 512, 1, 1, 0),
+    (1, 8, 8, 128, 64, 3, 1, 1),
+]
+
+
+def rounded(x, dtype):
+    if dtype == "fp32":
+        return x.astype(np.float32), torch.from_numpy(x.astype(np.float32)).cuda()
+    bits = rne_bf16_bits(x)
+    return bf16_bits_to_f32(bits), torch.from_numpy(bits.view(np.int16)).cuda()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_layer_gemm(mode, shape, dtype):
+    hs = require_gpu()
+    n, H, W, C, K, R, st, pad = shape
+    log("layer_gemm mode=%d shape=%s %s" % (mode, shape, dtype))
+    Ho, Wo = (H + 2 * pad - R) // st + 1, (W + 2 * pad - R) // st + 1
+    rng = np.random.default_rng(sum(shape) + mode)
+    x, xd = rounded(rng.standard_normal((n, H, W, C)), dtype)
+    w, wd = rounded(rng.standard_normal((K, R, R, C)) / np.sqrt(R * R * C), dtype)
+    dy, dyd = rounded(rng.standard_normal((n, Ho, Wo, K)), dtype)
+    x64, w64, dy64 = x.astype(np.float64), w.astype(np.float64), dy.astype(np.float64)
+    scratch = torch.empty(1 << 22, device="cuda")
+    if mode == 0:
+        bias = rng.standard_normal(K).astype(np.float32)
+        out = torch.empty(n * Ho * Wo * K, device="cuda")
+        hs.layer_gemm(0, dtype, n, H, W, C, K, R, st, pad, xd.data_ptr(), wd.data_ptr(),
+                      out.data_ptr(), torch.from_numpy(bias).cuda().data_ptr(), relu=True,
+                      out_f32=True)
+        ref = np.maximum(L.conv_forward(x64, w64, st, pad, bias.astype(np.float64)), 0.0)
+    elif mode == 1:
+        out = torch.empty(n * H * W * C, device="cuda", dtype=torch.float32 if dtype == "fp32" else torch.int16)
+        hs.layer_gemm(1, dtype, n, H, W, C, K, R, st, pad, dyd.data_ptr(), wd.data_ptr(),
+                      out.data_ptr())
+        ref = L.conv_backward(x64, w64, dy64, st, pad)[0]
+    else:
+        out = torch.empty(K * R * R * C, device="cuda")
+        hs.layer_gemm(2, dtype, n, H, W, C, K, R, st, pad, dyd.data_ptr(), xd.data_ptr(),
+                      out.data_ptr(), scratch=scratch.data_ptr(), scratch_floats=scratch.numel())
+        ref = L.conv_backward(x64, w64, dy64, st, pad)[1]
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    if got.dtype == np.int16:
+        got = bf16_bits_to_f32(got.view(np.uint16))
+    err = normwise(got.reshape(-1), ref.reshape(-1))
+    log("  normwise err %.3e" % err)
+    tol = 1e-5 if dtype == "fp32" else (5e-3 if mode == 1 else 1e-5)
+    assert err <= tol

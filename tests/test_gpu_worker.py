@@ -1,0 +1,172 @@
+"""GPU parity of the worker gradient (hs_worker_grad) against the oracle.
+
+Tolerances (normwise: max |a - b| / max |b| over the whole gradient vector):
+fp32 1e-4 against the float64 oracle; bf16 2e-2 against the oracle with bf16
+storage emulation (the decisions -- ReLU masks, max-pool choices -- are then
+taken on the same bf16 values as in the kernels).
+
+Decisions.  A ReLU whose input is within the arithmetic's rounding error of
+zero may go either way; both outcomes are correct, and in deep batch-norm
+networks one such flip moves gradient entries by percents.  Two regimes:
+  * separated: batch-norm parameters that keep every ReLU input far from zero
+    (synth.separate_decisions); the comparison is direct.
+  * He init (the workloads' distribution): the oracle lists every ReLU
+    decision within 1e-6 (relative) of zero and computes the gradient change
+    of flipping each; the GPU result must equal the oracle's for SOME choice
+    of those flips (least squares, rounded to 0/1), within the tolerance.
+Every case prints its name before it runs."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import models as Mo
+from paper_2110_08941_amd import synth
+from tests.gpu_util import require_gpu, normwise, dev, log
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+STORAGE = {"fp32": "exact", "bf16": "bf16"}
+AMBIGUOUS = 1e-6
+
+
+def run_worker(arch, dtype, n, seed=0, theta=None, data_seed=None):
+    """GPU gradient of one worker on n synthetic samples; returns
+    (theta, x, y, g_gpu, loss_gpu)."""
+    hs = require_gpu()
+    m = hs.model_create(arch, dtype)
+    try:
+        table = hs.param_table(m)
+        P = hs.num_params(m)
+        if theta is None:
+            theta = synth.he_normal(table, P, seed)
+        shape = (784,) if arch == "mlp" else (3, 32, 32)
+        x, y = synth.batch(shape, n, seed if data_seed is None else data_seed, 1)
+        th_d = dev(theta)
+        tb = None
+        if dtype == "bf16":
+            tb = torch.empty(P, dtype=torch.int16, device="cuda")
+            hs.params_to_bf16(th_d.data_ptr(), tb.data_ptr(), P)
+        x_d, y_d = dev(x), dev(y)
+        g_d = torch.full((P,), float("nan"), device="cuda")     # must be fully overwritten
+        loss_d = torch.zeros(1, device="cuda")
+        ws = hs.workspace_create(m, n)
+        hs.worker_grad(m, ws, th_d.data_ptr(), tb.data_ptr() if tb is not None else 0,
+                       x_d.data_ptr(), y_d.data_ptr(), n, g_d.data_ptr(), loss_d.data_ptr(), 0)
+        torch.cuda.synchronize()
+        hs.workspace_destroy(ws)
+        return theta, x, y, g_d.cpu().numpy(), float(loss_d.cpu()[0])
+    finally:
+        hs.model_destroy(m)
+
+
+def decision_aware(net, theta, x, y, storage, g_gpu):
+    """Normwise error of g_gpu against the oracle, minimised over the outcomes
+    of the ambiguous ReLU decisions.  Returns (err, n_ambiguous, flips, loss,
+    g_oracle, ctx)."""
+    th = np.asarray(theta, dtype=np.float64)
+    ctx = Mo.Ctx(storage, capture=AMBIGUOUS)
+    loss, g0 = Mo.worker_grad(net, th, x, y, ctx=ctx)
+    amb = [(c, i) for c, i, _ in ctx.ambiguous]
+    if not amb:
+        return normwise(g_gpu, g0), 0, 0, loss, g0, ctx
+    D = np.stack([Mo.worker_grad(net, th, x, y, ctx=Mo.Ctx(storage, toggles={a}))[1] - g0
+                  for a in amb], axis=1)
+    s = np.linalg.lstsq(D, np.asarray(g_gpu, dtype=np.float64) - g0, rcond=None)[0]
+    s = np.clip(np.round(s), 0.0, 1.0)
+    return normwise(g_gpu, g0 + D @ s), len(amb), int(s.sum()), loss, g0, ctx
+
+
+def check_padding(arch, g):
+    net = Mo.build(arch)
+    table, P = Mo.param_table(net)
+    used = np.zeros(P, dtype=bool)
+    for name, kind, shape, off in table:
+        used[off:off + int(np.prod(shape))] = True
+    assert np.all(g[~used] == 0.0)
+
+
+REGULAR = [("mlp", "fp32", 1), ("mlp", "fp32", 7), ("mlp", "fp32", 64),
+           ("small_cnn", "fp32", 1), ("small_cnn", "fp32", 5), ("small_cnn", "fp32", 19),
+           ("resnet18", "fp32", 2), ("resnet18", "fp32", 3),
+           ("vgg16", "fp32", 3),
+           ("mlp", "bf16", 9), ("mlp", "bf16", 64), ("small_cnn", "bf16", 3),
+           ("small_cnn", "bf16", 11)]
+
+
+@pytest.mark.parametrize("arch,dtype,n", REGULAR)
+def test_worker_grad_he_init(arch, dtype, n):
+    log("worker_grad he-init %s %s n=%d" % (arch, dtype, n))
+    theta, x, y, g, loss = run_worker(arch, dtype, n, seed=n)
+    assert np.all(np.isfinite(g)), "gradient has non-finite entries"
+    check_padding(arch, g)
+    net = Mo.build(arch)
+    err, namb, flips, ref_loss, _, ctx = decision_aware(net, theta, x, y, STORAGE[dtype], g)
+    pool = [m[1][0] for m in ctx.margins if m[0] == "maxpool" and m[1].size]
+    log("  normwise err %.3e (ambiguous ReLU %d, flipped %d, min pool margin %.1e) loss %.6f vs %.6f"
+        % (err, namb, flips, min(pool) if pool else float("inf"), loss, ref_loss))
+    assert err <= TOL[dtype]
+    assert abs(loss - ref_loss) <= TOL[dtype] * max(1.0, abs(ref_loss))
+
+
+SEPARATED = [("resnet18", "fp32", 4), ("resnet18", "fp32", 13),
+             ("vgg16", "fp32", 4), ("vgg16", "fp32", 6),
+             ("resnet18", "bf16", 4), ("resnet18", "bf16", 16),
+             ("vgg16", "bf16", 4), ("vgg16", "bf16", 12)]
+
+
+@pytest.mark.parametrize("arch,dtype,n", SEPARATED)
+def test_worker_grad_separated(arch, dtype, n):
+    """Batch-norm networks with every ReLU decision far from zero: direct
+    comparison.  Max-pool decisions (VGG) are checked to be unambiguous in the
+    oracle; the first data seed whose pool margins exceed 1e-6 is used."""
+    log("worker_grad separated %s %s n=%d" % (arch, dtype, n))
+    net = Mo.build(arch)
+    table, P = Mo.param_table(net)
+    theta = synth.separate_decisions(table, synth.he_normal(table, P, n), n)
+    for data_seed in range(n, n + 60):
+        x, y = synth.batch((3, 32, 32), n, data_seed, 1)
+        ctx = Mo.Ctx(STORAGE[dtype])
+        ref_loss, ref = Mo.worker_grad(net, theta.astype(np.float64), x, y, ctx=ctx)
+        relu = [m[1][0] for m in ctx.margins if m[0] == "relu" and m[1].size]
+        pool = [m[1][0] for m in ctx.margins if m[0] == "maxpool" and m[1].size]
+        if min(pool, default=1.0) > AMBIGUOUS or dtype == "bf16":
+            break
+    else:
+        pytest.fail("no data seed with unambiguous max-pool decisions")
+    assert min(relu) > 1e-4
+    _, _, _, g, loss = run_worker(arch, dtype, n, theta=theta, data_seed=data_seed)
+    assert np.all(np.isfinite(g))
+    err = normwise(g, ref)
+    log("  normwise err %.3e (min relu margin %.1e, min pool margin %.1e, data seed %d) loss %.6f vs %.6f"
+        % (err, min(relu), min(pool, default=float("inf")), data_seed, loss, ref_loss))
+    assert err <= TOL[dtype]
+    assert abs(loss - ref_loss) <= TOL[dtype] * max(1.0, abs(ref_loss))
+
+
+@pytest.mark.parametrize("arch,n", [("resnet18", 4), ("vgg16", 6)])
+def test_bf16_he_init_error_is_that_of_bf16_storage(arch, n):
+    """He-init batch-norm networks in bf16: the GPU gradient is as far from the
+    exact gradient as the oracle's own bf16-storage gradient is (the spread
+    comes from ReLU decisions that bf16 rounding flips), and the loss matches
+    the bf16-storage oracle."""
+    log("bf16 he-init spread %s n=%d" % (arch, n))
+    theta, x, y, g, loss = run_worker(arch, "bf16", n, seed=n)
+    net = Mo.build(arch)
+    th = theta.astype(np.float64)
+    _, ge = Mo.worker_grad(net, th, x, y)
+    lb, gb = Mo.worker_grad(net, th, x, y, storage="bf16")
+    spread = normwise(gb, ge)
+    err = normwise(g, ge)
+    log("  gpu-vs-exact %.3e, bf16-oracle-vs-exact %.3e, loss %.6f vs %.6f" % (err, spread, loss, lb))
+    assert err <= 1.5 * spread + TOL["bf16"]
+    assert abs(loss - lb) <= TOL["bf16"] * max(1.0, abs(lb))
+
+
+@pytest.mark.parametrize("arch,dtype,n", [("small_cnn", "fp32", 37), ("resnet18", "bf16", 19),
+                                          ("vgg16", "fp32", 5)])
+def test_worker_grad_deterministic(arch, dtype, n):
+    log("determinism %s %s n=%d" % (arch, dtype, n))
+    a = run_worker(arch, dtype, n, seed=2)[3]
+    b = run_worker(arch, dtype, n, seed=2)[3]
+    assert np.array_equal(a, b)

@@ -264,3 +264,52 @@ def test_pins_catch_planted_mistakes(monkeypatch, mutation):
     _, g = Mo.worker_grad(net, theta, x, y)
     _, tg = torch_grad(net, table, total, theta, x, y)
     assert np.max(np.abs(g - tg)) > 1e-6 * np.max(np.abs(tg))
+
+
+def test_bf16_round_matches_torch():
+    """Round-to-nearest-even bf16 of the storage emulation against torch's
+    float32 -> bfloat16 conversion (ties, subnormals, large values)."""
+    from oracle import layers as L
+    rng = np.random.default_rng(12)
+    x = np.concatenate([rng.standard_normal(100000) * 10.0 ** rng.integers(-30, 30, 100000),
+                        np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -1.0 - 2.0 ** -8,
+                                  1e-40, -3e-39, 0.0, 3.0e38])]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(L.bf16_round(x), ref)
+
+
+def test_storage_emulation_and_decision_toggles():
+    """bf16 storage stays close to the exact gradient on a network without
+    batch-norm; toggling a listed ambiguous ReLU decision changes the gradient
+    only along that decision's direction; exact storage lists no decision with
+    a margin above the capture threshold."""
+    kw, in_shape, n = TINY["small_cnn"]
+    net, table, total, theta, x, y = rand_problem("small_cnn", kw, in_shape, 6, seed=61)
+    _, ge = Mo.worker_grad(net, theta, x, y)
+    _, gb = Mo.worker_grad(net, theta, x, y, storage="bf16")
+    assert 0 < np.max(np.abs(gb - ge)) <= 5e-2 * np.max(np.abs(ge))
+    ctx = Mo.Ctx("exact", capture=0.05)
+    _, g0 = Mo.worker_grad(net, theta, x, y, ctx=ctx)
+    assert np.array_equal(g0, ge)
+    assert ctx.ambiguous and all(m < 0.05 for _, _, m in ctx.ambiguous)
+    c, i, _ = ctx.ambiguous[0]
+    _, g1 = Mo.worker_grad(net, theta, x, y, ctx=Mo.Ctx("exact", toggles={(c, i)}))
+    assert np.max(np.abs(g1 - g0)) > 0
+    _, g2 = Mo.worker_grad(net, theta, x, y, ctx=Mo.Ctx("exact", toggles={(c, i), (c, i)}))
+    assert np.array_equal(g1, g2)
+
+
+def test_separated_decisions_have_large_margins():
+    """The separated batch-norm parameters keep every ReLU input of the BN
+    networks well away from zero (the regime of the direct GPU comparisons)."""
+    from paper_2110_08941_amd import synth
+    for arch in ("resnet18", "vgg16"):
+        kw, in_shape, n = TINY[arch]
+        net = Mo.build(arch, **kw)
+        table, total = Mo.param_table(net)
+        theta = synth.separate_decisions(table, synth.he_normal(table, total, 1), 1)
+        x, y = synth.batch(in_shape, 6, 1, 0, classes=3)
+        ctx = Mo.Ctx("exact")
+        Mo.worker_grad(net, theta.astype(np.float64), x, y, ctx=ctx)
+        relu = [m[1][0] for m in ctx.margins if m[0] == "relu"]
+        assert min(relu) > 1e-3
