@@ -1,0 +1,147 @@
+"""Benchmark of the heterogeneous data-parallel training step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload resnet18_bf16]
+                    [--no-cpu-baseline] [--gpus 1]
+
+One step = every simulated worker's forward+backward on its partition of a
+synthetic CIFAR-shaped batch (each on its own HIP stream, timed by events),
+the fused partition-weighted gradient average + momentum SGD, and -- at the
+end of every repartition window -- the compute-power estimate and the
+repartition of the next window.  W untimed steps, then K timed steps between
+two device synchronisations; the batches are resident in HBM before timing.
+
+Prints ONE JSON line: samples/s over the K steps, the roofline position of
+the dominant GEMM kernel (timed live with HIP events on the worker streams
+during the timed steps), and the CPU oracle's throughput on a bounded sample
+of the same step, timed on this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "train samples/s (fwd+bwd+wavg+SGD), CIFAR-shape ResNet-18; MFMA/HBM % peak"
+PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}   # MI355X dense MFMA peaks
+HBM_PEAK_GBS = 8000.0
+
+# GEMM instantiation probed for the roofline (mode, bm, bn), per workload:
+# the forward convolution kernel with 128 x 64 tiles (every 64-channel layer).
+PROBE = {"resnet18_bf16": (0, 128, 64), "resnet18_fp32": (0, 128, 64),
+         "vgg16_bf16": (0, 128, 64), "smallcnn_fp32": (0, 128, 64), "mlp_fp32": (0, 64, 64)}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet18_bf16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=192,
+                    help="samples of the CPU oracle's bounded step")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, seed, samples):
+    """The CPU oracle (float64, numpy) on a bounded sample of the step: the same
+    workers and speeds, each with its share of `samples` samples, followed by
+    the weighted average and the SGD step."""
+    import numpy as np
+    from oracle import models as Mo
+    from oracle import step as S
+    from paper_2110_08941_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    net = Mo.build(wl.arch)
+    table, P = Mo.param_table(net)
+    theta = synth.he_normal(table, P, seed).astype(np.float64)
+    n = S.repartition(list(wl.speeds), samples) if samples >= wl.workers else [1] * wl.workers
+    x, y = synth.batch(wl.in_shape, sum(n), seed, 0)
+    t0 = time.perf_counter()
+    out = S.step(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym), theta, None, x, y, n,
+                 wl.lr, wl.mu, wl.wd)
+    cp = S.estimate_cp(n, [float(v) for v in n])
+    S.repartition(cp, sum(n))
+    dt = time.perf_counter() - t0
+    assert np.all(np.isfinite(out["theta"]))
+    return {"value": round(sum(n) / dt, 3), "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "one float64 step of %s on %d samples split %s over the %d workers "
+                      "(worker gradients, weighted average, SGD, repartition); %.1f s"
+                      % (wl.arch, sum(n), n, wl.workers, dt)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build runs all simulated workers on a single "
+              "MI355X and has no multi-GPU path (--gpus %d requested)" % args.gpus)
+        sys.exit(2)
+    import torch
+    from paper_2110_08941_amd import hs
+    from paper_2110_08941_amd.configs import WORKLOADS
+    from paper_2110_08941_amd.driver import Trainer
+
+    wl = WORKLOADS[args.workload]
+    tr = Trainer(wl, seed=args.seed, clock="measured",
+                 steps=args.warmup + args.steps)
+    mode, bm, bn = PROBE[args.workload]
+    for w in tr.ws:
+        hs.probe_enable(w, mode, bm, bn, capacity=64 * (args.steps + 1))
+    for _ in range(args.warmup):
+        tr.step()
+    tr.flush()
+    torch.cuda.synchronize()
+    for w in tr.ws:
+        hs.probe_read(w)                    # drop the warm-up launches
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        tr.step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tr.flush()
+    ms, launches, flops = 0.0, 0, 0.0
+    for w in tr.ws:
+        a, b, c = hs.probe_read(w)
+        ms, launches, flops = ms + a, launches + b, flops + c
+    value = wl.total * args.steps / elapsed
+    achieved = flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
+    peak = PEAK_TFLOPS[wl.dtype]
+    loss = tr.losses.cpu().tolist()
+    parts = [e["n"] for e in tr.log]
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": "%s: %s CIFAR-shape (3x32x32, 10 classes), N=%d over M=%d "
+                               "workers, speeds %s%s, repartition every %s steps"
+                               % (wl.name, wl.arch, wl.total, wl.workers, list(wl.speeds),
+                                  " drifting (sigma %.2f)" % wl.drift_sigma if wl.drift_sigma else "",
+                                  wl.window or "never"),
+                   "global_batch": wl.total, "workers": wl.workers, "parallelism": "simulated-dp%d-1gpu" % wl.workers},
+        "roofline": {"bound": "mfma", "kernel": "igemm_kernel mode=%d tile=%dx%d %s" % (mode, bm, bn, wl.dtype),
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),
+                     "flops_per_launch": flops / max(launches, 1)},
+        "partitions_last": parts[-1] if parts else None,
+        "loss_last": [round(v, 4) for v in loss],
+    }
+    tr.close()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_samples)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -180,6 +180,24 @@ hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n);
 hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
                                  int32_t* repartitioned, double* cp_out);
 
+/* ------------------------------------------------------------- probing -- */
+
+/* Timing probe of one implicit-GEMM kernel instantiation inside
+ * hs_worker_grad (for roofline reports).  While enabled, every launch of the
+ * GEMM kernel with the given mode (0 forward, 1 data gradient, 2 weight
+ * gradient) and output tile (bm x bn, each 64 or 128) on this workspace is
+ * bracketed by two HIP events on the worker's stream, and its algorithmic
+ * FLOPs (2 x pixels x c_out x taps x c_in, i.e. dense 3x3 taps, independent of
+ * the stride handling) are added up.  At most `capacity` launches are
+ * recorded (events are created here, not on the step path); later launches
+ * are not timed.  mode = -1 disables the probe and releases the events. */
+hs_status hs_probe_enable(hs_workspace* ws, int32_t mode, int32_t bm, int32_t bn,
+                          int32_t capacity);
+/* Waits for the recorded events and returns the summed kernel time (ms), the
+ * number of timed launches and their summed algorithmic FLOPs, then clears
+ * the record (the probe stays enabled). */
+hs_status hs_probe_read(hs_workspace* ws, double* total_ms, int64_t* launches, double* flops);
+
 /* ------------------------------------------------------ layer-level access -- */
 
 /* One contraction of a convolution or linear layer, as hs_worker_grad runs it

@@ -60,6 +60,14 @@ hs_status hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+void probe_release(Workspace& w) {
+  for (hipEvent_t e : w.probe_ev) (void)hipEventDestroy(e);
+  w.probe_ev.clear();
+  w.probe_flops.clear();
+  w.probe_used = 0;
+  w.probe_mode = -1;
+}
+
 }  // namespace
 
 extern "C" {
@@ -147,6 +155,7 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
 
 hs_status hs_workspace_destroy(hs_workspace* ws) {
   if (!ws) return ok();
+  probe_release(ws->ws);
   if (ws->ws.arena) (void)hipFree(ws->ws.arena);
   delete ws;
   return ok();
@@ -257,6 +266,51 @@ hs_status hs_params_to_bf16(const float* theta, uint16_t* theta_bf16, int64_t P,
   if (!theta || !theta_bf16) return fail(HS_ERR_INVALID, "hs_params_to_bf16: NULL pointer");
   hipError_t e = launch_to_bf16(theta, theta_bf16, P, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hs_params_to_bf16");
+  return ok();
+}
+
+
+hs_status hs_probe_enable(hs_workspace* ws, int32_t mode, int32_t bm, int32_t bn,
+                          int32_t capacity) {
+  if (!ws) return fail(HS_ERR_INVALID, "hs_probe_enable: workspace is NULL");
+  probe_release(ws->ws);
+  if (mode < 0) return ok();
+  if (mode > 2 || (bm != 64 && bm != 128) || (bn != 64 && bn != 128) || capacity < 1 ||
+      capacity > 1000000)
+    return fail(HS_ERR_INVALID, "hs_probe_enable: bad mode/tile/capacity");
+  ws->ws.probe_ev.resize(2 * (size_t)capacity + 1, nullptr);
+  for (size_t i = 0; i < ws->ws.probe_ev.size(); ++i) {
+    hipError_t e = hipEventCreate(&ws->ws.probe_ev[i]);
+    if (e != hipSuccess) {
+      ws->ws.probe_ev.resize(i);
+      probe_release(ws->ws);
+      return hip_fail(e, "hs_probe_enable");
+    }
+  }
+  ws->ws.probe_flops.assign(capacity, 0.0);
+  ws->ws.probe_mode = mode;
+  ws->ws.probe_bm = bm;
+  ws->ws.probe_bn = bn;
+  return ok();
+}
+
+hs_status hs_probe_read(hs_workspace* ws, double* total_ms, int64_t* launches, double* flops) {
+  if (!ws || !total_ms || !launches || !flops) return fail(HS_ERR_INVALID, "hs_probe_read: NULL");
+  Workspace& w = ws->ws;
+  double t = 0.0, f = 0.0;
+  for (size_t i = 0; i < w.probe_used; ++i) {
+    hipError_t e = hipEventSynchronize(w.probe_ev[2 * i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hs_probe_read");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, w.probe_ev[2 * i], w.probe_ev[2 * i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hs_probe_read");
+    t += ms;
+    f += w.probe_flops[i];
+  }
+  *total_ms = t;
+  *launches = (int64_t)w.probe_used;
+  *flops = f;
+  w.probe_used = 0;
   return ok();
 }
 

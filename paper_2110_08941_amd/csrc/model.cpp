@@ -307,6 +307,28 @@ void pick_tiles(int M, int N, int& bm, int& bn) {
   bn = 64;
 }
 
+// Launch one GEMM; brackets it with probe events when it is the probed
+// instantiation.
+hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
+                int splits, double flops) {
+  Workspace& ws = c.ws;
+  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn && veca &&
+                     vecb && ws.probe_used * 2 + 1 < ws.probe_ev.size();
+  if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
+  HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
+  if (probe) {
+    HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
+    ws.probe_flops[ws.probe_used] = flops;
+    ws.probe_used += 1;
+  }
+  return hipSuccess;
+}
+
+// algorithmic FLOPs of one contraction of layer L over n samples
+double layer_flops(const ConvL& L, int n) {
+  return 2.0 * n * L.Ho * L.Wo * (double)L.cout * L.k * L.k * L.cin;
+}
+
 // y = conv(x) (+ bias, ReLU); out_f32 forces an fp32 output
 hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32) {
   GemmParams p = base_params(L, c.n);
@@ -322,7 +344,7 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   const bool vec = (L.cin % c.V) == 0;
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
-  return launch_igemm(MODE_FWD, c.bf, p, vec, vec, bm, bn, 1, c.s);
+  return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, layer_flops(L, c.n));
 }
 
 // dx = dgrad(dy) (+ addend) (* [mask > 0])
@@ -342,7 +364,7 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   const bool vecb = (L.cin % c.V) == 0;
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
-  return launch_igemm(MODE_DGRAD, c.bf, p, veca, vecb, bm, bn, 1, c.s);
+  return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
 }
 
 // g[L.w] = wgrad(dy, x); split-K over pixels when the tile grid is small
@@ -372,11 +394,11 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
   if (splits == 1) {
     p.out = dst;
     p.split_stride = 0;
-    return launch_igemm(MODE_WGRAD, c.bf, p, veca, vecb, bm, bn, 1, c.s);
+    return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
   }
   p.out = c.ws.splitk;
   p.split_stride = mn;
-  HS_TRY(launch_igemm(MODE_WGRAD, c.bf, p, veca, vecb, bm, bn, splits, c.s));
+  HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, layer_flops(L, c.n)));
   return launch_splitk_reduce(c.ws.splitk, splits, mn, mn, dst, c.s);
 }
 

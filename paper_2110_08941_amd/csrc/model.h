@@ -75,6 +75,11 @@ struct Workspace {
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
   int64_t* gaps = nullptr;     // device copy of the padding ranges
+  // timing probe of one GEMM instantiation (mode, tile); see hs_probe_enable
+  int probe_mode = -1, probe_bm = 0, probe_bn = 0;
+  std::vector<hipEvent_t> probe_ev;   // 2 per launch
+  std::vector<double> probe_flops;
+  size_t probe_used = 0;
 };
 
 int64_t plan_workspace(const Model& m, int max_n, Workspace* ws);  // ws->arena set => bind

@@ -113,6 +113,8 @@ class Trainer:
         """Report the pending steps' times to the partitioner, in step order."""
         for t, n, events in self.pending:
             if self.clock == "measured":
+                for _, e1 in events:
+                    e1.synchronize()
                 tau = [float(e0.elapsed_time(e1)) for e0, e1 in events]
             else:
                 tau = [float(v) for v in n]

@@ -66,6 +66,8 @@ def _load():
         "hs_partitioner_observe": (I32, [P, PD, PD, PI32, PD]),
         "hs_layer_gemm": (I32, [I32, I32, I32, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, I32,
                                 I32, P, I64, P]),
+        "hs_probe_enable": (I32, [P, I32, I32, I32, I32]),
+        "hs_probe_read": (I32, [P, PD, PI64, PD]),
         "hs_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():
@@ -90,7 +92,7 @@ EXPORTED = (
     "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
     "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
-    "hs_layer_gemm", "hs_last_error")
+    "hs_layer_gemm", "hs_probe_enable", "hs_probe_read", "hs_last_error")
 
 
 def lib():
@@ -194,6 +196,17 @@ def wavg_sgd(g, n, theta, mom, P, lr, mu, wd, theta_bf16=0, stream=0):
 
 def params_to_bf16(theta, theta_bf16, P, stream=0):
     _check(_lib.hs_params_to_bf16(theta, theta_bf16, int(P), stream or None))
+
+
+def probe_enable(ws, mode, bm, bn, capacity=4096):
+    _check(_lib.hs_probe_enable(ws, int(mode), int(bm), int(bn), int(capacity)))
+
+
+def probe_read(ws):
+    """(total_ms, launches, flops) of the probed launches since the last read."""
+    t, n, f = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
+    _check(_lib.hs_probe_read(ws, ctypes.byref(t), ctypes.byref(n), ctypes.byref(f)))
+    return t.value, n.value, f.value
 
 
 def layer_gemm(mode, dtype, n, H, W, C, K, R, stride, pad, a, b, out, bias=0, relu=False,
