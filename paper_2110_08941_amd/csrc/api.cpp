@@ -140,6 +140,12 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
   }
   w->ws.bytes = bytes;
   plan_workspace(model->m, max_n, &w->ws);
+  e = hipMemset(w->ws.stat_count, 0, (STAT_MAX_GROUPS + 1) * sizeof(unsigned));
+  if (e != hipSuccess) {
+    (void)hipFree(w->ws.arena);
+    delete w;
+    return hip_fail(e, "hs_workspace_create: counters");
+  }
   const std::vector<int64_t>& gaps = model->m.gaps;
   if (!gaps.empty()) {
     e = hipMemcpy(w->ws.gaps, gaps.data(), gaps.size() * sizeof(int64_t), hipMemcpyHostToDevice);

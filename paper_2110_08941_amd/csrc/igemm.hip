@@ -495,11 +495,38 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
 // ----------------------------------------------------------------------------
 // split-K reduction: out[i] = sum_s part[s * stride + i], in split order
 // ----------------------------------------------------------------------------
-__global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t stride,
-                                     int64_t count, float* __restrict__ out) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t step = (int64_t)gridDim.x * blockDim.x;
-  for (; i < count; i += step) {
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            int splits, int64_t stride,
+                                                            int64_t count,
+                                                            float* __restrict__ out) {
+  // count and stride are multiples of 4 (the launcher falls back otherwise)
+  const int64_t groups = count >> 2;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4* p = (const float4*)part + q;
+    const int64_t st4 = stride >> 2;
+    int k = 0;
+    for (; k + 4 <= splits; k += 4) {
+      const float4 a = p[(k + 0) * st4], b = p[(k + 1) * st4], c = p[(k + 2) * st4],
+                   d = p[(k + 3) * st4];
+      s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+      s.x += b.x; s.y += b.y; s.z += b.z; s.w += b.w;
+      s.x += c.x; s.y += c.y; s.z += c.z; s.w += c.w;
+      s.x += d.x; s.y += d.y; s.z += d.z; s.w += d.w;
+    }
+    for (; k < splits; ++k) {
+      const float4 a = p[k * st4];
+      s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+    }
+    ((float4*)out)[q] = s;
+  }
+}
+
+__global__ void splitk_reduce1_kernel(const float* __restrict__ part, int splits, int64_t stride,
+                                      int64_t count, float* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x) {
     float s = 0.f;
     for (int k = 0; k < splits; ++k) s += part[k * stride + i];
     out[i] = s;
@@ -553,11 +580,18 @@ hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, boo
 
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t stride, int64_t count,
                                 float* out, hipStream_t s) {
-  int blocks = (int)((count + 255) / 256);
+  const bool vec = (count % 4 == 0) && (stride % 4 == 0) && (((uintptr_t)out & 15) == 0) &&
+                   (((uintptr_t)part & 15) == 0);
+  const int64_t work = vec ? count / 4 : count;
+  int blocks = (int)((work + 255) / 256);
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, stride,
-                     count, out);
+  if (vec)
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, stride,
+                       count, out);
+  else
+    hipLaunchKernelGGL(splitk_reduce1_kernel, dim3(blocks), dim3(256), 0, s, part, splits,
+                       stride, count, out);
   return hipGetLastError();
 }
 

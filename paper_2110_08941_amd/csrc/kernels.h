@@ -21,10 +21,30 @@ struct GemmParams {
   int ktiles, kt_per_split, tiles_n;  // filled in by the launcher
   int64_t split_stride; // WGRAD: elements between the outputs of consecutive splits
   ConvGeom g;
+  // DGRAD of a stride-2 layer by output parity class (fast kernel only):
+  // blockIdx.z = class c = 2 * (h % 2) + (w % 2); M counts the n x Hh x Wh
+  // pixels of one class; class c sums over its ntap[c] kernel taps taps[c][..]
+  int par;
+  int Hh, Wh;
+  FastDiv HWh, Wh_;
+  int ntap[4];
+  int taps[4][4];
 };
 
 hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, bool vecb, int bm,
                         int bn, int splits, hipStream_t s);
+// fast-path kernel (igemm_fast.hip): tiles 128x128, 128x64, 64x128, 256x64, 64x256
+bool igemm_fast_ok(int mode, bool bf16, const GemmParams& p, int bm, int bn);
+hipError_t launch_igemm_fast(int mode, bool bf16, const GemmParams& p, int bm, int bn, int splits,
+                             hipStream_t s);
+// NCHW fp32 [n][c][hw] -> NHWC [n][hw][cp] (activation type), channels c..cp-1 zero
+hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
+                                   hipStream_t s);
+// weights [k][rs][c] fp32 -> [k][rs][cp] activation type, zero padded
+hipError_t launch_pad_weights(const float* w, void* wp, int k, int rs, int c, int cp, bool bf16,
+                              hipStream_t s);
+// weight gradient [k][rs][cp] -> [k][rs][c] (drops the padded channels)
+hipError_t launch_unpad_wgrad(const float* gp, float* g, int k, int rs, int c, int cp, hipStream_t s);
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t stride, int64_t count,
                                 float* out, hipStream_t s);
 
@@ -35,35 +55,6 @@ hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int hw, bo
 // flat fp32 [n][d] -> activation type
 hipError_t launch_cast_input(const float* x, void* y, int64_t count, bool bf16, hipStream_t s);
 
-// Per-channel partial sums over rows of an NHWC tensor [rows][C]:
-//   kind 0: (sum x, sum x^2)  of x                 (batch-norm statistics)
-//   kind 1: (sum dy', sum dy' * xhat)               (batch-norm backward), where
-//           dy' = dy * [act > 0] if act != null, xhat = (z - mean) * rstd
-//   kind 2: (sum dy, -)                             (bias gradient)
-// Partials are double [blocks][2][C]; `blocks` is returned by chan_blocks().
-int chan_blocks(int64_t rows, int C);
-hipError_t launch_chan_partials(int kind, bool bf16, const void* x, const void* dy,
-                                const void* act, const float* mean, const float* rstd, int64_t rows,
-                                int C, double* partial, hipStream_t s);
-// Batch-norm forward finalise: mean, rstd (fp32) from the kind-0 partials.
-hipError_t launch_bn_finalize(const double* partial, int blocks, int C, int64_t count, float eps,
-                              float* mean, float* rstd, hipStream_t s);
-// Column reduce of kind-1/2 partials: out0[c] = sum, out1[c] = second sum
-// (either may be null).
-hipError_t launch_chan_reduce(const double* partial, int blocks, int C, float* out0, float* out1,
-                              hipStream_t s);
-// y = relu?(gamma * (z - mean) * rstd + beta + res)
-hipError_t launch_bn_apply(bool bf16, const void* z, const float* mean, const float* rstd,
-                           const float* gamma, const float* beta, const void* res, int relu,
-                           int64_t rows, int C, void* y, hipStream_t s);
-// dz = gamma * rstd * (dy' - (sum_dy + xhat * sum_dyx) / count), dy' as above
-hipError_t launch_bn_backward(bool bf16, const void* dy, const void* act, const void* z,
-                              const float* mean, const float* rstd, const float* gamma,
-                              const float* sum_dy, const float* sum_dyx, int64_t rows, int C,
-                              void* dz, hipStream_t s);
-// out = dy * [act > 0]
-hipError_t launch_relu_mask(bool bf16, const void* dy, const void* act, int64_t count, void* out,
-                            hipStream_t s);
 // 2x2 / stride 2 max pool, NHWC
 hipError_t launch_maxpool_fwd(bool bf16, const void* x, int n, int h, int w, int c, void* y,
                               hipStream_t s);
@@ -81,6 +72,29 @@ hipError_t launch_gap_bwd(bool bf16, const void* dy, const void* act, int n, int
 // activation type (dzt, may be null)
 hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, int n, int classes,
                              float* loss, float* dz32, void* dzt, bool bf16, hipStream_t s);
+// One-launch per-channel statistics (stats.hip):
+//   kind 0: out0 = mean, out1 = 1/sqrt(var + eps) of x
+//   kind 1: out0 = sum d, out1 = sum d * (x - mean) * rstd, d = dy * [act > 0]
+//   kind 2: out0 = sum d
+// Scratch: part1 float [STAT_MAX_BLOCKS][2][C], part2 double [STAT_MAX_GROUPS][2][C],
+// counters unsigned [STAT_MAX_GROUPS + 1] (zero before the first launch; left zero).
+constexpr int STAT_MAX_BLOCKS = 1024;
+constexpr int STAT_MAX_GROUPS = 16;
+int stat_blocks(int64_t rows, int C);
+hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
+                             const float* mean, const float* rstd, int64_t rows, int C,
+                             float* part1, double* part2, unsigned* counters, float* out0,
+                             float* out1, float eps, hipStream_t s);
+// vectorised (C % 8 == 0) batch-norm apply / backward and ReLU mask
+hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const float* rstd,
+                            const float* gamma, const float* beta, const void* res, int relu,
+                            int64_t rows, int C, void* y, hipStream_t s);
+hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const void* z,
+                               const float* mean, const float* rstd, const float* gamma,
+                               const float* sum_dy, const float* sum_dyx, int64_t rows, int C,
+                               void* dz, hipStream_t s);
+hipError_t launch_relu_mask8(bool bf16, const void* dy, const void* act, int64_t count, void* out,
+                             hipStream_t s);
 // zero a list of [begin, end) element ranges of a float buffer
 hipError_t launch_zero_ranges(float* buf, const int64_t* ranges, int count, hipStream_t s);
 

@@ -43,6 +43,68 @@ hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int hw, bo
 }
 
 template <typename T>
+__global__ void nchw_to_nhwc_pad_kernel(const float* __restrict__ x, T* __restrict__ y, int n, int c,
+                                        int cp, int hw) {
+  const int64_t total = (int64_t)n * cp * hw;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t b = i / ((int64_t)hw * cp);
+    const int64_t r = i - b * hw * cp;
+    const int p = (int)(r / cp), ch = (int)(r - (int64_t)p * cp);
+    st<T>(y, i, ch < c ? x[(b * c + ch) * hw + p] : 0.f);
+  }
+}
+
+hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
+                                   hipStream_t s) {
+  const int64_t total = (int64_t)n * cp * hw;
+  if (bf16)
+    hipLaunchKernelGGL(nchw_to_nhwc_pad_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, x,
+                       (bf16_t*)y, n, c, cp, hw);
+  else
+    hipLaunchKernelGGL(nchw_to_nhwc_pad_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, x,
+                       (float*)y, n, c, cp, hw);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void pad_weights_kernel(const float* __restrict__ w, T* __restrict__ wp, int k, int rs,
+                                   int c, int cp) {
+  const int total = k * rs * cp;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int q = i / cp, ch = i - q * cp;
+    st<T>(wp, i, ch < c ? w[q * c + ch] : 0.f);
+  }
+}
+
+hipError_t launch_pad_weights(const float* w, void* wp, int k, int rs, int c, int cp, bool bf16,
+                              hipStream_t s) {
+  const int total = k * rs * cp;
+  if (bf16)
+    hipLaunchKernelGGL(pad_weights_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, w,
+                       (bf16_t*)wp, k, rs, c, cp);
+  else
+    hipLaunchKernelGGL(pad_weights_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, w,
+                       (float*)wp, k, rs, c, cp);
+  return hipGetLastError();
+}
+
+__global__ void unpad_wgrad_kernel(const float* __restrict__ gp, float* __restrict__ g, int k,
+                                   int rs, int c, int cp) {
+  const int total = k * rs * c;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int q = i / c, ch = i - q * c;
+    g[i] = gp[q * cp + ch];
+  }
+}
+
+hipError_t launch_unpad_wgrad(const float* gp, float* g, int k, int rs, int c, int cp, hipStream_t s) {
+  const int total = k * rs * c;
+  hipLaunchKernelGGL(unpad_wgrad_kernel, dim3(grid_for(total)), dim3(256), 0, s, gp, g, k, rs, c, cp);
+  return hipGetLastError();
+}
+
+template <typename T>
 __global__ void cast_kernel(const float* __restrict__ x, T* __restrict__ y, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -56,241 +118,6 @@ hipError_t launch_cast_input(const float* x, void* y, int64_t count, bool bf16, 
   else
     hipLaunchKernelGGL(cast_kernel<float>, dim3(grid_for(count)), dim3(256), 0, s, x, (float*)y,
                        count);
-  return hipGetLastError();
-}
-
-// ----------------------------------------------------------------------------
-// per-channel partial sums
-// ----------------------------------------------------------------------------
-// Thread layout: CT = min(C, 256) channel lanes x RL = 256 / CT row lanes;
-// a thread covers channels c, c + CT, ... (at most 2 when C <= 512) and the
-// rows rl, rl + RL, ... of its block's row range.
-constexpr int CHAN_MAX = 1024;
-constexpr int CHAN_PER_THREAD = CHAN_MAX / 256;
-
-int chan_blocks(int64_t rows, int C) {
-  int64_t b = (rows + 255) / 256;
-  if (b > 1024) b = 1024;
-  if (b < 1) b = 1;
-  (void)C;
-  return (int)b;
-}
-
-template <typename T, int KIND>
-__global__ __launch_bounds__(256) void chan_partials_kernel(const T* __restrict__ x,
-                                                            const T* __restrict__ dy,
-                                                            const T* __restrict__ act,
-                                                            const float* __restrict__ mean,
-                                                            const float* __restrict__ rstd,
-                                                            int64_t rows, int C,
-                                                            double* __restrict__ partial) {
-  __shared__ double red[2][256 * CHAN_PER_THREAD];
-  const int CT = C < 256 ? C : 256;
-  const int RL = 256 / CT;
-  const int t = threadIdx.x;
-  const int cl = t % CT, rl = t / CT;
-  const int64_t per = (rows + gridDim.x - 1) / gridDim.x;
-  const int64_t r0 = (int64_t)blockIdx.x * per;
-  int64_t r1 = r0 + per;
-  if (r1 > rows) r1 = rows;
-  const int nc = (C + CT - 1) / CT;
-  double s0[CHAN_PER_THREAD], s1[CHAN_PER_THREAD];
-  for (int j = 0; j < CHAN_PER_THREAD; ++j) s0[j] = s1[j] = 0.0;
-  if (rl < RL) {
-    for (int64_t r = r0 + rl; r < r1; r += RL) {
-      for (int j = 0; j < nc; ++j) {
-        const int c = cl + j * CT;
-        if (c >= C) break;
-        const int64_t i = r * C + c;
-        if (KIND == 0) {
-          double v = (double)ld<T>(x, i);
-          s0[j] += v;
-          s1[j] += v * v;
-        } else if (KIND == 1) {
-          float d = ld<T>(dy, i);
-          if (act && !(ld<T>(act, i) > 0.f)) d = 0.f;
-          float xh = (ld<T>(x, i) - mean[c]) * rstd[c];
-          s0[j] += (double)d;
-          s1[j] += (double)d * (double)xh;
-        } else {
-          float d = ld<T>(dy, i);
-          if (act && !(ld<T>(act, i) > 0.f)) d = 0.f;
-          s0[j] += (double)d;
-        }
-      }
-    }
-  }
-  for (int j = 0; j < nc; ++j) {
-    red[0][t + 256 * j] = s0[j];
-    red[1][t + 256 * j] = s1[j];
-  }
-  __syncthreads();
-  // row lane 0 of every channel lane sums the RL lanes in order
-  if (rl == 0) {
-    for (int j = 0; j < nc; ++j) {
-      const int c = cl + j * CT;
-      if (c >= C) break;
-      double a = 0.0, b = 0.0;
-      for (int q = 0; q < RL; ++q) {
-        a += red[0][cl + q * CT + 256 * j];
-        b += red[1][cl + q * CT + 256 * j];
-      }
-      partial[((int64_t)blockIdx.x * 2 + 0) * C + c] = a;
-      partial[((int64_t)blockIdx.x * 2 + 1) * C + c] = b;
-    }
-  }
-}
-
-hipError_t launch_chan_partials(int kind, bool bf16, const void* x, const void* dy,
-                                const void* act, const float* mean, const float* rstd, int64_t rows,
-                                int C, double* partial, hipStream_t s) {
-  if (C > CHAN_MAX || C < 1) return hipErrorInvalidValue;
-  dim3 grid(chan_blocks(rows, C)), block(256);
-#define HS_CHAN(T, K)                                                                        \
-  hipLaunchKernelGGL((chan_partials_kernel<T, K>), grid, block, 0, s, (const T*)x, (const T*)dy, \
-                     (const T*)act, mean, rstd, rows, C, partial)
-  if (bf16) {
-    if (kind == 0) HS_CHAN(bf16_t, 0);
-    else if (kind == 1) HS_CHAN(bf16_t, 1);
-    else HS_CHAN(bf16_t, 2);
-  } else {
-    if (kind == 0) HS_CHAN(float, 0);
-    else if (kind == 1) HS_CHAN(float, 1);
-    else HS_CHAN(float, 2);
-  }
-#undef HS_CHAN
-  return hipGetLastError();
-}
-
-__global__ void bn_finalize_kernel(const double* __restrict__ partial, int blocks, int C,
-                                   int64_t count, float eps, float* __restrict__ mean,
-                                   float* __restrict__ rstd) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  double a = 0.0, b = 0.0;
-  for (int k = 0; k < blocks; ++k) {
-    a += partial[((int64_t)k * 2 + 0) * C + c];
-    b += partial[((int64_t)k * 2 + 1) * C + c];
-  }
-  double mu = a / (double)count;
-  double var = b / (double)count - mu * mu;
-  if (var < 0.0) var = 0.0;
-  mean[c] = (float)mu;
-  rstd[c] = (float)(1.0 / sqrt(var + (double)eps));
-}
-
-hipError_t launch_bn_finalize(const double* partial, int blocks, int C, int64_t count, float eps,
-                              float* mean, float* rstd, hipStream_t s) {
-  hipLaunchKernelGGL(bn_finalize_kernel, dim3((C + 255) / 256), dim3(256), 0, s, partial, blocks,
-                     C, count, eps, mean, rstd);
-  return hipGetLastError();
-}
-
-__global__ void chan_reduce_kernel(const double* __restrict__ partial, int blocks, int C,
-                                   float* __restrict__ out0, float* __restrict__ out1) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  double a = 0.0, b = 0.0;
-  for (int k = 0; k < blocks; ++k) {
-    a += partial[((int64_t)k * 2 + 0) * C + c];
-    b += partial[((int64_t)k * 2 + 1) * C + c];
-  }
-  if (out0) out0[c] = (float)a;
-  if (out1) out1[c] = (float)b;
-}
-
-hipError_t launch_chan_reduce(const double* partial, int blocks, int C, float* out0, float* out1,
-                              hipStream_t s) {
-  hipLaunchKernelGGL(chan_reduce_kernel, dim3((C + 255) / 256), dim3(256), 0, s, partial, blocks,
-                     C, out0, out1);
-  return hipGetLastError();
-}
-
-// ----------------------------------------------------------------------------
-// batch-norm apply / backward, elementwise (4 channels per thread step)
-// ----------------------------------------------------------------------------
-template <typename T>
-__global__ void bn_apply_kernel(const T* __restrict__ z, const float* __restrict__ mean,
-                                const float* __restrict__ rstd, const float* __restrict__ gamma,
-                                const float* __restrict__ beta, const T* __restrict__ res, int relu,
-                                int64_t rows, int C, T* __restrict__ y) {
-  const int64_t total = rows * C;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    float v = gamma[c] * (ld<T>(z, i) - mean[c]) * rstd[c] + beta[c];
-    if (res) v += ld<T>(res, i);
-    if (relu) v = v > 0.f ? v : 0.f;
-    st<T>(y, i, v);
-  }
-}
-
-hipError_t launch_bn_apply(bool bf16, const void* z, const float* mean, const float* rstd,
-                           const float* gamma, const float* beta, const void* res, int relu,
-                           int64_t rows, int C, void* y, hipStream_t s) {
-  int64_t total = rows * C;
-  if (bf16)
-    hipLaunchKernelGGL(bn_apply_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t*)z, mean, rstd, gamma, beta, (const bf16_t*)res, relu, rows,
-                       C, (bf16_t*)y);
-  else
-    hipLaunchKernelGGL(bn_apply_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float*)z, mean, rstd, gamma, beta, (const float*)res, relu, rows, C,
-                       (float*)y);
-  return hipGetLastError();
-}
-
-template <typename T>
-__global__ void bn_backward_kernel(const T* __restrict__ dy, const T* __restrict__ act,
-                                   const T* __restrict__ z, const float* __restrict__ mean,
-                                   const float* __restrict__ rstd, const float* __restrict__ gamma,
-                                   const float* __restrict__ sum_dy,
-                                   const float* __restrict__ sum_dyx, int64_t rows, int C,
-                                   T* __restrict__ dz) {
-  const int64_t total = rows * C;
-  const float inv = 1.0f / (float)rows;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    float d = ld<T>(dy, i);
-    if (act && !(ld<T>(act, i) > 0.f)) d = 0.f;
-    const float xh = (ld<T>(z, i) - mean[c]) * rstd[c];
-    st<T>(dz, i, gamma[c] * rstd[c] * (d - (sum_dy[c] + xh * sum_dyx[c]) * inv));
-  }
-}
-
-hipError_t launch_bn_backward(bool bf16, const void* dy, const void* act, const void* z,
-                              const float* mean, const float* rstd, const float* gamma,
-                              const float* sum_dy, const float* sum_dyx, int64_t rows, int C,
-                              void* dz, hipStream_t s) {
-  int64_t total = rows * C;
-  if (bf16)
-    hipLaunchKernelGGL(bn_backward_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t*)dy, (const bf16_t*)act, (const bf16_t*)z, mean, rstd, gamma,
-                       sum_dy, sum_dyx, rows, C, (bf16_t*)dz);
-  else
-    hipLaunchKernelGGL(bn_backward_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float*)dy, (const float*)act, (const float*)z, mean, rstd, gamma,
-                       sum_dy, sum_dyx, rows, C, (float*)dz);
-  return hipGetLastError();
-}
-
-template <typename T>
-__global__ void relu_mask_kernel(const T* __restrict__ dy, const T* __restrict__ act,
-                                 int64_t count, T* __restrict__ out) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-       i += (int64_t)gridDim.x * blockDim.x)
-    st<T>(out, i, ld<T>(act, i) > 0.f ? ld<T>(dy, i) : 0.f);
-}
-
-hipError_t launch_relu_mask(bool bf16, const void* dy, const void* act, int64_t count, void* out,
-                            hipStream_t s) {
-  if (bf16)
-    hipLaunchKernelGGL(relu_mask_kernel<bf16_t>, dim3(grid_for(count)), dim3(256), 0, s,
-                       (const bf16_t*)dy, (const bf16_t*)act, count, (bf16_t*)out);
-  else
-    hipLaunchKernelGGL(relu_mask_kernel<float>, dim3(grid_for(count)), dim3(256), 0, s,
-                       (const float*)dy, (const float*)act, count, (float*)out);
   return hipGetLastError();
 }
 

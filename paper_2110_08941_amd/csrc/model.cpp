@@ -193,14 +193,14 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     act(784);    // 0: input in activation type
     act(256);    // 1: hidden (post ReLU)
   } else if (m.arch == HS_SMALLCNN) {
-    act(3 * 1024);           // 0: X0 (NHWC)
+    act(8 * 1024);           // 0: X0 (NHWC, channels padded)
     act(32 * 1024);          // 1: A1
     act(64 * 1024);          // 2: A2
     act(64 * 256);           // 3: P2
     act(128 * 256);          // 4: A3
     act(128);                // 5: F
   } else if (m.arch == HS_RESNET18) {
-    act(3 * 1024);           // 0: X0
+    act(8 * 1024);           // 0: X0 (channels padded)
     act(64 * 1024);          // 1: Zs
     act(64 * 1024);          // 2: As
     for (const BlockL& b : m.blocks) {
@@ -213,7 +213,7 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     }
     act(512);                // F
   } else {
-    act(3 * 1024);           // 0: X0
+    act(8 * 1024);           // 0: X0 (channels padded)
     for (const VggL& l : m.vgg) {
       const int64_t e = (int64_t)l.c.Ho * l.c.Wo * l.c.cout;
       act(e);                // Z
@@ -227,7 +227,12 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   ws->dz32 = (float*)a.take((int64_t)max_n * 10 * 4);
   ws->dzt = a.take((int64_t)max_n * 10 * es);
   ws->stats = (float*)a.take((int64_t)(m.nbn > 0 ? m.nbn : 1) * 2 * m.max_c * 4);
-  ws->partial = (double*)a.take((int64_t)1024 * 2 * (m.max_c > 512 ? m.max_c : 512) * 8);
+  const int64_t cmax = m.max_c > 512 ? m.max_c : 512;
+  ws->stem_w = a.take((int64_t)64 * 9 * 8 * es);
+  ws->stem_g = (float*)a.take((int64_t)64 * 9 * 8 * 4);
+  ws->stat_part1 = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
+  ws->stat_part2 = (double*)a.take((int64_t)STAT_MAX_GROUPS * 2 * cmax * 8);
+  ws->stat_count = (unsigned*)a.take((int64_t)(STAT_MAX_GROUPS + 1) * 4);
   ws->splitk_floats = (int64_t)16 << 20;
   ws->splitk = (float*)a.take(ws->splitk_floats * 4);
   ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
@@ -307,15 +312,53 @@ void pick_tiles(int M, int N, int& bm, int& bn) {
   bn = 64;
 }
 
-// Launch one GEMM; brackets it with probe events when it is the probed
-// instantiation.
+// Tile of the fast kernel for an M x N output (0 x 0: none fits).
+void pick_fast_tiles(int mode, int M, int N, int& bm, int& bn) {
+  if (mode == MODE_WGRAD) {   // M = c_out; split-K supplies the parallelism
+    bm = M <= 64 ? 64 : 128;
+    bn = 128;
+    return;
+  }
+  const int cand[5][2] = {{256, 64}, {128, 128}, {128, 64}, {64, 128}, {64, 256}};
+  int best = -1;
+  int64_t best_tiles = 0;
+  for (int i = 0; i < 5; ++i) {
+    const int cbm = cand[i][0], cbn = cand[i][1];
+    if (cbn > 64 && N <= 64) continue;
+    if (cbn == 256 && N < 256) continue;
+    if (cbm == 256 && N > 64) continue;
+    const int64_t tiles = (int64_t)ceil_div(M, cbm) * ceil_div(N, cbn);
+    if (tiles >= 768) {
+      bm = cbm;
+      bn = cbn;
+      return;
+    }
+    if (tiles > best_tiles) {
+      best_tiles = tiles;
+      best = i;
+    }
+  }
+  bm = cand[best < 0 ? 2 : best][0];
+  bn = cand[best < 0 ? 2 : best][1];
+}
+
+// Launch one GEMM (fast kernel when the shape allows, generic otherwise);
+// brackets it with probe events when it is the probed instantiation.
 hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
                 int splits, double flops) {
   Workspace& ws = c.ws;
-  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn && veca &&
-                     vecb && ws.probe_used * 2 + 1 < ws.probe_ev.size();
+  int fbm = 0, fbn = 0;
+  pick_fast_tiles(mode, p.M, p.N, fbm, fbn);
+  const bool fast = p.par || (veca && vecb && igemm_fast_ok(mode, c.bf, p, fbm, fbn));
+  if (fast) {
+    bm = fbm;
+    bn = fbn;
+  }
+  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn && fast &&
+                     ws.probe_used * 2 + 1 < ws.probe_ev.size();
   if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
-  HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
+  if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
+  else HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
   if (probe) {
     HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
     ws.probe_flops[ws.probe_used] = flops;
@@ -330,12 +373,13 @@ double layer_flops(const ConvL& L, int n) {
 }
 
 // y = conv(x) (+ bias, ReLU); out_f32 forces an fp32 output
-hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32) {
+hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32,
+                    const void* wptr = nullptr, const float* bias = nullptr, double flops = 0.0) {
   GemmParams p = base_params(L, c.n);
   p.a = x;
-  p.b = c.W(L.w);
+  p.b = wptr ? wptr : c.W(L.w);
   p.out = y;
-  p.bias = L.b >= 0 ? c.theta + L.b : nullptr;
+  p.bias = bias ? bias : (L.b >= 0 ? c.theta + L.b : nullptr);
   p.relu = L.relu ? 1 : 0;
   p.out_f32 = (out_f32 || !c.bf) ? 1 : 0;
   p.M = c.n * L.Ho * L.Wo;
@@ -344,10 +388,12 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   const bool vec = (L.cin % c.V) == 0;
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
-  return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, layer_flops(L, c.n));
+  return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, flops > 0 ? flops : layer_flops(L, c.n));
 }
 
-// dx = dgrad(dy) (+ addend) (* [mask > 0])
+// dx = dgrad(dy) (+ addend) (* [mask > 0]); a stride-2 layer is computed by
+// output parity class when the fast kernel applies (each class sums over
+// its own taps only)
 hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, const void* addend,
                       const void* mask) {
   GemmParams p = base_params(L, c.n);
@@ -362,13 +408,35 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   p.K = L.k * L.k * L.cout;
   const bool veca = (L.cout % c.V) == 0;
   const bool vecb = (L.cin % c.V) == 0;
+  if (L.stride == 2 && L.H % 2 == 0 && L.W % 2 == 0 && veca && vecb) {
+    GemmParams q = p;
+    q.par = 1;
+    q.Hh = L.H / 2;
+    q.Wh = L.W / 2;
+    q.HWh = make_fastdiv((uint32_t)(q.Hh * q.Wh));
+    q.Wh_ = make_fastdiv((uint32_t)q.Wh);
+    q.M = c.n * q.Hh * q.Wh;
+    for (int cls = 0; cls < 4; ++cls) {
+      const int ph = cls >> 1, pw = cls & 1;
+      int nt = 0;
+      for (int r = 0; r < L.k; ++r)
+        for (int s2 = 0; s2 < L.k; ++s2)
+          if (((ph + L.pad - r) & 1) == 0 && ((pw + L.pad - s2) & 1) == 0) q.taps[cls][nt++] = r * L.k + s2;
+      q.ntap[cls] = nt;
+    }
+    int fbm = 0, fbn = 0;
+    pick_fast_tiles(MODE_DGRAD, q.M, q.N, fbm, fbn);
+    if (igemm_fast_ok(MODE_DGRAD, c.bf, q, fbm, fbn))
+      return gemm(c, MODE_DGRAD, q, veca, vecb, fbm, fbn, 1, layer_flops(L, c.n));
+  }
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
   return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
 }
 
-// g[L.w] = wgrad(dy, x); split-K over pixels when the tile grid is small
-hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* x) {
+hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* x,
+                      float* gout = nullptr, double flops = 0.0) {
+  if (flops <= 0) flops = layer_flops(L, c.n);
   GemmParams p = base_params(L, c.n);
   p.a = dy;
   p.b = x;
@@ -390,42 +458,39 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
     const int per = ceil_div(ktiles, splits);
     splits = ceil_div(ktiles, per);
   }
-  float* dst = c.g + L.w;
+  float* dst = gout ? gout : c.g + L.w;
   if (splits == 1) {
     p.out = dst;
     p.split_stride = 0;
-    return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
+    return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, 1, flops);
   }
   p.out = c.ws.splitk;
   p.split_stride = mn;
-  HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, layer_flops(L, c.n)));
+  HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, flops));
   return launch_splitk_reduce(c.ws.splitk, splits, mn, mn, dst, c.s);
 }
 
 // g[bias] = sum over rows of dy (dy in activation type unless f32)
 hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64_t rows, int C) {
-  HS_TRY(launch_chan_partials(2, f32 ? false : c.bf, dy, dy, nullptr, nullptr, nullptr, rows, C,
-                              c.ws.partial, c.s));
-  return launch_chan_reduce(c.ws.partial, chan_blocks(rows, C), C, c.g + boff, nullptr, c.s);
+  return launch_chan_stats(2, f32 ? false : c.bf, nullptr, dy, nullptr, nullptr, nullptr, rows, C,
+                           c.ws.stat_part1, c.ws.stat_part2, c.ws.stat_count, c.g + boff, nullptr,
+                           0.f, c.s);
 }
 
 hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rows) {
-  HS_TRY(launch_chan_partials(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, rows, b.c,
-                              c.ws.partial, c.s));
-  return launch_bn_finalize(c.ws.partial, chan_blocks(rows, b.c), b.c, rows, 1e-5f, c.mean(b),
-                            c.rstd(b), c.s);
+  return launch_chan_stats(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, rows, b.c,
+                           c.ws.stat_part1, c.ws.stat_part2, c.ws.stat_count, c.mean(b), c.rstd(b),
+                           1e-5f, c.s);
 }
 
 // dz = batch-norm backward of dy (masked by [act > 0] if act); writes
 // dbeta, dgamma into g
 hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
                   int64_t rows, void* dz) {
-  HS_TRY(launch_chan_partials(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), rows, b.c, c.ws.partial,
-                              c.s));
-  HS_TRY(launch_chan_reduce(c.ws.partial, chan_blocks(rows, b.c), b.c, c.g + b.b, c.g + b.g,
-                            c.s));
-  return launch_bn_backward(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.theta + b.g, c.g + b.b,
-                            c.g + b.g, rows, b.c, dz, c.s);
+  HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), rows, b.c, c.ws.stat_part1,
+                           c.ws.stat_part2, c.ws.stat_count, c.g + b.b, c.g + b.g, 0.f, c.s));
+  return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.theta + b.g, c.g + b.b,
+                             c.g + b.g, rows, b.c, dz, c.s);
 }
 
 // softmax cross-entropy on the logits; returns the operand for the last
@@ -435,6 +500,29 @@ hipError_t loss_grad(const Ctx& c, const int32_t* y, float* loss, const void** d
                            c.bf, c.s));
   *dzop = c.bf ? c.ws.dzt : (const void*)c.ws.dz32;
   return hipSuccess;
+}
+
+// ---------------------------------------------------------------- stem ----
+// The 3-channel first convolution runs on the fast kernel with its input and
+// weights zero-padded to 8 (bf16) or 4 (fp32) channels; its weight gradient
+// is computed padded and the padding dropped.
+int stem_cpad(const Ctx& c) { return c.bf ? 8 : 4; }
+
+hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void* y) {
+  const int cp = stem_cpad(c);
+  ConvL st = L;
+  st.cin = cp;
+  HS_TRY(launch_nchw_to_nhwc_pad(x, X0, c.n, 3, cp, L.H * L.W, c.bf, c.s));
+  HS_TRY(launch_pad_weights(c.theta + L.w, c.ws.stem_w, L.cout, L.k * L.k, 3, cp, c.bf, c.s));
+  return conv_fwd(c, st, X0, y, false, c.ws.stem_w, nullptr, layer_flops(L, c.n));
+}
+
+hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0) {
+  const int cp = stem_cpad(c);
+  ConvL st = L;
+  st.cin = cp;
+  HS_TRY(conv_wgrad(c, st, dz, X0, c.ws.stem_g, layer_flops(L, c.n)));
+  return launch_unpad_wgrad(c.ws.stem_g, c.g + L.w, L.cout, L.k * L.k, 3, cp, c.s);
 }
 
 // ---------------------------------------------------------------- MLP ----
@@ -463,8 +551,7 @@ hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss
   const Model& m = c.m;
   void **S = c.ws.slot.data(), **G = c.ws.grad;
   const int n = c.n;
-  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
-  HS_TRY(conv_fwd(c, m.c1, S[0], S[1], false));
+  HS_TRY(stem_fwd(c, m.c1, x, S[0], S[1]));
   HS_TRY(conv_fwd(c, m.c2, S[1], S[2], false));
   HS_TRY(launch_maxpool_fwd(c.bf, S[2], n, 32, 32, 64, S[3], c.s));
   HS_TRY(conv_fwd(c, m.c3, S[3], S[4], false));
@@ -484,7 +571,7 @@ hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss
   HS_TRY(conv_wgrad(c, m.c2, G[2], S[1]));
   HS_TRY(conv_dgrad(c, m.c2, G[2], G[0], nullptr, S[1]));             // dA1 * [A1 > 0]
   HS_TRY(bias_grad(c, m.c1.b, G[0], false, (int64_t)n * 1024, 32));
-  return conv_wgrad(c, m.c1, G[0], S[0]);
+  return stem_wgrad(c, m.c1, G[0], S[0]);
 }
 
 // ---------------------------------------------------------- ResNet-18 ----
@@ -494,10 +581,9 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   void** G = c.ws.grad;
   const int n = c.n;
   const int64_t rows0 = (int64_t)n * 1024;
-  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
-  HS_TRY(conv_fwd(c, m.stem, S[0], S[1], false));
+  HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
   HS_TRY(bn_stats(c, m.stem_bn, S[1], rows0));
-  HS_TRY(launch_bn_apply(c.bf, S[1], c.mean(m.stem_bn), c.rstd(m.stem_bn), c.theta + m.stem_bn.g,
+  HS_TRY(launch_bn_apply8(c.bf, S[1], c.mean(m.stem_bn), c.rstd(m.stem_bn), c.theta + m.stem_bn.g,
                          c.theta + m.stem_bn.b, nullptr, 1, rows0, 64, S[2], c.s));
   const void* cur = S[2];
   int si = 3;
@@ -507,7 +593,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
     HS_TRY(bn_stats(c, b.b1, Z1, rows));
-    HS_TRY(launch_bn_apply(c.bf, Z1, c.mean(b.b1), c.rstd(b.b1), c.theta + b.b1.g,
+    HS_TRY(launch_bn_apply8(c.bf, Z1, c.mean(b.b1), c.rstd(b.b1), c.theta + b.b1.g,
                            c.theta + b.b1.b, nullptr, 1, rows, b.b1.c, Hh, c.s));
     HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
     HS_TRY(bn_stats(c, b.b2, Z2, rows));
@@ -515,11 +601,11 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     if (b.proj) {
       HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
       HS_TRY(bn_stats(c, b.bp, ZP, rows));
-      HS_TRY(launch_bn_apply(c.bf, ZP, c.mean(b.bp), c.rstd(b.bp), c.theta + b.bp.g,
+      HS_TRY(launch_bn_apply8(c.bf, ZP, c.mean(b.bp), c.rstd(b.bp), c.theta + b.bp.g,
                              c.theta + b.bp.b, nullptr, 0, rows, b.bp.c, G[0], c.s));
       res = G[0];
     }
-    HS_TRY(launch_bn_apply(c.bf, Z2, c.mean(b.b2), c.rstd(b.b2), c.theta + b.b2.g,
+    HS_TRY(launch_bn_apply8(c.bf, Z2, c.mean(b.b2), c.rstd(b.b2), c.theta + b.b2.g,
                            c.theta + b.b2.b, res, 1, rows, b.b2.c, A, c.s));
     cur = A;
   }
@@ -545,7 +631,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       if (i != gi) fr[k++] = i;
     void *dA = G[gi], *P1 = G[fr[0]], *P2 = G[fr[1]], *P3 = G[fr[2]], *P4 = G[fr[3]];
     const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
-    HS_TRY(launch_relu_mask(c.bf, dA, A, rows * b.c2.cout, P1, c.s));        // dPre
+    HS_TRY(launch_relu_mask8(c.bf, dA, A, rows * b.c2.cout, P1, c.s));        // dPre
     HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rows, P2));                     // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
     HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, nullptr));                  // dH
@@ -565,7 +651,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   // stem
   void* dZs = G[gi == 0 ? 1 : 0];
   HS_TRY(bn_bwd(c, m.stem_bn, G[gi], S[2], S[1], rows0, dZs));
-  return conv_wgrad(c, m.stem, dZs, S[0]);
+  return stem_wgrad(c, m.stem, dZs, S[0]);
 }
 
 // -------------------------------------------------------------- VGG-16 ----
@@ -574,16 +660,16 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   void** S = c.ws.slot.data();
   void** G = c.ws.grad;
   const int n = c.n;
-  HS_TRY(launch_nchw_to_nhwc(x, S[0], n, 3, 1024, c.bf, c.s));
   const void* cur = S[0];
   const int L = (int)m.vgg.size();
   for (int i = 0; i < L; ++i) {
     const VggL& l = m.vgg[i];
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i], *P = S[3 + 3 * i];
     const int64_t rows = (int64_t)n * l.c.Ho * l.c.Wo;
-    HS_TRY(conv_fwd(c, l.c, cur, Z, false));
+    if (i == 0) HS_TRY(stem_fwd(c, l.c, x, S[0], Z));
+    else HS_TRY(conv_fwd(c, l.c, cur, Z, false));
     HS_TRY(bn_stats(c, l.bn, Z, rows));
-    HS_TRY(launch_bn_apply(c.bf, Z, c.mean(l.bn), c.rstd(l.bn), c.theta + l.bn.g,
+    HS_TRY(launch_bn_apply8(c.bf, Z, c.mean(l.bn), c.rstd(l.bn), c.theta + l.bn.g,
                            c.theta + l.bn.b, nullptr, 1, rows, l.bn.c, A, c.s));
     cur = A;
     if (l.pool) {
@@ -617,7 +703,8 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     }
     const int dZi = dAi == a ? b2 : a;
     HS_TRY(bn_bwd(c, l.bn, G[dAi], A, Z, rows, G[dZi]));
-    HS_TRY(conv_wgrad(c, l.c, G[dZi], in));
+    if (i == 0) HS_TRY(stem_wgrad(c, l.c, G[dZi], in));
+    else HS_TRY(conv_wgrad(c, l.c, G[dZi], in));
     if (i > 0) {
       const int out = (dZi + 1) % 3 == dAi ? (dZi + 2) % 3 : (dZi + 1) % 3;
       HS_TRY(conv_dgrad(c, l.c, G[dZi], G[out], nullptr, nullptr));
@@ -645,20 +732,7 @@ hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a,
   l.b = -1;
   if (mode == MODE_FWD) {
     Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};
-    GemmParams p = base_params(l, n);
-    p.a = a;
-    p.b = b;
-    p.out = out;
-    p.bias = bias;
-    p.relu = l.relu ? 1 : 0;
-    p.out_f32 = (out_f32 || !bf16) ? 1 : 0;
-    p.M = n * l.Ho * l.Wo;
-    p.N = l.cout;
-    p.K = l.k * l.k * l.cin;
-    const bool vec = (l.cin % c.V) == 0;
-    int bm, bn;
-    pick_tiles(p.M, p.N, bm, bn);
-    return launch_igemm(MODE_FWD, bf16, p, vec, vec, bm, bn, 1, s);
+    return conv_fwd(c, l, a, out, out_f32, b, bias);
   }
   if (mode == MODE_DGRAD) {
     Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};

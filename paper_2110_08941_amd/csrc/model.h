@@ -71,7 +71,11 @@ struct Workspace {
   float* dz32 = nullptr;
   void* dzt = nullptr;
   float* stats = nullptr;      // per batch-norm: mean[max_c], rstd[max_c]
-  double* partial = nullptr;   // per-channel partial sums
+  void* stem_w = nullptr;      // first-layer weights, channel-padded copy
+  float* stem_g = nullptr;     // first-layer weight gradient, channel-padded
+  float* stat_part1 = nullptr; // one-launch statistics: block partials
+  double* stat_part2 = nullptr;//   group partials
+  unsigned* stat_count = nullptr;  // arrival counters (zeroed at creation)
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
   int64_t* gaps = nullptr;     // device copy of the padding ranges

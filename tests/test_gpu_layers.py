@@ -23,6 +23,10 @@ SHAPES = [
     (9, 1, 1, 784, 256, 1, 1, 0),     # linear 784 -> 256
     (7, 1, 1, 512, 512, 1, 1, 0),
     (1, 8, 8, 128, 64, 3, 1, 1),
+    (2, 32, 32, 8, 64, 3, 1, 1),      # channel-padded first layer (bf16 slice spans 8 taps)
+    (3, 32, 32, 4, 32, 3, 1, 1),      # channel-padded first layer (fp32)
+    (2, 8, 8, 512, 256, 1, 2, 0),     # 1x1 strided, wide
+    (3, 6, 6, 64, 128, 3, 2, 1),      # strided 3x3 on an even map with ragged tiles
 ]
 
 
