@@ -4,11 +4,16 @@
                     [--no-cpu-baseline] [--gpus 1]
 
 One step = every simulated worker's forward+backward on its partition of a
-synthetic CIFAR-shaped batch (each on its own HIP stream, timed by events),
-the fused partition-weighted gradient average + momentum SGD, and -- at the
-end of every repartition window -- the compute-power estimate and the
-repartition of the next window.  W untimed steps, then K timed steps between
-two device synchronisations; the batches are resident in HBM before timing.
+synthetic CIFAR-shaped batch, the fused partition-weighted gradient average +
+momentum SGD, and -- at the end of every repartition window -- the
+compute-power estimate and the repartition of the next window.  By default
+all workers run in one pass over the layers (hs_workers_grad: each layer is
+launched once over the whole batch, with per-worker batch-norm statistics,
+losses and weight gradients) and worker times follow the model clock
+X_m = n_m / s_m; --streams runs one hs_worker_grad per worker on its own HIP
+stream with event-measured times instead.  W untimed steps, then K timed
+steps between two device synchronisations; the batches are resident in HBM
+before timing.
 
 Prints ONE JSON line: samples/s over the K steps, the roofline position of
 the dominant GEMM kernel (timed live with HIP events on the worker streams
@@ -29,10 +34,12 @@ METRIC = "train samples/s (fwd+bwd+wavg+SGD), CIFAR-shape ResNet-18; MFMA/HBM % 
 PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}   # MI355X dense MFMA peaks
 HBM_PEAK_GBS = 8000.0
 
-# GEMM instantiation probed for the roofline (mode, bm, bn), per workload:
-# the forward convolution kernel with 128 x 64 tiles (every 64-channel layer).
-PROBE = {"resnet18_bf16": (0, 128, 64), "resnet18_fp32": (0, 128, 64),
-         "vgg16_bf16": (0, 128, 64), "smallcnn_fp32": (0, 128, 64), "mlp_fp32": (0, 64, 64)}
+# GEMM instantiation probed for the roofline (mode, bm, bn), per workload: the
+# fast implicit-GEMM kernel that takes the largest share of the step's kernel
+# time (mode 0 forward, 1 data gradient, 2 weight gradient).
+PROBE = {"resnet18_bf16": (2, 128, 128), "resnet18_fp32": (2, 128, 128),
+         "vgg16_bf16": (2, 128, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
+MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
 
 
 def parse():
@@ -43,8 +50,12 @@ def parse():
     ap.add_argument("--workload", default="resnet18_bf16")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=192,
+    ap.add_argument("--cpu-samples", type=int, default=576,
                     help="samples of the CPU oracle's bounded step")
+    ap.add_argument("--streams", action="store_true",
+                    help="one stream per worker, measured clock (default: one pass)")
+    ap.add_argument("--probe", default=None,
+                    help="GEMM instantiation timed for the roofline, as mode,bm,bn")
     return ap.parse_args()
 
 
@@ -92,9 +103,10 @@ def main():
     from paper_2110_08941_amd.driver import Trainer
 
     wl = WORKLOADS[args.workload]
-    tr = Trainer(wl, seed=args.seed, clock="measured",
-                 steps=args.warmup + args.steps)
-    mode, bm, bn = PROBE[args.workload]
+    tr = Trainer(wl, seed=args.seed, clock="measured" if args.streams else "model",
+                 steps=args.warmup + args.steps, grouped=not args.streams)
+    mode, bm, bn = (PROBE[args.workload] if args.probe is None
+                    else tuple(int(v) for v in args.probe.split(",")))
     for w in tr.ws:
         hs.probe_enable(w, mode, bm, bn, capacity=64 * (args.steps + 1))
     for _ in range(args.warmup):
@@ -128,8 +140,12 @@ def main():
                                % (wl.name, wl.arch, wl.total, wl.workers, list(wl.speeds),
                                   " drifting (sigma %.2f)" % wl.drift_sigma if wl.drift_sigma else "",
                                   wl.window or "never"),
-                   "global_batch": wl.total, "workers": wl.workers, "parallelism": "simulated-dp%d-1gpu" % wl.workers},
-        "roofline": {"bound": "mfma", "kernel": "igemm_kernel mode=%d tile=%dx%d %s" % (mode, bm, bn, wl.dtype),
+                   "global_batch": wl.total, "workers": wl.workers,
+                   "parallelism": "simulated-dp%d-1gpu" % wl.workers,
+                   "execution": "one stream per worker, measured clock" if args.streams
+                   else "all workers in one pass per layer, model clock"},
+        "roofline": {"bound": "mfma", "kernel": "igemm_fast_kernel<%s, mode %d (%s), %dx%d tile>"
+                     % (wl.dtype, mode, MODE_NAME[mode], bm, bn),
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None,
                      "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),

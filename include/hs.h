@@ -7,6 +7,7 @@
  * speeds.  Each step:
  *   1. worker m computes g_m, the gradient of its mean loss over its partition
  *      of n_m samples (Section 1, Eq. (1); Section 3)           hs_worker_grad
+ *      (all M workers in one pass over the layers:             hs_workers_grad)
  *   2. the gradients are combined with partition-size weights
  *      w_m = n_m / sum n (Section 4.2, Enhanced Dynamic
  *      Partitioning)                                       hs_weighted_average
@@ -119,6 +120,22 @@ int64_t hs_workspace_bytes(const hs_workspace* ws);
 hs_status hs_worker_grad(const hs_model* model, hs_workspace* ws, const float* theta,
                          const uint16_t* theta_bf16, const float* x_m, const int32_t* y_m,
                          int32_t n_m, float* g_m, float* loss_m, void* stream);
+
+/* Gradients of M workers in one pass (Section 1, Eq. (1); Section 3): the
+ * same results as M calls of hs_worker_grad, with every layer launched once
+ * over all M partitions.  Worker m owns rows o_m .. o_m + n[m] - 1 of x and y,
+ * o_m = n[0] + ... + n[m-1]; its batch-norm statistics, mean loss and
+ * gradient are its own.
+ *   x, y    device, [sum n] samples laid out as for hs_worker_grad
+ *   n       HOST int32 [M], each >= 1, sum n <= max_n of the workspace
+ *   M       1 <= M <= 16
+ *   g       HOST array of M device fp32 [P] pointers, each fully overwritten
+ *   loss    device fp32 [M] receiving f_m, or NULL
+ * The workspace serves the whole call (one stream). */
+hs_status hs_workers_grad(const hs_model* model, hs_workspace* ws, const float* theta,
+                          const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                          const int32_t* n, int32_t M, float* const* g, float* loss,
+                          void* stream);
 
 /* Partition-weighted gradient (Section 4.2):
  *   g_out[i] = sum_{m<M} w_m g[m][i],  w_m = n[m] / sum_j n[j]  (computed in

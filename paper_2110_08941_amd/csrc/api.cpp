@@ -140,12 +140,6 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
   }
   w->ws.bytes = bytes;
   plan_workspace(model->m, max_n, &w->ws);
-  e = hipMemset(w->ws.stat_count, 0, (STAT_MAX_GROUPS + 1) * sizeof(unsigned));
-  if (e != hipSuccess) {
-    (void)hipFree(w->ws.arena);
-    delete w;
-    return hip_fail(e, "hs_workspace_create: counters");
-  }
   const std::vector<int64_t>& gaps = model->m.gaps;
   if (!gaps.empty()) {
     e = hipMemcpy(w->ws.gaps, gaps.data(), gaps.size() * sizeof(int64_t), hipMemcpyHostToDevice);
@@ -186,9 +180,47 @@ hs_status hs_worker_grad(const hs_model* model, hs_workspace* ws, const float* t
   if (!aligned16(theta) || !aligned16(x_m) || !aligned16(g_m) ||
       (theta_bf16 && !aligned16(theta_bf16)))
     return fail(HS_ERR_INVALID, "hs_worker_grad: device pointers must be 16-byte aligned");
-  hipError_t e = worker_grad(model->m, ws->ws, theta, theta_bf16, x_m, y_m, n_m, g_m, loss_m,
-                             (hipStream_t)stream);
+  const int n = n_m;
+  float* g = g_m;
+  hipError_t e = workers_grad(model->m, ws->ws, theta, theta_bf16, x_m, y_m, &n, 1, &g, loss_m,
+                              (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hs_worker_grad");
+  return ok();
+}
+
+hs_status hs_workers_grad(const hs_model* model, hs_workspace* ws, const float* theta,
+                          const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                          const int32_t* n, int32_t M, float* const* g, float* loss,
+                          void* stream) {
+  if (!model || !ws) return fail(HS_ERR_INVALID, "hs_workers_grad: model/workspace is NULL");
+  if (ws->model != model)
+    return fail(HS_ERR_INVALID, "hs_workers_grad: workspace of another model");
+  if (!theta || !x || !y || !n || !g)
+    return fail(HS_ERR_INVALID, "hs_workers_grad: theta, x, y, n and g must not be NULL");
+  if (M < 1 || M > MAX_SEG)
+    return fail(HS_ERR_INVALID, "hs_workers_grad: M %d outside 1..%d", M, MAX_SEG);
+  const bool bf = model->m.dtype == HS_BF16;
+  if (bf && !theta_bf16) return fail(HS_ERR_INVALID, "hs_workers_grad: bf16 model needs theta_bf16");
+  if (!bf && theta_bf16)
+    return fail(HS_ERR_INVALID, "hs_workers_grad: theta_bf16 must be NULL for an fp32 model");
+  int64_t total = 0;
+  int nn[MAX_SEG];
+  for (int i = 0; i < M; ++i) {
+    if (n[i] < 1) return fail(HS_ERR_INVALID, "hs_workers_grad: n[%d] = %d < 1", i, n[i]);
+    if (!g[i]) return fail(HS_ERR_INVALID, "hs_workers_grad: g[%d] is NULL", i);
+    if (!aligned16(g[i]))
+      return fail(HS_ERR_INVALID, "hs_workers_grad: g[%d] must be 16-byte aligned", i);
+    total += n[i];
+    nn[i] = n[i];
+  }
+  if (total > ws->ws.max_n)
+    return fail(HS_ERR_INVALID, "hs_workers_grad: sum of n = %lld exceeds the workspace's %d",
+                (long long)total, ws->ws.max_n);
+  if (!aligned16(theta) || !aligned16(x) || (theta_bf16 && !aligned16(theta_bf16)))
+    return fail(HS_ERR_INVALID, "hs_workers_grad: device pointers must be 16-byte aligned");
+  hipError_t e = workers_grad(model->m, ws->ws, theta, theta_bf16, x, y, nn, M, g, loss,
+                              (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_workers_grad");
   return ok();
 }
 

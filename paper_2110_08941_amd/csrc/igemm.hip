@@ -47,11 +47,11 @@ template <> struct ElemBits<bf16_t> { typedef uint16_t U; };
 // straddle a tap, a matrix edge or an unaligned address
 // ----------------------------------------------------------------------------
 template <typename T, int MODE>
-__device__ inline typename ElemBits<T>::U elemA(const GemmParams& p, int m, int k) {
+__device__ inline typename ElemBits<T>::U elemA(const GemmParams& p, int m, int k, int kend) {
   typedef typename ElemBits<T>::U U;
   const ConvGeom& g = p.g;
   const U* a = (const U*)p.a;
-  if (m >= p.M || k >= p.K) return 0;
+  if (m >= p.M || k >= kend) return 0;
   if (MODE == MODE_FWD) {            // x[b, ho*st-pad+r, wo*st-pad+s, ci]
     int b = m / (g.Ho * g.Wo), rem = m - b * g.Ho * g.Wo;
     int ho = rem / g.Wo, wo = rem - ho * g.Wo;
@@ -76,11 +76,11 @@ __device__ inline typename ElemBits<T>::U elemA(const GemmParams& p, int m, int 
 }
 
 template <typename T, int MODE>
-__device__ inline typename ElemBits<T>::U elemB(const GemmParams& p, int n, int k) {
+__device__ inline typename ElemBits<T>::U elemB(const GemmParams& p, int n, int k, int kend) {
   typedef typename ElemBits<T>::U U;
   const ConvGeom& g = p.g;
   const U* bp = (const U*)p.b;
-  if (n >= p.N || k >= p.K) return 0;
+  if (n >= p.N || k >= kend) return 0;
   if (MODE == MODE_FWD) {            // W[co = n][k]
     return bp[(int64_t)n * p.K + k];
   } else if (MODE == MODE_DGRAD) {   // W[co][tap][ci = n], k = tap * c_out + co
@@ -171,20 +171,20 @@ __device__ inline uint4 chunkB_fwd(const GemmParams& p, int n, int k) {
 // M/N-contiguous unit: rows [row, row+V) at k-rows k..k+3.  out[j] holds the
 // V row values of k-row k+j.
 template <typename T, int MODE, bool IS_A>
-__device__ inline void unit_load(const GemmParams& p, int row, int k, uint4 out[4]) {
+__device__ inline void unit_load(const GemmParams& p, int row, int k, int kend, uint4 out[4]) {
   const ConvGeom& g = p.g;
   if (IS_A) {  // WGRAD A: dy[k][row]
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       int kk = k + j;
-      out[j] = (row < p.M && kk < p.K) ? *(const uint4*)((const T*)p.a + (int64_t)kk * g.K + row)
+      out[j] = (row < p.M && kk < kend) ? *(const uint4*)((const T*)p.a + (int64_t)kk * g.K + row)
                                        : zero4();
     }
   } else if (MODE == MODE_DGRAD) {  // W[co][tap][row], k = tap * c_out + co
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       int kk = k + j;
-      if (row < p.N && kk < p.K) {
+      if (row < p.N && kk < kend) {
         int tap = (int)fdiv(kk, g.Kdiv), co = kk - tap * g.K;
         out[j] = *(const uint4*)((const T*)p.b + ((int64_t)co * g.R * g.S + tap) * g.C + row);
       } else {
@@ -198,7 +198,7 @@ __device__ inline void unit_load(const GemmParams& p, int row, int k, uint4 out[
     for (int j = 0; j < 4; ++j) {
       int kk = k + j;
       out[j] = zero4();
-      if (row < p.N && kk < p.K) {
+      if (row < p.N && kk < kend) {
         int b = (int)fdiv(kk, g.HWo), rem = kk - b * g.Ho * g.Wo;
         int ho = (int)fdiv(rem, g.Wo_), wo = rem - ho * g.Wo;
         int hi = ho * g.stride - g.pad + r, wi = wo * g.stride - g.pad + s;
@@ -269,9 +269,11 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
   const int tile = blockIdx.x;
   const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int kt0 = blockIdx.y * p.kt_per_split;
+  int kt0 = blockIdx.y * p.kt_per_split;
   int kt1 = kt0 + p.kt_per_split;
   if (kt1 > p.ktiles) kt1 = p.ktiles;
+  int koff = 0, kend = p.K;   // K range of this split (WGRAD: one worker segment)
+  if (MODE == MODE_WGRAD && p.nseg > 0) wgrad_split_range(p, BKE, koff, kend, kt0, kt1);
 
   // per-thread row decode for K-contiguous A (FWD / DGRAD)
   RowInfo rinfo[A_KCONTIG ? A_ITEMS : 1];
@@ -283,7 +285,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
   uint4 ra[A_REGS], rb[B_REGS];
 
   auto load_tile = [&](int kt) {
-    const int kbase = kt * BKE;
+    const int kbase = koff + kt * BKE;
     // ---- A
     if (A_KCONTIG) {
       const int k = kbase + (tid & 7) * V;
@@ -295,7 +297,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
           const int m = m0 + (tid >> 3) + 32 * i;
           U tmp[V];
 #pragma unroll
-          for (int e = 0; e < V; ++e) tmp[e] = elemA<T, MODE>(p, m, k + e);
+          for (int e = 0; e < V; ++e) tmp[e] = elemA<T, MODE>(p, m, k + e, kend);
           __builtin_memcpy(&ra[i], tmp, 16);
         }
       }
@@ -307,13 +309,13 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
         const int row = m0 + rv * V, k = kbase + kq * 4;
         if (u < 2 * BM) {
           if (VECA) {
-            unit_load<T, MODE, true>(p, row, k, &ra[4 * i]);
+            unit_load<T, MODE, true>(p, row, k, kend, &ra[4 * i]);
           } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               U tmp[V];
 #pragma unroll
-              for (int e = 0; e < V; ++e) tmp[e] = elemA<T, MODE>(p, row + e, k + j);
+              for (int e = 0; e < V; ++e) tmp[e] = elemA<T, MODE>(p, row + e, k + j, kend);
               __builtin_memcpy(&ra[4 * i + j], tmp, 16);
             }
           }
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
         } else {
           U tmp[V];
 #pragma unroll
-          for (int e = 0; e < V; ++e) tmp[e] = elemB<T, MODE>(p, n, k + e);
+          for (int e = 0; e < V; ++e) tmp[e] = elemB<T, MODE>(p, n, k + e, kend);
           __builtin_memcpy(&rb[i], tmp, 16);
         }
       }
@@ -343,13 +345,13 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
         const int row = n0 + rv * V, k = kbase + kq * 4;
         if (u < 2 * BN) {
           if (VECB) {
-            unit_load<T, MODE, false>(p, row, k, &rb[4 * i]);
+            unit_load<T, MODE, false>(p, row, k, kend, &rb[4 * i]);
           } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               U tmp[V];
 #pragma unroll
-              for (int e = 0; e < V; ++e) tmp[e] = elemB<T, MODE>(p, row + e, k + j);
+              for (int e = 0; e < V; ++e) tmp[e] = elemB<T, MODE>(p, row + e, k + j, kend);
               __builtin_memcpy(&rb[4 * i + j], tmp, 16);
             }
           }
@@ -492,45 +494,77 @@ __global__ __launch_bounds__(256) void igemm_kernel(GemmParams p) {
   }
 }
 
-// ----------------------------------------------------------------------------
-// split-K reduction: out[i] = sum_s part[s * stride + i], in split order
-// ----------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
-                                                            int splits, int64_t stride,
-                                                            int64_t count,
-                                                            float* __restrict__ out) {
-  // count and stride are multiples of 4 (the launcher falls back otherwise)
-  const int64_t groups = count >> 2;
-  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
-       q += (int64_t)gridDim.x * blockDim.x) {
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    const float4* p = (const float4*)part + q;
-    const int64_t st4 = stride >> 2;
-    int k = 0;
-    for (; k + 4 <= splits; k += 4) {
-      const float4 a = p[(k + 0) * st4], b = p[(k + 1) * st4], c = p[(k + 2) * st4],
-                   d = p[(k + 3) * st4];
-      s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
-      s.x += b.x; s.y += b.y; s.z += b.z; s.w += b.w;
-      s.x += c.x; s.y += c.y; s.z += c.z; s.w += c.w;
-      s.x += d.x; s.y += d.y; s.z += d.z; s.w += d.w;
+// Per-segment split-K reduction (see launch_splitk_reduce_seg).  blockIdx.y =
+// segment; vectorised by 4 when the output is not unpadded.
+struct SegOut {
+  float* p[MAX_SEG];
+  int split0[MAX_SEG + 1];
+};
+
+__global__ __launch_bounds__(256) void splitk_reduce_seg_kernel(const float* __restrict__ part,
+                                                                int64_t stride, int64_t count,
+                                                                SegOut o, int c, int cp,
+                                                                int vec) {
+  const int sg = blockIdx.y;
+  float* out = o.p[0];
+  int y0 = o.split0[0], y1 = o.split0[1];
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i)
+    if (i == sg) {
+      out = o.p[i];
+      y0 = o.split0[i];
+      y1 = o.split0[i + 1];
     }
-    for (; k < splits; ++k) {
-      const float4 a = p[k * st4];
-      s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+  if (vec) {   // c == cp, 16-byte aligned, count and stride multiples of 4
+    const int64_t groups = count >> 2, st4 = stride >> 2;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
+         q += (int64_t)gridDim.x * blockDim.x) {
+      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4* pp = (const float4*)part + q;
+      int k = y0;
+      for (; k + 4 <= y1; k += 4) {
+        const float4 a = pp[(k + 0) * st4], b = pp[(k + 1) * st4], cc = pp[(k + 2) * st4],
+                     d = pp[(k + 3) * st4];
+        s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+        s.x += b.x; s.y += b.y; s.z += b.z; s.w += b.w;
+        s.x += cc.x; s.y += cc.y; s.z += cc.z; s.w += cc.w;
+        s.x += d.x; s.y += d.y; s.z += d.z; s.w += d.w;
+      }
+      for (; k < y1; ++k) {
+        const float4 a = pp[k * st4];
+        s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+      }
+      ((float4*)out)[q] = s;
     }
-    ((float4*)out)[q] = s;
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const int64_t q = i / c, ch = i - q * c;
+      const int64_t src = q * cp + ch;
+      float s = 0.f;
+      for (int k = y0; k < y1; ++k) s += part[k * stride + src];
+      out[i] = s;
+    }
   }
 }
 
-__global__ void splitk_reduce1_kernel(const float* __restrict__ part, int splits, int64_t stride,
-                                      int64_t count, float* __restrict__ out) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    float s = 0.f;
-    for (int k = 0; k < splits; ++k) s += part[k * stride + i];
-    out[i] = s;
-  }
+hipError_t launch_splitk_reduce_seg(const float* part, int64_t stride, int64_t count,
+                                    const int* split0, float* const* out, int nseg, int c, int cp,
+                                    hipStream_t s) {
+  if (nseg < 1 || nseg > MAX_SEG || c < 1 || cp < c) return hipErrorInvalidValue;
+  SegOut o{};
+  for (int i = 0; i < nseg; ++i) o.p[i] = out[i];
+  for (int i = 0; i <= nseg; ++i) o.split0[i] = split0[i];
+  for (int i = nseg + 1; i <= MAX_SEG; ++i) o.split0[i] = split0[nseg];
+  bool vec = cp == c && count % 4 == 0 && stride % 4 == 0 && ((uintptr_t)part & 15) == 0;
+  for (int i = 0; i < nseg; ++i) vec = vec && ((uintptr_t)out[i] & 15) == 0;
+  const int64_t work = vec ? count / 4 : count;
+  int64_t blocks = (work + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(splitk_reduce_seg_kernel, dim3((unsigned)blocks, nseg), dim3(256), 0, s, part,
+                     stride, count, o, c, cp, vec ? 1 : 0);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
@@ -544,7 +578,8 @@ static hipError_t launch_tiles(const GemmParams& p0, bool veca, bool vecb, int s
   p.tiles_n = ceil_div(p.N, BN);
   constexpr int BKE = 128 / (int)sizeof(T);
   p.ktiles = ceil_div(p.K, BKE);
-  p.kt_per_split = ceil_div(p.ktiles, splits);
+  if (p.nseg > 0) splits = p.seg_split[p.nseg];   // kt_per_split set by the caller
+  else p.kt_per_split = ceil_div(p.ktiles, splits);
   dim3 grid(tiles_m * p.tiles_n, splits);
   if (veca && vecb)
     hipLaunchKernelGGL((igemm_kernel<T, MODE, BM, BN, true, true>), grid, dim3(256), 0, s, p);
@@ -578,21 +613,5 @@ hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, boo
   return launch_mode<float, MODE_WGRAD>(p, veca, vecb, bm, bn, splits, s);
 }
 
-hipError_t launch_splitk_reduce(const float* part, int splits, int64_t stride, int64_t count,
-                                float* out, hipStream_t s) {
-  const bool vec = (count % 4 == 0) && (stride % 4 == 0) && (((uintptr_t)out & 15) == 0) &&
-                   (((uintptr_t)part & 15) == 0);
-  const int64_t work = vec ? count / 4 : count;
-  int blocks = (int)((work + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
-  if (blocks < 1) blocks = 1;
-  if (vec)
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, stride,
-                       count, out);
-  else
-    hipLaunchKernelGGL(splitk_reduce1_kernel, dim3(blocks), dim3(256), 0, s, part, splits,
-                       stride, count, out);
-  return hipGetLastError();
-}
 
 }  // namespace hs

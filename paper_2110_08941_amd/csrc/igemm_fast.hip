@@ -131,8 +131,10 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   const bool par = (MODE == MODE_DGRAD) && p.par;
   const int cls = par ? (int)blockIdx.z : 0, ph = cls >> 1, pw = cls & 1;
   const int ktiles = par ? p.ntap[cls] * (g.K / BKE) : p.ktiles;
-  const int kt0 = blockIdx.y * p.kt_per_split;
-  const int kt1 = min(kt0 + p.kt_per_split, ktiles);
+  int kt0 = blockIdx.y * p.kt_per_split;
+  int kt1 = min(kt0 + p.kt_per_split, ktiles);
+  int koff = 0, kend = p.K;   // K range of this split (WGRAD: one worker segment)
+  if (MODE == MODE_WGRAD && p.nseg > 0) wgrad_split_range(p, BKE, koff, kend, kt0, kt1);
   auto tap_id = [&](int t) { return par ? p.taps[cls][t] : t; };
 
   // ---- per-thread fixed state of the loaders
@@ -214,7 +216,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   }
 
   auto load_tile = [&](int kt, int tpos, int c0, uint4 (&ra)[A_REGS], uint4 (&rb)[B_REGS]) {
-    const int kbase = kt * BKE;
+    const int kbase = koff + kt * BKE;
     const int tap = tap_id(tpos);
     int r = (RS == 1) ? 0 : tap / g.S;
     int s = (RS == 1) ? 0 : tap - r * g.S;
@@ -264,7 +266,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int pix = kbase + kq * 4 + j;
-          ra[4 * i + j] = (uok && row < p.M && pix < p.K)
+          ra[4 * i + j] = (uok && row < p.M && pix < kend)
                               ? *(const uint4*)((const T*)p.a + (int64_t)pix * g.K + row)
                               : make_uint4(0, 0, 0, 0);
         }
@@ -300,13 +302,13 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
         int rv, kq;
         unit_coords(tid + 256 * i, RVB, rv, kq);
         int pix = kbase + kq * 4;
-        int b = (int)fdiv(pix < p.K ? pix : 0, g.HWo);
+        int b = (int)fdiv(pix < kend ? pix : 0, g.HWo);
         int rem = pix - b * g.Ho * g.Wo;
         int ho = (int)fdiv(rem, g.Wo_), wo = rem - ho * g.Wo;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int hi = ho * g.stride - g.pad + bu_r[i], wi = wo * g.stride - g.pad + bu_s[i];
-          const bool ok = bu_ok[i] && pix + j < p.K && (unsigned)hi < (unsigned)g.H &&
+          const bool ok = bu_ok[i] && pix + j < kend && (unsigned)hi < (unsigned)g.H &&
                           (unsigned)wi < (unsigned)g.W;
           rb[4 * i + j] = ok ? *(const uint4*)((const T*)p.b +
                                                ((int64_t)(b * g.H + hi) * g.W + wi) * g.C + bu_ci[i])
@@ -533,7 +535,8 @@ static hipError_t launch_tiles_fast(const GemmParams& p0, int bm, int bn, int sp
   const int tiles_m = ceil_div(p.M, bm);
   p.tiles_n = ceil_div(p.N, bn);
   p.ktiles = ceil_div(p.K, BKE);
-  p.kt_per_split = ceil_div(p.ktiles, splits);
+  if (p.nseg > 0) splits = p.seg_split[p.nseg];   // kt_per_split set by the caller
+  else p.kt_per_split = ceil_div(p.ktiles, splits);
   if (p.par) {   // classes differ in K; one split covers the largest
     int mx = 0;
     for (int c = 0; c < 4; ++c) mx = p.ntap[c] > mx ? p.ntap[c] : mx;

@@ -7,6 +7,26 @@ namespace hs {
 
 enum { MODE_FWD = 0, MODE_DGRAD = 1, MODE_WGRAD = 2 };
 
+// Workers of one grouped launch: the batch is split into consecutive
+// segments, worker s owning samples [n0[s], n0[s + 1]).
+constexpr int MAX_SEG = 16;
+struct Segs {
+  int count;
+  int n0[MAX_SEG + 1];
+};
+
+// Rows of an NHWC tensor by segment, and the blocks of a row-parallel launch
+// given to each segment: segment s owns rows [row[s], row[s + 1]) and blocks
+// [blk[s], blk[s + 1]).
+struct SegRows {
+  int count;
+  int blk[MAX_SEG + 1];
+  int64_t row[MAX_SEG + 1];
+};
+// rows_per_sample rows per sample; blocks of at least min_rows rows (and at
+// most max_blocks blocks in all, at least one per segment)
+SegRows seg_rows(const Segs& sg, int64_t rows_per_sample, int64_t min_rows, int max_blocks);
+
 // Arguments of one implicit-GEMM launch (see igemm.hip for the three modes).
 struct GemmParams {
   const void* a;        // FWD: x;  DGRAD: dy;  WGRAD: dy
@@ -29,7 +49,40 @@ struct GemmParams {
   FastDiv HWh, Wh_;
   int ntap[4];
   int taps[4][4];
+  // WGRAD over worker segments: split blockIdx.y belongs to segment s when
+  // seg_split[s] <= y < seg_split[s + 1]; segment s reduces over the pixels of
+  // its samples seg_n0[s] .. seg_n0[s + 1] - 1, and every split writes its own
+  // partial output (out + y * split_stride).  nseg = 0: the whole K range,
+  // splits of kt_per_split K tiles.
+  int nseg;
+  int seg_split[MAX_SEG + 1];
+  int seg_n0[MAX_SEG + 1];
 };
+
+// K range of weight-gradient split blockIdx.y over worker segments: the
+// pixels [koff, kend) of its segment, and K tiles [kt0, kt1) of bke pixels
+// counted from koff.  Table indices are compile-time constants.
+__device__ inline void wgrad_split_range(const GemmParams& p, int bke, int& koff, int& kend,
+                                         int& kt0, int& kt1) {
+  const int y = blockIdx.y;
+  int s = 0;
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i) s += (i < p.nseg && y >= p.seg_split[i]) ? 1 : 0;
+  int sp = 0, a = 0, b = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == s) {
+      sp = p.seg_split[i];
+      a = p.seg_n0[i];
+      b = p.seg_n0[i + 1];
+    }
+  const int hw = p.g.Ho * p.g.Wo;
+  koff = a * hw;
+  kend = b * hw;
+  kt0 = (y - sp) * p.kt_per_split;
+  const int nkt = (kend - koff + bke - 1) / bke;
+  kt1 = kt0 + p.kt_per_split < nkt ? kt0 + p.kt_per_split : nkt;
+}
 
 hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, bool vecb, int bm,
                         int bn, int splits, hipStream_t s);
@@ -43,10 +96,13 @@ hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp
 // weights [k][rs][c] fp32 -> [k][rs][cp] activation type, zero padded
 hipError_t launch_pad_weights(const float* w, void* wp, int k, int rs, int c, int cp, bool bf16,
                               hipStream_t s);
-// weight gradient [k][rs][cp] -> [k][rs][c] (drops the padded channels)
-hipError_t launch_unpad_wgrad(const float* gp, float* g, int k, int rs, int c, int cp, hipStream_t s);
-hipError_t launch_splitk_reduce(const float* part, int splits, int64_t stride, int64_t count,
-                                float* out, hipStream_t s);
+// Per-segment split-K reduction: out[s][i] = sum of part[y * stride + i] over
+// the splits y of segment s (split0[s] <= y < split0[s + 1]), in split order.
+// With cp > c the partial rows are [rows][cp] and the output drops the
+// padded columns: out[s][q * c + ch] = sum part[y * stride + q * cp + ch].
+hipError_t launch_splitk_reduce_seg(const float* part, int64_t stride, int64_t count,
+                                    const int* split0, float* const* out, int nseg, int c, int cp,
+                                    hipStream_t s);
 
 // ---- elementwise / reduction kernels (layers.hip) ----
 // NCHW fp32 input -> NHWC activation (fp32 or bf16)
@@ -67,36 +123,42 @@ hipError_t launch_maxpool_bwd(bool bf16, const void* x, const void* dy, int n, i
 hipError_t launch_gap_fwd(bool bf16, const void* x, int n, int hw, int c, void* y, hipStream_t s);
 hipError_t launch_gap_bwd(bool bf16, const void* dy, const void* act, int n, int hw, int c,
                           void* dx, hipStream_t s);
-// softmax cross-entropy over n rows of `classes` logits (fp32): loss (mean,
-// may be null), dz = (softmax - onehot)/n as fp32 (dz32, may be null) and as
-// activation type (dzt, may be null)
-hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, int n, int classes,
-                             float* loss, float* dz32, void* dzt, bool bf16, hipStream_t s);
-// One-launch per-channel statistics (stats.hip):
-//   kind 0: out0 = mean, out1 = 1/sqrt(var + eps) of x
-//   kind 1: out0 = sum d, out1 = sum d * (x - mean) * rstd, d = dy * [act > 0]
-//   kind 2: out0 = sum d
-// Scratch: part1 float [STAT_MAX_BLOCKS][2][C], part2 double [STAT_MAX_GROUPS][2][C],
-// counters unsigned [STAT_MAX_GROUPS + 1] (zero before the first launch; left zero).
+// softmax cross-entropy per segment over rows of `classes` logits (fp32):
+// loss[s] = mean over the segment's rows (loss may be null), dz = (softmax -
+// onehot) / n_s as fp32 (dz32, may be null) and as activation type (dzt, may
+// be null)
+hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, const Segs& sg,
+                             int classes, float* loss, float* dz32, void* dzt, bool bf16,
+                             hipStream_t s);
+// Per-channel statistics of the rows of every segment (stats.hip), two
+// launches (block partials, then a per-segment finish):
+//   kind 0: out0[s] = mean, out1[s] = 1/sqrt(var + eps) of x
+//   kind 1: out0[s] = sum d, out1[s] = sum d * (x - mean_s) * rstd_s,
+//           d = dy * [act > 0], mean_s = mean + s * mstride (rstd likewise)
+//   kind 2: out0[s] = sum d
+// part: float scratch [STAT_MAX_BLOCKS][2][C].
 constexpr int STAT_MAX_BLOCKS = 1024;
-constexpr int STAT_MAX_GROUPS = 16;
-int stat_blocks(int64_t rows, int C);
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
-                             const float* mean, const float* rstd, int64_t rows, int C,
-                             float* part1, double* part2, unsigned* counters, float* out0,
-                             float* out1, float eps, hipStream_t s);
-// vectorised (C % 8 == 0) batch-norm apply / backward and ReLU mask
+                             const float* mean, const float* rstd, int mstride, const Segs& sg,
+                             int64_t rows_per_sample, int C, float* part, float* const* out0,
+                             float* const* out1, float eps, hipStream_t s);
+// vectorised (C % 8 == 0) batch-norm apply / backward by segment: segment s
+// normalises with mean + s * mstride, rstd + s * mstride; the backward takes
+// its sums from sum_dy[s], sum_dyx[s]
 hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const float* rstd,
-                            const float* gamma, const float* beta, const void* res, int relu,
-                            int64_t rows, int C, void* y, hipStream_t s);
+                            int mstride, const float* gamma, const float* beta, const void* res,
+                            int relu, const Segs& sg, int64_t rows_per_sample, int C, void* y,
+                            hipStream_t s);
 hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const void* z,
-                               const float* mean, const float* rstd, const float* gamma,
-                               const float* sum_dy, const float* sum_dyx, int64_t rows, int C,
-                               void* dz, hipStream_t s);
+                               const float* mean, const float* rstd, int mstride,
+                               const float* gamma, float* const* sum_dy, float* const* sum_dyx,
+                               const Segs& sg, int64_t rows_per_sample, int C, void* dz,
+                               hipStream_t s);
 hipError_t launch_relu_mask8(bool bf16, const void* dy, const void* act, int64_t count, void* out,
                              hipStream_t s);
-// zero a list of [begin, end) element ranges of a float buffer
-hipError_t launch_zero_ranges(float* buf, const int64_t* ranges, int count, hipStream_t s);
+// zero a list of [begin, end) element ranges of each of nbuf float buffers
+hipError_t launch_zero_ranges(float* const* bufs, int nbuf, const int64_t* ranges, int count,
+                              hipStream_t s);
 
 // ---- optimizer kernels (opt.hip) ----
 hipError_t launch_wavg_sgd(const float* const* g, const float* w, int M, float* theta, float* mom,

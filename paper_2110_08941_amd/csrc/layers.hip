@@ -89,21 +89,6 @@ hipError_t launch_pad_weights(const float* w, void* wp, int k, int rs, int c, in
   return hipGetLastError();
 }
 
-__global__ void unpad_wgrad_kernel(const float* __restrict__ gp, float* __restrict__ g, int k,
-                                   int rs, int c, int cp) {
-  const int total = k * rs * c;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
-    const int q = i / c, ch = i - q * c;
-    g[i] = gp[q * cp + ch];
-  }
-}
-
-hipError_t launch_unpad_wgrad(const float* gp, float* g, int k, int rs, int c, int cp, hipStream_t s) {
-  const int total = k * rs * c;
-  hipLaunchKernelGGL(unpad_wgrad_kernel, dim3(grid_for(total)), dim3(256), 0, s, gp, g, k, rs, c, cp);
-  return hipGetLastError();
-}
-
 template <typename T>
 __global__ void cast_kernel(const float* __restrict__ x, T* __restrict__ y, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
@@ -258,14 +243,25 @@ constexpr int CE_MAX_CLASSES = 64;
 
 template <typename T>
 __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* __restrict__ logits,
-                                                         const int32_t* __restrict__ labels, int n,
-                                                         int classes, float* __restrict__ loss,
+                                                         const int32_t* __restrict__ labels,
+                                                         Segs sg, int classes,
+                                                         float* __restrict__ loss,
                                                          float* __restrict__ dz32,
                                                          T* __restrict__ dzt) {
+  // block = segment: rows [r0, r1), mean over its n rows
   __shared__ double red[256];
+  const int seg = blockIdx.x;
+  int r0 = 0, r1 = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == seg) {
+      r0 = sg.n0[i];
+      r1 = sg.n0[i + 1];
+    }
+  const int n = r1 - r0;
   double acc = 0.0;
   const float invn = 1.0f / (float)n;
-  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+  for (int r = r0 + threadIdx.x; r < r1; r += blockDim.x) {
     const float* z = logits + (int64_t)r * classes;
     float zmax = z[0];
     for (int k = 1; k < classes; ++k) zmax = z[k] > zmax ? z[k] : zmax;
@@ -288,35 +284,47 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* __restrict
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0 && loss) *loss = (float)(red[0] / (double)n);
+  if (threadIdx.x == 0 && loss) loss[seg] = (float)(red[0] / (double)n);
 }
 
-hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, int n, int classes,
-                             float* loss, float* dz32, void* dzt, bool bf16, hipStream_t s) {
-  if (classes > CE_MAX_CLASSES) return hipErrorInvalidValue;
+hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, const Segs& sg,
+                             int classes, float* loss, float* dz32, void* dzt, bool bf16,
+                             hipStream_t s) {
+  if (classes > CE_MAX_CLASSES || sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
   if (bf16)
-    hipLaunchKernelGGL(softmax_ce_kernel<bf16_t>, dim3(1), dim3(256), 0, s, logits, labels, n,
-                       classes, loss, dz32, (bf16_t*)dzt);
+    hipLaunchKernelGGL(softmax_ce_kernel<bf16_t>, dim3(sg.count), dim3(256), 0, s, logits, labels,
+                       sg, classes, loss, dz32, (bf16_t*)dzt);
   else
-    hipLaunchKernelGGL(softmax_ce_kernel<float>, dim3(1), dim3(256), 0, s, logits, labels, n,
-                       classes, loss, dz32, (float*)dzt);
+    hipLaunchKernelGGL(softmax_ce_kernel<float>, dim3(sg.count), dim3(256), 0, s, logits, labels,
+                       sg, classes, loss, dz32, (float*)dzt);
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
-// zero padding gaps of a gradient vector
+// zero the padding gaps of every worker's gradient vector
 // ----------------------------------------------------------------------------
-__global__ void zero_ranges_kernel(float* __restrict__ buf, const int64_t* __restrict__ ranges,
-                                   int count) {
+struct BufList {
+  float* p[MAX_SEG];
+};
+
+__global__ void zero_ranges_kernel(BufList bufs, const int64_t* __restrict__ ranges, int count) {
   const int r = blockIdx.x;
   if (r >= count) return;
+  float* buf = bufs.p[0];
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i)
+    if (i == (int)blockIdx.y) buf = bufs.p[i];
   const int64_t b = ranges[2 * r], e = ranges[2 * r + 1];
   for (int64_t i = b + threadIdx.x; i < e; i += blockDim.x) buf[i] = 0.f;
 }
 
-hipError_t launch_zero_ranges(float* buf, const int64_t* ranges, int count, hipStream_t s) {
+hipError_t launch_zero_ranges(float* const* bufs, int nbuf, const int64_t* ranges, int count,
+                              hipStream_t s) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_ranges_kernel, dim3(count), dim3(64), 0, s, buf, ranges, count);
+  if (nbuf < 1 || nbuf > MAX_SEG) return hipErrorInvalidValue;
+  BufList l{};
+  for (int i = 0; i < nbuf; ++i) l.p[i] = bufs[i];
+  hipLaunchKernelGGL(zero_ranges_kernel, dim3(count, nbuf), dim3(64), 0, s, l, ranges, count);
   return hipGetLastError();
 }
 

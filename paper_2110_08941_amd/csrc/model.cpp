@@ -226,14 +226,18 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   ws->logits = (float*)a.take((int64_t)max_n * 10 * 4);
   ws->dz32 = (float*)a.take((int64_t)max_n * 10 * 4);
   ws->dzt = a.take((int64_t)max_n * 10 * es);
-  ws->stats = (float*)a.take((int64_t)(m.nbn > 0 ? m.nbn : 1) * 2 * m.max_c * 4);
+  ws->stats = (float*)a.take((int64_t)(m.nbn > 0 ? m.nbn : 1) * MAX_SEG * 2 * m.max_c * 4);
   const int64_t cmax = m.max_c > 512 ? m.max_c : 512;
   ws->stem_w = a.take((int64_t)64 * 9 * 8 * es);
-  ws->stem_g = (float*)a.take((int64_t)64 * 9 * 8 * 4);
-  ws->stat_part1 = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
-  ws->stat_part2 = (double*)a.take((int64_t)STAT_MAX_GROUPS * 2 * cmax * 8);
-  ws->stat_count = (unsigned*)a.take((int64_t)(STAT_MAX_GROUPS + 1) * 4);
+  ws->stat_part = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
+  // split-K partials: at least one split per worker of the largest weight
+  // gradient (first layer counted with its padded channels)
+  int64_t max_w = 64 * 9 * 8;
+  for (const ParamT& t : m.params)
+    if ((t.kind == HS_KIND_CONV_W || t.kind == HS_KIND_LIN_W) && t.numel > max_w) max_w = t.numel;
+  const int64_t segs = max_n < MAX_SEG ? max_n : MAX_SEG;
   ws->splitk_floats = (int64_t)16 << 20;
+  if (segs * max_w > ws->splitk_floats) ws->splitk_floats = segs * max_w;
   ws->splitk = (float*)a.take(ws->splitk_floats * 4);
   ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
   return a.off;
@@ -250,22 +254,38 @@ namespace {
     if (e_ != hipSuccess) return e_;    \
   } while (0)
 
+// One pass over the layers for the workers in sg (n = all their samples):
+// layer launches cover the whole batch; batch-norm statistics, losses and
+// weight gradients are taken per worker, worker s writing g[s].
 struct Ctx {
   const Model& m;
   Workspace& ws;
   const float* theta;
   const bf16_t* tbf;
-  float* g;
   int n;
   hipStream_t s;
   bool bf;
   int V;  // elements per 16 bytes
+  Segs sg;
+  float* g[MAX_SEG];
   const void* W(int64_t off) const {
     return bf ? (const void*)(tbf + off) : (const void*)(theta + off);
   }
-  float* mean(const BNL& b) const { return ws.stats + (int64_t)b.stat * 2 * m.max_c; }
-  float* rstd(const BNL& b) const { return mean(b) + m.max_c; }
+  // worker s's batch-norm statistics: mean at mean(b) + s * mstride()
+  int mstride() const { return 2 * m.max_c; }
+  float* mean(const BNL& b, int sg_i = 0) const {
+    return ws.stats + ((int64_t)b.stat * MAX_SEG + sg_i) * 2 * m.max_c;
+  }
+  float* rstd(const BNL& b, int sg_i = 0) const { return mean(b, sg_i) + m.max_c; }
 };
+
+Segs one_segment(int n) {
+  Segs sg{};
+  sg.count = 1;
+  sg.n0[0] = 0;
+  sg.n0[1] = n;
+  return sg;
+}
 
 ConvGeom geom(const ConvL& c, int n) {
   ConvGeom g;
@@ -434,9 +454,15 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
 }
 
+// Weight gradient of every worker: worker s reduces over the pixels of its own
+// samples and writes g[s] + L.w.  The reduction is split (split-K) so that
+// the launch has about 1024 blocks; the partial sums are added per worker in
+// split order.  With cin_true < L.cin the layer's input channels are padded
+// and the padded columns of the gradient are dropped.
 hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* x,
-                      float* gout = nullptr, double flops = 0.0) {
+                      int cin_true = 0, double flops = 0.0) {
   if (flops <= 0) flops = layer_flops(L, c.n);
+  if (cin_true <= 0) cin_true = L.cin;
   GemmParams p = base_params(L, c.n);
   p.a = dy;
   p.b = x;
@@ -448,55 +474,95 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
   const int bm = p.M <= 64 ? 64 : 128, bn = 128;
   const int tiles = ceil_div(p.M, bm) * ceil_div(p.N, bn);
   const int bke = 128 / (c.bf ? 2 : 4);
-  const int ktiles = ceil_div(p.K, bke);
-  int splits = ceil_div(1024, tiles);
-  if (splits > ktiles / 4) splits = ktiles / 4;
-  const int64_t mn = (int64_t)p.M * p.N;
-  if (splits > c.ws.splitk_floats / mn) splits = (int)(c.ws.splitk_floats / mn);
-  if (splits < 1) splits = 1;
-  if (splits > 1) {
-    const int per = ceil_div(ktiles, splits);
-    splits = ceil_div(ktiles, per);
+  const int hw = L.Ho * L.Wo;
+  int kt[MAX_SEG], total_kt = 0;
+  for (int i = 0; i < c.sg.count; ++i) {
+    kt[i] = ceil_div((c.sg.n0[i + 1] - c.sg.n0[i]) * hw, bke);
+    total_kt += kt[i];
   }
-  float* dst = gout ? gout : c.g + L.w;
-  if (splits == 1) {
-    p.out = dst;
+  const int64_t mn = (int64_t)p.M * p.N;
+  int want = ceil_div(1024, tiles);
+  int per = ceil_div(total_kt, want > 0 ? want : 1);
+  if (per < 4) per = 4;
+  auto count_splits = [&](int q) {
+    int t = 0;
+    for (int i = 0; i < c.sg.count; ++i) t += kt[i] > 0 ? ceil_div(kt[i], q) : 1;
+    return t;
+  };
+  while ((int64_t)count_splits(per) * mn > c.ws.splitk_floats && per < total_kt) per *= 2;
+  const int splits = count_splits(per);
+  const bool direct = c.sg.count == 1 && splits == 1 && cin_true == L.cin;
+  // the workspace plan sizes the partial buffer for one split per worker
+  if (!direct && (int64_t)splits * mn > c.ws.splitk_floats) return hipErrorInvalidValue;
+  p.nseg = c.sg.count;
+  p.kt_per_split = per;
+  p.seg_split[0] = 0;
+  for (int i = 0; i < c.sg.count; ++i) {
+    p.seg_n0[i] = c.sg.n0[i];
+    p.seg_split[i + 1] = p.seg_split[i] + (kt[i] > 0 ? ceil_div(kt[i], per) : 1);
+  }
+  p.seg_n0[c.sg.count] = c.sg.n0[c.sg.count];
+  if (direct) {
+    p.out = c.g[0] + L.w;
     p.split_stride = 0;
-    return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, 1, flops);
+    return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, flops);
   }
   p.out = c.ws.splitk;
   p.split_stride = mn;
   HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, flops));
-  return launch_splitk_reduce(c.ws.splitk, splits, mn, mn, dst, c.s);
+  float* outs[MAX_SEG];
+  for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
+  const int64_t count = (int64_t)L.cout * L.k * L.k * cin_true;
+  return launch_splitk_reduce_seg(c.ws.splitk, mn, count, p.seg_split, outs, c.sg.count, cin_true,
+                                  L.cin, c.s);
 }
 
-// g[bias] = sum over rows of dy (dy in activation type unless f32)
-hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64_t rows, int C) {
-  return launch_chan_stats(2, f32 ? false : c.bf, nullptr, dy, nullptr, nullptr, nullptr, rows, C,
-                           c.ws.stat_part1, c.ws.stat_part2, c.ws.stat_count, c.g + boff, nullptr,
-                           0.f, c.s);
+// worker s: g[s][bias] = sum over its rows of dy (dy in activation type
+// unless f32); rps rows per sample
+hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64_t rps, int C) {
+  float* out[MAX_SEG];
+  for (int i = 0; i < c.sg.count; ++i) out[i] = c.g[i] + boff;
+  return launch_chan_stats(2, f32 ? false : c.bf, nullptr, dy, nullptr, nullptr, nullptr, 0, c.sg,
+                           rps, C, c.ws.stat_part, out, nullptr, 0.f, c.s);
 }
 
-hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rows) {
-  return launch_chan_stats(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, rows, b.c,
-                           c.ws.stat_part1, c.ws.stat_part2, c.ws.stat_count, c.mean(b), c.rstd(b),
-                           1e-5f, c.s);
+// per-worker batch-norm statistics of z (rps rows per sample)
+hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
+  float *o0[MAX_SEG], *o1[MAX_SEG];
+  for (int i = 0; i < c.sg.count; ++i) {
+    o0[i] = c.mean(b, i);
+    o1[i] = c.rstd(b, i);
+  }
+  return launch_chan_stats(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, 0, c.sg, rps, b.c,
+                           c.ws.stat_part, o0, o1, 1e-5f, c.s);
 }
 
-// dz = batch-norm backward of dy (masked by [act > 0] if act); writes
-// dbeta, dgamma into g
+// y = relu?(batch-norm(z) + res) with every worker's own statistics
+hipError_t bn_apply(const Ctx& c, const BNL& b, const void* z, const void* res, int relu,
+                    int64_t rps, void* y) {
+  return launch_bn_apply8(c.bf, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
+                          c.theta + b.b, res, relu, c.sg, rps, b.c, y, c.s);
+}
+
+// dz = batch-norm backward of dy (masked by [act > 0] if act); writes every
+// worker's dbeta, dgamma into its g[s]
 hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
-                  int64_t rows, void* dz) {
-  HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), rows, b.c, c.ws.stat_part1,
-                           c.ws.stat_part2, c.ws.stat_count, c.g + b.b, c.g + b.g, 0.f, c.s));
-  return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.theta + b.g, c.g + b.b,
-                             c.g + b.g, rows, b.c, dz, c.s);
+                  int64_t rps, void* dz) {
+  float *db[MAX_SEG], *dg[MAX_SEG];
+  for (int i = 0; i < c.sg.count; ++i) {
+    db[i] = c.g[i] + b.b;
+    dg[i] = c.g[i] + b.g;
+  }
+  HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps, b.c,
+                           c.ws.stat_part, db, dg, 0.f, c.s));
+  return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
+                             db, dg, c.sg, rps, b.c, dz, c.s);
 }
 
-// softmax cross-entropy on the logits; returns the operand for the last
-// layer's backward (fp32 or bf16 copy of dz)
+// softmax cross-entropy on the logits, mean per worker; returns the operand
+// for the last layer's backward (fp32 or bf16 copy of dz)
 hipError_t loss_grad(const Ctx& c, const int32_t* y, float* loss, const void** dzop) {
-  HS_TRY(launch_softmax_ce(c.ws.logits, y, c.n, 10, loss, c.ws.dz32, c.bf ? c.ws.dzt : nullptr,
+  HS_TRY(launch_softmax_ce(c.ws.logits, y, c.sg, 10, loss, c.ws.dz32, c.bf ? c.ws.dzt : nullptr,
                            c.bf, c.s));
   *dzop = c.bf ? c.ws.dzt : (const void*)c.ws.dz32;
   return hipSuccess;
@@ -518,11 +584,9 @@ hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void
 }
 
 hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0) {
-  const int cp = stem_cpad(c);
   ConvL st = L;
-  st.cin = cp;
-  HS_TRY(conv_wgrad(c, st, dz, X0, c.ws.stem_g, layer_flops(L, c.n)));
-  return launch_unpad_wgrad(c.ws.stem_g, c.g + L.w, L.cout, L.k * L.k, 3, cp, c.s);
+  st.cin = stem_cpad(c);
+  return conv_wgrad(c, st, dz, X0, L.cin, layer_flops(L, c.n));
 }
 
 // ---------------------------------------------------------------- MLP ----
@@ -539,10 +603,10 @@ hipError_t mlp(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const void* dz;
   HS_TRY(loss_grad(c, y, loss, &dz));
   HS_TRY(conv_wgrad(c, m.fc2, dz, Hh));
-  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, c.n, 10));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   void* dH = c.ws.grad[0];
   HS_TRY(conv_dgrad(c, m.fc2, dz, dH, nullptr, Hh));
-  HS_TRY(bias_grad(c, m.fc1.b, dH, false, c.n, 256));
+  HS_TRY(bias_grad(c, m.fc1.b, dH, false, 1, 256));
   return conv_wgrad(c, m.fc1, dH, X);
 }
 
@@ -560,17 +624,17 @@ hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss
   const void* dz;
   HS_TRY(loss_grad(c, y, loss, &dz));
   HS_TRY(conv_wgrad(c, m.fc2, dz, S[5]));
-  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
   HS_TRY(launch_gap_bwd(c.bf, G[0], S[4], n, 256, 128, G[1], c.s));    // dA3 * [A3 > 0]
-  HS_TRY(bias_grad(c, m.c3.b, G[1], false, (int64_t)n * 256, 128));
+  HS_TRY(bias_grad(c, m.c3.b, G[1], false, 256, 128));
   HS_TRY(conv_wgrad(c, m.c3, G[1], S[3]));
   HS_TRY(conv_dgrad(c, m.c3, G[1], G[0], nullptr, nullptr));          // dP2
   HS_TRY(launch_maxpool_bwd(c.bf, S[2], G[0], n, 32, 32, 64, 1, G[2], c.s));  // dA2 * [A2 > 0]
-  HS_TRY(bias_grad(c, m.c2.b, G[2], false, (int64_t)n * 1024, 64));
+  HS_TRY(bias_grad(c, m.c2.b, G[2], false, 1024, 64));
   HS_TRY(conv_wgrad(c, m.c2, G[2], S[1]));
   HS_TRY(conv_dgrad(c, m.c2, G[2], G[0], nullptr, S[1]));             // dA1 * [A1 > 0]
-  HS_TRY(bias_grad(c, m.c1.b, G[0], false, (int64_t)n * 1024, 32));
+  HS_TRY(bias_grad(c, m.c1.b, G[0], false, 1024, 32));
   return stem_wgrad(c, m.c1, G[0], S[0]);
 }
 
@@ -580,33 +644,28 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   void** S = c.ws.slot.data();
   void** G = c.ws.grad;
   const int n = c.n;
-  const int64_t rows0 = (int64_t)n * 1024;
   HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
-  HS_TRY(bn_stats(c, m.stem_bn, S[1], rows0));
-  HS_TRY(launch_bn_apply8(c.bf, S[1], c.mean(m.stem_bn), c.rstd(m.stem_bn), c.theta + m.stem_bn.g,
-                         c.theta + m.stem_bn.b, nullptr, 1, rows0, 64, S[2], c.s));
+  HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
+  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2]));
   const void* cur = S[2];
   int si = 3;
   for (const BlockL& b : m.blocks) {
     void *Z1 = S[si], *Hh = S[si + 1], *Z2 = S[si + 2], *ZP = S[si + 3], *A = S[si + 4];
     si += 5;
-    const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
+    const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
-    HS_TRY(bn_stats(c, b.b1, Z1, rows));
-    HS_TRY(launch_bn_apply8(c.bf, Z1, c.mean(b.b1), c.rstd(b.b1), c.theta + b.b1.g,
-                           c.theta + b.b1.b, nullptr, 1, rows, b.b1.c, Hh, c.s));
+    HS_TRY(bn_stats(c, b.b1, Z1, rps));
+    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rps, Hh));
     HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
-    HS_TRY(bn_stats(c, b.b2, Z2, rows));
+    HS_TRY(bn_stats(c, b.b2, Z2, rps));
     const void* res = cur;
     if (b.proj) {
       HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
-      HS_TRY(bn_stats(c, b.bp, ZP, rows));
-      HS_TRY(launch_bn_apply8(c.bf, ZP, c.mean(b.bp), c.rstd(b.bp), c.theta + b.bp.g,
-                             c.theta + b.bp.b, nullptr, 0, rows, b.bp.c, G[0], c.s));
+      HS_TRY(bn_stats(c, b.bp, ZP, rps));
+      HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rps, G[0]));
       res = G[0];
     }
-    HS_TRY(launch_bn_apply8(c.bf, Z2, c.mean(b.b2), c.rstd(b.b2), c.theta + b.b2.g,
-                           c.theta + b.b2.b, res, 1, rows, b.b2.c, A, c.s));
+    HS_TRY(bn_apply(c, b.b2, Z2, res, 1, rps, A));
     cur = A;
   }
   void* F = S[si];
@@ -616,7 +675,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const void* dz;
   HS_TRY(loss_grad(c, y, loss, &dz));
   HS_TRY(conv_wgrad(c, m.fc2, dz, F));
-  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
   HS_TRY(launch_gap_bwd(c.bf, G[0], nullptr, n, 16, 512, G[1], c.s));
   int gi = 1;  // buffer holding the gradient of the current block output
@@ -630,15 +689,15 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     for (int i = 0; i < 5; ++i)
       if (i != gi) fr[k++] = i;
     void *dA = G[gi], *P1 = G[fr[0]], *P2 = G[fr[1]], *P3 = G[fr[2]], *P4 = G[fr[3]];
-    const int64_t rows = (int64_t)n * b.c1.Ho * b.c1.Wo;
-    HS_TRY(launch_relu_mask8(c.bf, dA, A, rows * b.c2.cout, P1, c.s));        // dPre
-    HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rows, P2));                     // dZ2
+    const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
+    HS_TRY(launch_relu_mask8(c.bf, dA, A, (int64_t)n * rps * b.c2.cout, P1, c.s));   // dPre
+    HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
     HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, nullptr));                  // dH
-    HS_TRY(bn_bwd(c, b.b1, P3, Hh, Z1, rows, P2));                          // dZ1
+    HS_TRY(bn_bwd(c, b.b1, P3, Hh, Z1, rps, P2));                           // dZ1
     HS_TRY(conv_wgrad(c, b.c1, P2, in));
     if (b.proj) {
-      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rows, P3));                   // dZP
+      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
       HS_TRY(conv_wgrad(c, b.cp, P3, in));
       HS_TRY(conv_dgrad(c, b.cp, P3, dA, nullptr, nullptr));                // shortcut grad
       HS_TRY(conv_dgrad(c, b.c1, P2, P4, dA, nullptr));                     // dIn
@@ -650,7 +709,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   }
   // stem
   void* dZs = G[gi == 0 ? 1 : 0];
-  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], S[2], S[1], rows0, dZs));
+  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], S[2], S[1], 1024, dZs));
   return stem_wgrad(c, m.stem, dZs, S[0]);
 }
 
@@ -665,12 +724,11 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   for (int i = 0; i < L; ++i) {
     const VggL& l = m.vgg[i];
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i], *P = S[3 + 3 * i];
-    const int64_t rows = (int64_t)n * l.c.Ho * l.c.Wo;
+    const int64_t rps = (int64_t)l.c.Ho * l.c.Wo;
     if (i == 0) HS_TRY(stem_fwd(c, l.c, x, S[0], Z));
     else HS_TRY(conv_fwd(c, l.c, cur, Z, false));
-    HS_TRY(bn_stats(c, l.bn, Z, rows));
-    HS_TRY(launch_bn_apply8(c.bf, Z, c.mean(l.bn), c.rstd(l.bn), c.theta + l.bn.g,
-                           c.theta + l.bn.b, nullptr, 1, rows, l.bn.c, A, c.s));
+    HS_TRY(bn_stats(c, l.bn, Z, rps));
+    HS_TRY(bn_apply(c, l.bn, Z, nullptr, 1, rps, A));
     cur = A;
     if (l.pool) {
       HS_TRY(launch_maxpool_fwd(c.bf, A, n, l.c.Ho, l.c.Wo, l.c.cout, P, c.s));
@@ -684,9 +742,9 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const void* dz;
   HS_TRY(loss_grad(c, y, loss, &dz));
   HS_TRY(conv_wgrad(c, m.fc2, dz, Hf));
-  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, n, 10));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, Hf));                // dHf * [Hf > 0]
-  HS_TRY(bias_grad(c, m.fc1.b, G[0], false, n, 512));
+  HS_TRY(bias_grad(c, m.fc1.b, G[0], false, 1, 512));
   HS_TRY(conv_wgrad(c, m.fc1, G[0], F));
   HS_TRY(conv_dgrad(c, m.fc1, G[0], G[1], nullptr, nullptr));         // dF
   int gi = 1;
@@ -694,7 +752,7 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const VggL& l = m.vgg[i];
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i];
     const void* in = i == 0 ? S[0] : (m.vgg[i - 1].pool ? S[3 + 3 * (i - 1)] : S[2 + 3 * (i - 1)]);
-    const int64_t rows = (int64_t)n * l.c.Ho * l.c.Wo;
+    const int64_t rps = (int64_t)l.c.Ho * l.c.Wo;
     const int a = (gi + 1) % 3, b2 = (gi + 2) % 3;
     int dAi = gi;
     if (l.pool) {
@@ -702,7 +760,7 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       dAi = a;
     }
     const int dZi = dAi == a ? b2 : a;
-    HS_TRY(bn_bwd(c, l.bn, G[dAi], A, Z, rows, G[dZi]));
+    HS_TRY(bn_bwd(c, l.bn, G[dAi], A, Z, rps, G[dZi]));
     if (i == 0) HS_TRY(stem_wgrad(c, l.c, G[dZi], in));
     else HS_TRY(conv_wgrad(c, l.c, G[dZi], in));
     if (i > 0) {
@@ -730,24 +788,30 @@ hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a,
   ConvL l = L;
   l.w = 0;
   l.b = -1;
-  if (mode == MODE_FWD) {
-    Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};
-    return conv_fwd(c, l, a, out, out_f32, b, bias);
-  }
+  Ctx c{m, ws, th, tb, n, s, bf16, bf16 ? 8 : 4, one_segment(n), {}};
+  if (mode == MODE_FWD) return conv_fwd(c, l, a, out, out_f32, b, bias);
   if (mode == MODE_DGRAD) {
-    Ctx c{m, ws, th, tb, nullptr, n, s, bf16, bf16 ? 8 : 4};
     if (out_f32 && bf16) return hipErrorInvalidValue;
     return conv_dgrad(c, l, a, out, nullptr, nullptr);
   }
-  Ctx c{m, ws, nullptr, nullptr, (float*)out, n, s, bf16, bf16 ? 8 : 4};
+  c.theta = nullptr;
+  c.tbf = nullptr;
+  c.g[0] = (float*)out;
   return conv_wgrad(c, l, a, b);
 }
 
-hipError_t worker_grad(const Model& m, Workspace& ws, const float* theta, const bf16_t* theta_bf16,
-                       const float* x, const int32_t* y, int n, float* g, float* loss,
-                       hipStream_t s) {
-  Ctx c{m, ws, theta, theta_bf16, g, n, s, m.dtype == HS_BF16, m.dtype == HS_BF16 ? 8 : 4};
-  HS_TRY(launch_zero_ranges(g, ws.gaps, (int)(m.gaps.size() / 2), s));
+hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
+                        const bf16_t* theta_bf16, const float* x, const int32_t* y, const int* n,
+                        int M, float* const* g, float* loss, hipStream_t s) {
+  if (M < 1 || M > MAX_SEG) return hipErrorInvalidValue;
+  Segs sg{};
+  sg.count = M;
+  sg.n0[0] = 0;
+  for (int i = 0; i < M; ++i) sg.n0[i + 1] = sg.n0[i] + n[i];
+  Ctx c{m, ws, theta, theta_bf16, sg.n0[M], s, m.dtype == HS_BF16, m.dtype == HS_BF16 ? 8 : 4, sg,
+        {}};
+  for (int i = 0; i < M; ++i) c.g[i] = g[i];
+  HS_TRY(launch_zero_ranges(c.g, M, ws.gaps, (int)(m.gaps.size() / 2), s));
   if (m.arch == HS_MLP) return mlp(c, x, y, loss);
   if (m.arch == HS_SMALLCNN) return small_cnn(c, x, y, loss);
   if (m.arch == HS_RESNET18) return resnet(c, x, y, loss);

@@ -70,12 +70,9 @@ struct Workspace {
   float* logits = nullptr;
   float* dz32 = nullptr;
   void* dzt = nullptr;
-  float* stats = nullptr;      // per batch-norm: mean[max_c], rstd[max_c]
+  float* stats = nullptr;      // per batch-norm and worker: mean[max_c], rstd[max_c]
   void* stem_w = nullptr;      // first-layer weights, channel-padded copy
-  float* stem_g = nullptr;     // first-layer weight gradient, channel-padded
-  float* stat_part1 = nullptr; // one-launch statistics: block partials
-  double* stat_part2 = nullptr;//   group partials
-  unsigned* stat_count = nullptr;  // arrival counters (zeroed at creation)
+  float* stat_part = nullptr;  // per-channel statistics: block partials
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
   int64_t* gaps = nullptr;     // device copy of the padding ranges
@@ -88,9 +85,12 @@ struct Workspace {
 
 int64_t plan_workspace(const Model& m, int max_n, Workspace* ws);  // ws->arena set => bind
 
-hipError_t worker_grad(const Model& m, Workspace& ws, const float* theta, const bf16_t* theta_bf16,
-                       const float* x, const int32_t* y, int n, float* g, float* loss,
-                       hipStream_t s);
+// Gradients of M workers in one pass over the layers: worker s owns samples
+// [o_s, o_s + n[s]) of x / y (o_s = n[0] + ... + n[s-1]); its gradient goes to
+// g[s] and its mean loss to loss[s] (loss may be null).
+hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
+                        const bf16_t* theta_bf16, const float* x, const int32_t* y, const int* n,
+                        int M, float* const* g, float* loss, hipStream_t s);
 
 // One layer contraction (mode 0 forward, 1 data gradient, 2 weight gradient)
 // with the schedule hs_worker_grad uses.

@@ -1,38 +1,106 @@
-// Per-channel sums over the rows of an NHWC tensor, finished in one launch:
+// Per-channel sums over the rows of an NHWC tensor, per worker segment:
 //   kind 0 (batch-norm forward):  mean and 1/sqrt(var + eps) of x
 //   kind 1 (batch-norm backward): sum d and sum d * xhat, d = dy * [act > 0],
 //                                 xhat = (x - mean) * rstd
 //   kind 2 (bias gradient):       sum d
-// Each thread reads V consecutive channels (16-byte vectors) over a strided
-// set of rows and accumulates in fp32; the block sums its row lanes in LDS and
-// writes one partial.  The last block of every group of 64 blocks to finish
-// sums that group's partials (double), and the last group to finish sums the
-// group partials and writes the result.  Every sum is taken in a fixed
-// order, so the result does not depend on which block finishes last.  The
-// arrival counters live in the caller's workspace, start at zero and are
-// reset by the blocks that consume them.
-// Batch-norm forward sums are shifted by the first row's value per channel
-// (var = E[(x-k)^2] - E[x-k]^2) so that a large mean does not cancel.
+// Two launches.  chan_partial_kernel: every block owns a row range of one
+// segment; each thread reads V consecutive channels (16-byte vectors) of a
+// strided set of rows, accumulating in fp32; the block adds its row lanes in
+// LDS and writes one partial per channel.  chan_finish_kernel: per segment and
+// group of 8 channels, 32 lanes per channel add the segment's block partials
+// in double, then a fixed-order tree adds the lanes.  Every sum is taken in a
+// fixed order: the result does not depend on scheduling.
+// Batch-norm forward sums are shifted by the segment's first row, per channel
+// (var = E[(x-k)^2] - E[x-k]^2), so that a large mean does not cancel.
 #include "kernels.h"
 
 namespace hs {
 
-constexpr int STAT_GROUP = 64;
+SegRows seg_rows(const Segs& sg, int64_t rows_per_sample, int64_t min_rows, int max_blocks) {
+  SegRows r{};
+  r.count = sg.count;
+  const int64_t total = (int64_t)(sg.n0[sg.count] - sg.n0[0]) * rows_per_sample;
+  int64_t per = min_rows > 0 ? min_rows : 1;
+  const int64_t cap = (int64_t)max_blocks - sg.count;   // sum of ceil() <= total/per + count
+  if (cap >= 1) {
+    const int64_t need = (total + cap - 1) / cap;
+    if (need > per) per = need;
+  }
+  r.blk[0] = 0;
+  for (int s = 0; s < sg.count; ++s) {
+    r.row[s] = (int64_t)sg.n0[s] * rows_per_sample;
+    const int64_t rows = (int64_t)(sg.n0[s + 1] - sg.n0[s]) * rows_per_sample;
+    int64_t b = (rows + per - 1) / per;
+    if (b < 1) b = 1;
+    r.blk[s + 1] = r.blk[s] + (int)b;
+  }
+  r.row[sg.count] = (int64_t)sg.n0[sg.count] * rows_per_sample;
+  for (int s = sg.count + 1; s <= MAX_SEG; ++s) {
+    r.blk[s] = r.blk[sg.count];
+    r.row[s] = r.row[sg.count];
+  }
+  return r;
+}
+
+namespace {
+
+// Segment of block b and the block's share [r0, r1) of the segment's rows.
+// Every table index is a compile-time constant (the tables stay in the
+// kernel-argument segment).
+__device__ inline void block_rows(const SegRows& sr, int b, int& s, int64_t& r0, int64_t& r1,
+                                  int64_t& seg0, int64_t& seg1) {
+  s = 0;
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i) s += (i < sr.count && b >= sr.blk[i]) ? 1 : 0;
+  int b0 = 0, b1 = 1;
+  seg0 = 0;
+  seg1 = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == s) {
+      b0 = sr.blk[i];
+      b1 = sr.blk[i + 1];
+      seg0 = sr.row[i];
+      seg1 = sr.row[i + 1];
+    }
+  const int64_t nb = b1 - b0 > 0 ? b1 - b0 : 1;
+  const int64_t per = (seg1 - seg0 + nb - 1) / nb;
+  r0 = seg0 + (int64_t)(b - b0) * per;
+  if (r0 > seg1) r0 = seg1;
+  r1 = r0 + per < seg1 ? r0 + per : seg1;
+}
+
+template <typename P>
+__device__ inline P pick(const P (&arr)[MAX_SEG], int s) {
+  P v = arr[0];
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i)
+    if (i == s) v = arr[i];
+  return v;
+}
+
+}  // namespace
 
 struct StatArgs {
   const void* x;
   const void* dy;
   const void* act;
-  const float* mean;
+  const float* mean;    // kind 1: segment s at mean + s * mstride
   const float* rstd;
-  int64_t rows;
+  int mstride;
   int C;
-  float* part1;        // [blocks][2][C]
-  double* part2;       // [groups][2][C]
-  unsigned* counters;  // [groups + 1]
-  float* out0;
-  float* out1;
+  float* part;          // [blocks][2][C]
+  SegRows sr;
+};
+
+struct FinishArgs {
+  const void* x;        // kind 0: the shift rows
+  const float* part;
+  int C;
   float eps;
+  SegRows sr;
+  float* out0[MAX_SEG];
+  float* out1[MAX_SEG];
 };
 
 template <typename T, int V>
@@ -59,28 +127,27 @@ template <>
 __device__ inline void load_vec<float, 1>(const float* p, int64_t i, float* v) { v[0] = p[i]; }
 
 template <typename T, int V, int KIND>
-__global__ __launch_bounds__(256) void chan_stats_kernel(StatArgs a) {
+__global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
   __shared__ float red[2][256 * 8];
-  __shared__ int s_last;
   const int C = a.C;
   const int TPR = C / V;
   const int RPB = 256 / TPR;
   const int t = threadIdx.x;
   const int cg = t % TPR, rl = t / TPR;
   const int c0 = cg * V;
-  const int64_t per = (a.rows + gridDim.x - 1) / gridDim.x;
-  const int64_t r0 = (int64_t)blockIdx.x * per;
-  const int64_t r1 = r0 + per < a.rows ? r0 + per : a.rows;
+  int s;
+  int64_t r0, r1, seg0, seg1;
+  block_rows(a.sr, blockIdx.x, s, r0, r1, seg0, seg1);
   float s0[V], s1[V], k[V], mu[V], rs[V];
 #pragma unroll
   for (int j = 0; j < V; ++j) s0[j] = s1[j] = 0.f;
   if (rl < RPB) {
-    if (KIND == 0) load_vec<T, V>((const T*)a.x, c0, k);          // shift: row 0
+    if (KIND == 0) load_vec<T, V>((const T*)a.x, seg0 * C + c0, k);   // shift: segment row 0
     if (KIND == 1) {
 #pragma unroll
       for (int j = 0; j < V; ++j) {
-        mu[j] = a.mean[c0 + j];
-        rs[j] = a.rstd[c0 + j];
+        mu[j] = a.mean[(int64_t)s * a.mstride + c0 + j];
+        rs[j] = a.rstd[(int64_t)s * a.mstride + c0 + j];
       }
     }
     int64_t r = r0 + rl;
@@ -153,7 +220,8 @@ __global__ __launch_bounds__(256) void chan_stats_kernel(StatArgs a) {
       }
     }
   }
-  // ---- block: sum the row lanes of every channel, in lane order
+  // ---- block: add the row lanes of every channel.  L lanes per channel
+  // each add every L-th row lane, then the L lane sums are added in order.
   if (rl < RPB) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
@@ -162,105 +230,144 @@ __global__ __launch_bounds__(256) void chan_stats_kernel(StatArgs a) {
     }
   }
   __syncthreads();
-  for (int c = t; c < C; c += 256) {
-    float a0 = 0.f, a1 = 0.f;
-    for (int q = 0; q < RPB; ++q) {
+  const int L = C >= 256 ? 1 : 256 / C;
+  float a0 = 0.f, a1 = 0.f;
+  int c = t, lane = 0;
+  if (L > 1) {
+    c = t % C;
+    lane = t / C;
+  }
+  if (lane < L && c < C) {
+    for (int q = lane; q < RPB; q += L) {
       a0 += red[0][q * C + c];
       a1 += red[1][q * C + c];
     }
-    a.part1[((int64_t)blockIdx.x * 2 + 0) * C + c] = a0;
-    a.part1[((int64_t)blockIdx.x * 2 + 1) * C + c] = a1;
   }
-  // ---- group: the last block of the group sums the group's partials
-  const int nb = gridDim.x;
-  const int groups = (nb + STAT_GROUP - 1) / STAT_GROUP;
-  const int g = blockIdx.x / STAT_GROUP;
-  const int gsize = (g == groups - 1) ? nb - g * STAT_GROUP : STAT_GROUP;
-  __threadfence();
   __syncthreads();
-  if (t == 0) s_last = (atomicAdd(&a.counters[g], 1u) == (unsigned)(gsize - 1));
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  {
-    // L lanes per channel, each summing every L-th block of the group; then
-    // the lanes are added in lane order
-    __shared__ double dred[2][256];
-    const int L = C >= 256 ? 1 : 256 / C;
-    for (int cb = 0; cb < C; cb += 256) {
-      const int c = cb + (L == 1 ? t : t % C), lane = L == 1 ? 0 : t / C;
-      double a0 = 0.0, a1 = 0.0;
-      if (c < C && lane < L) {
-        const int b0 = g * STAT_GROUP;
-#pragma unroll 4
-        for (int b = b0 + lane; b < b0 + gsize; b += L) {
-          a0 += (double)__builtin_nontemporal_load(&a.part1[((int64_t)b * 2 + 0) * C + c]);
-          a1 += (double)__builtin_nontemporal_load(&a.part1[((int64_t)b * 2 + 1) * C + c]);
-        }
+  if (L > 1) {
+    if (lane < L) {
+      red[0][lane * C + c] = a0;
+      red[1][lane * C + c] = a1;
+    }
+    __syncthreads();
+    if (t < C) {
+      a0 = a1 = 0.f;
+      for (int q = 0; q < L; ++q) {
+        a0 += red[0][q * C + t];
+        a1 += red[1][q * C + t];
       }
-      dred[0][t] = a0;
-      dred[1][t] = a1;
-      __syncthreads();
-      if (t < 256 / L && cb + t < C) {
-        double b0s = 0.0, b1s = 0.0;
-        for (int q = 0; q < L; ++q) {
-          b0s += dred[0][t + q * C];
-          b1s += dred[1][t + q * C];
-        }
-        a.part2[((int64_t)g * 2 + 0) * C + cb + t] = b0s;
-        a.part2[((int64_t)g * 2 + 1) * C + cb + t] = b1s;
+      a.part[((int64_t)blockIdx.x * 2 + 0) * C + t] = a0;
+      a.part[((int64_t)blockIdx.x * 2 + 1) * C + t] = a1;
+    }
+  } else {
+    for (int cc = t; cc < C; cc += 256) {
+      float b0 = 0.f, b1 = 0.f;
+      for (int q = 0; q < RPB; ++q) {
+        b0 += red[0][q * C + cc];
+        b1 += red[1][q * C + cc];
       }
-      __syncthreads();
+      a.part[((int64_t)blockIdx.x * 2 + 0) * C + cc] = b0;
+      a.part[((int64_t)blockIdx.x * 2 + 1) * C + cc] = b1;
     }
   }
-  if (t == 0) a.counters[g] = 0u;
-  __threadfence();
-  __syncthreads();
-  if (t == 0) s_last = (atomicAdd(&a.counters[groups], 1u) == (unsigned)(groups - 1));
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  for (int c = t; c < C; c += 256) {
-    double a0 = 0.0, a1 = 0.0;
-    for (int q = 0; q < groups; ++q) {
-      a0 += __builtin_nontemporal_load(&a.part2[((int64_t)q * 2 + 0) * C + c]);
-      a1 += __builtin_nontemporal_load(&a.part2[((int64_t)q * 2 + 1) * C + c]);
-    }
-    if (KIND == 0) {
-      const double cnt = (double)a.rows;
-      const double m1 = a0 / cnt;
-      double var = a1 / cnt - m1 * m1;
-      if (var < 0.0) var = 0.0;
-      const float shift = ld<T>((const T*)a.x, c);
-      a.out0[c] = (float)((double)shift + m1);
-      a.out1[c] = (float)(1.0 / sqrt(var + (double)a.eps));
-    } else {
-      if (a.out0) a.out0[c] = (float)a0;
-      if (KIND == 1 && a.out1) a.out1[c] = (float)a1;
-    }
-  }
-  if (t == 0) a.counters[groups] = 0u;
 }
 
-int stat_blocks(int64_t rows, int C) {
-  const int V = (C % 8 == 0 && C / 8 <= 256) ? 8 : 1;
-  const int TPR = C / V;
-  const int RPB = 256 / TPR;
-  int64_t b = (rows + (int64_t)RPB * 16 - 1) / ((int64_t)RPB * 16);   // >= 16 rows per lane
-  if (b > STAT_MAX_BLOCKS) b = STAT_MAX_BLOCKS;
-  if (b < 1) b = 1;
-  return (int)b;
+// blockIdx.y = segment, blockIdx.x = group of 8 channels; thread = channel
+// (t & 7) x lane (t >> 3)
+template <typename T, int KIND>
+__global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
+  __shared__ double red[2][256];
+  const int s = blockIdx.y;
+  const int t = threadIdx.x, lane = t >> 3;
+  const int c = blockIdx.x * 8 + (t & 7);
+  const int C = a.C;
+  int b0 = 0, b1 = 0;
+  int64_t seg0 = 0, seg1 = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == s) {
+      b0 = a.sr.blk[i];
+      b1 = a.sr.blk[i + 1];
+      seg0 = a.sr.row[i];
+      seg1 = a.sr.row[i + 1];
+    }
+  double s0 = 0.0, s1 = 0.0;
+  if (c < C) {
+    int b = b0 + lane;
+    for (; b + 96 < b1; b += 128) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v[2 * u] = a.part[((int64_t)(b + 32 * u) * 2 + 0) * C + c];
+        v[2 * u + 1] = a.part[((int64_t)(b + 32 * u) * 2 + 1) * C + c];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s0 += (double)v[2 * u];
+        s1 += (double)v[2 * u + 1];
+      }
+    }
+    for (; b < b1; b += 32) {
+      s0 += (double)a.part[((int64_t)b * 2 + 0) * C + c];
+      s1 += (double)a.part[((int64_t)b * 2 + 1) * C + c];
+    }
+  }
+  red[0][t] = s0;
+  red[1][t] = s1;
+  __syncthreads();
+  for (int w = 16; w >= 1; w >>= 1) {
+    if (lane < w) {
+      red[0][t] += red[0][t + 8 * w];
+      red[1][t] += red[1][t + 8 * w];
+    }
+    __syncthreads();
+  }
+  if (lane != 0 || c >= C) return;
+  float* o0 = pick(a.out0, s);
+  float* o1 = pick(a.out1, s);
+  const double t0 = red[0][t], t1 = red[1][t];
+  if (KIND == 0) {
+    const double cnt = (double)(seg1 - seg0);
+    const double m1 = t0 / cnt;
+    double var = t1 / cnt - m1 * m1;
+    if (var < 0.0) var = 0.0;
+    const float shift = ld<T>((const T*)a.x, seg0 * C + c);
+    o0[c] = (float)((double)shift + m1);
+    o1[c] = (float)(1.0 / sqrt(var + (double)a.eps));
+  } else {
+    if (o0) o0[c] = (float)t0;
+    if (KIND == 1 && o1) o1[c] = (float)t1;
+  }
 }
 
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
-                             const float* mean, const float* rstd, int64_t rows, int C,
-                             float* part1, double* part2, unsigned* counters, float* out0,
-                             float* out1, float eps, hipStream_t s) {
+                             const float* mean, const float* rstd, int mstride, const Segs& sg,
+                             int64_t rows_per_sample, int C, float* part, float* const* out0,
+                             float* const* out1, float eps, hipStream_t s) {
   if (C < 1 || C > 256 * 8 || (C % 8 != 0 && C > 256)) return hipErrorInvalidValue;
-  StatArgs a{x, dy, act, mean, rstd, rows, C, part1, part2, counters, out0, out1, eps};
+  if (sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
   const bool vec = (C % 8 == 0 && C / 8 <= 256);
-  dim3 grid(stat_blocks(rows, C)), block(256);
-#define HS_STAT(T, V, K) hipLaunchKernelGGL((chan_stats_kernel<T, V, K>), grid, block, 0, s, a)
+  const int V = vec ? 8 : 1;
+  const int RPB = 256 / (C / V);
+  StatArgs a{x, dy, act, mean, rstd, mstride, C, part,
+             seg_rows(sg, rows_per_sample, (int64_t)RPB * 16, STAT_MAX_BLOCKS)};
+  FinishArgs f{};
+  f.x = x;
+  f.part = part;
+  f.C = C;
+  f.eps = eps;
+  f.sr = a.sr;
+  for (int i = 0; i < sg.count; ++i) {
+    f.out0[i] = out0 ? out0[i] : nullptr;
+    f.out1[i] = out1 ? out1[i] : nullptr;
+  }
+  const dim3 grid(a.sr.blk[sg.count]), block(256);
+  const dim3 fgrid((C + 7) / 8, sg.count);
+#define HS_STAT(T, VV, K)                                                             \
+  do {                                                                                \
+    hipLaunchKernelGGL((chan_partial_kernel<T, VV, K>), grid, block, 0, s, a);        \
+    hipLaunchKernelGGL((chan_finish_kernel<T, K>), fgrid, block, 0, s, f);            \
+  } while (0)
   if (bf16) {
     if (vec) {
       if (kind == 0) HS_STAT(bf16_t, 8, 0);
@@ -313,52 +420,69 @@ static inline int vgrid(int64_t groups) {
   return (int)b;
 }
 
-// Row-major elementwise work over [rows][C] with C % 8 == 0: a thread owns
-// one group of 8 channels (its per-channel coefficients stay in registers) and
-// walks rows rl, rl + RPB, ... of its block's row range, 4 rows per step.
+// Row-major elementwise work over [rows][C] with C % 8 == 0: every block
+// owns a row range of one segment; a thread owns one group of 8 channels (its
+// per-channel coefficients stay in registers) and walks rows rl, rl + RPB, ...
+// of the block's range, 4 rows per step.
 struct RowSplit {
-  int TPR, RPB, cg, rl, c0;
-  int64_t r0, r1;
+  int TPR, RPB, cg, rl, c0, seg;
+  int64_t r0, r1, rows;   // block range; rows of the segment
 };
 
-__device__ inline RowSplit row_split(int64_t rows, int C) {
+__device__ inline RowSplit row_split(const SegRows& sr, int C) {
   RowSplit w;
   w.TPR = C / 8;
   w.RPB = 256 / w.TPR;
   w.cg = threadIdx.x % w.TPR;
   w.rl = threadIdx.x / w.TPR;
   w.c0 = w.cg * 8;
-  const int64_t per = (rows + gridDim.x - 1) / gridDim.x;
-  w.r0 = (int64_t)blockIdx.x * per;
-  w.r1 = w.r0 + per < rows ? w.r0 + per : rows;
+  int64_t seg0, seg1;
+  block_rows(sr, blockIdx.x, w.seg, w.r0, w.r1, seg0, seg1);
+  w.rows = seg1 - seg0;
   return w;
 }
 
-static inline int row_grid(int64_t rows, int C) {
+// about 8 rows per thread, at most 16384 blocks
+static inline SegRows row_segs(const Segs& sg, int64_t rows_per_sample, int C) {
   const int RPB = 256 / (C / 8);
-  int64_t b = (rows + (int64_t)RPB * 8 - 1) / ((int64_t)RPB * 8);   // ~8 rows per thread
-  if (b > 16384) b = 16384;
-  if (b < 1) b = 1;
-  return (int)b;
+  return seg_rows(sg, rows_per_sample, (int64_t)RPB * 8, 16384);
 }
+
+struct BnArgs {
+  const void* z;
+  const void* res;      // apply: added before the ReLU, or null
+  const void* dy;       // backward
+  const void* act;      // backward: dy masked by [act > 0], or null
+  const float* mean;    // segment s at mean + s * mstride
+  const float* rstd;
+  int mstride;
+  const float* gamma;
+  const float* beta;
+  int relu;
+  int C;
+  void* out;
+  SegRows sr;
+  float* sum0[MAX_SEG]; // backward: per segment sum d and sum d * xhat
+  float* sum1[MAX_SEG];
+};
 
 // y = relu?(gamma * (z - mean) * rstd + beta + res)
 template <typename T>
-__global__ __launch_bounds__(256) void bn_apply8_kernel(const T* __restrict__ z,
-                                                        const float* __restrict__ mean,
-                                                        const float* __restrict__ rstd,
-                                                        const float* __restrict__ gamma,
-                                                        const float* __restrict__ beta,
-                                                        const T* __restrict__ res, int relu,
-                                                        int64_t rows, int C, T* __restrict__ y) {
-  const RowSplit w = row_split(rows, C);
+__global__ __launch_bounds__(256) void bn_apply8_kernel(BnArgs a) {
+  const int C = a.C;
+  const RowSplit w = row_split(a.sr, C);
   if (w.rl >= w.RPB) return;
+  const T* __restrict__ z = (const T*)a.z;
+  const T* __restrict__ res = (const T*)a.res;
+  T* __restrict__ y = (T*)a.out;
+  const float* mean = a.mean + (int64_t)w.seg * a.mstride;
+  const float* rstd = a.rstd + (int64_t)w.seg * a.mstride;
   float sa[8], sb[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int c = w.c0 + j;
-    sa[j] = gamma[c] * rstd[c];
-    sb[j] = beta[c] - mean[c] * sa[j];
+    sa[j] = a.gamma[c] * rstd[c];
+    sb[j] = a.beta[c] - mean[c] * sa[j];
   }
   for (int64_t r = w.r0 + w.rl; r < w.r1; r += 4 * w.RPB) {
     float v[4][8], q[4][8];
@@ -378,7 +502,7 @@ __global__ __launch_bounds__(256) void bn_apply8_kernel(const T* __restrict__ z,
       for (int j = 0; j < 8; ++j) {
         float o = sa[j] * v[u][j] + sb[j];
         if (res) o += q[u][j];
-        if (relu) o = o > 0.f ? o : 0.f;
+        if (a.relu) o = o > 0.f ? o : 0.f;
         v[u][j] = o;
       }
       store_vec8<T>(y, rr * C + w.c0, v[u]);
@@ -387,34 +511,49 @@ __global__ __launch_bounds__(256) void bn_apply8_kernel(const T* __restrict__ z,
 }
 
 hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const float* rstd,
-                            const float* gamma, const float* beta, const void* res, int relu,
-                            int64_t rows, int C, void* y, hipStream_t s) {
-  if (C % 8 || C / 8 > 256) return hipErrorInvalidValue;
-  const dim3 grid(row_grid(rows, C));
-  if (bf16)
-    hipLaunchKernelGGL(bn_apply8_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)z, mean,
-                       rstd, gamma, beta, (const bf16_t*)res, relu, rows, C, (bf16_t*)y);
-  else
-    hipLaunchKernelGGL(bn_apply8_kernel<float>, grid, dim3(256), 0, s, (const float*)z, mean,
-                       rstd, gamma, beta, (const float*)res, relu, rows, C, (float*)y);
+                            int mstride, const float* gamma, const float* beta, const void* res,
+                            int relu, const Segs& sg, int64_t rows_per_sample, int C, void* y,
+                            hipStream_t s) {
+  if (C % 8 || C / 8 > 256 || sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
+  BnArgs a{};
+  a.z = z;
+  a.res = res;
+  a.mean = mean;
+  a.rstd = rstd;
+  a.mstride = mstride;
+  a.gamma = gamma;
+  a.beta = beta;
+  a.relu = relu;
+  a.C = C;
+  a.out = y;
+  a.sr = row_segs(sg, rows_per_sample, C);
+  const dim3 grid(a.sr.blk[sg.count]);
+  if (bf16) hipLaunchKernelGGL(bn_apply8_kernel<bf16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(bn_apply8_kernel<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 // dz = gamma * rstd * (d - (sum_d + xhat * sum_dx) / rows), d = dy * [act > 0]
 template <typename T>
-__global__ __launch_bounds__(256) void bn_backward8_kernel(
-    const T* __restrict__ dy, const T* __restrict__ act, const T* __restrict__ z,
-    const float* __restrict__ mean, const float* __restrict__ rstd, const float* __restrict__ gamma,
-    const float* __restrict__ sum_dy, const float* __restrict__ sum_dyx, int64_t rows, int C,
-    float inv_rows, T* __restrict__ dz) {
-  const RowSplit w = row_split(rows, C);
+__global__ __launch_bounds__(256) void bn_backward8_kernel(BnArgs a) {
+  const int C = a.C;
+  const RowSplit w = row_split(a.sr, C);
   if (w.rl >= w.RPB) return;
+  const T* __restrict__ dy = (const T*)a.dy;
+  const T* __restrict__ act = (const T*)a.act;
+  const T* __restrict__ z = (const T*)a.z;
+  T* __restrict__ dz = (T*)a.out;
+  const float* mean = a.mean + (int64_t)w.seg * a.mstride;
+  const float* rstd = a.rstd + (int64_t)w.seg * a.mstride;
+  const float* sum_dy = pick(a.sum0, w.seg);
+  const float* sum_dyx = pick(a.sum1, w.seg);
+  const float inv_rows = 1.0f / (float)w.rows;
   float gr[8], mu[8], rs[8], k1[8], k2[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int c = w.c0 + j;
     rs[j] = rstd[c];
-    gr[j] = gamma[c] * rs[j];
+    gr[j] = a.gamma[c] * rs[j];
     mu[j] = mean[c];
     k1[j] = sum_dy[c] * inv_rows;
     k2[j] = sum_dyx[c] * inv_rows;
@@ -447,20 +586,29 @@ __global__ __launch_bounds__(256) void bn_backward8_kernel(
 }
 
 hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const void* z,
-                               const float* mean, const float* rstd, const float* gamma,
-                               const float* sum_dy, const float* sum_dyx, int64_t rows, int C,
-                               void* dz, hipStream_t s) {
-  if (C % 8 || C / 8 > 256) return hipErrorInvalidValue;
-  const float inv = 1.0f / (float)rows;
-  const dim3 grid(row_grid(rows, C));
-  if (bf16)
-    hipLaunchKernelGGL(bn_backward8_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)dy,
-                       (const bf16_t*)act, (const bf16_t*)z, mean, rstd, gamma, sum_dy, sum_dyx,
-                       rows, C, inv, (bf16_t*)dz);
-  else
-    hipLaunchKernelGGL(bn_backward8_kernel<float>, grid, dim3(256), 0, s, (const float*)dy,
-                       (const float*)act, (const float*)z, mean, rstd, gamma, sum_dy, sum_dyx, rows,
-                       C, inv, (float*)dz);
+                               const float* mean, const float* rstd, int mstride,
+                               const float* gamma, float* const* sum_dy, float* const* sum_dyx,
+                               const Segs& sg, int64_t rows_per_sample, int C, void* dz,
+                               hipStream_t s) {
+  if (C % 8 || C / 8 > 256 || sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
+  BnArgs a{};
+  a.z = z;
+  a.dy = dy;
+  a.act = act;
+  a.mean = mean;
+  a.rstd = rstd;
+  a.mstride = mstride;
+  a.gamma = gamma;
+  a.C = C;
+  a.out = dz;
+  a.sr = row_segs(sg, rows_per_sample, C);
+  for (int i = 0; i < sg.count; ++i) {
+    a.sum0[i] = sum_dy[i];
+    a.sum1[i] = sum_dyx[i];
+  }
+  const dim3 grid(a.sr.blk[sg.count]);
+  if (bf16) hipLaunchKernelGGL(bn_backward8_kernel<bf16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(bn_backward8_kernel<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -11,6 +11,11 @@ Each step (all device work through libhs):
     to the estimated compute powers (Eq. (2), Algorithm 1).
 With clock="model" the time of worker m is n_m (X_m = n_m / s_m), which
 makes the partition sequence independent of the hardware.
+
+grouped=True runs all workers in one hs_workers_grad call on the main stream
+(every layer launched once over the whole batch, statistics, losses and
+weight gradients per worker).  Per-worker device times do not exist there,
+so it requires clock="model".
 PyTorch is used for device memory, streams and events only.
 """
 import numpy as np
@@ -22,12 +27,15 @@ from .configs import WORKLOADS, Workload
 
 class Trainer:
     def __init__(self, workload, seed=0, clock="measured", device="cuda:0", n_batches=4,
-                 max_n=None, steps=None, theta0=None):
+                 max_n=None, steps=None, theta0=None, grouped=False):
         self.wl = wl = WORKLOADS[workload] if isinstance(workload, str) else workload
         assert isinstance(wl, Workload)
         if clock not in ("measured", "model"):
             raise ValueError("clock must be 'measured' or 'model'")
+        if grouped and clock != "model":
+            raise ValueError("grouped workers have no per-worker device time: use clock='model'")
         self.clock = clock
+        self.grouped = grouped
         self.dev = torch.device(device)
         self.M, self.N = wl.workers, wl.total
         self.steps = steps if steps is not None else wl.steps
@@ -43,9 +51,13 @@ class Trainer:
         self.mom = torch.zeros(self.P, device=self.dev) if wl.mu != 0.0 else None
         self.grads = [torch.empty(self.P, device=self.dev) for _ in range(self.M)]
         self.losses = torch.zeros(self.M, device=self.dev)
-        self.streams = [torch.cuda.Stream(device=self.dev) for _ in range(self.M)]
         self.max_n = max_n or self.N
-        self.ws = [hs.workspace_create(self.model, self.max_n) for _ in range(self.M)]
+        if grouped:
+            self.streams = []
+            self.ws = [hs.workspace_create(self.model, self.N)]
+        else:
+            self.streams = [torch.cuda.Stream(device=self.dev) for _ in range(self.M)]
+            self.ws = [hs.workspace_create(self.model, self.max_n) for _ in range(self.M)]
         self.part = hs.Partitioner(self.M, self.N, wl.window)
         if not wl.start_even:                       # fixed split in proportion to the speeds
             self.part.set_partition(hs.repartition(list(wl.speeds), self.N))
@@ -98,8 +110,15 @@ class Trainer:
         wl, t = self.wl, self.t
         n = self.part.partition()
         x, y = self.batch(t)
-        events = self.launch_workers(n, x, y, timed=(self.clock == "measured"))
         main = torch.cuda.current_stream(self.dev)
+        if self.grouped:
+            hs.workers_grad(self.model, self.ws[0], self.theta.data_ptr(),
+                            self.theta_bf16.data_ptr() if self.bf16 else 0, x.data_ptr(),
+                            y.data_ptr(), n, [g.data_ptr() for g in self.grads],
+                            self.losses.data_ptr(), main.cuda_stream)
+            events = None
+        else:
+            events = self.launch_workers(n, x, y, timed=(self.clock == "measured"))
         hs.wavg_sgd([g.data_ptr() for g in self.grads], n, self.theta.data_ptr(),
                     self.mom.data_ptr() if self.mom is not None else 0, self.P, wl.lr, wl.mu,
                     wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)

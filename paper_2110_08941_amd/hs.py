@@ -53,6 +53,7 @@ def _load():
         "hs_workspace_destroy": (I32, [P]),
         "hs_workspace_bytes": (I64, [P]),
         "hs_worker_grad": (I32, [P, P, P, P, P, P, I32, P, P, P]),
+        "hs_workers_grad": (I32, [P, P, P, P, P, P, PI32, I32, PP, P, P]),
         "hs_weighted_average": (I32, [PP, PI32, I32, I64, P, P]),
         "hs_sgd_step": (I32, [P, P, P, I64, F, F, F, P, P]),
         "hs_wavg_sgd": (I32, [PP, PI32, I32, P, P, I64, F, F, F, P, P]),
@@ -89,6 +90,7 @@ EXPORTED = (
     "hs_model_create", "hs_model_destroy", "hs_num_params", "hs_num_true_params",
     "hs_num_param_tensors", "hs_param_tensor", "hs_input_numel", "hs_forward_macs",
     "hs_workspace_create", "hs_workspace_destroy", "hs_workspace_bytes", "hs_worker_grad",
+    "hs_workers_grad",
     "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
     "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
@@ -178,6 +180,15 @@ def workspace_bytes(ws):
 def worker_grad(model, ws, theta, theta_bf16, x_m, y_m, n_m, g_m, loss_m=0, stream=0):
     _check(_lib.hs_worker_grad(model, ws, theta, theta_bf16 or None, x_m, y_m, int(n_m), g_m,
                                loss_m or None, stream or None))
+
+
+def workers_grad(model, ws, theta, theta_bf16, x, y, n, g, loss=0, stream=0):
+    """All len(n) workers' gradients in one pass; g: device pointers, one per
+    worker; loss: device fp32 [M] or 0."""
+    if len(g) != len(n):
+        raise ValueError("workers_grad: one gradient buffer per worker")
+    _check(_lib.hs_workers_grad(model, ws, theta, theta_bf16 or None, x, y, _i32(n), len(n),
+                                _ptrs(g), loss or None, stream or None))
 
 
 def weighted_average(g, n, P, g_out, stream=0):

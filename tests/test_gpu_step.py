@@ -34,17 +34,20 @@ def make_trainer(name, total=None, steps=None, clock="model", separated=False, s
     return tr, net, theta
 
 
+@pytest.mark.parametrize("grouped", [False, True])
 @pytest.mark.parametrize("name,total,separated", [
     ("mlp_fp32", 256, False),            # the full MLP workload
     ("smallcnn_fp32", 40, False),
     ("resnet18_fp32", 24, True),
     ("resnet18_bf16", 32, True),
     ("vgg16_bf16", 32, True)])
-def test_one_step(name, total, separated):
-    """theta' - theta after one step (worker gradients, weighted average,
-    momentum SGD) against the oracle's step on the same partition."""
-    log("one step %s N=%d" % (name, total))
-    tr, net, theta = make_trainer(name, total=total, steps=1, separated=separated)
+def test_one_step(name, total, separated, grouped):
+    """theta' - theta after one step (worker gradients -- on their own streams,
+    or all in one pass -- weighted average, momentum SGD) against the oracle's
+    step on the same partition."""
+    log("one step %s N=%d grouped=%s" % (name, total, grouped))
+    tr, net, theta = make_trainer(name, total=total, steps=1, separated=separated,
+                                  grouped=grouped)
     try:
         n = tr.part.partition()
         x, y = tr.batch(0)
@@ -106,10 +109,11 @@ def test_partition_sequence_replays_bit_exact(name, steps):
     assert int(np.argmax(last)) == int(np.argmax(speed)) or wl.drift_sigma > 0
 
 
-def test_model_clock_partitions():
+@pytest.mark.parametrize("grouped", [False, True])
+def test_model_clock_partitions(grouped):
     """Model clock (X_m = n_m / s_m): even split for the first window, then
     exactly proportional to the speeds 1:1:2:4 (64/64/128/256 of 512)."""
-    tr, _, _ = make_trainer("smallcnn_fp32", steps=10, clock="model")
+    tr, _, _ = make_trainer("smallcnn_fp32", steps=10, clock="model", grouped=grouped)
     try:
         tr.run(10)
         used = [e["n"] for e in tr.log]
@@ -119,17 +123,19 @@ def test_model_clock_partitions():
     assert used[5:] == [[64, 64, 128, 256]] * 5
 
 
-def test_multistep_theta_small_cnn():
+@pytest.mark.parametrize("grouped", [False, True])
+def test_multistep_theta_small_cnn(grouped):
     """Ten steps of the small CNN workload (reduced to N = 32, repartition
     every 5 steps with the model clock) against the oracle's driver."""
-    log("multistep small cnn")
+    log("multistep small cnn grouped=%s" % grouped)
     wl = dataclasses.replace(WORKLOADS["smallcnn_fp32"], total=32, window=5, steps=10)
     require_gpu()
     from paper_2110_08941_amd.driver import Trainer
     net = Mo.build(wl.arch)
     table, P = Mo.param_table(net)
     theta = synth.he_normal(table, P, 0)
-    tr = Trainer(wl, seed=0, clock="model", steps=10, theta0=theta, n_batches=10)
+    tr = Trainer(wl, seed=0, clock="model", steps=10, theta0=theta, n_batches=10,
+                 grouped=grouped)
     try:
         batches = [(x.cpu().numpy(), y.cpu().numpy()) for x, y in tr.batches]
         tr.run(10)
