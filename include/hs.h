@@ -227,6 +227,11 @@ hs_status hs_probe_read(hs_workspace* ws, double* total_ms, int64_t* launches, d
  *   mode 2 (weight grad):  out[K][R][R][C]  = gradient w.r.t. W, a = dy, b = x; fp32
  *                          output; split over pixels when scratch (fp32, scratch_floats
  *                          elements) is given, in one pass otherwise
+ * For bf16 modes 0 and 1 with a bf16 output, a scratch buffer large enough for
+ * a packed copy of the weights (K R R C bf16) selects the kernel the step
+ * uses for those layers (32x32 MFMA tiles on packed weights) where the shape
+ * allows it: C (mode 0) or K (mode 1) a multiple of 16, the output channel
+ * count a multiple of 64, 3x3 or 1x1 filters, stride 1 for mode 1.
  * dtype selects the operand type (HS_FP32: float, HS_BF16: bf16 bits);
  * out_f32 != 0 stores modes 0/1 as fp32 even for bf16 operands.
  * Ho = (H + 2 pad - R) / stride + 1.  stride is 1 or 2.  All pointers device,

@@ -1,0 +1,351 @@
+// Forward and stride-1 data-gradient convolutions in bf16 on the 32x32x16
+// MFMA, with the gathered operand read straight from global memory.
+//
+// C[m][n] = sum_k A[m][k] * B[n][k], k = (tap, channel):
+//   forward:        m = output pixel, n = output channel, A = input x gathered
+//                   at (ho*st - pad + r, wo*st - pad + s), B = W[n][tap][c];
+//   data gradient:  m = input pixel, n = input channel, A = dy gathered at
+//                   (h + pad - r, w + pad - s), B = W[c][tap][n] (stride 1).
+// The reduction runs over slices of 16 channels; within a slice every tap of
+// the filter is applied in turn, so the 3x3 taps re-read neighbouring pixels
+// of the same 32-byte channel group and those re-reads hit the L1 cache.
+//
+// Block: 8 waves, 512 x BN output tile; wave w owns rows 64 w .. 64 w + 63 and
+// all BN columns.  A fragments never touch LDS: lane l loads the 16 bytes
+// (8 channels) of row l % 32 at channel offset 8 (l / 32) that the MFMA
+// expects, two taps ahead of their use.  B -- the same for every wave -- is
+// staged in LDS once per slice from a packed copy of the weights,
+// Bp[slice][tap][kh][N][8] (kh: channel half of the slice), so that both the
+// global read and the LDS write of a slice are contiguous and the fragment
+// reads (32 consecutive n of one kh plane) are free of bank conflicts.
+// One barrier per slice; the next slice's B is fetched into registers while
+// the current slice computes.
+#include "kernels.h"
+
+namespace hs {
+
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16 };
+
+constexpr int C2_WAVES = 8;
+constexpr int C2_BM = 64 * C2_WAVES;   // rows per block
+constexpr int C2_CK = 16;              // channels per slice
+
+__device__ inline uint32_t pack2(float a, float b) {
+  f32x2 v = {a, b};
+  bf16x2 h = __builtin_convertvector(v, bf16x2);
+  uint32_t u;
+  __builtin_memcpy(&u, &h, 4);
+  return u;
+}
+
+__device__ inline float bfl(const bf16_t* p, int64_t i) { return bf2f(p[i]); }
+
+}  // namespace
+
+// Bp[((s * RS + tap) * 2 + kh) * N + n][e] = B[n][tap][16 s + 8 kh + e]
+// forward: B[n][tap][c] = W[n][tap][c]        (W is [N][RS][C])
+// data gradient: B[n][tap][c] = W[c][tap][n]  (W is [C][RS][N])
+__global__ void pack_weights_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Bp, int N,
+                                    int RS, int C, int transpose) {
+  const int64_t chunks = (int64_t)(C / C2_CK) * RS * 2 * N;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < chunks;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int n = (int)(q % N);
+    int64_t r = q / N;
+    const int kh = (int)(r & 1);
+    r >>= 1;
+    const int tap = (int)(r % RS);
+    const int s = (int)(r / RS);
+    const int c0 = s * C2_CK + kh * 8;
+    uint4 v;
+    if (!transpose) {
+      v = *(const uint4*)(W + ((int64_t)n * RS + tap) * C + c0);
+    } else {
+      uint16_t e[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = W[((int64_t)(c0 + j) * RS + tap) * N + n];
+      v = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
+                     e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
+    }
+    *(uint4*)(Bp + q * 8) = v;
+  }
+}
+
+template <int MODE, int BN, int RS, int EPI>
+__global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
+  constexpr int NB = BN / 32;
+  constexpr int SEG = RS * 2 * BN;                 // 16-byte chunks of B per slice
+  constexpr int BREG = (SEG + 511) / 512;          // per thread
+  __shared__ uint4 Bs[2][RS][2][BN];
+
+  const ConvGeom& g = p.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  const int m0 = tm * C2_BM + wave * 64, n0 = tn * BN;
+  const int kh = lane >> 5;
+  const int Ctap = MODE == MODE_FWD ? g.C : g.K;   // channels per tap (A side)
+  const int Wsrc = MODE == MODE_FWD ? g.W : g.Wo;  // image width of the A tensor
+  const int Hsrc = MODE == MODE_FWD ? g.H : g.Ho;
+  const int nslices = Ctap / C2_CK;
+
+  // rows of this lane: element offset of the pixel origin (may point outside
+  // the image; only read when the tap lands inside) and its coordinates
+  int apix[2], ay[2], ax[2];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int m = m0 + 32 * mb + (lane & 31);
+    const bool ok = m < p.M;
+    const int mm = ok ? m : 0;
+    int base;
+    if (MODE == MODE_FWD) {
+      const int b = (int)fdiv(mm, g.HWo), rem = mm - b * g.Ho * g.Wo;
+      const int ho = (int)fdiv(rem, g.Wo_), wo = rem - ho * g.Wo;
+      base = b * g.H * g.W * g.C;
+      ay[mb] = ho * g.stride - g.pad;
+      ax[mb] = wo * g.stride - g.pad;
+    } else {
+      const int b = (int)fdiv(mm, g.HWi), rem = mm - b * g.H * g.W;
+      const int h = (int)fdiv(rem, g.Wi_), w = rem - h * g.W;
+      base = b * g.Ho * g.Wo * g.K;
+      ay[mb] = h + g.pad;
+      ax[mb] = w + g.pad;
+    }
+    apix[mb] = base + (ay[mb] * Wsrc + ax[mb]) * Ctap + 8 * kh;
+    if (!ok) ay[mb] = -(1 << 20);   // every tap out of range
+  }
+  const bf16_t* A = (const bf16_t*)p.a;
+  const bf16_t* B = (const bf16_t*)p.b;
+
+  // A fragment of (slice, tap) for both row blocks: the tap's shift is the
+  // same for every lane (dr, ds, element offset)
+  auto load_a = [&](int sl, int tap, uint4 (&ra)[2]) {
+    const int r = RS == 1 ? 0 : tap / 3, s = RS == 1 ? 0 : tap - 3 * (tap / 3);
+    const int dr = MODE == MODE_FWD ? r : -r, ds = MODE == MODE_FWD ? s : -s;
+    const int toff = (dr * Wsrc + ds) * Ctap + sl * C2_CK;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const bool ok = (unsigned)(ay[mb] + dr) < (unsigned)Hsrc &&
+                      (unsigned)(ax[mb] + ds) < (unsigned)Wsrc;
+      ra[mb] = ok ? *(const uint4*)(A + apix[mb] + toff) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  // B chunk i of slice sl (global -> register) and its LDS slot
+  auto load_b1 = [&](int sl, int i) -> uint4 {
+    const int q = tid + 512 * i;
+    uint4 r = make_uint4(0, 0, 0, 0);
+    if (q < SEG) {
+      const int n = q % BN, rest = q / BN;    // rest = tap * 2 + kh
+      r = *(const uint4*)(B + (((int64_t)sl * RS * 2 + rest) * p.N + n0 + n) * 8);
+    }
+    return r;
+  };
+  auto store_b1 = [&](int buf, int i, const uint4& r) {
+    const int q = tid + 512 * i;
+    if (q < SEG) {
+      const int n = q % BN, rest = q / BN;
+      Bs[buf][rest >> 1][rest & 1][n] = r;
+    }
+  };
+
+  f32x16 acc[2][NB];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = (f32x16){};
+
+  {
+    uint4 r0[BREG];
+#pragma unroll
+    for (int i = 0; i < BREG; ++i) r0[i] = load_b1(0, i);
+#pragma unroll
+    for (int i = 0; i < BREG; ++i) store_b1(0, i, r0[i]);
+  }
+  // A fragments two steps ahead: cur = step u, nxt = step u + 1
+  uint4 cur[2], nxt[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+  load_a(0, 0, cur);
+  if (RS > 1) load_a(0, 1, nxt);
+  else if (nslices > 1) load_a(1, 0, nxt);
+  __syncthreads();
+
+  // Next slice's B: with RS >= BREG + 2 taps, chunk i is loaded at tap i and
+  // written to the free LDS buffer at tap i + 2 (few registers live);
+  // otherwise all chunks are loaded at the first tap and written at the end.
+  constexpr bool SPREAD = RS >= BREG + 2;
+  for (int sl = 0; sl < nslices; ++sl) {
+    const bool more = sl + 1 < nslices;
+    const int buf = sl & 1;
+    uint4 rb[BREG];
+    if (!SPREAD && more) {
+#pragma unroll
+      for (int i = 0; i < BREG; ++i) rb[i] = load_b1(sl + 1, i);
+    }
+#pragma unroll
+    for (int t = 0; t < RS; ++t) {
+      if (SPREAD && more) {
+        if (t < BREG) rb[t] = load_b1(sl + 1, t);
+        if (t >= 2 && t - 2 < BREG) store_b1(buf ^ 1, t - 2, rb[t - 2]);
+      }
+      const uint4 fa[2] = {cur[0], cur[1]};
+      cur[0] = nxt[0];
+      cur[1] = nxt[1];
+      {   // prefetch step u + 2
+        int nt = t + 2, ns = sl;
+        while (nt >= RS) {
+          nt -= RS;
+          ++ns;
+        }
+        if (ns < nslices) load_a(ns, nt, nxt);
+      }
+      uint4 fb[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) fb[nb] = Bs[buf][t][kh][nb * 32 + (lane & 31)];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        bf16x8 av;
+        __builtin_memcpy(&av, &fa[mb], 16);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          bf16x8 bv;
+          __builtin_memcpy(&bv, &fb[nb], 16);
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
+        }
+      }
+    }
+    if (more) {
+      if (SPREAD) {
+#pragma unroll
+        for (int i = (RS - 2 > 0 ? RS - 2 : 0); i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane holds rows m, columns n = 8 q + 4 (l / 32) + 0..3 of
+  // every 32 x 32 fragment (q = 0..3)
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int m = m0 + 32 * mb + (lane & 31);
+    if (m >= p.M) continue;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + nb * 32 + 8 * q + 4 * kh;
+        float v[4] = {acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
+                      acc[mb][nb][4 * q + 3]};
+        const int64_t off = (int64_t)m * p.N + n;
+        if constexpr ((EPI & EPI_BIAS) != 0) {
+          const float4 bb = *(const float4*)(p.bias + n);
+          v[0] += bb.x; v[1] += bb.y; v[2] += bb.z; v[3] += bb.w;
+        }
+        if constexpr ((EPI & EPI_ADD) != 0) {
+          const uint2 u = *(const uint2*)((const bf16_t*)p.addend + off);
+          v[0] += bf2f((bf16_t)(u.x & 0xffffu));
+          v[1] += bf2f((bf16_t)(u.x >> 16));
+          v[2] += bf2f((bf16_t)(u.y & 0xffffu));
+          v[3] += bf2f((bf16_t)(u.y >> 16));
+        }
+        if constexpr ((EPI & EPI_RELU) != 0) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+        }
+        if constexpr ((EPI & EPI_MASK) != 0) {
+          const uint2 u = *(const uint2*)((const bf16_t*)p.mask + off);
+          if (!(bf2f((bf16_t)(u.x & 0xffffu)) > 0.f)) v[0] = 0.f;
+          if (!(bf2f((bf16_t)(u.x >> 16)) > 0.f)) v[1] = 0.f;
+          if (!(bf2f((bf16_t)(u.y & 0xffffu)) > 0.f)) v[2] = 0.f;
+          if (!(bf2f((bf16_t)(u.y >> 16)) > 0.f)) v[3] = 0.f;
+        }
+        *(uint2*)((bf16_t*)p.out + off) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// host side
+// ----------------------------------------------------------------------------
+int conv2_bn(int N) { return N % 128 == 0 ? 128 : (N % 64 == 0 ? 64 : 0); }
+
+bool conv2_ok(int mode, const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  const int RS = g.R * g.S;
+  if (p.par || p.out_f32) return false;
+  if (!(RS == 9 && g.R == 3) && RS != 1) return false;
+  if (conv2_bn(p.N) == 0) return false;
+  if (mode == MODE_FWD) return g.C % C2_CK == 0 && (g.stride == 1 || g.stride == 2);
+  if (mode == MODE_DGRAD) return g.K % C2_CK == 0 && g.stride == 1;
+  return false;
+}
+
+int64_t conv2_packed_elems(const GemmParams& p, int mode) {
+  const int RS = p.g.R * p.g.S;
+  const int C = mode == MODE_FWD ? p.g.C : p.g.K;
+  return (int64_t)C * RS * p.N;
+}
+
+hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
+                               hipStream_t s) {
+  const ConvGeom& g = p.g;
+  const int RS = g.R * g.S;
+  const int C = mode == MODE_FWD ? g.C : g.K;
+  const int64_t chunks = (int64_t)(C / C2_CK) * RS * 2 * p.N;
+  int64_t blocks = (chunks + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     (const bf16_t*)W, (bf16_t*)Bp, p.N, RS, C, mode == MODE_DGRAD ? 1 : 0);
+  return hipGetLastError();
+}
+
+template <int MODE, int BN, int RS>
+static void launch_epi2(const GemmParams& p, dim3 grid, hipStream_t s) {
+  if constexpr (MODE == MODE_FWD) {
+    const bool bias = p.bias != nullptr, relu = p.relu != 0;
+    if (bias && relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p);
+    else if (bias) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS>), grid, dim3(512), 0, s, p);
+    else if (relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_RELU>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0>), grid, dim3(512), 0, s, p);
+  } else {
+    const bool add = p.addend != nullptr, mask = p.mask != nullptr;
+    if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK>), grid, dim3(512), 0, s, p);
+    else if (add) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD>), grid, dim3(512), 0, s, p);
+    else if (mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0>), grid, dim3(512), 0, s, p);
+  }
+}
+
+template <int MODE>
+static hipError_t launch_mode2(const GemmParams& p0, hipStream_t s) {
+  GemmParams p = p0;
+  const int BN = conv2_bn(p.N);
+  const int RS = p.g.R * p.g.S;
+  p.tiles_n = p.N / BN;
+  const dim3 grid((unsigned)(ceil_div(p.M, C2_BM) * p.tiles_n));
+  if (BN == 128) {
+    if (RS == 9) launch_epi2<MODE, 128, 9>(p, grid, s);
+    else launch_epi2<MODE, 128, 1>(p, grid, s);
+  } else {
+    if (RS == 9) launch_epi2<MODE, 64, 9>(p, grid, s);
+    else launch_epi2<MODE, 64, 1>(p, grid, s);
+  }
+  return hipGetLastError();
+}
+
+// p.b must point to the packed weights (launch_pack_weights of the same p)
+hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s) {
+  if (!conv2_ok(mode, p)) return hipErrorInvalidValue;
+  if (mode == MODE_FWD) return launch_mode2<MODE_FWD>(p, s);
+  return launch_mode2<MODE_DGRAD>(p, s);
+}
+
+}  // namespace hs

@@ -90,6 +90,16 @@ hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, boo
 bool igemm_fast_ok(int mode, bool bf16, const GemmParams& p, int bm, int bn);
 hipError_t launch_igemm_fast(int mode, bool bf16, const GemmParams& p, int bm, int bn, int splits,
                              hipStream_t s);
+// bf16 forward / stride-1 data gradient on the 32x32x16 MFMA (conv2.hip):
+// 8 waves, 512-row tiles, 16-channel slices with every tap per slice.
+// p.b must hold the weights packed by launch_pack_weights for the same mode
+// and shape (conv2_packed_elems bf16 elements).
+bool conv2_ok(int mode, const GemmParams& p);
+int conv2_bn(int N);
+int64_t conv2_packed_elems(const GemmParams& p, int mode);
+hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
+                               hipStream_t s);
+hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
 // NCHW fp32 [n][c][hw] -> NHWC [n][hw][cp] (activation type), channels c..cp-1 zero
 hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
                                    hipStream_t s);

@@ -239,6 +239,10 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   ws->splitk_floats = (int64_t)16 << 20;
   if (segs * max_w > ws->splitk_floats) ws->splitk_floats = segs * max_w;
   ws->splitk = (float*)a.take(ws->splitk_floats * 4);
+  if (m.dtype == HS_BF16) {
+    ws->wpack_elems = max_w;
+    ws->wpack = a.take(max_w * 2);
+  }
   ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
   return a.off;
 }
@@ -374,10 +378,25 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     bm = fbm;
     bn = fbn;
   }
-  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn && fast &&
-                     ws.probe_used * 2 + 1 < ws.probe_ev.size();
+  // bf16 stride-1 forward / data gradient with at least 128 channels per tap
+  // on the gathered side: 32x32 MFMA kernel on packed weights (measured faster
+  // there; with 64 channels or stride 2 the 128-byte K slices of the kernel
+  // above use the cache lines of the gathered operand better)
+  const int ctap = mode == MODE_FWD ? p.g.C : p.g.K;
+  const bool mfma32 = c.bf && mode != MODE_WGRAD && ws.wpack && p.g.stride == 1 && ctap >= 128 &&
+                      conv2_ok(mode, p) && conv2_packed_elems(p, mode) <= ws.wpack_elems;
+  GemmParams q = p;
+  if (mfma32) {
+    HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
+    q.b = ws.wpack;
+    bm = 512;
+    bn = conv2_bn(p.N);
+  }
+  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn &&
+                     (fast || mfma32) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
   if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
-  if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
+  if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
+  else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
   else HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
   if (probe) {
     HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
@@ -782,6 +801,10 @@ hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a,
   Workspace ws;
   ws.splitk = scratch;
   ws.splitk_floats = scratch ? scratch_floats : 0;
+  if (bf16 && mode != MODE_WGRAD && scratch) {   // scratch holds the packed weights
+    ws.wpack = scratch;
+    ws.wpack_elems = scratch_floats * 2;
+  }
   // weights are addressed at offset 0 of the given operand
   const float* th = bf16 ? nullptr : (const float*)b;
   const bf16_t* tb = bf16 ? (const bf16_t*)b : nullptr;

@@ -75,6 +75,8 @@ struct Workspace {
   float* stat_part = nullptr;  // per-channel statistics: block partials
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
+  void* wpack = nullptr;       // bf16 weights packed for the 32x32 MFMA kernel
+  int64_t wpack_elems = 0;
   int64_t* gaps = nullptr;     // device copy of the padding ranges
   // timing probe of one GEMM instantiation (mode, tile); see hs_probe_enable
   int probe_mode = -1, probe_bm = 0, probe_bn = 0;

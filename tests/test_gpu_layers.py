@@ -27,6 +27,9 @@ SHAPES = [
     (3, 32, 32, 4, 32, 3, 1, 1),      # channel-padded first layer (fp32)
     (2, 8, 8, 512, 256, 1, 2, 0),     # 1x1 strided, wide
     (3, 6, 6, 64, 128, 3, 2, 1),      # strided 3x3 on an even map with ragged tiles
+    (3, 8, 8, 128, 128, 3, 1, 1),     # 128-channel 3x3 (32x32 MFMA tiles in the step)
+    (5, 4, 4, 256, 512, 3, 1, 1),
+    (7, 1, 1, 512, 256, 1, 1, 0),     # linear with 128+ inputs
 ]
 
 
@@ -41,9 +44,21 @@ def rounded(x, dtype):
 @pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
 @pytest.mark.parametrize("mode", [0, 1, 2])
 def test_layer_gemm(mode, shape, dtype):
+    check_layer_gemm(mode, shape, dtype, packed=False)
+
+
+# bf16 forward (bf16 output) and data gradient given a scratch buffer: the
+# 32x32 MFMA kernel on packed weights wherever the shape allows it
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+@pytest.mark.parametrize("mode", [0, 1])
+def test_layer_gemm_packed(mode, shape):
+    check_layer_gemm(mode, shape, "bf16", packed=True)
+
+
+def check_layer_gemm(mode, shape, dtype, packed):
     hs = require_gpu()
     n, H, W, C, K, R, st, pad = shape
-    log("layer_gemm mode=%d shape=%s %s" % (mode, shape, dtype))
+    log("layer_gemm mode=%d shape=%s %s%s" % (mode, shape, dtype, " packed" if packed else ""))
     Ho, Wo = (H + 2 * pad - R) // st + 1, (W + 2 * pad - R) // st + 1
     rng = np.random.default_rng(sum(shape) + mode)
     x, xd = rounded(rng.standard_normal((n, H, W, C)), dtype)
@@ -51,17 +66,19 @@ def test_layer_gemm(mode, shape, dtype):
     dy, dyd = rounded(rng.standard_normal((n, Ho, Wo, K)), dtype)
     x64, w64, dy64 = x.astype(np.float64), w.astype(np.float64), dy.astype(np.float64)
     scratch = torch.empty(1 << 22, device="cuda")
+    sp, sf = (scratch.data_ptr(), scratch.numel()) if packed else (0, 0)
     if mode == 0:
         bias = rng.standard_normal(K).astype(np.float32)
-        out = torch.empty(n * Ho * Wo * K, device="cuda")
+        out = torch.empty(n * Ho * Wo * K, device="cuda",
+                          dtype=torch.int16 if packed else torch.float32)
         hs.layer_gemm(0, dtype, n, H, W, C, K, R, st, pad, xd.data_ptr(), wd.data_ptr(),
                       out.data_ptr(), torch.from_numpy(bias).cuda().data_ptr(), relu=True,
-                      out_f32=True)
+                      out_f32=not packed, scratch=sp, scratch_floats=sf)
         ref = np.maximum(L.conv_forward(x64, w64, st, pad, bias.astype(np.float64)), 0.0)
     elif mode == 1:
         out = torch.empty(n * H * W * C, device="cuda", dtype=torch.float32 if dtype == "fp32" else torch.int16)
         hs.layer_gemm(1, dtype, n, H, W, C, K, R, st, pad, dyd.data_ptr(), wd.data_ptr(),
-                      out.data_ptr())
+                      out.data_ptr(), scratch=sp, scratch_floats=sf)
         ref = L.conv_backward(x64, w64, dy64, st, pad)[0]
     else:
         out = torch.empty(K * R * R * C, device="cuda")
@@ -74,5 +91,6 @@ def test_layer_gemm(mode, shape, dtype):
         got = bf16_bits_to_f32(got.view(np.uint16))
     err = normwise(got.reshape(-1), ref.reshape(-1))
     log("  normwise err %.3e" % err)
-    tol = 1e-5 if dtype == "fp32" else (5e-3 if mode == 1 else 1e-5)
+    # bf16 outputs (data gradient, packed forward) carry the output rounding
+    tol = 1e-5 if dtype == "fp32" else (5e-3 if mode == 1 or packed else 1e-5)
     assert err <= tol
