@@ -100,6 +100,14 @@ int64_t conv2_packed_elems(const GemmParams& p, int mode);
 hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
                                hipStream_t s);
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
+// bf16 weight gradient of 3x3 stride-1 pad-1 layers (wgrad3.hip): the input
+// patch of a slice of output pixels staged once in LDS, the 9 taps as
+// shifted transposing reads.  kt_per_split counts slices (wgrad3_slices per
+// worker segment); the split table (nseg, seg_split, seg_n0) is the caller's;
+// out / split_stride as WGRAD.
+bool wgrad3_ok(const GemmParams& p);
+int wgrad3_slices(const GemmParams& p, int nimg);
+hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s);
 // NCHW fp32 [n][c][hw] -> NHWC [n][hw][cp] (activation type), channels c..cp-1 zero
 hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
                                    hipStream_t s);

@@ -385,6 +385,13 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   const int ctap = mode == MODE_FWD ? p.g.C : p.g.K;
   const bool mfma32 = c.bf && mode != MODE_WGRAD && ws.wpack && p.g.stride == 1 && ctap >= 128 &&
                       conv2_ok(mode, p) && conv2_packed_elems(p, mode) <= ws.wpack_elems;
+  // bf16 3x3 stride-1 weight gradient: patch kernel (split table in slices)
+  const bool wg3 = c.bf && mode == MODE_WGRAD && p.nseg > 0 && wgrad3_ok(p) &&
+                   p.split_stride > 0;
+  if (wg3) {
+    bm = 64;
+    bn = 64;
+  }
   GemmParams q = p;
   if (mfma32) {
     HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
@@ -393,9 +400,10 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     bn = conv2_bn(p.N);
   }
   const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn &&
-                     (fast || mfma32) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
+                     (fast || mfma32 || wg3) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
   if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
-  if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
+  if (wg3) HS_TRY(launch_wgrad3(p, c.s));
+  else if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
   else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
   else HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
   if (probe) {
@@ -490,6 +498,41 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
   p.K = c.n * L.Ho * L.Wo;
   const bool veca = (L.cout % c.V) == 0;
   const bool vecb = (L.cin % c.V) == 0;
+  const int64_t mn = (int64_t)p.M * p.N;
+  if (c.bf && cin_true == L.cin && wgrad3_ok(p)) {
+    // patch kernel: splits of 64-pixel slices, about 512 blocks in all
+    int ns[MAX_SEG], total = 0;
+    for (int i = 0; i < c.sg.count; ++i) {
+      ns[i] = wgrad3_slices(p, c.sg.n0[i + 1] - c.sg.n0[i]);
+      total += ns[i];
+    }
+    const int tiles = (L.cout / 64) * (L.cin / 64);
+    const int want = tiles >= 512 ? 1 : 512 / tiles;
+    int per = ceil_div(total, want);
+    if (per < 1) per = 1;
+    auto count = [&](int q) {
+      int t = 0;
+      for (int i = 0; i < c.sg.count; ++i) t += ns[i] > 0 ? ceil_div(ns[i], q) : 1;
+      return t;
+    };
+    while ((int64_t)count(per) * mn > c.ws.splitk_floats && per < total) per *= 2;
+    if ((int64_t)count(per) * mn > c.ws.splitk_floats) return hipErrorInvalidValue;
+    p.nseg = c.sg.count;
+    p.kt_per_split = per;
+    p.seg_split[0] = 0;
+    for (int i = 0; i < c.sg.count; ++i) {
+      p.seg_n0[i] = c.sg.n0[i];
+      p.seg_split[i + 1] = p.seg_split[i] + (ns[i] > 0 ? ceil_div(ns[i], per) : 1);
+    }
+    p.seg_n0[c.sg.count] = c.sg.n0[c.sg.count];
+    p.out = c.ws.splitk;
+    p.split_stride = mn;
+    HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, 64, 64, p.seg_split[c.sg.count], flops));
+    float* outs[MAX_SEG];
+    for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
+    return launch_splitk_reduce_seg(c.ws.splitk, mn, mn, p.seg_split, outs, c.sg.count, L.cin,
+                                    L.cin, c.s);
+  }
   const int bm = p.M <= 64 ? 64 : 128, bn = 128;
   const int tiles = ceil_div(p.M, bm) * ceil_div(p.N, bn);
   const int bke = 128 / (c.bf ? 2 : 4);
@@ -499,7 +542,6 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
     kt[i] = ceil_div((c.sg.n0[i + 1] - c.sg.n0[i]) * hw, bke);
     total_kt += kt[i];
   }
-  const int64_t mn = (int64_t)p.M * p.N;
   int want = ceil_div(1024, tiles);
   int per = ceil_div(total_kt, want > 0 ? want : 1);
   if (per < 4) per = 4;

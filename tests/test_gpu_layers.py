@@ -28,6 +28,8 @@ SHAPES = [
     (2, 8, 8, 512, 256, 1, 2, 0),     # 1x1 strided, wide
     (3, 6, 6, 64, 128, 3, 2, 1),      # strided 3x3 on an even map with ragged tiles
     (3, 8, 8, 128, 128, 3, 1, 1),     # 128-channel 3x3 (32x32 MFMA tiles in the step)
+    (2, 16, 16, 128, 128, 3, 1, 1),
+    (3, 16, 16, 64, 128, 3, 1, 1),
     (5, 4, 4, 256, 512, 3, 1, 1),
     (7, 1, 1, 512, 256, 1, 1, 0),     # linear with 128+ inputs
 ]
