@@ -34,12 +34,22 @@ METRIC = "train samples/s (fwd+bwd+wavg+SGD), CIFAR-shape ResNet-18; MFMA/HBM % 
 PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}   # MI355X dense MFMA peaks
 HBM_PEAK_GBS = 8000.0
 
-# GEMM instantiation probed for the roofline (mode, bm, bn), per workload: the
-# fast implicit-GEMM kernel that takes the largest share of the step's kernel
-# time (mode 0 forward, 1 data gradient, 2 weight gradient).
-PROBE = {"resnet18_bf16": (2, 128, 128), "resnet18_fp32": (2, 128, 128),
-         "vgg16_bf16": (2, 128, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
+# GEMM kernel probed for the roofline (mode, bm, bn), per workload: the
+# implicit-GEMM kernel that takes the largest share of the step's time (mode 0
+# forward, 1 data gradient, 2 weight gradient; bm = 512 selects the 32x32x16
+# MFMA forward / data-gradient kernel with 512-row tiles, bm = bn = 64 in mode
+# 2 the patch weight-gradient kernel).
+PROBE = {"resnet18_bf16": (0, 512, 128), "resnet18_fp32": (2, 128, 128),
+         "vgg16_bf16": (0, 512, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
 MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
+
+
+def kernel_name(mode, bm, bn, dtype):
+    if bm == 512:
+        return "conv2_kernel<%s, %dx%d tile, 32x32x16 MFMA, %s>" % (MODE_NAME[mode], bm, bn, dtype)
+    if mode == 2 and bm == 64 and bn == 64 and dtype == "bf16":
+        return "wgrad3_kernel<3x3 weight gradient, 64x64x9 tile, %s>" % dtype
+    return "igemm_fast_kernel<%s, mode %d (%s), %dx%d tile>" % (dtype, mode, MODE_NAME[mode], bm, bn)
 
 
 def parse():
@@ -144,8 +154,7 @@ def main():
                    "parallelism": "simulated-dp%d-1gpu" % wl.workers,
                    "execution": "one stream per worker, measured clock" if args.streams
                    else "all workers in one pass per layer, model clock"},
-        "roofline": {"bound": "mfma", "kernel": "igemm_fast_kernel<%s, mode %d (%s), %dx%d tile>"
-                     % (wl.dtype, mode, MODE_NAME[mode], bm, bn),
+        "roofline": {"bound": "mfma", "kernel": kernel_name(mode, bm, bn, wl.dtype),
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None,
                      "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),

@@ -83,7 +83,16 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   constexpr int NB = BN / 32;
   constexpr int SEG = RS * 2 * BN;                 // 16-byte chunks of B per slice
   constexpr int BREG = (SEG + 511) / 512;          // per thread
-  __shared__ uint4 Bs[2][RS][2][BN];
+  // epilogues that read the addend / mask stage each wave's 64 x 32 fp32
+  // sub-tile in LDS (row stride 36 floats: conflict-free) and handle it row by
+  // row: 4 lanes per row, 8 contiguous channels each
+  constexpr bool STAGE_EPI = (EPI & (EPI_ADD | EPI_MASK)) != 0;
+  constexpr int EROW = 36;
+  constexpr int BS_BYTES = 2 * RS * 2 * BN * 16;
+  constexpr int EPI_BYTES = STAGE_EPI ? C2_WAVES * 64 * EROW * 4 : 0;
+  __shared__ __attribute__((aligned(16))) char smem[BS_BYTES > EPI_BYTES ? BS_BYTES : EPI_BYTES];
+  typedef uint4 BsT[RS][2][BN];
+  BsT* Bs = (BsT*)smem;
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -228,6 +237,55 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
       }
     }
     __syncthreads();
+  }
+
+  if constexpr (STAGE_EPI) {
+    // the loop ended with a barrier: B is no longer read
+    float* E = (float*)smem + wave * 64 * EROW;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *(float4*)(E + (32 * mb + (lane & 31)) * EROW + 8 * q + 4 * kh) =
+              make_float4(acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
+                          acc[mb][nb][4 * q + 3]);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+        const int m = m0 + row;
+        if (m < p.M) {
+          const float4 lo = *(const float4*)(E + row * EROW + c8);
+          const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+          float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          const int64_t off = (int64_t)m * p.N + n0 + nb * 32 + c8;
+          if constexpr ((EPI & EPI_ADD) != 0) {
+            const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
+              v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
+            }
+          }
+          if constexpr ((EPI & EPI_MASK) != 0) {
+            const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
+              if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
+            }
+          }
+          *(uint4*)((bf16_t*)p.out + off) =
+              make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+        }
+      }
+      __syncthreads();
+    }
+    return;
   }
 
   // ---- epilogue: lane holds rows m, columns n = 8 q + 4 (l / 32) + 0..3 of

@@ -427,6 +427,72 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
     __syncthreads();
   }
 
+  // ---- data-gradient epilogues that read the addend / mask: each wave
+  // stages its WTM x CW fp32 sub-tile (CW = WTN, or WTN / 2 when LDS is
+  // short; row stride CW + 4 floats, conflict-free) and handles it row by
+  // row, 8 channels per lane, so the loads and stores cover contiguous rows
+  constexpr bool STAGE_EPI = MODE == MODE_DGRAD && EB == 2 && (EPI & (EPI_ADD | EPI_MASK)) != 0;
+  if constexpr (STAGE_EPI) {
+    constexpr int SMEM = 2 * (BM + BN) * 128;
+    constexpr int CW = 4 * WTM * (WTN + 4) * 4 <= SMEM ? WTN : WTN / 2;
+    constexpr int EROW = CW + 4, LPR = CW / 8, RPP = 64 / LPR;
+    static_assert(4 * WTM * EROW * 4 <= SMEM, "epilogue staging exceeds LDS");
+    float* E = (float*)smem + wave * WTM * EROW;
+#pragma unroll
+    for (int c0 = 0; c0 < WTN; c0 += CW) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = 16 * j + (lane >> 4) * 4 - c0;
+          if (col >= 0 && col < CW)
+            *(float4*)(E + (16 * i + (lane & 15)) * EROW + col) =
+                make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        }
+      __syncthreads();
+#pragma unroll
+      for (int r0 = 0; r0 < WTM; r0 += RPP) {
+        const int row = r0 + lane / LPR, c8 = 8 * (lane % LPR);
+        const int m = m0 + wm * WTM + row;
+        const int n = n0 + wn * WTN + c0 + c8;
+        if (m < p.M && n < p.N) {
+          int64_t orow = m;
+          if (par) {
+            const int b = (int)fdiv(m, p.HWh), rem = m - b * p.Hh * p.Wh;
+            const int h2 = (int)fdiv(rem, p.Wh_), w2 = rem - h2 * p.Wh;
+            orow = ((int64_t)b * g.H + 2 * h2 + ph) * g.W + 2 * w2 + pw;
+          }
+          const int64_t off = orow * p.N + n;
+          const float4 lo = *(const float4*)(E + row * EROW + c8);
+          const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+          float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          if constexpr ((EPI & EPI_ADD) != 0) {
+            const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
+              v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
+            }
+          }
+          if constexpr ((EPI & EPI_MASK) != 0) {
+            const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
+              if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
+            }
+          }
+          *(uint4*)((bf16_t*)p.out + off) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+        }
+      }
+      __syncthreads();
+    }
+    return;
+  }
+
   // ---- epilogue: lane holds C[m][n .. n+3] of every 16 x 16 fragment
 #pragma unroll
   for (int i = 0; i < FM; ++i) {

@@ -172,8 +172,6 @@ hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const
                                const float* gamma, float* const* sum_dy, float* const* sum_dyx,
                                const Segs& sg, int64_t rows_per_sample, int C, void* dz,
                                hipStream_t s);
-hipError_t launch_relu_mask8(bool bf16, const void* dy, const void* act, int64_t count, void* out,
-                             hipStream_t s);
 // zero a list of [begin, end) element ranges of each of nbuf float buffers
 hipError_t launch_zero_ranges(float* const* bufs, int nbuf, const int64_t* ranges, int count,
                               hipStream_t s);

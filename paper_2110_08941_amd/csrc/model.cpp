@@ -738,20 +738,22 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   HS_TRY(conv_wgrad(c, m.fc2, dz, F));
   HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
-  HS_TRY(launch_gap_bwd(c.bf, G[0], nullptr, n, 16, 512, G[1], c.s));
-  int gi = 1;  // buffer holding the gradient of the current block output
+  // gradient of the last block's output, masked by its ReLU ([A > 0])
+  HS_TRY(launch_gap_bwd(c.bf, G[0], cur, n, 16, 512, G[1], c.s));
+  // G[gi]: gradient of the current block's output, already multiplied by the
+  // ReLU mask of that output: the data gradient that produces it applies
+  // [input of the next block > 0] in its epilogue
+  int gi = 1;
   for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
     const BlockL& b = m.blocks[bi];
     const int base = 3 + 5 * bi;
-    void *Z1 = S[base], *Hh = S[base + 1], *Z2 = S[base + 2], *ZP = S[base + 3],
-         *A = S[base + 4];
-    const void* in = bi == 0 ? S[2] : S[3 + 5 * (bi - 1) + 4];
+    void *Z1 = S[base], *Hh = S[base + 1], *Z2 = S[base + 2], *ZP = S[base + 3];
+    const void* in = bi == 0 ? S[2] : S[3 + 5 * (bi - 1) + 4];   // post-ReLU input
     int fr[4], k = 0;
     for (int i = 0; i < 5; ++i)
       if (i != gi) fr[k++] = i;
-    void *dA = G[gi], *P1 = G[fr[0]], *P2 = G[fr[1]], *P3 = G[fr[2]], *P4 = G[fr[3]];
+    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]];
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
-    HS_TRY(launch_relu_mask8(c.bf, dA, A, (int64_t)n * rps * b.c2.cout, P1, c.s));   // dPre
     HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
     HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, nullptr));                  // dH
@@ -760,17 +762,17 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     if (b.proj) {
       HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
       HS_TRY(conv_wgrad(c, b.cp, P3, in));
-      HS_TRY(conv_dgrad(c, b.cp, P3, dA, nullptr, nullptr));                // shortcut grad
-      HS_TRY(conv_dgrad(c, b.c1, P2, P4, dA, nullptr));                     // dIn
-      gi = fr[3];
-    } else {
-      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, nullptr));                     // dIn
+      HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));                // shortcut grad
+      HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in));                          // dIn * [in > 0]
       gi = fr[2];
+    } else {
+      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in));                          // dIn * [in > 0]
+      gi = fr[1];
     }
   }
-  // stem
+  // stem (its ReLU mask is already applied)
   void* dZs = G[gi == 0 ? 1 : 0];
-  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], S[2], S[1], 1024, dZs));
+  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], nullptr, S[1], 1024, dZs));
   return stem_wgrad(c, m.stem, dZs, S[0]);
 }
 

@@ -413,13 +413,6 @@ __device__ inline void store_vec8<float>(float* p, int64_t i, const float* v) {
   *(float4*)(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
-static inline int vgrid(int64_t groups) {
-  int64_t b = (groups + 255) / 256;
-  if (b > 16384) b = 16384;
-  if (b < 1) b = 1;
-  return (int)b;
-}
-
 // Row-major elementwise work over [rows][C] with C % 8 == 0: every block
 // owns a row range of one segment; a thread owns one group of 8 channels (its
 // per-channel coefficients stay in registers) and walks rows rl, rl + RPB, ...
@@ -609,36 +602,6 @@ hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const
   const dim3 grid(a.sr.blk[sg.count]);
   if (bf16) hipLaunchKernelGGL(bn_backward8_kernel<bf16_t>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(bn_backward8_kernel<float>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-// out = dy * [act > 0]
-template <typename T>
-__global__ __launch_bounds__(256) void relu_mask8_kernel(const T* __restrict__ dy,
-                                                         const T* __restrict__ act, int64_t groups,
-                                                         T* __restrict__ out) {
-  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
-       q += (int64_t)gridDim.x * blockDim.x) {
-    float d[8], m[8];
-    load_vec<T, 8>(dy, q * 8, d);
-    load_vec<T, 8>(act, q * 8, m);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (!(m[j] > 0.f)) d[j] = 0.f;
-    store_vec8<T>(out, q * 8, d);
-  }
-}
-
-hipError_t launch_relu_mask8(bool bf16, const void* dy, const void* act, int64_t count, void* out,
-                             hipStream_t s) {
-  if (count % 8) return hipErrorInvalidValue;
-  const int64_t groups = count / 8;
-  if (bf16)
-    hipLaunchKernelGGL(relu_mask8_kernel<bf16_t>, dim3(vgrid(groups)), dim3(256), 0, s,
-                       (const bf16_t*)dy, (const bf16_t*)act, groups, (bf16_t*)out);
-  else
-    hipLaunchKernelGGL(relu_mask8_kernel<float>, dim3(vgrid(groups)), dim3(256), 0, s,
-                       (const float*)dy, (const float*)act, groups, (float*)out);
   return hipGetLastError();
 }
 
