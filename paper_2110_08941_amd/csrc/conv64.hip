@@ -1,0 +1,230 @@
+// Forward and data gradient of 64 -> 64 channel 3x3, stride-1, pad-1
+// convolutions on 32-wide maps in bf16 (the widest layers of the CIFAR
+// networks), 32x32x16 MFMA.
+//
+// A persistent block keeps the whole packed weight tensor in LDS (64 x 576
+// bf16, 72 KB, [kq][tap][kh][n][8] as packed for the 32x32 kernel) and walks
+// output tiles of 16 image rows x 32 columns (512 pixels).  Per tile it stages
+// the input patch those pixels read -- 18 rows x 34 columns with the zero
+// border, 64 channels, one 128-byte row per slot -- once, and applies the 9
+// taps as shifted reads of it: the operand traffic from L2 drops about 9x
+// against gathering every tap from global memory.  The next tile's patch is
+// loaded into registers while the current tile computes.
+//
+// Wave w owns output rows 2w and 2w + 1 of the tile (two 32-pixel MFMA row
+// blocks) and all 64 output channels.  Patch slots are XOR-swizzled by 16-byte
+// chunk, chunk ^ ((slot >> 1) & 7), so 16 lanes reading 16 consecutive slots
+// hit distinct banks.  The data gradient reads dy with the taps mirrored
+// (slot offset 2 - r, 2 - s) and the transposed weights.  The epilogue stages
+// each wave's 64 x 32 accumulator half-tiles in the patch area and writes
+// whole rows.
+#include "kernels.h"
+
+namespace hs {
+
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16 };
+
+constexpr int P_W = 32;                     // map width
+constexpr int P_ROWS = 16;                  // output rows per tile
+constexpr int P_FW = P_W + 2, P_FR = P_ROWS + 2;
+constexpr int P_SLOTS = P_FW * P_FR;        // 612
+constexpr int P_CH = P_SLOTS * 8;           // 16-byte chunks per patch
+constexpr int P_IT = (P_CH + 511) / 512;    // per thread
+constexpr int W_CH = 4 * 9 * 2 * 64;        // 16-byte chunks of packed weights
+constexpr int EROW = 36;                    // epilogue staging row stride (floats)
+
+__device__ inline int pslot_off(int slot, int chunk) {
+  return slot * 128 + ((chunk ^ ((slot >> 1) & 7)) << 4);
+}
+
+__device__ inline uint32_t pack2(float a, float b) {
+  f32x2 v = {a, b};
+  bf16x2 h = __builtin_convertvector(v, bf16x2);
+  uint32_t u;
+  __builtin_memcpy(&u, &h, 4);
+  return u;
+}
+
+}  // namespace
+
+template <int MODE, int EPI>
+__global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
+  __shared__ __attribute__((aligned(16))) char smem[W_CH * 16 + P_SLOTS * 128];
+  uint4* Wl = (uint4*)smem;
+  char* Pl = smem + W_CH * 16;
+  const ConvGeom& g = p.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kh = lane >> 5, x = lane & 31;
+  const int H = g.H;                        // map height (output = input size)
+  const int tiles_per_img = H / P_ROWS;
+  const bf16_t* A = (const bf16_t*)p.a;     // x (forward) or dy (data gradient), 64 channels
+
+  for (int q = tid; q < W_CH; q += 512) Wl[q] = ((const uint4*)p.b)[q];
+
+  // patch of tile t: slot (ry, cx) holds pixel (y0 - 1 + ry, cx - 1) of image b
+  auto load_patch = [&](int t, uint4 (&r)[P_IT]) {
+    const int b = t / tiles_per_img, y0 = (t - b * tiles_per_img) * P_ROWS;
+#pragma unroll
+    for (int i = 0; i < P_IT; ++i) {
+      const int q = tid + 512 * i;
+      r[i] = make_uint4(0, 0, 0, 0);
+      if (q < P_CH) {
+        const int slot = q >> 3, ch = q & 7;
+        const int ry = slot / P_FW, cx = slot - ry * P_FW;
+        const int y = y0 - 1 + ry, xx = cx - 1;
+        if ((unsigned)y < (unsigned)H && (unsigned)xx < (unsigned)P_W)
+          r[i] = *(const uint4*)(A + (((int64_t)b * H + y) * P_W + xx) * 64 + ch * 8);
+      }
+    }
+  };
+  auto store_patch = [&](const uint4 (&r)[P_IT]) {
+#pragma unroll
+    for (int i = 0; i < P_IT; ++i) {
+      const int q = tid + 512 * i;
+      if (q < P_CH) *(uint4*)(Pl + pslot_off(q >> 3, q & 7)) = r[i];
+    }
+  };
+
+  int t = blockIdx.x;
+  uint4 pre[P_IT];
+  if (t < ntiles) load_patch(t, pre);
+  for (; t < ntiles; t += gridDim.x) {
+    store_patch(pre);
+    __syncthreads();
+    if (t + gridDim.x < ntiles) load_patch(t + gridDim.x, pre);
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = (f32x16){};
+    // taps: forward reads slot (row + r, x + s); data gradient (row + 2 - r, x + 2 - s)
+#pragma unroll 1
+    for (int tap = 0; tap < 9; ++tap) {
+      const int r = tap / 3, s = tap - 3 * (tap / 3);
+      const int dr = MODE == MODE_FWD ? r : 2 - r, ds = MODE == MODE_FWD ? s : 2 - s;
+      const int slot0 = (2 * wave + dr) * P_FW + x + ds;
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq) {
+        uint4 fa[2], fb[2];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+          fa[mb] = *(const uint4*)(Pl + pslot_off(slot0 + mb * P_FW, 2 * kq + kh));
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) fb[nb] = Wl[((kq * 9 + tap) * 2 + kh) * 64 + nb * 32 + x];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+          bf16x8 av;
+          __builtin_memcpy(&av, &fa[mb], 16);
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) {
+            bf16x8 bv;
+            __builtin_memcpy(&bv, &fb[nb], 16);
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();   // patch area free: stage the epilogue there
+
+    // ---- epilogue, one 32-channel half at a time: lane holds pixel x of
+    // output row 2 wave + mb and channels 8 q + 4 kh + 0..3 of half nb
+    const int b = t / tiles_per_img, y0 = (t - b * tiles_per_img) * P_ROWS;
+    float* E = (float*)Pl + wave * 64 * EROW;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          *(float4*)(E + (32 * mb + x) * EROW + 8 * q4 + 4 * kh) =
+              make_float4(acc[mb][nb][4 * q4], acc[mb][nb][4 * q4 + 1], acc[mb][nb][4 * q4 + 2],
+                          acc[mb][nb][4 * q4 + 3]);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);   // row: mb * 32 + pixel
+        const int y = y0 + 2 * wave + (row >> 5), xx = row & 31;
+        const int64_t off = (((int64_t)b * H + y) * P_W + xx) * 64 + nb * 32 + c8;
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if constexpr ((EPI & EPI_BIAS) != 0) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += p.bias[nb * 32 + c8 + e];
+        }
+        if constexpr ((EPI & EPI_ADD) != 0) {
+          const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
+          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
+            v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
+          }
+        }
+        if constexpr ((EPI & EPI_RELU) != 0) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+        }
+        if constexpr ((EPI & EPI_MASK) != 0) {
+          const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
+          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
+            if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
+          }
+        }
+        *(uint4*)((bf16_t*)p.out + off) =
+            make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+      }
+      __syncthreads();
+    }
+  }
+}
+
+bool conv64_ok(int mode, const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  if (p.par || p.out_f32 || (mode != MODE_FWD && mode != MODE_DGRAD)) return false;
+  return g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 && g.C == 64 && g.K == 64 &&
+         g.W == P_W && g.H % P_ROWS == 0 && g.H == g.Ho && g.W == g.Wo;
+}
+
+template <int MODE>
+static void launch64(const GemmParams& p, int ntiles, dim3 grid, hipStream_t s) {
+  if constexpr (MODE == MODE_FWD) {
+    const bool bias = p.bias != nullptr, relu = p.relu != 0;
+    if (bias && relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
+    else if (bias) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS>), grid, dim3(512), 0, s, p, ntiles);
+    else if (relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
+    else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);
+  } else {
+    const bool add = p.addend != nullptr, mask = p.mask != nullptr;
+    if (add && mask) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD | EPI_MASK>), grid, dim3(512), 0, s, p, ntiles);
+    else if (add) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD>), grid, dim3(512), 0, s, p, ntiles);
+    else if (mask) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_MASK>), grid, dim3(512), 0, s, p, ntiles);
+    else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);
+  }
+}
+
+// p.b: packed weights (launch_pack_weights for the same mode); one block per CU
+hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s) {
+  if (!conv64_ok(mode, p)) return hipErrorInvalidValue;
+  const int ntiles = p.g.n * (p.g.H / P_ROWS);
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess)
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const dim3 grid((unsigned)(ntiles < cus ? ntiles : cus));
+  if (mode == MODE_FWD) launch64<MODE_FWD>(p, ntiles, grid, s);
+  else launch64<MODE_DGRAD>(p, ntiles, grid, s);
+  return hipGetLastError();
+}
+
+}  // namespace hs

@@ -100,6 +100,11 @@ int64_t conv2_packed_elems(const GemmParams& p, int mode);
 hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
                                hipStream_t s);
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
+// bf16 forward / data gradient of 64 -> 64 channel 3x3 stride-1 layers on
+// 32-wide maps (conv64.hip): packed weights resident in LDS, input patch of 16
+// output rows staged once per tile, taps as shifted LDS reads
+bool conv64_ok(int mode, const GemmParams& p);
+hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s);
 // bf16 weight gradient of 3x3 stride-1 pad-1 layers (wgrad3.hip): the input
 // patch of a slice of output pixels staged once in LDS, the 9 taps as
 // shifted transposing reads.  kt_per_split counts slices (wgrad3_slices per

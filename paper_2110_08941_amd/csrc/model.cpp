@@ -392,17 +392,21 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     bm = 64;
     bn = 64;
   }
+  // 64 -> 64 channel 3x3 stride-1 on 32-wide maps: LDS patch kernel
+  const bool w64 = c.bf && mode != MODE_WGRAD && ws.wpack && conv64_ok(mode, p) &&
+                   conv2_ok(mode, p) && conv2_packed_elems(p, mode) <= ws.wpack_elems;
   GemmParams q = p;
-  if (mfma32) {
+  if (mfma32 || w64) {
     HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
     q.b = ws.wpack;
-    bm = 512;
-    bn = conv2_bn(p.N);
+    bm = w64 ? 64 : 512;
+    bn = w64 ? 64 : conv2_bn(p.N);
   }
   const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn &&
-                     (fast || mfma32 || wg3) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
+                     (fast || mfma32 || wg3 || w64) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
   if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
   if (wg3) HS_TRY(launch_wgrad3(p, c.s));
+  else if (w64) HS_TRY(launch_conv64(mode, q, c.s));
   else if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
   else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
   else HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
