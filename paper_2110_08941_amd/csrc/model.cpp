@@ -760,8 +760,8 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
-    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, nullptr));                  // dH
-    HS_TRY(bn_bwd(c, b.b1, P3, Hh, Z1, rps, P2));                           // dZ1
+    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, Hh));                       // dH * [H > 0]
+    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rps, P2));                      // dZ1
     HS_TRY(conv_wgrad(c, b.c1, P2, in));
     if (b.proj) {
       HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
