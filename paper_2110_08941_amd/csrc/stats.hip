@@ -103,30 +103,80 @@ struct FinishArgs {
   float* out1[MAX_SEG];
 };
 
-template <typename T, int V>
-__device__ inline void load_vec(const T* p, int64_t i, float* v);
-template <>
-__device__ inline void load_vec<bf16_t, 8>(const bf16_t* p, int64_t i, float* v) {
-  uint4 u = *(const uint4*)(p + i);
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    v[2 * k] = bf2f((bf16_t)(w[k] & 0xffffu));
-    v[2 * k + 1] = bf2f((bf16_t)(w[k] >> 16));
+// V consecutive channels of one row kept in their storage format until they
+// are used (a bf16 row of 8 channels is 4 registers, not 8).  NT: the load
+// bypasses the caches' retention (tensors far larger than the L2 and the
+// last-level cache are read once).
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <bool NT>
+__device__ inline uint4 ld16(const void* p) {
+  if (NT) {
+    const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  return *(const uint4*)p;
+}
+template <bool NT>
+__device__ inline void st16(void* p, const uint4& u) {
+  if (NT) {
+    const u32x4_t v = {u.x, u.y, u.z, u.w};
+    __builtin_nontemporal_store(v, (u32x4_t*)p);
+  } else {
+    *(uint4*)p = u;
   }
 }
-template <>
-__device__ inline void load_vec<float, 8>(const float* p, int64_t i, float* v) {
-  float4 a = *(const float4*)(p + i), b = *(const float4*)(p + i + 4);
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+__device__ inline float f_of(uint32_t u) {
+  float f;
+  __builtin_memcpy(&f, &u, 4);
+  return f;
 }
-template <>
-__device__ inline void load_vec<bf16_t, 1>(const bf16_t* p, int64_t i, float* v) { v[0] = bf2f(p[i]); }
-template <>
-__device__ inline void load_vec<float, 1>(const float* p, int64_t i, float* v) { v[0] = p[i]; }
 
-template <typename T, int V, int KIND>
+template <typename T, int V> struct Raw;
+template <> struct Raw<bf16_t, 8> {
+  uint4 u;
+  template <bool NT> __device__ void load(const bf16_t* p, int64_t i) { u = ld16<NT>(p + i); }
+  __device__ float operator[](int j) const {
+    const uint32_t w = j < 2 ? u.x : j < 4 ? u.y : j < 6 ? u.z : u.w;
+    return f_of((j & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+template <> struct Raw<float, 8> {
+  uint4 a, b;
+  template <bool NT> __device__ void load(const float* p, int64_t i) {
+    a = ld16<NT>(p + i);
+    b = ld16<NT>(p + i + 4);
+  }
+  __device__ float operator[](int j) const {
+    const uint4& h = j < 4 ? a : b;
+    const int k = j & 3;
+    return f_of(k == 0 ? h.x : k == 1 ? h.y : k == 2 ? h.z : h.w);
+  }
+};
+template <> struct Raw<bf16_t, 1> {
+  bf16_t v;
+  template <bool NT> __device__ void load(const bf16_t* p, int64_t i) { v = p[i]; }
+  __device__ float operator[](int) const { return bf2f(v); }
+};
+template <> struct Raw<float, 1> {
+  float v;
+  template <bool NT> __device__ void load(const float* p, int64_t i) { v = p[i]; }
+  __device__ float operator[](int) const { return v; }
+};
+
+template <typename T, int V>
+__device__ inline void load_vec(const T* p, int64_t i, float* v) {
+  Raw<T, V> r;
+  r.template load<false>(p, i);
+#pragma unroll
+  for (int j = 0; j < V; ++j) v[j] = r[j];
+}
+
+// tensors of at least this many bytes are streamed with nontemporal accesses
+constexpr int64_t NT_BYTES = 100ll << 20;
+
+template <typename T, int V, int KIND, bool NT>
 __global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
   __shared__ float red[2][256 * 8];
   const int C = a.C;
@@ -138,11 +188,14 @@ __global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
   int s;
   int64_t r0, r1, seg0, seg1;
   block_rows(a.sr, blockIdx.x, s, r0, r1, seg0, seg1);
+  const T* __restrict__ x = (const T*)a.x;
+  const T* __restrict__ dy = (const T*)a.dy;
+  const T* __restrict__ act = (const T*)a.act;
   float s0[V], s1[V], k[V], mu[V], rs[V];
 #pragma unroll
   for (int j = 0; j < V; ++j) s0[j] = s1[j] = 0.f;
   if (rl < RPB) {
-    if (KIND == 0) load_vec<T, V>((const T*)a.x, seg0 * C + c0, k);   // shift: segment row 0
+    if (KIND == 0) load_vec<T, V>(x, seg0 * C + c0, k);   // shift: segment row 0
     if (KIND == 1) {
 #pragma unroll
       for (int j = 0; j < V; ++j) {
@@ -150,72 +203,39 @@ __global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
         rs[j] = a.rstd[(int64_t)s * a.mstride + c0 + j];
       }
     }
-    int64_t r = r0 + rl;
-    // four rows per iteration: four independent 16-byte loads in flight
-    for (; r + 3 * RPB < r1; r += 4 * RPB) {
-      float v[4][V];
-      if (KIND == 0) {
+    // four rows per step: up to twelve independent loads in flight; the last
+    // step masks the rows past the range
+    for (int64_t r = r0 + rl; r < r1; r += 4 * RPB) {
+      Raw<T, V> v[4], m[4], z[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) load_vec<T, V>((const T*)a.x, (r + u * RPB) * C + c0, v[u]);
+      for (int u = 0; u < 4; ++u) {
+        const int64_t rr = r + u * RPB;
+        if (rr < r1) {
+          const int64_t i = rr * C + c0;
+          if (KIND == 0) {
+            v[u].template load<NT>(x, i);
+          } else {
+            v[u].template load<NT>(dy, i);
+            if (act) m[u].template load<NT>(act, i);
+            if (KIND == 1) z[u].template load<NT>(x, i);
+          }
+        }
+      }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 4; ++u) {
+        if (r + u * RPB >= r1) continue;
 #pragma unroll
-          for (int j = 0; j < V; ++j) {
+        for (int j = 0; j < V; ++j) {
+          if (KIND == 0) {
             const float d = v[u][j] - k[j];
             s0[j] += d;
             s1[j] += d * d;
-          }
-      } else {
-        float m[4][V], z[4][V];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int64_t i = (r + u * RPB) * C + c0;
-          load_vec<T, V>((const T*)a.dy, i, v[u]);
-          if (a.act) load_vec<T, V>((const T*)a.act, i, m[u]);
-          if (KIND == 1) load_vec<T, V>((const T*)a.x, i, z[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int j = 0; j < V; ++j) {
+          } else {
             float d = v[u][j];
-            if (a.act && !(m[u][j] > 0.f)) d = 0.f;
+            if (act && !(m[u][j] > 0.f)) d = 0.f;
             s0[j] += d;
             if (KIND == 1) s1[j] += d * ((z[u][j] - mu[j]) * rs[j]);
           }
-      }
-    }
-    for (; r < r1; r += RPB) {
-      const int64_t i = r * C + c0;
-      float v[V];
-      if (KIND == 0) {
-        load_vec<T, V>((const T*)a.x, i, v);
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const float d = v[j] - k[j];
-          s0[j] += d;
-          s1[j] += d * d;
-        }
-      } else {
-        load_vec<T, V>((const T*)a.dy, i, v);
-        if (a.act) {
-          float m[V];
-          load_vec<T, V>((const T*)a.act, i, m);
-#pragma unroll
-          for (int j = 0; j < V; ++j)
-            if (!(m[j] > 0.f)) v[j] = 0.f;
-        }
-        if (KIND == 1) {
-          float z[V];
-          load_vec<T, V>((const T*)a.x, i, z);
-#pragma unroll
-          for (int j = 0; j < V; ++j) {
-            s0[j] += v[j];
-            s1[j] += v[j] * ((z[j] - mu[j]) * rs[j]);
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < V; ++j) s0[j] += v[j];
         }
       }
     }
@@ -363,9 +383,17 @@ hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy,
   }
   const dim3 grid(a.sr.blk[sg.count]), block(256);
   const dim3 fgrid((C + 7) / 8, sg.count);
+  const int64_t rows = (int64_t)(sg.n0[sg.count] - sg.n0[0]) * rows_per_sample;
+  // the sums over two or three tensors gain from streaming loads only when
+  // they are far beyond the last-level cache; the single-tensor forward sums
+  // do not
+  const bool nt = kind != 0 && rows * C * (bf16 ? 2 : 4) >= 2 * NT_BYTES;
 #define HS_STAT(T, VV, K)                                                             \
   do {                                                                                \
-    hipLaunchKernelGGL((chan_partial_kernel<T, VV, K>), grid, block, 0, s, a);        \
+    if (nt && VV == 8)                                                                \
+      hipLaunchKernelGGL((chan_partial_kernel<T, VV, K, true>), grid, block, 0, s, a); \
+    else                                                                              \
+      hipLaunchKernelGGL((chan_partial_kernel<T, VV, K, false>), grid, block, 0, s, a); \
     hipLaunchKernelGGL((chan_finish_kernel<T, K>), fgrid, block, 0, s, f);            \
   } while (0)
   if (bf16) {
@@ -396,21 +424,40 @@ hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy,
 // ----------------------------------------------------------------------------
 // vectorised elementwise batch-norm kernels (8 channels per thread step)
 // ----------------------------------------------------------------------------
-template <typename T>
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16, round to nearest even (hardware conversion)
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  const bf16x2_t h = __builtin_convertvector(v, bf16x2_t);
+  uint32_t u;
+  __builtin_memcpy(&u, &h, 4);
+  return u;
+}
+
+template <typename T, bool NT>
 __device__ inline void store_vec8(T* p, int64_t i, const float* v);
 template <>
-__device__ inline void store_vec8<bf16_t>(bf16_t* p, int64_t i, const float* v) {
-  uint4 u;
-  u.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  u.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-  u.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-  u.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-  *(uint4*)(p + i) = u;
+__device__ inline void store_vec8<bf16_t, false>(bf16_t* p, int64_t i, const float* v) {
+  st16<false>(p + i, make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])));
 }
 template <>
-__device__ inline void store_vec8<float>(float* p, int64_t i, const float* v) {
+__device__ inline void store_vec8<bf16_t, true>(bf16_t* p, int64_t i, const float* v) {
+  st16<true>(p + i, make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])));
+}
+template <>
+__device__ inline void store_vec8<float, false>(float* p, int64_t i, const float* v) {
   *(float4*)(p + i) = make_float4(v[0], v[1], v[2], v[3]);
   *(float4*)(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <>
+__device__ inline void store_vec8<float, true>(float* p, int64_t i, const float* v) {
+  const f32x4_t lo = {v[0], v[1], v[2], v[3]}, hi = {v[4], v[5], v[6], v[7]};
+  __builtin_nontemporal_store(lo, (f32x4_t*)(p + i));
+  __builtin_nontemporal_store(hi, (f32x4_t*)(p + i + 4));
 }
 
 // Row-major elementwise work over [rows][C] with C % 8 == 0: every block
@@ -460,7 +507,7 @@ struct BnArgs {
 };
 
 // y = relu?(gamma * (z - mean) * rstd + beta + res)
-template <typename T>
+template <typename T, bool NT>
 __global__ __launch_bounds__(256) void bn_apply8_kernel(BnArgs a) {
   const int C = a.C;
   const RowSplit w = row_split(a.sr, C);
@@ -478,27 +525,27 @@ __global__ __launch_bounds__(256) void bn_apply8_kernel(BnArgs a) {
     sb[j] = a.beta[c] - mean[c] * sa[j];
   }
   for (int64_t r = w.r0 + w.rl; r < w.r1; r += 4 * w.RPB) {
-    float v[4][8], q[4][8];
+    Raw<T, 8> v[4], q[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int64_t rr = r + u * w.RPB;
       if (rr < w.r1) {
-        load_vec<T, 8>(z, rr * C + w.c0, v[u]);
-        if (res) load_vec<T, 8>(res, rr * C + w.c0, q[u]);
+        v[u].template load<NT>(z, rr * C + w.c0);
+        if (res) q[u].template load<NT>(res, rr * C + w.c0);
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int64_t rr = r + u * w.RPB;
       if (rr >= w.r1) continue;
+      float o[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        float o = sa[j] * v[u][j] + sb[j];
-        if (res) o += q[u][j];
-        if (a.relu) o = o > 0.f ? o : 0.f;
-        v[u][j] = o;
+        o[j] = sa[j] * v[u][j] + sb[j];
+        if (res) o[j] += q[u][j];
+        if (a.relu) o[j] = o[j] > 0.f ? o[j] : 0.f;
       }
-      store_vec8<T>(y, rr * C + w.c0, v[u]);
+      store_vec8<T, NT>(y, rr * C + w.c0, o);
     }
   }
 }
@@ -521,13 +568,19 @@ hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const f
   a.out = y;
   a.sr = row_segs(sg, rows_per_sample, C);
   const dim3 grid(a.sr.blk[sg.count]);
-  if (bf16) hipLaunchKernelGGL(bn_apply8_kernel<bf16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(bn_apply8_kernel<float>, grid, dim3(256), 0, s, a);
+  const bool nt = a.sr.row[sg.count] - a.sr.row[0] >= NT_BYTES / (C * (bf16 ? 2 : 4));
+  if (bf16) {
+    if (nt) hipLaunchKernelGGL((bn_apply8_kernel<bf16_t, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bn_apply8_kernel<bf16_t, false>), grid, dim3(256), 0, s, a);
+  } else {
+    if (nt) hipLaunchKernelGGL((bn_apply8_kernel<float, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bn_apply8_kernel<float, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
 // dz = gamma * rstd * (d - (sum_d + xhat * sum_dx) / rows), d = dy * [act > 0]
-template <typename T>
+template <typename T, bool NT>
 __global__ __launch_bounds__(256) void bn_backward8_kernel(BnArgs a) {
   const int C = a.C;
   const RowSplit w = row_split(a.sr, C);
@@ -552,28 +605,29 @@ __global__ __launch_bounds__(256) void bn_backward8_kernel(BnArgs a) {
     k2[j] = sum_dyx[c] * inv_rows;
   }
   for (int64_t r = w.r0 + w.rl; r < w.r1; r += 4 * w.RPB) {
-    float d[4][8], zz[4][8], m[4][8];
+    Raw<T, 8> d[4], zz[4], m[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int64_t rr = r + u * w.RPB;
       if (rr < w.r1) {
-        load_vec<T, 8>(dy, rr * C + w.c0, d[u]);
-        load_vec<T, 8>(z, rr * C + w.c0, zz[u]);
-        if (act) load_vec<T, 8>(act, rr * C + w.c0, m[u]);
+        d[u].template load<NT>(dy, rr * C + w.c0);
+        zz[u].template load<NT>(z, rr * C + w.c0);
+        if (act) m[u].template load<NT>(act, rr * C + w.c0);
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int64_t rr = r + u * w.RPB;
       if (rr >= w.r1) continue;
+      float o[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         float g = d[u][j];
         if (act && !(m[u][j] > 0.f)) g = 0.f;
         const float xh = (zz[u][j] - mu[j]) * rs[j];
-        d[u][j] = gr[j] * (g - (k1[j] + xh * k2[j]));
+        o[j] = gr[j] * (g - (k1[j] + xh * k2[j]));
       }
-      store_vec8<T>(dz, rr * C + w.c0, d[u]);
+      store_vec8<T, NT>(dz, rr * C + w.c0, o);
     }
   }
 }
@@ -600,8 +654,14 @@ hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const
     a.sum1[i] = sum_dyx[i];
   }
   const dim3 grid(a.sr.blk[sg.count]);
-  if (bf16) hipLaunchKernelGGL(bn_backward8_kernel<bf16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(bn_backward8_kernel<float>, grid, dim3(256), 0, s, a);
+  const bool nt = a.sr.row[sg.count] - a.sr.row[0] >= NT_BYTES / (C * (bf16 ? 2 : 4));
+  if (bf16) {
+    if (nt) hipLaunchKernelGGL((bn_backward8_kernel<bf16_t, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bn_backward8_kernel<bf16_t, false>), grid, dim3(256), 0, s, a);
+  } else {
+    if (nt) hipLaunchKernelGGL((bn_backward8_kernel<float, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bn_backward8_kernel<float, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
