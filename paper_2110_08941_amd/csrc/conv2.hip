@@ -20,6 +20,17 @@
 // reads (32 consecutive n of one kh plane) are free of bank conflicts.
 // One barrier per slice; the next slice's B is fetched into registers while
 // the current slice computes.
+//
+// Patch form (3x3, stride 1, pad 1, whole images per tile: H*W divides 512):
+// the gathered loads above cost one L1 tag lookup per row and tap, and that
+// address traffic, not the MFMA, bounds the kernel.  In the patch form the
+// tile's 512 pixels x 16 channels of a slice are copied once into LDS (two
+// planes of 512 x 16 bytes, one per 8-channel half) and every tap reads its A
+// fragment there: a tap is a uniform row offset dr * W + ds, and a neighbour
+// that lies in the image lies in the tile, so out-of-image taps are a
+// per-lane predicate and no zero frame is stored.  Sixteen consecutive lanes
+// read sixteen consecutive pixels of one plane: no bank conflicts.  The next
+// tap's A and B fragments are read while the current tap's MFMAs run.
 #include "kernels.h"
 
 namespace hs {
@@ -78,7 +89,7 @@ __global__ void pack_weights_kernel(const bf16_t* __restrict__ W, bf16_t* __rest
   }
 }
 
-template <int MODE, int BN, int RS, int EPI>
+template <int MODE, int BN, int RS, int EPI, bool PATCH>
 __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   constexpr int NB = BN / 32;
   constexpr int SEG = RS * 2 * BN;                 // 16-byte chunks of B per slice
@@ -89,10 +100,15 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   constexpr bool STAGE_EPI = (EPI & (EPI_ADD | EPI_MASK)) != 0;
   constexpr int EROW = 36;
   constexpr int BS_BYTES = 2 * RS * 2 * BN * 16;
+  // patch planes: 512 pixels x 16 bytes, every second plane offset by 128
+  // bytes (the two halves of a pixel in different banks); two buffers
+  constexpr int PPLANE = C2_BM * 16 + 128;
+  constexpr int MAIN_BYTES = BS_BYTES + (PATCH ? 2 * 2 * PPLANE : 0);
   constexpr int EPI_BYTES = STAGE_EPI ? C2_WAVES * 64 * EROW * 4 : 0;
-  __shared__ __attribute__((aligned(16))) char smem[BS_BYTES > EPI_BYTES ? BS_BYTES : EPI_BYTES];
+  __shared__ __attribute__((aligned(16))) char smem[MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES];
   typedef uint4 BsT[RS][2][BN];
   BsT* Bs = (BsT*)smem;
+  char* Pa = smem + BS_BYTES;
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -104,47 +120,13 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   const int Hsrc = MODE == MODE_FWD ? g.H : g.Ho;
   const int nslices = Ctap / C2_CK;
 
-  // rows of this lane: element offset of the pixel origin (may point outside
-  // the image; only read when the tap lands inside) and its coordinates
-  int apix[2], ay[2], ax[2];
+  f32x16 acc[2][NB];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int m = m0 + 32 * mb + (lane & 31);
-    const bool ok = m < p.M;
-    const int mm = ok ? m : 0;
-    int base;
-    if (MODE == MODE_FWD) {
-      const int b = (int)fdiv(mm, g.HWo), rem = mm - b * g.Ho * g.Wo;
-      const int ho = (int)fdiv(rem, g.Wo_), wo = rem - ho * g.Wo;
-      base = b * g.H * g.W * g.C;
-      ay[mb] = ho * g.stride - g.pad;
-      ax[mb] = wo * g.stride - g.pad;
-    } else {
-      const int b = (int)fdiv(mm, g.HWi), rem = mm - b * g.H * g.W;
-      const int h = (int)fdiv(rem, g.Wi_), w = rem - h * g.W;
-      base = b * g.Ho * g.Wo * g.K;
-      ay[mb] = h + g.pad;
-      ax[mb] = w + g.pad;
-    }
-    apix[mb] = base + (ay[mb] * Wsrc + ax[mb]) * Ctap + 8 * kh;
-    if (!ok) ay[mb] = -(1 << 20);   // every tap out of range
-  }
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = (f32x16){};
   const bf16_t* A = (const bf16_t*)p.a;
   const bf16_t* B = (const bf16_t*)p.b;
-
-  // A fragment of (slice, tap) for both row blocks: the tap's shift is the
-  // same for every lane (dr, ds, element offset)
-  auto load_a = [&](int sl, int tap, uint4 (&ra)[2]) {
-    const int r = RS == 1 ? 0 : tap / 3, s = RS == 1 ? 0 : tap - 3 * (tap / 3);
-    const int dr = MODE == MODE_FWD ? r : -r, ds = MODE == MODE_FWD ? s : -s;
-    const int toff = (dr * Wsrc + ds) * Ctap + sl * C2_CK;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      const bool ok = (unsigned)(ay[mb] + dr) < (unsigned)Hsrc &&
-                      (unsigned)(ax[mb] + ds) < (unsigned)Wsrc;
-      ra[mb] = ok ? *(const uint4*)(A + apix[mb] + toff) : make_uint4(0, 0, 0, 0);
-    }
-  };
   // B chunk i of slice sl (global -> register) and its LDS slot
   auto load_b1 = [&](int sl, int i) -> uint4 {
     const int q = tid + 512 * i;
@@ -163,80 +145,235 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
     }
   };
 
-  f32x16 acc[2][NB];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = (f32x16){};
 
-  {
-    uint4 r0[BREG];
+  if constexpr (PATCH) {
+    // tile rows are whole images: the image-local pixel of tile row q is
+    // q % (H * W); bit t of vm[mb] = tap t of that row lies in the image
+    const int tile_m0 = tm * C2_BM;
+    const int HW = Hsrc * Wsrc;
+    int qa[2];
+    uint32_t vm[2];
 #pragma unroll
-    for (int i = 0; i < BREG; ++i) r0[i] = load_b1(0, i);
+    for (int mb = 0; mb < 2; ++mb) {
+      const int q = wave * 64 + 32 * mb + (lane & 31);
+      const int pix = q % HW, y = pix / Wsrc, x = pix - (pix / Wsrc) * Wsrc;
+      uint32_t bits = 0;
 #pragma unroll
-    for (int i = 0; i < BREG; ++i) store_b1(0, i, r0[i]);
-  }
-  // A fragments two steps ahead: cur = step u, nxt = step u + 1
-  uint4 cur[2], nxt[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
-  load_a(0, 0, cur);
-  if (RS > 1) load_a(0, 1, nxt);
-  else if (nslices > 1) load_a(1, 0, nxt);
-  __syncthreads();
-
-  // Next slice's B: with RS >= BREG + 2 taps, chunk i is loaded at tap i and
-  // written to the free LDS buffer at tap i + 2 (few registers live);
-  // otherwise all chunks are loaded at the first tap and written at the end.
-  constexpr bool SPREAD = RS >= BREG + 2;
-  for (int sl = 0; sl < nslices; ++sl) {
-    const bool more = sl + 1 < nslices;
-    const int buf = sl & 1;
-    uint4 rb[BREG];
-    if (!SPREAD && more) {
-#pragma unroll
-      for (int i = 0; i < BREG; ++i) rb[i] = load_b1(sl + 1, i);
+      for (int t = 0; t < 9; ++t) {
+        const int r = t / 3, c = t % 3;
+        const int dr = MODE == MODE_FWD ? r - 1 : 1 - r, dc = MODE == MODE_FWD ? c - 1 : 1 - c;
+        if ((unsigned)(y + dr) < (unsigned)Hsrc && (unsigned)(x + dc) < (unsigned)Wsrc) bits |= 1u << t;
+      }
+      qa[mb] = q;
+      vm[mb] = tile_m0 + q < p.M ? bits : 0u;
     }
-#pragma unroll
-    for (int t = 0; t < RS; ++t) {
-      if (SPREAD && more) {
-        if (t < BREG) rb[t] = load_b1(sl + 1, t);
-        if (t >= 2 && t - 2 < BREG) store_b1(buf ^ 1, t - 2, rb[t - 2]);
-      }
-      const uint4 fa[2] = {cur[0], cur[1]};
-      cur[0] = nxt[0];
-      cur[1] = nxt[1];
-      {   // prefetch step u + 2
-        int nt = t + 2, ns = sl;
-        while (nt >= RS) {
-          nt -= RS;
-          ++ns;
-        }
-        if (ns < nslices) load_a(ns, nt, nxt);
-      }
-      uint4 fb[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fb[nb] = Bs[buf][t][kh][nb * 32 + (lane & 31)];
+    // A fragments of tap t from patch buffer buf
+    auto read_a = [&](int buf, int t, uint4 (&ra)[2]) {
+      const int r = t / 3, c = t % 3;
+      const int dr = MODE == MODE_FWD ? r - 1 : 1 - r, dc = MODE == MODE_FWD ? c - 1 : 1 - c;
+      const int toff = dr * Wsrc + dc;
+      const char* base = Pa + (buf * 2 + kh) * PPLANE;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
-        bf16x8 av;
-        __builtin_memcpy(&av, &fa[mb], 16);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          bf16x8 bv;
-          __builtin_memcpy(&bv, &fb[nb], 16);
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
-        }
+        const uint4 v = *(const uint4*)(base + ((qa[mb] + toff) & (C2_BM - 1)) * 16);
+        ra[mb] = ((vm[mb] >> t) & 1u) ? v : make_uint4(0, 0, 0, 0);
       }
-    }
-    if (more) {
-      if (SPREAD) {
+    };
+    auto read_b = [&](int buf, int t, uint4 (&rb)[NB]) {
 #pragma unroll
-        for (int i = (RS - 2 > 0 ? RS - 2 : 0); i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
-      } else {
+      for (int nb = 0; nb < NB; ++nb) rb[nb] = Bs[buf][t][kh][nb * 32 + (lane & 31)];
+    };
+    // patch chunk i (0, 1) of slice sl: pixel (tid + 512 i) / 2, half (tid + 512 i) & 1
+    auto load_p = [&](int sl, int i) -> uint4 {
+      const int cidx = tid + 512 * i, q = cidx >> 1, h = cidx & 1;
+      const int64_t m = (int64_t)tile_m0 + q;
+      uint4 r = make_uint4(0, 0, 0, 0);
+      if (m < p.M) r = *(const uint4*)(A + m * Ctap + sl * C2_CK + 8 * h);
+      return r;
+    };
+    auto store_p = [&](int buf, int i, const uint4& r) {
+      const int cidx = tid + 512 * i, q = cidx >> 1, h = cidx & 1;
+      *(uint4*)(Pa + (buf * 2 + h) * PPLANE + q * 16) = r;
+    };
+
+    {
+      uint4 r0[BREG], rp0[2];
 #pragma unroll
-        for (int i = 0; i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
-      }
+      for (int i = 0; i < BREG; ++i) r0[i] = load_b1(0, i);
+      rp0[0] = load_p(0, 0);
+      rp0[1] = load_p(0, 1);
+#pragma unroll
+      for (int i = 0; i < BREG; ++i) store_b1(0, i, r0[i]);
+      store_p(0, 0, rp0[0]);
+      store_p(0, 1, rp0[1]);
     }
     __syncthreads();
+    uint4 fa[2], fb[NB];
+    read_a(0, 0, fa);
+    read_b(0, 0, fb);
+    constexpr bool SPREAD = RS >= BREG + 2;
+    static_assert(RS == 9 && SPREAD, "patch form: 3x3 filters");
+    for (int sl = 0; sl < nslices; ++sl) {
+      const bool more = sl + 1 < nslices;
+      const int buf = sl & 1;
+      uint4 rb[BREG], rp[2];
+#pragma unroll
+      for (int t = 0; t < RS; ++t) {
+        if (more) {
+          if (t < BREG) rb[t] = load_b1(sl + 1, t);
+          if (t >= 2 && t - 2 < BREG) store_b1(buf ^ 1, t - 2, rb[t - 2]);
+          if (t == 1) {
+            rp[0] = load_p(sl + 1, 0);
+            rp[1] = load_p(sl + 1, 1);
+          }
+          if (t == 5) {
+            store_p(buf ^ 1, 0, rp[0]);
+            store_p(buf ^ 1, 1, rp[1]);
+          }
+        }
+        uint4 na[2], nbv[NB];
+        if (t + 1 < RS) {
+          read_a(buf, t + 1, na);
+          read_b(buf, t + 1, nbv);
+        }
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+          bf16x8 av;
+          __builtin_memcpy(&av, &fa[mb], 16);
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            bf16x8 bv;
+            __builtin_memcpy(&bv, &fb[nb], 16);
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
+          }
+        }
+        if (t + 1 < RS) {
+          fa[0] = na[0];
+          fa[1] = na[1];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
+        }
+      }
+      if (more) {
+#pragma unroll
+        for (int i = RS - 2; i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
+      }
+      __syncthreads();
+      if (more) {
+        read_a(buf ^ 1, 0, fa);
+        read_b(buf ^ 1, 0, fb);
+      }
+    }
+  } else {
+    // rows of this lane: element offset of the pixel origin (may point outside
+    // the image; only read when the tap lands inside) and its coordinates
+    int apix[2], ay[2], ax[2];
+  #pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int m = m0 + 32 * mb + (lane & 31);
+      const bool ok = m < p.M;
+      const int mm = ok ? m : 0;
+      int base;
+      if (MODE == MODE_FWD) {
+        const int b = (int)fdiv(mm, g.HWo), rem = mm - b * g.Ho * g.Wo;
+        const int ho = (int)fdiv(rem, g.Wo_), wo = rem - ho * g.Wo;
+        base = b * g.H * g.W * g.C;
+        ay[mb] = ho * g.stride - g.pad;
+        ax[mb] = wo * g.stride - g.pad;
+      } else {
+        const int b = (int)fdiv(mm, g.HWi), rem = mm - b * g.H * g.W;
+        const int h = (int)fdiv(rem, g.Wi_), w = rem - h * g.W;
+        base = b * g.Ho * g.Wo * g.K;
+        ay[mb] = h + g.pad;
+        ax[mb] = w + g.pad;
+      }
+      apix[mb] = base + (ay[mb] * Wsrc + ax[mb]) * Ctap + 8 * kh;
+      if (!ok) ay[mb] = -(1 << 20);   // every tap out of range
+    }
+
+    // A fragment of (slice, tap) for both row blocks: the tap's shift is the
+    // same for every lane (dr, ds, element offset)
+    auto load_a = [&](int sl, int tap, uint4 (&ra)[2]) {
+      const int r = RS == 1 ? 0 : tap / 3, s = RS == 1 ? 0 : tap - 3 * (tap / 3);
+      const int dr = MODE == MODE_FWD ? r : -r, ds = MODE == MODE_FWD ? s : -s;
+      const int toff = (dr * Wsrc + ds) * Ctap + sl * C2_CK;
+  #pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const bool ok = (unsigned)(ay[mb] + dr) < (unsigned)Hsrc &&
+                        (unsigned)(ax[mb] + ds) < (unsigned)Wsrc;
+        ra[mb] = ok ? *(const uint4*)(A + apix[mb] + toff) : make_uint4(0, 0, 0, 0);
+      }
+    };
+    {
+      uint4 r0[BREG];
+  #pragma unroll
+      for (int i = 0; i < BREG; ++i) r0[i] = load_b1(0, i);
+  #pragma unroll
+      for (int i = 0; i < BREG; ++i) store_b1(0, i, r0[i]);
+    }
+    // A fragments two steps ahead: cur = step u, nxt = step u + 1
+    uint4 cur[2], nxt[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+    load_a(0, 0, cur);
+    if (RS > 1) load_a(0, 1, nxt);
+    else if (nslices > 1) load_a(1, 0, nxt);
+    __syncthreads();
+
+    // Next slice's B: with RS >= BREG + 2 taps, chunk i is loaded at tap i and
+    // written to the free LDS buffer at tap i + 2 (few registers live);
+    // otherwise all chunks are loaded at the first tap and written at the end.
+    constexpr bool SPREAD = RS >= BREG + 2;
+    for (int sl = 0; sl < nslices; ++sl) {
+      const bool more = sl + 1 < nslices;
+      const int buf = sl & 1;
+      uint4 rb[BREG];
+      if (!SPREAD && more) {
+  #pragma unroll
+        for (int i = 0; i < BREG; ++i) rb[i] = load_b1(sl + 1, i);
+      }
+  #pragma unroll
+      for (int t = 0; t < RS; ++t) {
+        if (SPREAD && more) {
+          if (t < BREG) rb[t] = load_b1(sl + 1, t);
+          if (t >= 2 && t - 2 < BREG) store_b1(buf ^ 1, t - 2, rb[t - 2]);
+        }
+        const uint4 fa[2] = {cur[0], cur[1]};
+        cur[0] = nxt[0];
+        cur[1] = nxt[1];
+        {   // prefetch step u + 2
+          int nt = t + 2, ns = sl;
+          while (nt >= RS) {
+            nt -= RS;
+            ++ns;
+          }
+          if (ns < nslices) load_a(ns, nt, nxt);
+        }
+        uint4 fb[NB];
+  #pragma unroll
+        for (int nb = 0; nb < NB; ++nb) fb[nb] = Bs[buf][t][kh][nb * 32 + (lane & 31)];
+  #pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+          bf16x8 av;
+          __builtin_memcpy(&av, &fa[mb], 16);
+  #pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            bf16x8 bv;
+            __builtin_memcpy(&bv, &fb[nb], 16);
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
+          }
+        }
+      }
+      if (more) {
+        if (SPREAD) {
+  #pragma unroll
+          for (int i = (RS - 2 > 0 ? RS - 2 : 0); i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
+        } else {
+  #pragma unroll
+          for (int i = 0; i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
+        }
+      }
+      __syncthreads();
+    }
+
   }
 
   if constexpr (STAGE_EPI) {
@@ -365,21 +502,30 @@ hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmPara
   return hipGetLastError();
 }
 
-template <int MODE, int BN, int RS>
+template <int MODE, int BN, int RS, bool PATCH>
 static void launch_epi2(const GemmParams& p, dim3 grid, hipStream_t s) {
   if constexpr (MODE == MODE_FWD) {
     const bool bias = p.bias != nullptr, relu = p.relu != 0;
-    if (bias && relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p);
-    else if (bias) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS>), grid, dim3(512), 0, s, p);
-    else if (relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_RELU>), grid, dim3(512), 0, s, p);
-    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0>), grid, dim3(512), 0, s, p);
+    if (bias && relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS | EPI_RELU, PATCH>), grid, dim3(512), 0, s, p);
+    else if (bias) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS, PATCH>), grid, dim3(512), 0, s, p);
+    else if (relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_RELU, PATCH>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0, PATCH>), grid, dim3(512), 0, s, p);
   } else {
     const bool add = p.addend != nullptr, mask = p.mask != nullptr;
-    if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK>), grid, dim3(512), 0, s, p);
-    else if (add) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD>), grid, dim3(512), 0, s, p);
-    else if (mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK>), grid, dim3(512), 0, s, p);
-    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0>), grid, dim3(512), 0, s, p);
+    if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
+    else if (add) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD, PATCH>), grid, dim3(512), 0, s, p);
+    else if (mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0, PATCH>), grid, dim3(512), 0, s, p);
   }
+}
+
+// the patch form: 3x3, stride 1, pad 1, same-size output, whole images per
+// 512-row tile
+static bool conv2_patch(const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  const int64_t hw = (int64_t)g.H * g.W;
+  return g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 && g.Ho == g.H && g.Wo == g.W &&
+         hw >= 1 && C2_BM % hw == 0;
 }
 
 template <int MODE>
@@ -389,12 +535,15 @@ static hipError_t launch_mode2(const GemmParams& p0, hipStream_t s) {
   const int RS = p.g.R * p.g.S;
   p.tiles_n = p.N / BN;
   const dim3 grid((unsigned)(ceil_div(p.M, C2_BM) * p.tiles_n));
+  const bool patch = conv2_patch(p);
   if (BN == 128) {
-    if (RS == 9) launch_epi2<MODE, 128, 9>(p, grid, s);
-    else launch_epi2<MODE, 128, 1>(p, grid, s);
+    if (patch) launch_epi2<MODE, 128, 9, true>(p, grid, s);
+    else if (RS == 9) launch_epi2<MODE, 128, 9, false>(p, grid, s);
+    else launch_epi2<MODE, 128, 1, false>(p, grid, s);
   } else {
-    if (RS == 9) launch_epi2<MODE, 64, 9>(p, grid, s);
-    else launch_epi2<MODE, 64, 1>(p, grid, s);
+    if (patch) launch_epi2<MODE, 64, 9, true>(p, grid, s);
+    else if (RS == 9) launch_epi2<MODE, 64, 9, false>(p, grid, s);
+    else launch_epi2<MODE, 64, 1, false>(p, grid, s);
   }
   return hipGetLastError();
 }

@@ -49,9 +49,22 @@ def test_layer_gemm(mode, shape, dtype):
     check_layer_gemm(mode, shape, dtype, packed=False)
 
 
+# 3x3 stride-1 layers whose 512-row tiles hold whole images (the LDS-patch
+# form of the 32x32 MFMA kernel): several tiles with a ragged last one, 64-
+# and 128-column tiles, images of 16x16 down to 2x2
+PATCH_SHAPES = [
+    (9, 16, 16, 128, 128, 3, 1, 1),   # 4.5 tiles of 2 images
+    (37, 8, 8, 128, 256, 3, 1, 1),    # 4.6 tiles of 8 images
+    (70, 4, 4, 256, 128, 3, 1, 1),    # 2.2 tiles of 32 images
+    (130, 2, 2, 512, 512, 3, 1, 1),   # 128 images per tile, 2 left over
+    (4, 8, 8, 192, 192, 3, 1, 1),     # 64-column tiles, one partial tile
+    (5, 8, 8, 128, 64, 3, 1, 1),
+]
+
+
 # bf16 forward (bf16 output) and data gradient given a scratch buffer: the
 # 32x32 MFMA kernel on packed weights wherever the shape allows it
-@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+@pytest.mark.parametrize("shape", SHAPES + PATCH_SHAPES, ids=[str(s) for s in SHAPES + PATCH_SHAPES])
 @pytest.mark.parametrize("mode", [0, 1])
 def test_layer_gemm_packed(mode, shape):
     check_layer_gemm(mode, shape, "bf16", packed=True)
