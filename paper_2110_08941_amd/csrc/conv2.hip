@@ -41,6 +41,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void* lds_ptr;          // LDS
+typedef __attribute__((address_space(1))) const void* gbl_cptr;   // global
 
 enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16 };
 
@@ -103,12 +105,12 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   // patch planes: 512 pixels x 16 bytes, every second plane offset by 128
   // bytes (the two halves of a pixel in different banks); two buffers
   constexpr int PPLANE = C2_BM * 16 + 128;
-  constexpr int MAIN_BYTES = BS_BYTES + (PATCH ? 2 * 2 * PPLANE : 0);
   constexpr int EPI_BYTES = STAGE_EPI ? C2_WAVES * 64 * EROW * 4 : 0;
-  __shared__ __attribute__((aligned(16))) char smem[MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES];
+  constexpr int SMEM_BYTES = PATCH ? 16 : (BS_BYTES > EPI_BYTES ? BS_BYTES : EPI_BYTES);
+  __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
   typedef uint4 BsT[RS][2][BN];
   BsT* Bs = (BsT*)smem;
-  char* Pa = smem + BS_BYTES;
+  float* Ewave = (float*)smem + (threadIdx.x >> 6) * 64 * EROW;   // epilogue staging of this wave
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -147,8 +149,23 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
 
 
   if constexpr (PATCH) {
-    // tile rows are whole images: the image-local pixel of tile row q is
-    // q % (H * W); bit t of vm[mb] = tap t of that row lies in the image
+    // The two buffers of B and of the patch are distinct LDS arrays and the
+    // slice loop is unrolled by two, so that every access names its buffer:
+    // the compiler then knows that the copies into one buffer do not alias
+    // the fragment reads from the other and waits for them only at the
+    // slice's end.  Each B buffer is padded to whole rounds of 512 chunks (no
+    // thread's copy is conditional) and is large enough to stage four waves'
+    // epilogue tiles.
+    constexpr int BBUF = BREG * 512;
+    constexpr int BPAD = BBUF * 16 > 4 * 64 * EROW * 4 ? BBUF : 4 * 64 * EROW / 4;
+    __shared__ __attribute__((aligned(16))) uint4 sB0[BPAD];
+    __shared__ __attribute__((aligned(16))) uint4 sB1[BPAD];
+    __shared__ __attribute__((aligned(16))) char sP0[2 * PPLANE];
+    __shared__ __attribute__((aligned(16))) char sP1[2 * PPLANE];
+    Ewave = (float*)(wave < 4 ? sB0 : sB1) + (wave & 3) * 64 * EROW;
+
+    // Tile rows are whole images: the image-local pixel of tile row q is
+    // q % (H * W); bit t of vm[mb] = tap t of that row lies in the image.
     const int tile_m0 = tm * C2_BM;
     const int HW = Hsrc * Wsrc;
     int qa[2];
@@ -167,79 +184,71 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
       qa[mb] = q;
       vm[mb] = tile_m0 + q < p.M ? bits : 0u;
     }
-    // A fragments of tap t from patch buffer buf
-    auto read_a = [&](int buf, int t, uint4 (&ra)[2]) {
+    // A fragments of tap t from patch buffer P, as read (the read stays in
+    // the buffer); out-of-image taps are cleared by mask_a when consumed
+    auto read_a = [&](const char* P, int t, uint4 (&ra)[2]) {
       const int r = t / 3, c = t % 3;
       const int dr = MODE == MODE_FWD ? r - 1 : 1 - r, dc = MODE == MODE_FWD ? c - 1 : 1 - c;
       const int toff = dr * Wsrc + dc;
-      const char* base = Pa + (buf * 2 + kh) * PPLANE;
+      const char* base = P + kh * PPLANE;
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        const uint4 v = *(const uint4*)(base + ((qa[mb] + toff) & (C2_BM - 1)) * 16);
-        ra[mb] = ((vm[mb] >> t) & 1u) ? v : make_uint4(0, 0, 0, 0);
+      for (int mb = 0; mb < 2; ++mb)
+        ra[mb] = *(const uint4*)(base + ((qa[mb] + toff) & (C2_BM - 1)) * 16);
+    };
+    auto mask_a = [&](int t, const uint4& v, int mb) -> uint4 {
+      const uint32_t k = 0u - ((vm[mb] >> t) & 1u);
+      return make_uint4(v.x & k, v.y & k, v.z & k, v.w & k);
+    };
+    auto read_b = [&](const uint4* Bb, int t, uint4 (&rb)[NB]) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) rb[nb] = Bb[(t * 2 + kh) * BN + nb * 32 + (lane & 31)];
+    };
+    // Slice sl of B and of the patch into (Bb, P), straight from global memory
+    // into LDS (16 bytes per lane, written at the wave's base + 16 * lane; no
+    // registers held).  B chunk q = tid + 512 i = (tap * 2 + kh) * BN + n,
+    // clamped to the slice's last chunk (the surplus lands in the padding);
+    // patch plane h, pixel q = tid; rows past the last image re-read the last
+    // row (they only feed output rows that are not stored).
+    const int wbase = wave * 64;
+    auto dma_slice = [&](int sl, uint4* Bb, char* P) {
+#pragma unroll
+      for (int i = 0; i < BREG; ++i) {
+        int q = tid + 512 * i;
+        q = q < SEG ? q : SEG - 1;
+        const int n = q % BN, rest = q / BN;
+        const bf16_t* src = B + (((int64_t)sl * RS * 2 + rest) * p.N + n0 + n) * 8;
+        __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bb + 512 * i + wbase), 16, 0, 0);
+      }
+      int64_t m = (int64_t)tile_m0 + tid;
+      m = m < p.M ? m : p.M - 1;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const bf16_t* src = A + m * Ctap + sl * C2_CK + 8 * h;
+        __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(P + h * PPLANE + wbase * 16), 16, 0, 0);
       }
     };
-    auto read_b = [&](int buf, int t, uint4 (&rb)[NB]) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) rb[nb] = Bs[buf][t][kh][nb * 32 + (lane & 31)];
-    };
-    // patch chunk i (0, 1) of slice sl: pixel (tid + 512 i) / 2, half (tid + 512 i) & 1
-    auto load_p = [&](int sl, int i) -> uint4 {
-      const int cidx = tid + 512 * i, q = cidx >> 1, h = cidx & 1;
-      const int64_t m = (int64_t)tile_m0 + q;
-      uint4 r = make_uint4(0, 0, 0, 0);
-      if (m < p.M) r = *(const uint4*)(A + m * Ctap + sl * C2_CK + 8 * h);
-      return r;
-    };
-    auto store_p = [&](int buf, int i, const uint4& r) {
-      const int cidx = tid + 512 * i, q = cidx >> 1, h = cidx & 1;
-      *(uint4*)(Pa + (buf * 2 + h) * PPLANE + q * 16) = r;
-    };
 
-    {
-      uint4 r0[BREG], rp0[2];
-#pragma unroll
-      for (int i = 0; i < BREG; ++i) r0[i] = load_b1(0, i);
-      rp0[0] = load_p(0, 0);
-      rp0[1] = load_p(0, 1);
-#pragma unroll
-      for (int i = 0; i < BREG; ++i) store_b1(0, i, r0[i]);
-      store_p(0, 0, rp0[0]);
-      store_p(0, 1, rp0[1]);
-    }
-    __syncthreads();
     uint4 fa[2], fb[NB];
-    read_a(0, 0, fa);
-    read_b(0, 0, fb);
-    constexpr bool SPREAD = RS >= BREG + 2;
-    static_assert(RS == 9 && SPREAD, "patch form: 3x3 filters");
-    for (int sl = 0; sl < nslices; ++sl) {
+    // one slice from (Bc, Pc) while the next one is copied into (Bn, Pn)
+    auto slice = [&](int sl, const uint4* Bc, const char* Pc, uint4* Bn, char* Pn) {
       const bool more = sl + 1 < nslices;
-      const int buf = sl & 1;
-      uint4 rb[BREG], rp[2];
+      if (more) dma_slice(sl + 1, Bn, Pn);
+      // per tap: mask this tap's A fragments (read during the previous tap),
+      // issue the next tap's reads, then the MFMAs; the scheduling barriers
+      // keep the reads ahead of the MFMAs that hide their latency
 #pragma unroll
       for (int t = 0; t < RS; ++t) {
-        if (more) {
-          if (t < BREG) rb[t] = load_b1(sl + 1, t);
-          if (t >= 2 && t - 2 < BREG) store_b1(buf ^ 1, t - 2, rb[t - 2]);
-          if (t == 1) {
-            rp[0] = load_p(sl + 1, 0);
-            rp[1] = load_p(sl + 1, 1);
-          }
-          if (t == 5) {
-            store_p(buf ^ 1, 0, rp[0]);
-            store_p(buf ^ 1, 1, rp[1]);
-          }
-        }
+        const uint4 am[2] = {mask_a(t, fa[0], 0), mask_a(t, fa[1], 1)};
         uint4 na[2], nbv[NB];
         if (t + 1 < RS) {
-          read_a(buf, t + 1, na);
-          read_b(buf, t + 1, nbv);
+          read_a(Pc, t + 1, na);
+          read_b(Bc, t + 1, nbv);
         }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
           bf16x8 av;
-          __builtin_memcpy(&av, &fa[mb], 16);
+          __builtin_memcpy(&av, &am[mb], 16);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
             bf16x8 bv;
@@ -247,6 +256,7 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
         if (t + 1 < RS) {
           fa[0] = na[0];
           fa[1] = na[1];
@@ -254,15 +264,24 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
           for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
         }
       }
-      if (more) {
-#pragma unroll
-        for (int i = RS - 2; i < BREG; ++i) store_b1(buf ^ 1, i, rb[i]);
-      }
+      // this wave's copies have landed; after the barrier every wave's have
+      __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (more) {
-        read_a(buf ^ 1, 0, fa);
-        read_b(buf ^ 1, 0, fb);
+        read_a(Pn, 0, fa);
+        read_b(Bn, 0, fb);
       }
+    };
+
+    static_assert(RS == 9, "patch form: 3x3 filters");
+    dma_slice(0, sB0, sP0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    read_a(sP0, 0, fa);
+    read_b(sB0, 0, fb);
+    for (int sl = 0; sl < nslices; sl += 2) {
+      slice(sl, sB0, sP0, sB1, sP1);
+      if (sl + 1 < nslices) slice(sl + 1, sB1, sP1, sB0, sP0);
     }
   } else {
     // rows of this lane: element offset of the pixel origin (may point outside
@@ -378,7 +397,7 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
 
   if constexpr (STAGE_EPI) {
     // the loop ended with a barrier: B is no longer read
-    float* E = (float*)smem + wave * 64 * EROW;
+    float* E = Ewave;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
