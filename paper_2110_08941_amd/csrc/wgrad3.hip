@@ -8,7 +8,12 @@
 //   * the dy rows of the PIX pixels, 64 output channels:  PIX x 128 bytes;
 //   * the input patch those pixels read, with a one-pixel zero frame:
 //     (rows + 2) x (W + 2) slots per image, 64 input channels: slot x 128 B.
-// Both keep their natural channel-contiguous rows (plain 16-byte stores).
+// Both keep their natural channel-contiguous rows.  They are copied straight
+// from global memory into LDS (16 bytes per lane, no registers held); frame
+// slots and missing images copy a static zero vector, so no copy is
+// conditional, and the two stage buffers are distinct LDS arrays (the slice
+// loop is unrolled by two) so that the copies into one buffer are not mistaken
+// for writes to the one being read.
 // MFMA fragments need 8 consecutive pixels per lane; they come from the
 // transposing LDS read (ds_read_b64_tr_b16), 4 consecutive rows per read.  A
 // tap's shift is a row offset in the patch, and the frame supplies the zero
@@ -22,9 +27,10 @@
 // bytes (what 32 lanes read at once) then fall on distinct banks.  A read's
 // first row S is a compile-time constant plus a lane term that is a multiple
 // of 4 or a fixed lane value; the swizzled offset of the lane's element
-// depends only on S mod 4, so each lane precomputes 4 base offsets and every
-// read is base[S mod 4] + a compile-time offset (no address arithmetic in the
-// loop).  The reduction is split over slices (split-K, per worker segment):
+// depends only on S mod 4, so each lane precomputes 4 base offsets (with its
+// wave's filter-row shift folded in) and every read is base[S mod 4] + a
+// compile-time offset: no address arithmetic and no branches in the loop.
+// The next k step's fragments are read while the current step's MFMAs run.  The reduction is split over slices (split-K, per worker segment):
 // split y writes its partial gW at out + y * split_stride.
 #include "kernels.h"
 
@@ -37,6 +43,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short __attribute__((address_space(3))) * lds_i16p;
 typedef i16x4 __attribute__((address_space(3))) * lds_v4p;
+typedef __attribute__((address_space(3))) void* lds_ptr;          // LDS
+typedef __attribute__((address_space(1))) const void* gbl_cptr;   // global
+
+// source of the zero slots of the patch (frame, missing images)
+__device__ __attribute__((aligned(16))) uint4 g_zero16;
 
 constexpr int ROWB = 128;   // bytes per LDS row
 __device__ inline int swz_off(int row, int byte) {   // byte offset of (row, byte) in LDS
@@ -76,27 +87,41 @@ struct Slice {
 template <int W>
 __global__ __launch_bounds__(768) void wgrad3_kernel(GemmParams p) {
   typedef Slice<W> S;
-  constexpr int AROWS = S::PIX;
-  // bytes per buffer; the B region has 4 spare rows at its end (the 4-row
-  // reads at +8 may pass the last slot by up to 3 rows; those values are
-  // never used)
-  constexpr int STAGE = (AROWS + S::SLOTS + 4) * ROWB;
-  constexpr int ACH = AROWS * 8, BCH = S::SLOTS * 8;   // 16-byte chunks
   constexpr int NT = 768;
+  constexpr int AROWS = S::PIX;
+  constexpr int ACH = AROWS * 8, BCH = S::SLOTS * 8;   // 16-byte chunks
   constexpr int AIT = (ACH + NT - 1) / NT, BIT = (BCH + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+  static_assert(ACH % 64 == 0, "dy rows: whole waves per copy round");
+  // patch rows: the last copying wave writes whole 8-row groups, and the
+  // 4-row reads at +8 may pass the last slot by up to 3 rows (values unused)
+  constexpr int BR8 = (S::SLOTS + 7) / 8 * 8;
+  constexpr int BROWS = BR8 > S::SLOTS + 4 ? BR8 : S::SLOTS + 4;
+  __shared__ __attribute__((aligned(16))) char sA0[AROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sA1[AROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sB0[BROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sB1[BROWS * ROWB];
 
   const ConvGeom& g = p.g;
   const int C = g.C, K = g.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 2, wk = (wave >> 1) & 1, wc = wave & 1;
+  // Workgroups are handed to the 8 XCDs (each with its own L2) in turn.  The
+  // tiles of one split read the same dy rows and input patch, so the block
+  // index is remapped to put all tiles of a split on one XCD, where they run
+  // side by side and share those reads through its L2: the first 8 q blocks
+  // (q = blocks / 8) are dealt so that XCD k gets logical blocks
+  // [k q, (k + 1) q) in order; the rest keep their index.
+  const int nblk = (int)(gridDim.x * gridDim.y), q8 = nblk / 8;
+  int lb = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+  if (lb < 8 * q8) lb = (lb % 8) * q8 + lb / 8;
+  const int bx = lb % (int)gridDim.x, by = lb / (int)gridDim.x;
   const int tiles_c = C / 64;
-  const int k0 = (blockIdx.x / tiles_c) * 64, c0 = (blockIdx.x % tiles_c) * 64;
+  const int k0 = (bx / tiles_c) * 64, c0 = (bx % tiles_c) * 64;
 
-  // this split's slices: segment sg, slices [j0, j1) of the segment
+  // this split's slices: segment sg, slices [j0, j0 + cnt) of the segment
   int sg = 0;
 #pragma unroll
-  for (int i = 1; i < MAX_SEG; ++i) sg += (i < p.nseg && (int)blockIdx.y >= p.seg_split[i]) ? 1 : 0;
+  for (int i = 1; i < MAX_SEG; ++i) sg += (i < p.nseg && by >= p.seg_split[i]) ? 1 : 0;
   int sp = 0, s_n0 = 0, s_n1 = 0;
 #pragma unroll
   for (int i = 0; i < MAX_SEG; ++i)
@@ -108,66 +133,77 @@ __global__ __launch_bounds__(768) void wgrad3_kernel(GemmParams p) {
   const int nimg = s_n1 - s_n0;
   const int nsl = S::ROWS ? nimg * S::SPI : (nimg + S::NF - 1) / S::NF;
   // split i of the segment takes slices [i kt_per_split, (i + 1) kt_per_split)
-  const int j0 = ((int)blockIdx.y - sp) * p.kt_per_split;
+  const int j0 = (by - sp) * p.kt_per_split;
   const int cnt = max(0, min(p.kt_per_split, nsl - j0));   // slices of this split
-  const int jst = 1;
 
   const bf16_t* X = (const bf16_t*)p.b;    // x  [n][H][W][C]
   const bf16_t* DY = (const bf16_t*)p.a;   // dy [n][H][W][K]
+  // the zero vector's address, taken once and kept in registers (a reload
+  // inside the loop would be a scalar memory load, whose out-of-order return
+  // forces full waits on every LDS read)
+  const void* zero16 = &g_zero16;
+  __asm__ volatile("" : "+s"(zero16));
 
-  // image and first output row of frame f of slice j (image < 0: empty frame)
-  auto frame_origin = [&](int j, int f, int& img, int& y0) {
+
+  // Copy slice j into (As, Bs).  Copy round i of wave w writes LDS chunks
+  // NT i + 64 w + lane (row = chunk / 8, slot in the row = chunk % 8); the
+  // swizzle is applied on the global side: that slot holds channel chunk
+  // slot ^ (4 * bit 1 of the row).  What a lane copies depends on the slice
+  // only through a uniform base (image, first row): the lane parts are
+  // computed once here.
+  //   dy row:  element offset aoff (pixel in the slice + channel chunk) and,
+  //            for whole-image slices, the frame (image) index afr;
+  //   patch:   element offset boff relative to the slot (y0 - 1, -1) of the
+  //            frame, the row term bfy = fy - 1 for the image-row check, and
+  //            the frame index bfr; slots outside the image columns, or past
+  //            the last chunk, get bfy = bfr = a value no check passes.
+  constexpr int NEVER = 1 << 28;
+  int aoff[AIT], afr[AIT], boff[BIT], bfy[BIT], bfr[BIT];
+#pragma unroll
+  for (int i = 0; i < AIT; ++i) {
+    const int d = tid + NT * i, row = d >> 3;
+    const int ch = (d & 7) ^ (((row >> 1) & 1) << 2);
+    afr[i] = S::frame(row);
+    aoff[i] = ((afr[i] * S::HW * (S::ROWS ? 0 : 1)) + S::prow(row) * W + S::pcol(row)) * K + ch * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < BIT; ++i) {
+    const int d = tid + NT * i, sl = d >> 3;
+    const int ch = (d & 7) ^ (((sl >> 1) & 1) << 2);
+    const int f = sl / S::FS, rem = sl - f * S::FS;
+    const int fy = rem / S::FW, fx = rem - fy * S::FW;
+    const bool colok = d < BCH && (unsigned)(fx - 1) < (unsigned)W;
+    boff[i] = ((S::ROWS ? 0 : f * S::HW) + (fy - 1) * W + (fx - 1)) * C + ch * 8;
+    bfy[i] = colok ? fy - 1 : NEVER;
+    bfr[i] = colok ? f : NEVER;
+  }
+  auto copy_slice = [&](int j, char* As, char* Bs) {
+    // uniform part: first image and first output row of the slice; the
+    // number of frames that hold an image
+    int img0, y0, nfr;
     if (S::ROWS) {
-      img = s_n0 + j / S::SPI;
+      img0 = s_n0 + j / S::SPI;
       y0 = (j % S::SPI) * S::RG;
+      nfr = 1;
     } else {
-      img = s_n0 + j * S::NF + f;
+      img0 = s_n0 + j * S::NF;
       y0 = 0;
-      if (img >= s_n1) img = -1;
+      nfr = s_n1 - img0;
     }
-  };
-
-  auto load = [&](int j, uint4 (&ra)[AIT], uint4 (&rb)[BIT]) {
+    const bf16_t* dyb = DY + ((int64_t)(img0 * W + y0) * W) * K + k0;
+    const bf16_t* xb = X + ((int64_t)(img0 * W + y0) * W) * C + c0;
 #pragma unroll
     for (int i = 0; i < AIT; ++i) {
-      const int q = tid + NT * i;
-      if (q < ACH) {
-        const int px = q >> 3, ch = q & 7;
-        int img, y0;
-        frame_origin(j, S::frame(px), img, y0);
-        const int y = y0 + S::prow(px), x = S::pcol(px);
-        ra[i] = img >= 0 ? *(const uint4*)(DY + ((int64_t)(img * W + y) * W + x) * K + k0 + ch * 8)
-                         : make_uint4(0, 0, 0, 0);
-      }
+      if (NT * i + 64 * wave >= ACH) continue;              // wave-uniform
+      const void* src = afr[i] < nfr || S::ROWS ? (const void*)(dyb + aoff[i]) : zero16;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(As + (NT * i + 64 * wave) * 16), 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < BIT; ++i) {
-      const int q = tid + NT * i;
-      if (q < BCH) {
-        const int sl = q >> 3, ch = q & 7;
-        const int f = sl / S::FS, rem = sl - f * S::FS;
-        const int fy = rem / S::FW, fx = rem - fy * S::FW;
-        int img, y0;
-        frame_origin(j, f, img, y0);
-        const int y = y0 + fy - 1, x = fx - 1;
-        const bool ok = img >= 0 && (unsigned)y < (unsigned)W && (unsigned)x < (unsigned)W;
-        rb[i] = ok ? *(const uint4*)(X + ((int64_t)(img * W + y) * W + x) * C + c0 + ch * 8)
-                   : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store = [&](int buf, const uint4 (&ra)[AIT], const uint4 (&rb)[BIT]) {
-    char* As = smem + buf * STAGE;
-    char* Bs = As + AROWS * ROWB;
-#pragma unroll
-    for (int i = 0; i < AIT; ++i) {
-      const int q = tid + NT * i;
-      if (q < ACH) *(uint4*)(As + swz_off(q >> 3, (q & 7) * 16)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BIT; ++i) {
-      const int q = tid + NT * i;
-      if (q < BCH) *(uint4*)(Bs + swz_off(q >> 3, (q & 7) * 16)) = rb[i];
+      if (NT * i + 64 * wave >= BCH) continue;              // wave-uniform
+      const bool ok = bfr[i] < nfr && (unsigned)(y0 + bfy[i]) < (unsigned)W;
+      const void* src = ok ? (const void*)(xb + boff[i]) : zero16;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bs + (NT * i + 64 * wave) * 16), 16, 0, 0);
     }
   };
   // transposing read (ds_read_b64_tr_b16): lane q of a 16-lane group gives
@@ -186,107 +222,131 @@ __global__ __launch_bounds__(768) void wgrad3_kernel(GemmParams p) {
   const int colA = wk * 32 + 16 * (grp & 1);   // co column base of the group
   const int colB = wc * 32 + 16 * (grp & 1);   // ci column base
   const int kb = 8 * (lane >> 5);              // pixel offset of the lane's half
-  // base[ph]: offset of the lane's element for a read whose first row is
-  // congruent to ph mod 4 (the row's multiple of 4 is added at the read)
+  // base[ph]: offset of the lane's element for a read whose compile-time
+  // first row is congruent to ph mod 4 (its multiple of 4 is added at the
+  // read); the patch bases include the wave's filter-row shift wr * FW
+  // (adding 4k rows adds 4k * ROWB: the swizzle depends on bit 1 only)
   int baseA[4], baseB[4];
 #pragma unroll
   for (int ph = 0; ph < 4; ++ph) {
     baseA[ph] = swz_off(ph + kb + (q >> 2), (colA + 4 * (q & 3)) * 2);
-    baseB[ph] = swz_off(ph + S::lane_slot(kb) + (q >> 2), (colB + 4 * (q & 3)) * 2);
+    baseB[ph] = swz_off(ph + wr * S::FW + S::lane_slot(kb) + (q >> 2), (colB + 4 * (q & 3)) * 2);
   }
-
-  // two register sets: the global loads of slice j + 2 are in flight while
-  // slice j computes and slice j + 1 (loaded one slice earlier) is stored
-  uint4 ra0[AIT], rb0[BIT], ra1[AIT], rb1[BIT];
-  if (cnt > 0) {
-    load(j0, ra0, rb0);
-    store(0, ra0, rb0);
-  }
-  if (cnt > 1) load(j0 + jst, ra1, rb1);
-  __syncthreads();
-  // i-th slice of the split: j0 + i * jst
-  auto step = [&](int i, int buf, uint4 (&la)[AIT], uint4 (&lb)[BIT], const uint4 (&sa)[AIT],
-                  const uint4 (&sb)[BIT]) {
-    if (i + 2 < cnt) load(j0 + (i + 2) * jst, la, lb);
-    const char* pa = smem + buf * STAGE;
-    const char* pb = pa + AROWS * ROWB;
-    // read of the 4-row block whose first row is row0 (compile-time) + lane term
-    auto rd = [&](const char* base, const int (&lbase)[4], int row0) {
-      return tr_read(base + lbase[row0 & 3], (row0 & ~3) * ROWB);
-    };
+  auto rd = [&](const char* base, const int (&lbase)[4], int row0) {
+    return tr_read(base + lbase[row0 & 3], (row0 & ~3) * ROWB);
+  };
+  // fragments of k step kk: dy (2 reads) and the patch rows of the wave's
+  // filter row (3 reads; W = 4: 2 per image-row half)
+  constexpr int NBR = W >= 8 ? 3 : 4;
+  auto read_k = [&](const char* pa, const char* pb, int kk, i16x4 (&fa)[2], i16x4 (&fbv)[NBR]) {
+    fa[0] = rd(pa, baseA, 16 * kk);
+    fa[1] = rd(pa, baseA, 16 * kk + 4);
+    if constexpr (W >= 8) {
+      const int r0 = S::slot(16 * kk, 0, 0);
+      fbv[0] = rd(pb, baseB, r0);
+      fbv[1] = rd(pb, baseB, r0 + 4);
+      fbv[2] = rd(pb, baseB, r0 + 8);
+    } else {
 #pragma unroll
-    for (int kk = 0; kk < S::PIX / 16; ++kk) {
-      i16x4 a0 = rd(pa, baseA, 16 * kk), a1 = rd(pa, baseA, 16 * kk + 4);
-      bf16x8 av;
-      __builtin_memcpy(&av, &a0, 8);
-      __builtin_memcpy((char*)&av + 8, &a1, 8);
-      // the wave's filter row is uniform: the three row variants are
-      // compile-time code paths selected once per k step.  The taps s = 0, 1,
-      // 2 of a row read the patch rows s .. s + 7 after the lane's first
-      // slot; the lane holds all rows of its column, so 4-row blocks at +0,
-      // +4, +8 give every tap: s = 1 shifts by one bf16 (byte align), s = 2
-      // by one dword (register choice).  With W = 4 the lane's 8 pixels span
-      // two image rows: each half does the same with blocks at +0 and +4.
-#pragma unroll
-      for (int r = 0; r < 3; ++r) {
-        if (r != wr) continue;
-        uint32_t d[2][6];     // [half][dword] of the loaded rows
-        if constexpr (W >= 8) {
-          const int r0 = S::slot(16 * kk, r, 0);
-          i16x4 v0 = rd(pb, baseB, r0), v1 = rd(pb, baseB, r0 + 4), v2 = rd(pb, baseB, r0 + 8);
-          uint32_t w[6];
-          __builtin_memcpy(&w[0], &v0, 8);
-          __builtin_memcpy(&w[2], &v1, 8);
-          __builtin_memcpy(&w[4], &v2, 8);
-          // tap s uses rows s .. s + 7 = dwords (shifted by s bf16)
-#pragma unroll
-          for (int s = 0; s < 3; ++s) {
-            uint32_t f[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              f[i] = s == 0 ? w[i] : (s == 2 ? w[i + 1] : __builtin_amdgcn_alignbyte(w[i + 1], w[i], 2));
-            bf16x8 bv;
-            __builtin_memcpy(&bv, f, 16);
-            acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[s], 0, 0, 0);
-          }
-          (void)d;
-        } else {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int r0 = S::slot(16 * kk + 4 * h, r, 0);
-            i16x4 v0 = rd(pb, baseB, r0), v1 = rd(pb, baseB, r0 + 4);
-            __builtin_memcpy(&d[h][0], &v0, 8);
-            __builtin_memcpy(&d[h][2], &v1, 8);
-          }
-#pragma unroll
-          for (int s = 0; s < 3; ++s) {
-            uint32_t f[4];
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-              for (int i = 0; i < 2; ++i)
-                f[2 * h + i] = s == 0 ? d[h][i]
-                                      : (s == 2 ? d[h][i + 1]
-                                                : __builtin_amdgcn_alignbyte(d[h][i + 1], d[h][i], 2));
-            bf16x8 bv;
-            __builtin_memcpy(&bv, f, 16);
-            acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[s], 0, 0, 0);
-          }
-        }
+      for (int h = 0; h < 2; ++h) {
+        const int r0 = S::slot(16 * kk + 4 * h, 0, 0);
+        fbv[2 * h] = rd(pb, baseB, r0);
+        fbv[2 * h + 1] = rd(pb, baseB, r0 + 4);
       }
     }
-    if (i + 1 < cnt) store(buf ^ 1, sa, sb);
-    __syncthreads();
   };
+  // MFMA operands of a k step: the dy fragment and the patch fragment of
+  // each tap.  The three taps s = 0, 1, 2 of the wave's filter row read the
+  // patch rows s .. s + 7 after the lane's first slot; the lane holds all rows
+  // of its column, so 4-row blocks at +0, +4, +8 give every tap: s = 1 shifts
+  // by one bf16 (byte align), s = 2 by one dword (register choice).  With
+  // W = 4 the lane's 8 pixels span two image rows: each half does the same
+  // with blocks at +0 and +4.
+  auto prep_k = [&](const i16x4 (&fa)[2], const i16x4 (&fbv)[NBR], bf16x8& av, bf16x8 (&bv)[3]) {
+    __builtin_memcpy(&av, &fa[0], 8);
+    __builtin_memcpy((char*)&av + 8, &fa[1], 8);
+    if constexpr (W >= 8) {
+      uint32_t w[6];
+      __builtin_memcpy(&w[0], &fbv[0], 8);
+      __builtin_memcpy(&w[2], &fbv[1], 8);
+      __builtin_memcpy(&w[4], &fbv[2], 8);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        uint32_t f[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          f[i] = s == 0 ? w[i] : (s == 2 ? w[i + 1] : __builtin_amdgcn_alignbyte(w[i + 1], w[i], 2));
+        __builtin_memcpy(&bv[s], f, 16);
+      }
+    } else {
+      uint32_t d[2][4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        __builtin_memcpy(&d[h][0], &fbv[2 * h], 8);
+        __builtin_memcpy(&d[h][2], &fbv[2 * h + 1], 8);
+      }
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        uint32_t f[4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+            f[2 * h + i] = s == 0 ? d[h][i]
+                                  : (s == 2 ? d[h][i + 1] : __builtin_amdgcn_alignbyte(d[h][i + 1], d[h][i], 2));
+        __builtin_memcpy(&bv[s], f, 16);
+      }
+    }
+  };
+
+  constexpr int KK = S::PIX / 16;
+  i16x4 fa[2], fbv[NBR];
+  // the i-th slice of the split from (pa, pb) while slice i + 1 is copied into (na, nb)
+  auto slice = [&](int i, const char* pa, const char* pb, char* na, char* nb) {
+    const bool more = i + 1 < cnt;
+    if (more) copy_slice(j0 + i + 1, na, nb);
+    // per k step: assemble this step's operands (read during the previous
+    // step), issue the next step's reads, then the MFMAs; the scheduling
+    // barriers keep that order (a pending global-to-LDS copy makes every LDS
+    // wait a full one, so operands are consumed before new reads are issued)
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      bf16x8 av, bv[3];
+      prep_k(fa, fbv, av, bv);
+      __builtin_amdgcn_sched_barrier(0);
+      i16x4 ga[2], gb[NBR];
+      if (kk + 1 < KK) read_k(pa, pb, kk + 1, ga, gb);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[s], av, acc[s], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kk + 1 < KK) {
+        fa[0] = ga[0];
+        fa[1] = ga[1];
+#pragma unroll
+        for (int u = 0; u < NBR; ++u) fbv[u] = gb[u];
+      }
+    }
+    // this wave's copies have landed; after the barrier every wave's have
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (more) read_k(na, nb, 0, fa, fbv);
+  };
+  if (cnt > 0) {
+    copy_slice(j0, sA0, sB0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    read_k(sA0, sB0, 0, fa, fbv);
+  }
   for (int i = 0; i < cnt; i += 2) {
-    step(i, 0, ra0, rb0, ra1, rb1);
-    if (i + 1 < cnt) step(i + 1, 1, ra1, rb1, ra0, rb0);
+    slice(i, sA0, sB0, sA1, sB1);
+    if (i + 1 < cnt) slice(i + 1, sA1, sB1, sA0, sB0);
   }
 
   // ---- epilogue: lane holds co = k0 + 32 wk + (lane & 31) and, per group of
   // 4 registers, ci = c0 + 32 wc + 8 (r / 4) + 4 (lane >> 5) + 0..3
   const int co = k0 + wk * 32 + (lane & 31);
-  float* out = (float*)p.out + (int64_t)blockIdx.y * p.split_stride;
+  float* out = (float*)p.out + (int64_t)by * p.split_stride;
 #pragma unroll
   for (int s = 0; s < 3; ++s)
 #pragma unroll
