@@ -16,9 +16,11 @@ steps between two device synchronisations; the batches are resident in HBM
 before timing.
 
 Prints ONE JSON line: samples/s over the K steps, the roofline position of
-the dominant GEMM kernel (timed live with HIP events on the worker streams
-during the timed steps), and the CPU oracle's throughput on a bounded sample
-of the same step, timed on this host.
+the dominant GEMM kernel (timed live with HIP events on the stream it runs on
+during the timed steps), the HBM roofline position of the fused weighted
+average + SGD launch of every timed step (event-timed on the main stream),
+the same kernel alone on 8 fp32 buffers of 25M elements, and the CPU oracle's
+throughput on a bounded sample of the same step, timed on this host.
 """
 import argparse
 import json
@@ -101,6 +103,34 @@ def cpu_baseline(wl, seed, samples):
                       % (wl.arch, sum(n), n, wl.workers, dt)}
 
 
+def standalone_wavg(reps=20):
+    """The fused weighted average + plain SGD alone on 8 fp32 gradient buffers
+    of 25M elements (partition sizes of the VGG-16 workload), event-timed."""
+    import torch
+    from paper_2110_08941_amd import hs
+    from paper_2110_08941_amd.configs import STANDALONE_WAVG as W
+    P, n = W["numel"], list(W["n"])
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    g = [torch.randn(P, device="cuda", generator=gen) for _ in n]
+    th = torch.randn(P, device="cuda", generator=gen)
+    ptrs = [t.data_ptr() for t in g]
+    for _ in range(3):
+        hs.wavg_sgd(ptrs, n, th.data_ptr(), 0, P, W["lr"], 0.0, 0.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        hs.wavg_sgd(ptrs, n, th.data_ptr(), 0, P, W["lr"], 0.0, 0.0)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / reps
+    nbytes = (len(n) * 4 + 8) * P
+    del g, th
+    return {"buffers": "%d x %d fp32, plain SGD" % (len(n), P), "bytes_per_launch": nbytes,
+            "avg_launch_us": round(us, 2), "achieved": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -125,11 +155,15 @@ def main():
     torch.cuda.synchronize()
     for w in tr.ws:
         hs.probe_read(w)                    # drop the warm-up launches
+    tr.time_opt = True
     t0 = time.perf_counter()
     for _ in range(args.steps):
         tr.step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    tr.time_opt = False
+    opt_us = [1e3 * e0.elapsed_time(e1) for e0, e1 in tr.opt_events]
+    opt_avg = sum(opt_us) / max(len(opt_us), 1)
     tr.flush()
     ms, launches, flops = 0.0, 0, 0.0
     for w in tr.ws:
@@ -159,10 +193,19 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": None,
                      "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),
                      "flops_per_launch": flops / max(launches, 1)},
+        "hbm_roofline": {"bound": "hbm", "kernel": "wavg_sgd (fused partition-weighted average of "
+                                                   "%d fp32 gradients + momentum SGD%s)"
+                                                   % (wl.workers, " + bf16 copy" if tr.bf16 else ""),
+                         "achieved": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                         "bytes_per_launch": tr.opt_bytes(), "avg_launch_us": round(opt_avg, 3),
+                         "launches": len(opt_us)},
         "partitions_last": parts[-1] if parts else None,
         "loss_last": [round(v, 4) for v in loss],
     }
     tr.close()
+    result["wavg_sgd_standalone"] = standalone_wavg()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_samples)
     print(json.dumps(result), flush=True)

@@ -105,20 +105,31 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = (f32x16){};
-    // taps: forward reads slot (row + r, x + s); data gradient (row + 2 - r, x + 2 - s)
-#pragma unroll 1
-    for (int tap = 0; tap < 9; ++tap) {
+    // taps: forward reads slot (row + r, x + s); data gradient (row + 2 - r, x + 2 - s).
+    // The fragments of the next k step (the next tap's first one after the
+    // last) are read while the current step's MFMAs run; the scheduling
+    // barriers keep the reads ahead of the MFMAs that hide them.  After the
+    // last tap the "next" reads repeat tap 8 (in the patch, never used).
+    auto read_frag = [&](int tap, int kq, uint4 (&fa)[2], uint4 (&fb)[2]) {
       const int r = tap / 3, s = tap - 3 * (tap / 3);
       const int dr = MODE == MODE_FWD ? r : 2 - r, ds = MODE == MODE_FWD ? s : 2 - s;
       const int slot0 = (2 * wave + dr) * P_FW + x + ds;
 #pragma unroll
+      for (int mb = 0; mb < 2; ++mb) fa[mb] = *(const uint4*)(Pl + pslot_off(slot0 + mb * P_FW, 2 * kq + kh));
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) fb[nb] = Wl[((kq * 9 + tap) * 2 + kh) * 64 + nb * 32 + x];
+    };
+    uint4 fa[2], fb[2];
+    read_frag(0, 0, fa, fb);
+#pragma unroll 1
+    for (int tap = 0; tap < 9; ++tap) {
+      const int ntap = tap + 1 < 9 ? tap + 1 : 8;
+#pragma unroll
       for (int kq = 0; kq < 4; ++kq) {
-        uint4 fa[2], fb[2];
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-          fa[mb] = *(const uint4*)(Pl + pslot_off(slot0 + mb * P_FW, 2 * kq + kh));
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) fb[nb] = Wl[((kq * 9 + tap) * 2 + kh) * 64 + nb * 32 + x];
+        uint4 na[2], nbv[2];
+        if (kq < 3) read_frag(tap, kq + 1, na, nbv);
+        else read_frag(ntap, 0, na, nbv);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
           bf16x8 av;
@@ -130,6 +141,11 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[mb][nb], 0, 0, 0);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        fa[0] = na[0];
+        fa[1] = na[1];
+        fb[0] = nbv[0];
+        fb[1] = nbv[1];
       }
     }
     __syncthreads();   // patch area free: stage the epilogue there

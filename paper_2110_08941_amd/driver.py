@@ -68,6 +68,8 @@ class Trainer:
             x, y = synth.batch(wl.in_shape, self.N, seed, b)
             self.batches.append((torch.from_numpy(x).to(self.dev), torch.from_numpy(y).to(self.dev)))
         self.t = 0
+        self.time_opt = False   # record events around the weighted-average + SGD launch
+        self.opt_events = []
         self.pending = []       # (step, partition, [(e0, e1)] or None) awaiting observation
         self.log = []           # per step: partition, tau, cp (if a window closed)
 
@@ -119,9 +121,15 @@ class Trainer:
             events = None
         else:
             events = self.launch_workers(n, x, y, timed=(self.clock == "measured"))
+        if self.time_opt:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(main)
         hs.wavg_sgd([g.data_ptr() for g in self.grads], n, self.theta.data_ptr(),
                     self.mom.data_ptr() if self.mom is not None else 0, self.P, wl.lr, wl.mu,
                     wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)
+        if self.time_opt:
+            e1.record(main)
+            self.opt_events.append((e0, e1))
         self.pending.append((t, n, events))
         self.t += 1
         if wl.window > 0 and len(self.pending) >= wl.window:
@@ -141,6 +149,17 @@ class Trainer:
             cp = self.part.observe(tau, speed) if self.wl.window > 0 else None
             self.log.append({"step": t, "n": list(n), "tau": tau, "speed": list(speed), "cp": cp})
         self.pending = []
+
+    def opt_bytes(self):
+        """Algorithmic HBM bytes of one weighted-average + SGD launch: M fp32
+        gradients read, theta read and written, the momentum buffer read and
+        written (if any), the bf16 copy written (if any)."""
+        b = self.M * 4 + 8
+        if self.mom is not None:
+            b += 8
+        if self.bf16:
+            b += 2
+        return b * self.P
 
     def run(self, steps=None):
         for _ in range(steps if steps is not None else self.steps):
