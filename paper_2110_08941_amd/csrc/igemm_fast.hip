@@ -130,12 +130,17 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   // class's taps only
   const bool par = (MODE == MODE_DGRAD) && p.par;
   const int cls = par ? (int)blockIdx.z : 0, ph = cls >> 1, pw = cls & 1;
-  const int ktiles = par ? p.ntap[cls] * (g.K / BKE) : p.ktiles;
+  // class 0 with a fused 1x1 stride-2 term: one more "tap" (position ntap[0])
+  // whose A is a2 at the class pixel's own grid point and whose B is b2
+  const bool extra = par && cls == 0 && p.a2 != nullptr;
+  const int ktiles = par ? (p.ntap[cls] + (extra ? 1 : 0)) * (g.K / BKE) : p.ktiles;
   int kt0 = blockIdx.y * p.kt_per_split;
   int kt1 = min(kt0 + p.kt_per_split, ktiles);
   int koff = 0, kend = p.K;   // K range of this split (WGRAD: one worker segment)
   if (MODE == MODE_WGRAD && p.nseg > 0) wgrad_split_range(p, BKE, koff, kend, kt0, kt1);
-  auto tap_id = [&](int t) { return par ? p.taps[cls][t] : t; };
+  // the fused term reads the grid point (h / 2, w / 2): the centre tap (1, 1)
+  // of the 3x3 filter (the term only exists for 3x3, pad 1, stride 2)
+  auto tap_id = [&](int t) { return par ? (t < p.ntap[cls] ? p.taps[cls][t] : 4) : t; };
 
   // ---- per-thread fixed state of the loaders
   int a_base[A_KC ? A_ITEMS : 1], a_pix[A_KC ? A_ITEMS : 1], a_y[A_KC ? A_ITEMS : 1],
@@ -243,6 +248,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
     } else if constexpr (MODE == MODE_DGRAD) {
       const int co = c0 + cchunk;
       const bool kok = co < g.K;
+      const T* asrc = (const T*)(extra && tpos == p.ntap[0] ? p.a2 : p.a);
 #pragma unroll
       for (int i = 0; i < A_ITEMS; ++i) {
         int ho = a_y[i] - r, wo = a_x[i] - s;
@@ -253,7 +259,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
           wo >>= 1;
         }
         ok = ok && (unsigned)ho < (unsigned)g.Ho && (unsigned)wo < (unsigned)g.Wo;
-        ra[i] = ok ? *(const uint4*)((const T*)p.a + a_base[i] + (ho * g.Wo + wo) * g.K + co)
+        ra[i] = ok ? *(const uint4*)(asrc + a_base[i] + (ho * g.Wo + wo) * g.K + co)
                    : make_uint4(0, 0, 0, 0);
       }
     } else {  // WGRAD A: dy[pixel][co], rows = co
@@ -281,7 +287,10 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
         rb[i] = (n < p.N && k < p.K) ? *(const uint4*)((const T*)p.b + (int64_t)n * p.K + k)
                                      : make_uint4(0, 0, 0, 0);
       }
-    } else if constexpr (MODE == MODE_DGRAD) {  // W[co][tap][ci], rows = ci
+    } else if constexpr (MODE == MODE_DGRAD) {  // W[co][tap][ci], rows = ci (b2: [co][ci])
+      const bool xt = extra && tpos == p.ntap[0];
+      const T* bsrc = (const T*)(xt ? p.b2 : p.b);
+      const int brs = xt ? 1 : RS, btap = xt ? 0 : tap;
 #pragma unroll
       for (int i = 0; i < B_ITEMS; ++i) {
         int rv, kq;
@@ -292,7 +301,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
         for (int j = 0; j < 4; ++j) {
           const int co = c0 + kq * 4 + j;
           rb[4 * i + j] = (uok && row < p.N && co < g.K)
-                              ? *(const uint4*)((const T*)p.b + ((int64_t)co * RS + tap) * g.C + row)
+                              ? *(const uint4*)(bsrc + ((int64_t)co * brs + btap) * g.C + row)
                               : make_uint4(0, 0, 0, 0);
         }
       }
@@ -605,7 +614,10 @@ static hipError_t launch_tiles_fast(const GemmParams& p0, int bm, int bn, int sp
   else p.kt_per_split = ceil_div(p.ktiles, splits);
   if (p.par) {   // classes differ in K; one split covers the largest
     int mx = 0;
-    for (int c = 0; c < 4; ++c) mx = p.ntap[c] > mx ? p.ntap[c] : mx;
+    for (int c = 0; c < 4; ++c) {
+      const int nt = p.ntap[c] + (c == 0 && p.a2 ? 1 : 0);
+      mx = nt > mx ? nt : mx;
+    }
     p.kt_per_split = mx * (p.g.K / BKE);
   }
   const dim3 grid(tiles_m * p.tiles_n, splits, p.par ? 4 : 1);

@@ -49,6 +49,12 @@ struct GemmParams {
   FastDiv HWh, Wh_;
   int ntap[4];
   int taps[4][4];
+  // ... and, with a2 set, class 0 (even h, even w) adds one more term: the
+  // data gradient of a 1x1 stride-2 convolution of the same input with
+  // weights b2 ([K][C]) applied to a2 ([n][Hh][Wh][K], the grid of a): the
+  // projection shortcut of a residual block, summed in the same reduction
+  const void* a2;
+  const void* b2;
   // WGRAD over worker segments: split blockIdx.y belongs to segment s when
   // seg_split[s] <= y < seg_split[s + 1]; segment s reduces over the pixels of
   // its samples seg_n0[s] .. seg_n0[s + 1] - 1, and every split writes its own

@@ -445,8 +445,15 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
 // dx = dgrad(dy) (+ addend) (* [mask > 0]); a stride-2 layer is computed by
 // output parity class when the fast kernel applies (each class sums over
 // its own taps only)
+// Data gradient of layer L.  With proj set (a 1x1 stride-2 projection of
+// the same input, its output gradient dproj), dx also receives the
+// projection's data gradient, summed in the same reduction; that needs the
+// stride-2 parity path, and when it is not available nothing is launched and
+// *fused is false (the caller then runs the two data gradients itself).
 hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, const void* addend,
-                      const void* mask) {
+                      const void* mask, const ConvL* proj = nullptr, const void* dproj = nullptr,
+                      bool* fused = nullptr) {
+  if (fused) *fused = false;
   GemmParams p = base_params(L, c.n);
   p.a = dy;
   p.b = c.W(L.w);
@@ -475,11 +482,23 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
           if (((ph + L.pad - r) & 1) == 0 && ((pw + L.pad - s2) & 1) == 0) q.taps[cls][nt++] = r * L.k + s2;
       q.ntap[cls] = nt;
     }
+    double flops = layer_flops(L, c.n);
+    const bool fuse = proj && dproj && fused && L.k == 3 && L.pad == 1 && proj->k == 1 &&
+                      proj->stride == 2 && proj->pad == 0 && proj->cin == L.cin &&
+                      proj->cout == L.cout && proj->H == L.H && proj->W == L.W;
+    if (fuse) {
+      q.a2 = dproj;
+      q.b2 = c.W(proj->w);
+      flops += layer_flops(*proj, c.n);
+    }
     int fbm = 0, fbn = 0;
     pick_fast_tiles(MODE_DGRAD, q.M, q.N, fbm, fbn);
-    if (igemm_fast_ok(MODE_DGRAD, c.bf, q, fbm, fbn))
-      return gemm(c, MODE_DGRAD, q, veca, vecb, fbm, fbn, 1, layer_flops(L, c.n));
+    if (igemm_fast_ok(MODE_DGRAD, c.bf, q, fbm, fbn) && (fuse || !proj)) {
+      if (fuse) *fused = true;
+      return gemm(c, MODE_DGRAD, q, veca, vecb, fbm, fbn, 1, flops);
+    }
   }
+  if (proj) return hipSuccess;   // fusion requested but not possible
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
   return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
@@ -766,8 +785,14 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     if (b.proj) {
       HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
       HS_TRY(conv_wgrad(c, b.cp, P3, in));
-      HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));                // shortcut grad
-      HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in));                          // dIn * [in > 0]
+      // dIn * [in > 0], the shortcut's data gradient summed in the same pass
+      // where the layer shapes allow it, else added from its own output
+      bool fused = false;
+      HS_TRY(conv_dgrad(c, b.c1, P2, P4, nullptr, in, &b.cp, P3, &fused));
+      if (!fused) {
+        HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));              // shortcut grad
+        HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in));
+      }
       gi = fr[2];
     } else {
       HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in));                          // dIn * [in > 0]
