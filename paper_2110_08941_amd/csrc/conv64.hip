@@ -100,6 +100,28 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
     __syncthreads();
     if (t + gridDim.x < ntiles) load_patch(t + gridDim.x, pre);
 
+    // Epilogue operands (addend, mask) of this tile.  A lane's rows of the
+    // epilogue are fixed: row 16 i + lane / 4 of the wave's 64 (mb * 32 +
+    // pixel), channels 8 (lane & 3) + 0..7 of each 32-channel half.  The
+    // first half's are loaded now, while the taps run; the second half's when
+    // the epilogue starts, while the first half is written.
+    const int eb = t / tiles_per_img, ey0 = (t - eb * tiles_per_img) * P_ROWS;
+    auto epi_off = [&](int nb, int i) -> int64_t {
+      const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+      const int y = ey0 + 2 * wave + (row >> 5), xx = row & 31;
+      return (((int64_t)eb * H + y) * P_W + xx) * 64 + nb * 32 + c8;
+    };
+    constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
+    uint4 add_pre[2][EADD ? 4 : 1], mask_pre[2][EMASK ? 4 : 1];
+    auto load_epi = [&](int nb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (EADD) add_pre[nb][i] = *(const uint4*)((const bf16_t*)p.addend + epi_off(nb, i));
+        if constexpr (EMASK) mask_pre[nb][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
+      }
+    };
+    if constexpr (EADD || EMASK) load_epi(0);
+
     f32x16 acc[2][2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
@@ -149,10 +171,10 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
       }
     }
     __syncthreads();   // patch area free: stage the epilogue there
+    if constexpr (EADD || EMASK) load_epi(1);
 
     // ---- epilogue, one 32-channel half at a time: lane holds pixel x of
     // output row 2 wave + mb and channels 8 q + 4 kh + 0..3 of half nb
-    const int b = t / tiles_per_img, y0 = (t - b * tiles_per_img) * P_ROWS;
     float* E = (float*)Pl + wave * 64 * EROW;
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -167,8 +189,7 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);   // row: mb * 32 + pixel
-        const int y = y0 + 2 * wave + (row >> 5), xx = row & 31;
-        const int64_t off = (((int64_t)b * H + y) * P_W + xx) * 64 + nb * 32 + c8;
+        const int64_t off = epi_off(nb, i);
         const float4 lo = *(const float4*)(E + row * EROW + c8);
         const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
         float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
@@ -177,7 +198,7 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
           for (int e = 0; e < 8; ++e) v[e] += p.bias[nb * 32 + c8 + e];
         }
         if constexpr ((EPI & EPI_ADD) != 0) {
-          const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
+          const uint4 u = add_pre[nb][i];
           const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -190,7 +211,7 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
           for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
         }
         if constexpr ((EPI & EPI_MASK) != 0) {
-          const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
+          const uint4 u = mask_pre[nb][i];
           const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
