@@ -396,10 +396,30 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   }
 
   if constexpr (STAGE_EPI) {
-    // the loop ended with a barrier: B is no longer read
+    // The loop ended with a barrier: B is no longer read.  Each wave stages
+    // its tile in its own region and reads back only its own rows, so the
+    // chunks need no block barrier (one wave's LDS operations run in order).
+    // The addend / mask rows of chunk nb + 1 are loaded while chunk nb is
+    // written; rows past M re-read row M - 1 and are not stored.
     float* E = Ewave;
+    constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
+    auto epi_off = [&](int nb, int i) -> int64_t {
+      const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+      const int m = m0 + row < p.M ? m0 + row : p.M - 1;
+      return (int64_t)m * p.N + n0 + nb * 32 + c8;
+    };
+    uint4 addv[2][EADD ? 4 : 1], maskv[2][EMASK ? 4 : 1];
+    auto load_epi = [&](int nb, int slot) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (EADD) addv[slot][i] = *(const uint4*)((const bf16_t*)p.addend + epi_off(nb, i));
+        if constexpr (EMASK) maskv[slot][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
+      }
+    };
+    load_epi(0, 0);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
+      if (nb + 1 < NB) load_epi(nb + 1, (nb + 1) & 1);
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -407,39 +427,37 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
           *(float4*)(E + (32 * mb + (lane & 31)) * EROW + 8 * q + 4 * kh) =
               make_float4(acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
                           acc[mb][nb][4 * q + 3]);
-      __syncthreads();
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
         const int m = m0 + row;
-        if (m < p.M) {
-          const float4 lo = *(const float4*)(E + row * EROW + c8);
-          const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
-          float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-          const int64_t off = (int64_t)m * p.N + n0 + nb * 32 + c8;
-          if constexpr ((EPI & EPI_ADD) != 0) {
-            const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if constexpr (EADD) {
+          const uint4 u = addv[nb & 1][i];
+          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
-              v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
-            }
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
+            v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
           }
-          if constexpr ((EPI & EPI_MASK) != 0) {
-            const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
-              if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
-            }
-          }
-          *(uint4*)((bf16_t*)p.out + off) =
-              make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
         }
+        if constexpr (EMASK) {
+          const uint4 u = maskv[nb & 1][i];
+          const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
+            if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
+          }
+        }
+        if (m < p.M)
+          *(uint4*)((bf16_t*)p.out + (int64_t)m * p.N + n0 + nb * 32 + c8) =
+              make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
       }
-      __syncthreads();
+      __builtin_amdgcn_wave_barrier();
     }
     return;
   }
