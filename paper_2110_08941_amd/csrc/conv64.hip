@@ -185,7 +185,9 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
           *(float4*)(E + (32 * mb + x) * EROW + 8 * q4 + 4 * kh) =
               make_float4(acc[mb][nb][4 * q4], acc[mb][nb][4 * q4 + 1], acc[mb][nb][4 * q4 + 2],
                           acc[mb][nb][4 * q4 + 3]);
-      __syncthreads();
+      // a wave reads back only its own staging rows (its LDS operations run
+      // in order): no block barrier between the halves
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);   // row: mb * 32 + pixel
@@ -222,8 +224,9 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
         *(uint4*)((bf16_t*)p.out + off) =
             make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
       }
-      __syncthreads();
+      __builtin_amdgcn_wave_barrier();
     }
+    __syncthreads();   // every wave is done with the patch area: the next tile's patch goes there
   }
 }
 
