@@ -444,8 +444,15 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   if constexpr (STAGE_EPI) {
     constexpr int SMEM = 2 * (BM + BN) * 128;
     constexpr int CW = 4 * WTM * (WTN + 4) * 4 <= SMEM ? WTN : WTN / 2;
-    constexpr int EROW = CW + 4, LPR = CW / 8, RPP = 64 / LPR;
+    constexpr int EROW = CW + 4, LPR = CW / 8, RPP = 64 / LPR, NRI = WTM / RPP;
+    constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
     static_assert(4 * WTM * EROW * 4 <= SMEM, "epilogue staging exceeds LDS");
+    // The main loop ended with a barrier.  Each wave stages its sub-tile in
+    // its own region and reads back only its own rows (one wave's LDS
+    // operations run in order), so chunks need no block barrier.  All addend
+    // / mask rows of a chunk are loaded before any output row is stored (a
+    // store between them would order every load after it); rows or columns
+    // outside the output re-read element 0 and are not stored.
     float* E = (float*)smem + wave * WTM * EROW;
 #pragma unroll
     for (int c0 = 0; c0 < WTN; c0 += CW) {
@@ -458,46 +465,53 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
             *(float4*)(E + (16 * i + (lane & 15)) * EROW + col) =
                 make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
         }
-      __syncthreads();
+      __builtin_amdgcn_wave_barrier();
+      int64_t offs[NRI];
+      bool oks[NRI];
+      uint4 addv[EADD ? NRI : 1], maskv[EMASK ? NRI : 1];
 #pragma unroll
-      for (int r0 = 0; r0 < WTM; r0 += RPP) {
-        const int row = r0 + lane / LPR, c8 = 8 * (lane % LPR);
+      for (int k = 0; k < NRI; ++k) {
+        const int row = k * RPP + lane / LPR, c8 = 8 * (lane % LPR);
         const int m = m0 + wm * WTM + row;
         const int n = n0 + wn * WTN + c0 + c8;
-        if (m < p.M && n < p.N) {
-          int64_t orow = m;
-          if (par) {
-            const int b = (int)fdiv(m, p.HWh), rem = m - b * p.Hh * p.Wh;
-            const int h2 = (int)fdiv(rem, p.Wh_), w2 = rem - h2 * p.Wh;
-            orow = ((int64_t)b * g.H + 2 * h2 + ph) * g.W + 2 * w2 + pw;
-          }
-          const int64_t off = orow * p.N + n;
-          const float4 lo = *(const float4*)(E + row * EROW + c8);
-          const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
-          float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-          if constexpr ((EPI & EPI_ADD) != 0) {
-            const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
-              v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
-            }
-          }
-          if constexpr ((EPI & EPI_MASK) != 0) {
-            const uint4 u = *(const uint4*)((const bf16_t*)p.mask + off);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
-              if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
-            }
-          }
-          *(uint4*)((bf16_t*)p.out + off) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+        oks[k] = m < p.M && n < p.N;
+        int64_t orow = m;
+        if (par) {
+          const int b = (int)fdiv(m, p.HWh), rem = m - b * p.Hh * p.Wh;
+          const int h2 = (int)fdiv(rem, p.Wh_), w2 = rem - h2 * p.Wh;
+          orow = ((int64_t)b * g.H + 2 * h2 + ph) * g.W + 2 * w2 + pw;
         }
+        offs[k] = oks[k] ? orow * p.N + n : 0;
+        if constexpr (EADD) addv[k] = *(const uint4*)((const bf16_t*)p.addend + offs[k]);
+        if constexpr (EMASK) maskv[k] = *(const uint4*)((const bf16_t*)p.mask + offs[k]);
       }
-      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < NRI; ++k) {
+        const int row = k * RPP + lane / LPR, c8 = 8 * (lane % LPR);
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if constexpr (EADD) {
+          const uint32_t w[4] = {addv[k].x, addv[k].y, addv[k].z, addv[k].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += bf2f((bf16_t)(w[e] & 0xffffu));
+            v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
+          }
+        }
+        if constexpr (EMASK) {
+          const uint32_t w[4] = {maskv[k].x, maskv[k].y, maskv[k].z, maskv[k].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (!(bf2f((bf16_t)(w[e] & 0xffffu)) > 0.f)) v[2 * e] = 0.f;
+            if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
+          }
+        }
+        if (oks[k])
+          *(uint4*)((bf16_t*)p.out + offs[k]) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                           pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+      }
+      __builtin_amdgcn_wave_barrier();
     }
     return;
   }
