@@ -59,6 +59,11 @@ PATCH_SHAPES = [
     (130, 2, 2, 512, 512, 3, 1, 1),   # 128 images per tile, 2 left over
     (4, 8, 8, 192, 192, 3, 1, 1),     # 64-column tiles, one partial tile
     (5, 8, 8, 128, 64, 3, 1, 1),
+    # stride 2 with bf16 outputs (the data gradient by output parity class)
+    (3, 32, 32, 64, 128, 3, 2, 1),
+    (9, 16, 16, 128, 256, 3, 2, 1),
+    (37, 8, 8, 256, 128, 3, 2, 1),
+    (4, 16, 16, 64, 64, 3, 2, 1),
 ]
 
 
