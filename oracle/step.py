@@ -38,6 +38,23 @@ def weighted_average(grads, n):
     return out
 
 
+def mean_average(grads):
+    """g = (1/M) sum_m g_m: the exchange of Sync-SGD and of Dynamic
+    Partitioning without the enhancement (Section 5), whatever the partition
+    sizes."""
+    out = np.zeros_like(np.asarray(grads[0], dtype=np.float64))
+    for gm in grads:
+        out += np.asarray(gm, dtype=np.float64)
+    return out / float(len(grads))
+
+
+def cosine_lr(lr0, t, total, lr_min=0.0):
+    """Cosine annealing (Section 5 names the schedule; SGDR without restarts):
+    lr_t = lr_min + (lr0 - lr_min) (1 + cos(pi t / total)) / 2 for step t of
+    `total`."""
+    return lr_min + (lr0 - lr_min) * (1.0 + math.cos(math.pi * t / total)) / 2.0
+
+
 def sgd_step(theta, g, buf, lr, mu, wd):
     """One SGD step with momentum and coupled weight decay (Section 1 update
     rule; Section 5 hyper-parameters).  Returns (theta', buf')."""
@@ -109,10 +126,11 @@ def even_split(m, total):
 # ----------------------------------------------------------------------------
 # one step and many steps
 # ----------------------------------------------------------------------------
-def step(net_grad, theta, buf, x, y, n, lr, mu, wd):
+def step(net_grad, theta, buf, x, y, n, lr, mu, wd, exchange="edp"):
     """One synchronous step: every worker's gradient on its slice of the batch
-    (worker m owns rows [o_m, o_m + n_m), o_m = sum_{j<m} n_j), the weighted
-    average, the SGD update.  net_grad(theta, x_m, y_m) -> (loss_m, g_m).
+    (worker m owns rows [o_m, o_m + n_m), o_m = sum_{j<m} n_j), the exchange
+    (exchange="edp": partition-weighted average; "mean": the plain mean), the
+    SGD update.  net_grad(theta, x_m, y_m) -> (loss_m, g_m).
     Returns dict with grads, losses, gbar, theta, buf."""
     grads, losses, o = [], [], 0
     for nm in n:
@@ -123,41 +141,85 @@ def step(net_grad, theta, buf, x, y, n, lr, mu, wd):
         grads.append(g)
         losses.append(loss)
         o += nm
-    gbar = weighted_average(grads, n)
+    gbar = weighted_average(grads, n) if exchange == "edp" else mean_average(grads)
     theta2, buf2 = sgd_step(theta, gbar, buf, lr, mu, wd)
     return {"grads": grads, "losses": losses, "gbar": gbar, "theta": theta2, "buf": buf2}
 
 
-def run(net_grad, theta, batches, speeds, window, lr, mu, wd, times=None, n0=None):
-    """Multi-step driver of Dynamic Partitioning (Algorithm 1) with EDP weighting.
+def smooth_cp(estimator, c, state):
+    """Compute power across windows (Section 4.1: the previous epoch only, or a
+    history of epochs).  c: this window's estimate n / mean X.  estimator:
+    ("window",) -> c; ("ema", alpha) -> alpha c + (1 - alpha) previous (the
+    first window: c); ("history", h) -> mean of the last h windows' estimates,
+    summed oldest first.  state: dict carried across windows."""
+    kind = estimator[0]
+    if kind == "window":
+        return list(c)
+    if kind == "ema":
+        alpha = float(estimator[1])
+        prev = state.get("prev")
+        out = list(c) if prev is None else [alpha * cm + (1.0 - alpha) * pm for cm, pm in zip(c, prev)]
+        state["prev"] = out
+        return out
+    if kind == "history":
+        hist = state.setdefault("hist", [])
+        hist.append(list(c))
+        if len(hist) > int(estimator[1]):
+            hist.pop(0)
+        out = []
+        for j in range(len(c)):
+            s = 0.0
+            for h in hist:
+                s = s + h[j]
+            out.append(s / float(len(hist)))
+        return out
+    raise ValueError("unknown estimator %r" % (estimator,))
+
+
+def run(net_grad, theta, batches, speeds, window, lr, mu, wd, times=None, n0=None,
+        exchange="edp", delays=None, estimator=("window",), lr_total=None, lr_min=0.0):
+    """Multi-step driver of Dynamic Partitioning (Algorithm 1).
 
     batches[t] = (x_t, y_t); speeds[t][m] = s_m at step t.  The time worker m
-    needs for its mini-batch at step t is X_m = tau_m / s_m, where tau_m is the
-    measured device time of its gradient (``times[t][m]``), or, without
-    measured times, the model clock X_m = n_m / s_m.  After every ``window``
-    steps, X_m is averaged over the window (summed in step order), CP_m = n_m /
-    mean X_m (Eq. (2)), and the next window's partition is repartition(CP, N).
-    The first window uses the even split (Algorithm 1, t == 0) unless n0 is
-    given.  Returns dict with theta, buf, partitions (per step), losses."""
+    needs for its mini-batch at step t is X_m = tau_m / s_m + delay_m, where
+    tau_m is the measured device time of its gradient (``times[t][m]``), or,
+    without measured times, the model clock X_m = n_m / s_m; delay_m is the
+    additive per-batch delay by which Section 5 simulates heterogeneity (none
+    by default).  After every ``window`` steps, X_m is averaged over the window
+    (summed in step order), c_m = n_m / mean X_m (Eq. (2)), CP =
+    smooth_cp(estimator, c) and the next window's partition is repartition(CP,
+    N); window = 0 keeps the partition (Sync-SGD).  The first window uses the
+    even split (Algorithm 1, t == 0) unless n0 is given.  exchange: "edp"
+    (partition-weighted, Section 4.2) or "mean" (Sync-SGD and DP-SGD).  With
+    lr_total, step t uses cosine_lr(lr, t, lr_total, lr_min).  Returns dict
+    with theta, buf, partitions (per step), losses, cps, xs (X_m per step)."""
     total = int(np.shape(batches[0][1])[0])
     m = len(speeds[0])
     n = list(n0) if n0 is not None else even_split(m, total)
     buf = None
-    parts, losses, cps = [], [], []
+    parts, losses, cps, xs = [], [], [], []
     xsum = [0.0] * m
+    state = {}
     for t, (x, y) in enumerate(batches):
         parts.append(list(n))
-        out = step(net_grad, theta, buf, x, y, n, lr, mu, wd)
+        lr_t = cosine_lr(lr, t, lr_total, lr_min) if lr_total else lr
+        out = step(net_grad, theta, buf, x, y, n, lr_t, mu, wd, exchange)
         theta, buf = out["theta"], out["buf"]
         losses.append(out["losses"])
+        xt = []
         for j in range(m):
             tau = float(times[t][j]) if times is not None else float(n[j])
-            xsum[j] = xsum[j] + tau / float(speeds[t][j])
-        if (t + 1) % window == 0:
+            xj = tau / float(speeds[t][j])
+            if delays is not None:
+                xj = xj + float(delays[j])
+            xt.append(xj)
+            xsum[j] = xsum[j] + xj
+        xs.append(xt)
+        if window > 0 and (t + 1) % window == 0:
             xbar = [v / float(window) for v in xsum]
-            cp = estimate_cp(n, xbar)
+            cp = smooth_cp(estimator, estimate_cp(n, xbar), state)
             cps.append(cp)
             n = repartition(cp, total)
             xsum = [0.0] * m
     return {"theta": theta, "buf": buf, "partitions": parts, "losses": losses,
-            "cps": cps, "next_partition": n}
+            "cps": cps, "xs": xs, "next_partition": n}

@@ -165,3 +165,109 @@ def test_sgd_closed_form():
     # plain SGD (mu = 0, wd = 0) is the Section 1 update theta - lr g
     t0, _ = S.sgd_step(th, g1, None, lr, 0.0, 0.0)
     np.testing.assert_allclose(t0, th - lr * g1, rtol=0, atol=1e-15)
+
+
+# ----------------------------------------------------------------------------
+# Sync-SGD / DP-SGD exchange, estimators across windows, cosine schedule,
+# additive delays (Section 5 comparison)
+# ----------------------------------------------------------------------------
+def _quad_grad(theta, x, y):
+    """Per-worker loss (1/n) sum_i 0.5 ||theta - x_i||^2; gradient theta - mean x_i."""
+    d = theta[None, :] - x
+    return 0.5 * float((d * d).sum()) / len(x), d.mean(axis=0)
+
+
+def test_edp_weighting_recovers_full_batch_gradient():
+    """With per-worker mean gradients, weights n_m / N give exactly the gradient
+    of the whole batch (the reason for the Section 4.2 weighting); the plain mean
+    does so only for equal partitions."""
+    rng = np.random.default_rng(11)
+    theta = rng.standard_normal(5)
+    x = rng.standard_normal((12, 5))
+    y0 = np.zeros(12, dtype=np.int64)
+    n = [7, 3, 2]
+    full = theta - x.mean(axis=0)
+    edp = S.step(_quad_grad, theta, None, x, y0, n, 0.1, 0.0, 0.0, "edp")
+    mean = S.step(_quad_grad, theta, None, x, y0, n, 0.1, 0.0, 0.0, "mean")
+    np.testing.assert_allclose(edp["gbar"], full, rtol=0, atol=1e-14)
+    per = [theta - x[0:7].mean(0), theta - x[7:10].mean(0), theta - x[10:12].mean(0)]
+    np.testing.assert_allclose(mean["gbar"], (per[0] + per[1] + per[2]) / 3, rtol=0, atol=1e-14)
+    assert np.abs(mean["gbar"] - full).max() > 1e-3
+    eq = [4, 4, 4]
+    a = S.step(_quad_grad, theta, None, x, y0, eq, 0.1, 0.0, 0.0, "edp")["gbar"]
+    b = S.step(_quad_grad, theta, None, x, y0, eq, 0.1, 0.0, 0.0, "mean")["gbar"]
+    np.testing.assert_allclose(a, full, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(b, full, rtol=0, atol=1e-14)
+
+
+def test_mean_average_closed_form():
+    g = [np.full(3, 1.0), np.full(3, 2.0), np.full(3, 6.0)]
+    np.testing.assert_array_equal(S.mean_average(g), np.full(3, 3.0))
+
+
+def test_cosine_lr_closed_forms():
+    """Cosine annealing: lr0 at t = 0, lr_min at t = T, the midpoint at T / 2,
+    symmetric about T / 2 and non-increasing."""
+    lr0, lmin, T = 0.1, 0.001, 40
+    assert S.cosine_lr(lr0, 0, T, lmin) == lr0
+    assert abs(S.cosine_lr(lr0, T, T, lmin) - lmin) < 1e-17
+    assert abs(S.cosine_lr(lr0, T // 2, T, lmin) - (lr0 + lmin) / 2) < 1e-16
+    v = [S.cosine_lr(lr0, t, T, lmin) for t in range(T + 1)]
+    assert all(a >= b for a, b in zip(v, v[1:]))
+    for t in range(T + 1):
+        assert abs(v[t] + v[T - t] - (lr0 + lmin)) < 1e-16
+    assert abs(S.cosine_lr(1.0, 1, 3) - 0.75) < 1e-16        # (1 + cos(pi/3)) / 2
+
+
+def test_smooth_cp_special_cases_and_worked_examples():
+    """EMA with alpha = 1 and a history of 1 are the single-window estimate;
+    a constant estimate is a fixed point of both; hand-computed sequences."""
+    seq = [[2.0, 1.0], [4.0, 3.0], [6.0, 9.0]]
+    for est in (("ema", 1.0), ("history", 1)):
+        st = {}
+        for c in seq:
+            assert S.smooth_cp(est, c, st) == c
+    for est in (("ema", 0.3), ("history", 4)):
+        st = {}
+        for _ in range(6):
+            np.testing.assert_allclose(S.smooth_cp(est, [1.5, 0.25], st), [1.5, 0.25], rtol=4e-16)
+    st = {}
+    out = [S.smooth_cp(("ema", 0.5), c, st) for c in seq]
+    assert out == [[2.0, 1.0], [3.0, 2.0], [4.5, 5.5]]
+    st = {}
+    out = [S.smooth_cp(("history", 2), c, st) for c in seq]
+    assert out == [[2.0, 1.0], [3.0, 2.0], [5.0, 6.0]]
+    with pytest.raises(ValueError):
+        S.smooth_cp(("median", 3), [1.0], {})
+
+
+def _zero_grad(theta, x, y):
+    return 0.0, np.zeros_like(theta)
+
+
+def test_run_additive_delay_reaches_equal_times():
+    """Model clock with speeds 1 and a delay of 4 on worker 1: X_m = n_m + d_m.
+    From the even split [4, 4], Algorithm 1 moves to [5, 3], then [6, 2], where
+    both workers take 6 (Eq. (3): equal predicted times) and it stays."""
+    theta = np.zeros(2)
+    batches = [(np.zeros((8, 2)), np.zeros(8, dtype=np.int64))] * 5
+    out = S.run(_zero_grad, theta, batches, [[1.0, 1.0]] * 5, 1, 0.1, 0.0, 0.0, delays=[0.0, 4.0])
+    assert out["partitions"] == [[4, 4], [5, 3], [6, 2], [6, 2], [6, 2]]
+    assert out["xs"][0] == [4.0, 8.0] and out["xs"][2] == [6.0, 6.0]
+    # window 0: the partition never moves (Sync-SGD); the slowest worker sets the step
+    fixed = S.run(_zero_grad, theta, batches, [[1.0, 1.0]] * 5, 0, 0.1, 0.0, 0.0, delays=[0.0, 4.0])
+    assert fixed["partitions"] == [[4, 4]] * 5 and fixed["cps"] == []
+    assert [max(x) for x in fixed["xs"]] == [8.0] * 5
+
+
+def test_run_cosine_schedule_closed_form():
+    """With zero gradients and no momentum, theta_{t+1} = theta_t (1 - lr_t wd)."""
+    theta = np.array([1.0, -2.0])
+    T, wd = 6, 0.5
+    batches = [(np.zeros((4, 2)), np.zeros(4, dtype=np.int64))] * T
+    out = S.run(_zero_grad, theta, batches, [[1.0, 1.0]] * T, 2, 0.4, 0.0, wd, lr_total=T,
+                lr_min=0.1)
+    expect = theta.copy()
+    for t in range(T):
+        expect = expect * (1.0 - (0.1 + 0.3 * (1 + math.cos(math.pi * t / T)) / 2) * wd)
+    np.testing.assert_allclose(out["theta"], expect, rtol=1e-15, atol=0)
