@@ -197,6 +197,25 @@ hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n);
 hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
                                  int32_t* repartitioned, double* cp_out);
 
+/* Compute-power estimator across windows (Section 4.1: the estimate can use
+ * the previous epoch only, which follows changes quickly, or a history of
+ * epochs, which is steadier).  c_k is window k's estimate n / mean X
+ * (Eq. (2)); the partition of window k + 1 is repartition(CP_k) with
+ *   HS_CP_WINDOW  (the default):  CP_k = c_k;
+ *   HS_CP_EMA:      CP_k = alpha * c_k + (1 - alpha) * CP_{k-1}, CP_0 = c_0
+ *                   (0 < alpha <= 1);
+ *   HS_CP_HISTORY:  CP_k = (c_{k-h+1} + ... + c_k) / h, the mean of the last
+ *                   h = min(history, k + 1) estimates, summed oldest first
+ *                   (1 <= history <= 1024).
+ * Double arithmetic in exactly this order, no fused operations.  Setting an
+ * estimator clears its history; cp_out of hs_partitioner_observe receives
+ * CP_k. */
+#define HS_CP_WINDOW 0
+#define HS_CP_EMA 1
+#define HS_CP_HISTORY 2
+hs_status hs_partitioner_set_estimator(hs_partitioner* p, int32_t kind, double alpha,
+                                       int32_t history);
+
 /* ------------------------------------------------------------- probing -- */
 
 /* Timing probe of one implicit-GEMM kernel instantiation inside

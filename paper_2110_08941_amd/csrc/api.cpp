@@ -33,6 +33,11 @@ struct hs_partitioner {
   int32_t M, N, window, steps_in_window;
   std::vector<int32_t> n;
   std::vector<double> xsum;
+  // compute-power estimator across windows (hs_partitioner_set_estimator)
+  int32_t est_kind = HS_CP_WINDOW, est_history = 1;
+  double est_alpha = 1.0;
+  std::vector<double> cp_prev;                 // EMA: the previous estimate
+  std::vector<std::vector<double>> cp_hist;    // HISTORY: the last windows' estimates, oldest first
 };
 
 namespace {
@@ -491,6 +496,23 @@ hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n) {
   return ok();
 }
 
+hs_status hs_partitioner_set_estimator(hs_partitioner* p, int32_t kind, double alpha,
+                                       int32_t history) {
+  if (!p) return fail(HS_ERR_INVALID, "hs_partitioner_set_estimator: NULL pointer");
+  if (kind != HS_CP_WINDOW && kind != HS_CP_EMA && kind != HS_CP_HISTORY)
+    return fail(HS_ERR_INVALID, "hs_partitioner_set_estimator: unknown kind %d", kind);
+  if (kind == HS_CP_EMA && !(alpha > 0.0 && alpha <= 1.0))
+    return fail(HS_ERR_INVALID, "hs_partitioner_set_estimator: need 0 < alpha <= 1");
+  if (kind == HS_CP_HISTORY && (history < 1 || history > 1024))
+    return fail(HS_ERR_INVALID, "hs_partitioner_set_estimator: need 1 <= history <= 1024");
+  p->est_kind = kind;
+  p->est_alpha = alpha;
+  p->est_history = history;
+  p->cp_prev.clear();
+  p->cp_hist.clear();
+  return ok();
+}
+
 hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
                                  int32_t* repartitioned, double* cp_out) {
   if (!p || !tau || !speed) return fail(HS_ERR_INVALID, "hs_partitioner_observe: NULL pointer");
@@ -506,6 +528,21 @@ hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const dou
   for (int m = 0; m < p->M; ++m) xbar[m] = p->xsum[m] / (double)p->window;
   hs_status st = hs_estimate_cp(p->n.data(), xbar.data(), p->M, cp.data());
   if (st != HS_OK) return st;
+  // smoothing across windows (Section 4.1: the previous epoch only, or a
+  // history of epochs); every operation in this order, no fused ones
+  if (p->est_kind == HS_CP_EMA) {
+    if (!p->cp_prev.empty())
+      for (int m = 0; m < p->M; ++m) cp[m] = p->est_alpha * cp[m] + (1.0 - p->est_alpha) * p->cp_prev[m];
+    p->cp_prev = cp;
+  } else if (p->est_kind == HS_CP_HISTORY) {
+    p->cp_hist.push_back(cp);
+    if ((int32_t)p->cp_hist.size() > p->est_history) p->cp_hist.erase(p->cp_hist.begin());
+    for (int m = 0; m < p->M; ++m) {
+      double sum = 0.0;
+      for (const std::vector<double>& h : p->cp_hist) sum = sum + h[m];
+      cp[m] = sum / (double)p->cp_hist.size();
+    }
+  }
   std::vector<int32_t> next(p->M);
   st = hs_repartition(cp.data(), p->M, p->N, next.data());
   if (st != HS_OK) return st;

@@ -18,6 +18,8 @@ weight gradients per worker).  Per-worker device times do not exist there,
 so it requires clock="model".
 PyTorch is used for device memory, streams and events only.
 """
+import math
+
 import numpy as np
 import torch
 
@@ -27,15 +29,31 @@ from .configs import WORKLOADS, Workload
 
 class Trainer:
     def __init__(self, workload, seed=0, clock="measured", device="cuda:0", n_batches=4,
-                 max_n=None, steps=None, theta0=None, grouped=False):
+                 max_n=None, steps=None, theta0=None, grouped=False, exchange="edp",
+                 delays=None, estimator=("window",), lr_schedule=None, serial=False):
         self.wl = wl = WORKLOADS[workload] if isinstance(workload, str) else workload
         assert isinstance(wl, Workload)
         if clock not in ("measured", "model"):
             raise ValueError("clock must be 'measured' or 'model'")
+        if grouped and serial:
+            raise ValueError("serial applies to per-worker launches, not grouped ones")
         if grouped and clock != "model":
             raise ValueError("grouped workers have no per-worker device time: use clock='model'")
+        if exchange not in ("edp", "mean"):
+            raise ValueError("exchange must be 'edp' or 'mean'")
         self.clock = clock
         self.grouped = grouped
+        # exchange: "edp" weights g_m by n_m / N (Section 4.2); "mean" is the
+        # plain mean of Sync-SGD and DP-SGD.  delays: additive per-batch delay
+        # of each worker in the units of X (Section 5's simulated
+        # heterogeneity).  estimator: compute power across windows, ("window",),
+        # ("ema", alpha) or ("history", h).  lr_schedule: None (constant) or
+        # ("cosine", total_steps, lr_min).  serial: the workers run one after
+        # another on one stream (sharing one workspace), so that each worker's
+        # measured time is its own work alone, as on a device of its own.
+        self.exchange = exchange
+        self.delays = None if delays is None else [float(d) for d in delays]
+        self.lr_schedule = lr_schedule
         self.dev = torch.device(device)
         self.M, self.N = wl.workers, wl.total
         self.steps = steps if steps is not None else wl.steps
@@ -55,10 +73,21 @@ class Trainer:
         if grouped:
             self.streams = []
             self.ws = [hs.workspace_create(self.model, self.N)]
+        elif serial:
+            self.streams = [torch.cuda.Stream(device=self.dev)] * self.M
+            self.ws = [hs.workspace_create(self.model, self.max_n)]
         else:
             self.streams = [torch.cuda.Stream(device=self.dev) for _ in range(self.M)]
             self.ws = [hs.workspace_create(self.model, self.max_n) for _ in range(self.M)]
         self.part = hs.Partitioner(self.M, self.N, wl.window)
+        if estimator[0] == "ema":
+            self.part.set_estimator("ema", alpha=estimator[1])
+        elif estimator[0] == "history":
+            self.part.set_estimator("history", history=estimator[1])
+        elif estimator[0] != "window":
+            raise ValueError("unknown estimator %r" % (estimator,))
+        if self.delays is not None and len(self.delays) != self.M:
+            raise ValueError("one delay per worker")
         if not wl.start_even:                       # fixed split in proportion to the speeds
             self.part.set_partition(hs.repartition(list(wl.speeds), self.N))
         self.speeds = synth.speed_schedule(wl.speeds, max(self.steps, 1), seed, wl.drift_sigma)
@@ -91,7 +120,7 @@ class Trainer:
             if timed:
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(s)
-            hs.worker_grad(self.model, self.ws[m], self.theta.data_ptr(),
+            hs.worker_grad(self.model, self.ws[m % len(self.ws)], self.theta.data_ptr(),
                            self.theta_bf16.data_ptr() if self.bf16 else 0,
                            x.data_ptr() + o * ew, y.data_ptr() + o * 4, n[m],
                            self.grads[m].data_ptr(), self.losses.data_ptr() + 4 * m,
@@ -124,20 +153,34 @@ class Trainer:
         if self.time_opt:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(main)
-        hs.wavg_sgd([g.data_ptr() for g in self.grads], n, self.theta.data_ptr(),
-                    self.mom.data_ptr() if self.mom is not None else 0, self.P, wl.lr, wl.mu,
-                    wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)
+        # the kernel weights worker m by w[m] / sum w: the partition sizes, or
+        # ones for the plain mean
+        w = n if self.exchange == "edp" else [1] * self.M
+        hs.wavg_sgd([g.data_ptr() for g in self.grads], w, self.theta.data_ptr(),
+                    self.mom.data_ptr() if self.mom is not None else 0, self.P, self.lr(t),
+                    wl.mu, wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)
         if self.time_opt:
             e1.record(main)
             self.opt_events.append((e0, e1))
         self.pending.append((t, n, events))
         self.t += 1
-        if wl.window > 0 and len(self.pending) >= wl.window:
+        if len(self.pending) >= (wl.window if wl.window > 0 else 64):
             self.flush()
         return n
 
+    def lr(self, t):
+        """Learning rate of step t: constant, or cosine annealing
+        lr_min + (lr - lr_min) (1 + cos(pi t / total)) / 2."""
+        if self.lr_schedule is None:
+            return self.wl.lr
+        kind, total, lr_min = self.lr_schedule
+        if kind != "cosine":
+            raise ValueError("unknown lr schedule %r" % (kind,))
+        return lr_min + (self.wl.lr - lr_min) * (1.0 + math.cos(math.pi * t / total)) / 2.0
+
     def flush(self):
-        """Report the pending steps' times to the partitioner, in step order."""
+        """Report the pending steps' times to the partitioner, in step order.
+        The batch time of worker m is X_m = tau_m / s_m (+ delay_m)."""
         for t, n, events in self.pending:
             if self.clock == "measured":
                 for _, e1 in events:
@@ -146,8 +189,16 @@ class Trainer:
             else:
                 tau = [float(v) for v in n]
             speed = self.speeds[min(t, len(self.speeds) - 1)]
-            cp = self.part.observe(tau, speed) if self.wl.window > 0 else None
-            self.log.append({"step": t, "n": list(n), "tau": tau, "speed": list(speed), "cp": cp})
+            x = [tau[m] / float(speed[m]) for m in range(self.M)]
+            if self.delays is not None:
+                x = [x[m] + self.delays[m] for m in range(self.M)]
+            cp = None
+            if self.wl.window > 0:
+                # with delays the batch times are reported whole (speed 1)
+                cp = (self.part.observe(tau, speed) if self.delays is None
+                      else self.part.observe(x, [1.0] * self.M))
+            self.log.append({"step": t, "n": list(n), "tau": tau, "speed": list(speed), "x": x,
+                             "xmax": max(x), "cp": cp})
         self.pending = []
 
     def opt_bytes(self):

@@ -65,6 +65,7 @@ def _load():
         "hs_partitioner_partition": (I32, [P, PI32]),
         "hs_partitioner_set_partition": (I32, [P, PI32]),
         "hs_partitioner_observe": (I32, [P, PD, PD, PI32, PD]),
+        "hs_partitioner_set_estimator": (I32, [P, I32, ctypes.c_double, I32]),
         "hs_layer_gemm": (I32, [I32, I32, I32, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, I32,
                                 I32, P, I64, P]),
         "hs_probe_enable": (I32, [P, I32, I32, I32, I32]),
@@ -94,6 +95,7 @@ EXPORTED = (
     "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
     "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
+    "hs_partitioner_set_estimator",
     "hs_layer_gemm", "hs_probe_enable", "hs_probe_read", "hs_last_error")
 
 
@@ -255,6 +257,13 @@ class Partitioner:
 
     def set_partition(self, n):
         _check(_lib.hs_partitioner_set_partition(self.h, _i32(n)))
+
+    def set_estimator(self, kind, alpha=1.0, history=1):
+        """Compute-power estimator across windows: "window" (Eq. (2) on the
+        last window), "ema" (factor alpha) or "history" (mean of the last
+        `history` windows' estimates); see hs_partitioner_set_estimator."""
+        k = {"window": 0, "ema": 1, "history": 2}[kind]
+        _check(_lib.hs_partitioner_set_estimator(self.h, k, float(alpha), int(history)))
 
     def observe(self, tau, speed):
         """Returns the CP vector if this step closed a window, else None."""

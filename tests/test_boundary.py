@@ -104,6 +104,59 @@ def test_partitioner_matches_oracle_driver_logic():
         p.close()
 
 
+@pytest.mark.parametrize("est", [("ema", 0.5), ("ema", 0.37), ("history", 1), ("history", 3),
+                                 ("history", 7)])
+def test_partitioner_estimators_match_oracle(est):
+    """hs_partitioner_set_estimator: EMA and history smoothing of the compute
+    power across windows, against the oracle's smooth_cp on random traces;
+    every estimate and partition bit-exact."""
+    rng = np.random.default_rng(29)
+    for trial in range(12):
+        m = int(rng.integers(2, 9))
+        total = int(rng.integers(4 * m, 3000))
+        window = int(rng.integers(1, 4))
+        p = hs.Partitioner(m, total, window)
+        p.set_estimator(est[0], alpha=est[1] if est[0] == "ema" else 1.0,
+                        history=est[1] if est[0] == "history" else 1)
+        n, xsum, state = S.even_split(m, total), [0.0] * m, {}
+        for t in range(10 * window):
+            tau = [float(v) for v in rng.uniform(0.5, 5.0, size=m)]
+            speed = [float(v) for v in rng.uniform(0.5, 4.0, size=m)]
+            cp = p.observe(tau, speed)
+            for j in range(m):
+                xsum[j] = xsum[j] + tau[j] / speed[j]
+            if (t + 1) % window == 0:
+                ocp = S.smooth_cp(est, S.estimate_cp(n, [v / float(window) for v in xsum]), state)
+                assert cp == ocp
+                n = S.repartition(ocp, total)
+                xsum = [0.0] * m
+            assert p.partition() == n
+        p.close()
+
+
+def test_estimator_errors_and_reset():
+    p = hs.Partitioner(3, 30, 1)
+    for kind, alpha, hist in (("ema", 0.0, 1), ("ema", 1.5, 1), ("ema", float("nan"), 1),
+                              ("history", 1.0, 0), ("history", 1.0, 5000)):
+        with pytest.raises(hs.HSError):
+            p.set_estimator(kind, alpha=alpha, history=hist)
+    assert hs.lib().hs_partitioner_set_estimator(p.h, 9, 1.0, 1) == hs.HS_ERR_INVALID
+    # switching estimators clears the carried state: history 2 after a reset
+    # equals history 2 from scratch
+    p.set_estimator("history", history=2)
+    p.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+    p.set_estimator("history", history=2)
+    q = hs.Partitioner(3, 30, 1)
+    q.set_partition(p.partition())
+    q.set_estimator("history", history=2)
+    for _ in range(3):
+        a = p.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+        b = q.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+        assert a == b
+    p.close()
+    q.close()
+
+
 def test_model_clock_reaches_speed_proportional_partition():
     """Algorithm 1 with the model clock (X_m = n_m / s_m): even first window,
     then partitions proportional to the speeds (1:1:2:4 over 512 -> 64 64 128 256)."""

@@ -152,6 +152,64 @@ def test_multistep_theta_small_cnn(grouped):
     assert err <= TOL["fp32"]
 
 
+MODES = {
+    # Sync-SGD: even split throughout, plain mean
+    "sync": dict(window=0, exchange="mean"),
+    # Dynamic Partitioning without the enhancement: plain mean
+    "dp_mean": dict(window=2, exchange="mean"),
+    # EDP with an EMA estimator and cosine annealing
+    "edp_ema_cosine": dict(window=2, exchange="edp", estimator=("ema", 0.5),
+                           lr_schedule=("cosine", 10, 0.001)),
+    # EDP with the mean of the last 3 windows' estimates
+    "edp_history": dict(window=2, exchange="edp", estimator=("history", 3)),
+}
+
+
+@pytest.mark.parametrize("grouped", [False, True])
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_multistep_modes_small_cnn(mode, grouped):
+    """Ten steps of the small CNN (N = 32, 4 workers at speeds 1:1:2:4, an
+    additive delay on workers 0 and 2, model clock) in each exchange /
+    partitioning / estimator / schedule mode against the oracle's driver:
+    partitions and batch times bit-exact, theta within the fp32 bar."""
+    cfg = dict(MODES[mode])
+    window = cfg.pop("window")
+    log("multistep mode=%s grouped=%s" % (mode, grouped))
+    wl = dataclasses.replace(WORKLOADS["smallcnn_fp32"], total=32, window=window, steps=10,
+                             mu=0.9, wd=5e-4)
+    require_gpu()
+    from paper_2110_08941_amd.driver import Trainer
+    net = Mo.build(wl.arch)
+    table, P = Mo.param_table(net)
+    theta = synth.he_normal(table, P, 0)
+    delays = [3.0, 0.0, 1.5, 0.0]
+    tr = Trainer(wl, seed=0, clock="model", steps=10, theta0=theta, n_batches=10,
+                 grouped=grouped, delays=delays, **cfg)
+    try:
+        batches = [(x.cpu().numpy(), y.cpu().numpy()) for x, y in tr.batches]
+        tr.run(10)
+        got = tr.theta.cpu().numpy().astype(np.float64)
+        used = [e["n"] for e in tr.log]
+        xs = [e["x"] for e in tr.log]
+        speeds = tr.speeds
+    finally:
+        tr.close()
+    sched = cfg.get("lr_schedule")
+    out = S.run(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym), theta.astype(np.float64),
+                batches, speeds, window, wl.lr, wl.mu, wl.wd, exchange=cfg["exchange"],
+                delays=delays, estimator=cfg.get("estimator", ("window",)),
+                lr_total=sched[1] if sched else None, lr_min=sched[2] if sched else 0.0)
+    assert used == out["partitions"]
+    assert xs == out["xs"]
+    if window == 0:
+        assert used == [[8, 8, 8, 8]] * 10
+    else:
+        assert used[-1] != [8, 8, 8, 8]
+    err = normwise(got - theta, out["theta"] - theta)
+    log("  partitions %s ... %s, normwise err %.3e" % (used[0], used[-1], err))
+    assert err <= TOL["fp32"]
+
+
 def test_full_size_weighted_average_invariant():
     """At the full small-CNN size (N = 512, workers 1:1:2:4): the partition
     -weighted average of the GPU worker gradients equals the GPU gradient of
