@@ -44,6 +44,8 @@ HBM_PEAK_GBS = 8000.0
 PROBE = {"resnet18_bf16": (0, 512, 128), "resnet18_fp32": (2, 128, 128),
          "vgg16_bf16": (0, 512, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
 MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
+# template instance of each probed kernel whose HBM traffic has been counted
+PROBE_KERNEL = {(0, 512, 128, "bf16"): "conv2_kernel<0, 128, 9, 0, true>"}
 
 
 def kernel_name(mode, bm, bn, dtype):
@@ -66,6 +68,9 @@ def parse():
                     help="samples of the CPU oracle's bounded step")
     ap.add_argument("--streams", action="store_true",
                     help="one stream per worker, measured clock (default: one pass)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB four times (the reference "
+                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     ap.add_argument("--probe", default=None,
                     help="GEMM instantiation timed for the roofline, as mode,bm,bn")
     return ap.parse_args()
@@ -126,9 +131,52 @@ def standalone_wavg(reps=20):
     nbytes = (len(n) * 4 + 8) * P
     del g, th
     return {"buffers": "%d x %d fp32, plain SGD" % (len(n), P), "bytes_per_launch": nbytes,
+            "traffic": measured_traffic("wavg_sgd_kernel<2, false, false>"),
             "avg_launch_us": round(us, 2), "achieved": round(nbytes / (us * 1e-6) / 1e9, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def copy_calibration(mib, reps=4):
+    """A plain device-to-device copy of a known size: under rocprofv3 --pmc its
+    FETCH_SIZE and WRITE_SIZE per dispatch give the counters' scale."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_dispatch": 4 * n, "dispatches": reps}), flush=True)
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_resnet18_bf16_n2048_m8.md")
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when there is none or the kernel's sources changed since the
+    counters were taken (the summary records their SHA-256)."""
+    import hashlib
+    if kernel is None:
+        return None
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    start = text.find("```json")
+    if start < 0:
+        return None
+    table = json.loads(text[start + 7:text.index("```", start + 7)])
+    entry = table.get(kernel)
+    if entry is None:
+        return None
+    for path, digest in entry["sources"].items():
+        with open(os.path.join(ROOT, path), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
+    return entry["bytes_per_launch"]
 
 
 def main():
@@ -137,6 +185,9 @@ def main():
         print("bench.py measures one GPU: this build runs all simulated workers on a single "
               "MI355X and has no multi-GPU path (--gpus %d requested)" % args.gpus)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import torch
     from paper_2110_08941_amd import hs
     from paper_2110_08941_amd.configs import WORKLOADS
@@ -190,7 +241,8 @@ def main():
                    else "all workers in one pass per layer, model clock"},
         "roofline": {"bound": "mfma", "kernel": kernel_name(mode, bm, bn, wl.dtype),
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4),
+                     "traffic": measured_traffic(PROBE_KERNEL.get((mode, bm, bn, wl.dtype))),
                      "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),
                      "flops_per_launch": flops / max(launches, 1)},
         "hbm_roofline": {"bound": "hbm", "kernel": "wavg_sgd (fused partition-weighted average of "
@@ -199,6 +251,8 @@ def main():
                          "achieved": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9, 1),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                         "traffic": measured_traffic("wavg_sgd_kernel<2, true, true>"
+                                                     if tr.bf16 and tr.mom is not None else None),
                          "bytes_per_launch": tr.opt_bytes(), "avg_launch_us": round(opt_avg, 3),
                          "launches": len(opt_us)},
         "partitions_last": parts[-1] if parts else None,
