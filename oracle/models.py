@@ -4,14 +4,15 @@ The per-worker gradient is g_m = grad_theta of f_m, the mean loss over
 worker m's partition (Section 1, Eq. (1); Section 3 describes each worker
 computing the gradient of its mini-batch).  The paper trains ResNet50 and VGG16
 on CIFAR10 (Section 5); the networks here are the CIFAR-shaped MLP, small CNN,
-ResNet-18 and VGG-16 of the workloads, each buildable at reduced width and
-resolution so that finite differences stay cheap.
+ResNet-18, ResNet-50 and VGG-16 of the workloads, each buildable at reduced
+width and resolution so that finite differences stay cheap.
 
 Flat parameter vector layout (written here independently of the GPU library;
 a test checks that both tables agree):
   * tensors in forward order; a layer's bias follows its weight; batch-norm
     stores gamma then beta; in a residual block the order is conv1, bn1,
-    conv2, bn2, then the projection conv and its batch-norm;
+    conv2, bn2 (conv3, bn3 in a bottleneck block), then the projection conv
+    and its batch-norm;
   * every tensor starts at a multiple of 64 elements; the gaps are zero.
 """
 import numpy as np
@@ -299,6 +300,28 @@ class BasicBlock:
         return ctx.store(dx)
 
 
+class Bottleneck(BasicBlock):
+    """out = relu(bn3(conv3(relu(bn2(conv2(relu(bn1(conv1(x)))))))) + shortcut(x)):
+    1x1 conv to the block's inner width, 3x3 conv at that width (carrying the
+    block's stride), 1x1 conv to expansion x the inner width; the shortcut is
+    the identity, or a 1x1 strided conv + batch-norm when the stride or the
+    width changes.  Parameter order: conv1, bn1, conv2, bn2, conv3, bn3, then
+    the projection conv and its batch-norm."""
+
+    def __init__(self, name, cin, mid, stride, expansion=4):
+        cout = mid * expansion
+        self.main = Sequential([Conv(name + ".conv1", cin, mid, 1, 1, 0, False, raw_dx=True),
+                                BatchNorm(name + ".bn1", mid), ReLU(),
+                                Conv(name + ".conv2", mid, mid, 3, stride, 1, False),
+                                BatchNorm(name + ".bn2", mid), ReLU(),
+                                Conv(name + ".conv3", mid, cout, 1, 1, 0, False),
+                                BatchNorm(name + ".bn3", cout, raw_out=True)])
+        self.short = None
+        if stride != 1 or cin != cout:
+            self.short = Sequential([Conv(name + ".proj", cin, cout, 1, stride, 0, False),
+                                     BatchNorm(name + ".proj_bn", cout)])
+
+
 # ----------------------------------------------------------------------------
 # architectures
 # ----------------------------------------------------------------------------
@@ -337,6 +360,23 @@ def resnet18(in_ch=3, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2), classes=1
     return Sequential(mods)
 
 
+def resnet50(in_ch=3, widths=(64, 128, 256, 512), blocks=(3, 4, 6, 3), expansion=4, classes=10):
+    """CIFAR ResNet-50 (the paper's compute-heavy model, Section 5): 3x3 stem
+    conv + BN + ReLU (no max-pool), stages of bottleneck blocks of inner width
+    widths[i] and output width expansion x widths[i] (stride 2 on the 3x3 conv
+    of the first block of every stage after the first), global average pool,
+    linear."""
+    mods = [Conv("stem", in_ch, widths[0], 3, 1, 1, False), BatchNorm("stem_bn", widths[0]), ReLU()]
+    cin = widths[0]
+    for si, (w, nb) in enumerate(zip(widths, blocks)):
+        for bi in range(nb):
+            stride = 2 if (si > 0 and bi == 0) else 1
+            mods.append(Bottleneck("layer%d.%d" % (si + 1, bi), cin, w, stride, expansion))
+            cin = w * expansion
+    mods += [GlobalAvgPool(), Linear("fc", cin, classes, logits=True)]
+    return Sequential(mods)
+
+
 def vgg16(in_ch=3, cfg=VGG16_CFG, fc_hidden=512, classes=10):
     """VGG-16 for 32x32 inputs: conv3x3 (no bias) + BN + ReLU per width entry,
     2x2 max-pool per 'M'; then Linear(c, hidden) + ReLU + Linear(hidden,
@@ -354,7 +394,8 @@ def vgg16(in_ch=3, cfg=VGG16_CFG, fc_hidden=512, classes=10):
     return Sequential(mods)
 
 
-ARCHS = {"mlp": mlp, "small_cnn": small_cnn, "resnet18": resnet18, "vgg16": vgg16}
+ARCHS = {"mlp": mlp, "small_cnn": small_cnn, "resnet18": resnet18, "resnet50": resnet50,
+         "vgg16": vgg16}
 
 
 def build(arch, **kw):

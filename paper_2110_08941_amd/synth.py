@@ -56,18 +56,28 @@ def separate_decisions(table, theta, seed, gamma=0.5, shift=3.0):
     """Batch-norm parameters that keep every ReLU decision far from its
     threshold (for exact comparisons of deep ReLU/BN networks): gamma = 0.5
     and beta = +shift on every channel of a batch-norm that feeds a residual
-    sum (names containing "bn2" or "proj_bn"), and beta = +shift or -shift on
-    a random half of the channels of every other batch-norm.  With |xhat|
-    below shift / gamma, every pre-activation is then >= shift - gamma |xhat|
-    away from zero.  Returns a modified copy of theta."""
+    sum (in a residual block "layerS.B", the projection's batch-norm and the
+    highest-numbered "bnK" of the block: bn2 of a basic block, bn3 of a
+    bottleneck), and beta = +shift or -shift on a random half of the channels
+    of every other batch-norm.  With |xhat| below shift / gamma, every
+    pre-activation is then >= shift - gamma |xhat| away from zero.  Returns a
+    modified copy of theta."""
     th = np.array(theta, dtype=np.float32, copy=True)
     g = _rng(seed, 19)
+    last_bn = {}
+    for name, kind, shape, off in table:
+        block, _, leaf = name.rpartition(".")[0].rpartition(".")
+        if kind == "bn_beta" and name.startswith("layer") and leaf.startswith("bn"):
+            last_bn[block] = max(last_bn.get(block, 0), int(leaf[2:]))
     for name, kind, shape, off in table:
         numel = int(np.prod(shape))
+        block, _, leaf = name.rpartition(".")[0].rpartition(".")
+        residual = "proj_bn" in name or (name.startswith("layer") and leaf.startswith("bn") and
+                                         int(leaf[2:]) == last_bn.get(block))
         if kind == "bn_gamma":
             th[off:off + numel] = gamma
         elif kind == "bn_beta":
-            if "bn2" in name or "proj_bn" in name:
+            if residual:
                 th[off:off + numel] = shift
             else:
                 sign = np.where(g.random(numel) < 0.5, -1.0, 1.0)

@@ -20,6 +20,9 @@ TINY = {
     "mlp": (dict(in_dim=8, hidden=6, classes=3), (8,), 5),
     "small_cnn": (dict(in_ch=3, widths=(2, 3, 4), classes=3), (3, 6, 6), 4),
     "resnet18": (dict(in_ch=3, widths=(3, 4), blocks=(1, 2), classes=3), (3, 8, 8), 3),
+    # bottlenecks with a stride-1 projection, an identity shortcut and a
+    # stride-2 projection
+    "resnet50": (dict(in_ch=3, widths=(2, 3), blocks=(2, 1), expansion=2, classes=3), (3, 8, 8), 3),
     "vgg16": (dict(in_ch=3, cfg=(3, "M", 4, 4, "M"), fc_hidden=5, classes=3), (3, 4, 4), 4),
 }
 
@@ -123,7 +126,8 @@ def test_against_torch_autograd_small(arch):
     assert np.max(np.abs(g - tg)) <= 1e-11 * np.max(np.abs(tg))
 
 
-@pytest.mark.parametrize("arch,n", [("mlp", 6), ("small_cnn", 3), ("resnet18", 2), ("vgg16", 3)])
+@pytest.mark.parametrize("arch,n", [("mlp", 6), ("small_cnn", 3), ("resnet18", 2), ("resnet50", 1),
+                                    ("vgg16", 3)])
 def test_against_torch_autograd_full_size(arch, n):
     """The full-size networks of the workloads, He-normal parameters."""
     from paper_2110_08941_amd import synth
@@ -142,7 +146,7 @@ def test_param_counts():
     bias where batch-norm follows)."""
     expect = {"mlp": 784 * 256 + 256 + 256 * 10 + 10,
               "small_cnn": 27 * 32 + 32 + 288 * 64 + 64 + 576 * 128 + 128 + 1280 + 10,
-              "resnet18": 11173962, "vgg16": 14986698}
+              "resnet18": 11173962, "resnet50": 23520842, "vgg16": 14986698}
     for arch, count in expect.items():
         net = Mo.build(arch)
         assert Mo.true_param_count(net) == count
@@ -303,7 +307,7 @@ def test_separated_decisions_have_large_margins():
     """The separated batch-norm parameters keep every ReLU input of the BN
     networks well away from zero (the regime of the direct GPU comparisons)."""
     from paper_2110_08941_amd import synth
-    for arch in ("resnet18", "vgg16"):
+    for arch in ("resnet18", "resnet50", "vgg16"):
         kw, in_shape, n = TINY[arch]
         net = Mo.build(arch, **kw)
         table, total = Mo.param_table(net)
@@ -313,3 +317,105 @@ def test_separated_decisions_have_large_margins():
         Mo.worker_grad(net, theta.astype(np.float64), x, y, ctx=ctx)
         relu = [m[1][0] for m in ctx.margins if m[0] == "relu"]
         assert min(relu) > 1e-3
+
+
+# ----------------------------------------------------------------------------
+# ResNet-50 structure, written independently with torch.nn modules
+# ----------------------------------------------------------------------------
+class _TorchBottleneck(torch.nn.Module):
+    def __init__(self, cin, mid, stride, exp):
+        super().__init__()
+        tn = torch.nn
+        self.conv1, self.bn1 = tn.Conv2d(cin, mid, 1, bias=False), tn.BatchNorm2d(mid)
+        self.conv2 = tn.Conv2d(mid, mid, 3, stride=stride, padding=1, bias=False)
+        self.bn2 = tn.BatchNorm2d(mid)
+        self.conv3, self.bn3 = tn.Conv2d(mid, mid * exp, 1, bias=False), tn.BatchNorm2d(mid * exp)
+        self.proj = None
+        if stride != 1 or cin != mid * exp:
+            self.proj = tn.Conv2d(cin, mid * exp, 1, stride=stride, bias=False)
+            self.proj_bn = tn.BatchNorm2d(mid * exp)
+
+    def forward(self, x):
+        h = F.relu(self.bn1(self.conv1(x)))
+        h = F.relu(self.bn2(self.conv2(h)))
+        h = self.bn3(self.conv3(h))
+        return F.relu(h + (self.proj_bn(self.proj(x)) if self.proj is not None else x))
+
+
+class _TorchResNet50(torch.nn.Module):
+    """CIFAR ResNet-50 as commonly written for 32x32 inputs: 3x3 stem, stages
+    of [3, 4, 6, 3] bottlenecks at inner widths 64..512, expansion 4, stride 2
+    on the 3x3 conv of each later stage's first block."""
+
+    def __init__(self, in_ch=3, widths=(64, 128, 256, 512), blocks=(3, 4, 6, 3), exp=4,
+                 classes=10):
+        super().__init__()
+        tn = torch.nn
+        self.stem, self.stem_bn = tn.Conv2d(in_ch, widths[0], 3, padding=1, bias=False), \
+            tn.BatchNorm2d(widths[0])
+        layers, cin = [], widths[0]
+        for si, (w, nb) in enumerate(zip(widths, blocks)):
+            for bi in range(nb):
+                layers.append(_TorchBottleneck(cin, w, 2 if si > 0 and bi == 0 else 1, exp))
+                cin = w * exp
+        self.layers = tn.ModuleList(layers)
+        self.blocks = blocks
+        self.fc = tn.Linear(cin, classes)
+
+    def forward(self, x):
+        h = F.relu(self.stem_bn(self.stem(x)))
+        for b in self.layers:
+            h = b(h)
+        return self.fc(h.mean(dim=(2, 3)))
+
+    def oracle_names(self):
+        """(oracle tensor name, torch parameter) pairs."""
+        out = [("stem.weight", self.stem.weight), ("stem_bn.gamma", self.stem_bn.weight),
+               ("stem_bn.beta", self.stem_bn.bias)]
+        i = 0
+        for si, nb in enumerate(self.blocks):
+            for bi in range(nb):
+                b, pre = self.layers[i], "layer%d.%d." % (si + 1, bi)
+                i += 1
+                mods = [("conv1", b.conv1), ("bn1", b.bn1), ("conv2", b.conv2), ("bn2", b.bn2),
+                        ("conv3", b.conv3), ("bn3", b.bn3)]
+                if b.proj is not None:
+                    mods += [("proj", b.proj), ("proj_bn", b.proj_bn)]
+                for nm, m in mods:
+                    if isinstance(m, torch.nn.Conv2d):
+                        out.append((pre + nm + ".weight", m.weight))
+                    else:
+                        out += [(pre + nm + ".gamma", m.weight), (pre + nm + ".beta", m.bias)]
+        return out + [("fc.weight", self.fc.weight), ("fc.bias", self.fc.bias)]
+
+
+def test_resnet50_matches_independent_torch_modules():
+    """The oracle's bottleneck network against one built from torch.nn modules
+    (training-mode batch-norm): same parameter count at full size; at reduced
+    width the same loss and gradient, tensor by tensor, with the oracle's flat
+    layout mapped onto the module's parameters by name."""
+    full = _TorchResNet50()
+    assert sum(q.numel() for q in full.parameters()) == 23520842
+    kw, in_shape, n = TINY["resnet50"]
+    net, table, total, theta, x, y = rand_problem("resnet50", kw, in_shape, n, seed=71)
+    tm = _TorchResNet50(in_ch=3, widths=kw["widths"], blocks=kw["blocks"], exp=kw["expansion"],
+                        classes=kw["classes"]).double()
+    offs = {name: (off, shape) for name, kind, shape, off in table}
+    pairs = tm.oracle_names()
+    assert sorted(nm for nm, _ in pairs) == sorted(offs)
+    with torch.no_grad():
+        for nm, prm in pairs:
+            off, shape = offs[nm]
+            v = torch.tensor(theta[off:off + int(np.prod(shape))].reshape(shape))
+            prm.copy_(v.permute(0, 3, 1, 2) if v.ndim == 4 else v)    # OHWI -> OIHW
+    loss_t = F.cross_entropy(tm(torch.tensor(x)), torch.tensor(y, dtype=torch.int64))
+    loss_t.backward()
+    loss, g = Mo.worker_grad(net, theta, x, y)
+    assert abs(loss - float(loss_t.detach())) < 1e-12
+    scale = max(float(prm.grad.abs().max()) for _, prm in pairs)
+    for nm, prm in pairs:
+        off, shape = offs[nm]
+        gt = prm.grad.numpy()
+        gt = gt.transpose(0, 2, 3, 1) if gt.ndim == 4 else gt
+        np.testing.assert_allclose(g[off:off + int(np.prod(shape))].reshape(shape), gt,
+                                   rtol=0, atol=1e-11 * scale, err_msg=nm)
