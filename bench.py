@@ -33,6 +33,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "train samples/s (fwd+bwd+wavg+SGD), CIFAR-shape ResNet-18; MFMA/HBM % peak"
+ARCH_NAME = {"resnet18": "ResNet-18", "resnet50": "ResNet-50", "vgg16": "VGG-16",
+             "small_cnn": "small CNN", "mlp": "MLP"}
 PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}   # MI355X dense MFMA peaks
 HBM_PEAK_GBS = 8000.0
 
@@ -42,6 +44,7 @@ HBM_PEAK_GBS = 8000.0
 # MFMA forward / data-gradient kernel with 512-row tiles, bm = bn = 64 in mode
 # 2 the patch weight-gradient kernel).
 PROBE = {"resnet18_bf16": (0, 512, 128), "resnet18_fp32": (2, 128, 128),
+         "resnet50_bf16": (0, 512, 128),
          "vgg16_bf16": (0, 512, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
 MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
 # template instance of each probed kernel whose HBM traffic has been counted
@@ -131,7 +134,7 @@ def standalone_wavg(reps=20):
     nbytes = (len(n) * 4 + 8) * P
     del g, th
     return {"buffers": "%d x %d fp32, plain SGD" % (len(n), P), "bytes_per_launch": nbytes,
-            "traffic": measured_traffic("wavg_sgd_kernel<2, false, false>"),
+            "traffic": measured_traffic("resnet18_bf16", "wavg_sgd_kernel<2, false, false>"),
             "avg_launch_us": round(us, 2), "achieved": round(nbytes / (us * 1e-6) / 1e9, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
@@ -151,18 +154,21 @@ def copy_calibration(mib, reps=4):
     print(json.dumps({"copy_bytes_per_dispatch": 4 * n, "dispatches": reps}), flush=True)
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_resnet18_bf16_n2048_m8.md")
+# committed HBM-traffic counter summaries, per workload
+TRAFFIC_PROFILE = {"resnet18_bf16": os.path.join(ROOT, "profiles",
+                                                 "hbm_traffic_resnet18_bf16_n2048_m8.md")}
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or
-    None when there is none or the kernel's sources changed since the
-    counters were taken (the summary records their SHA-256)."""
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` in `workload` from the committed
+    counter summary, or None when there is none or the kernel's sources
+    changed since the counters were taken (the summary records their
+    SHA-256)."""
     import hashlib
-    if kernel is None:
+    if kernel is None or workload not in TRAFFIC_PROFILE:
         return None
     try:
-        text = open(TRAFFIC_PROFILE).read()
+        text = open(TRAFFIC_PROFILE[workload]).read()
     except OSError:
         return None
     start = text.find("```json")
@@ -226,7 +232,7 @@ def main():
     loss = tr.losses.cpu().tolist()
     parts = [e["n"] for e in tr.log]
     result = {
-        "metric": METRIC, "value": round(value, 2), "unit": "samples/s", "n_gpus": 1,
+        "metric": METRIC.replace("ResNet-18", ARCH_NAME[wl.arch]), "value": round(value, 2), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
@@ -242,7 +248,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": kernel_name(mode, bm, bn, wl.dtype),
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
-                     "traffic": measured_traffic(PROBE_KERNEL.get((mode, bm, bn, wl.dtype))),
+                     "traffic": measured_traffic(args.workload,
+                                                 PROBE_KERNEL.get((mode, bm, bn, wl.dtype))),
                      "launches": launches, "avg_launch_us": round(1e3 * ms / max(launches, 1), 3),
                      "flops_per_launch": flops / max(launches, 1)},
         "hbm_roofline": {"bound": "hbm", "kernel": "wavg_sgd (fused partition-weighted average of "
@@ -251,7 +258,8 @@ def main():
                          "achieved": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9, 1),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(tr.opt_bytes() / (opt_avg * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-                         "traffic": measured_traffic("wavg_sgd_kernel<2, true, true>"
+                         "traffic": measured_traffic(args.workload,
+                                                     "wavg_sgd_kernel<2, true, true>"
                                                      if tr.bf16 and tr.mom is not None else None),
                          "bytes_per_launch": tr.opt_bytes(), "avg_launch_us": round(opt_avg, 3),
                          "launches": len(opt_us)},

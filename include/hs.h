@@ -62,7 +62,8 @@ typedef enum {
   HS_ERR_UNSUPPORTED = -4  /* valid request this build does not support */
 } hs_status;
 
-typedef enum { HS_MLP = 0, HS_SMALLCNN = 1, HS_RESNET18 = 2, HS_VGG16 = 3 } hs_arch;
+typedef enum { HS_MLP = 0, HS_SMALLCNN = 1, HS_RESNET18 = 2, HS_VGG16 = 3,
+               HS_RESNET50 = 4 } hs_arch;
 typedef enum { HS_FP32 = 0, HS_BF16 = 1 } hs_dtype;
 typedef enum { HS_KIND_CONV_W = 0, HS_KIND_LIN_W = 1, HS_KIND_BIAS = 2,
                HS_KIND_BN_GAMMA = 3, HS_KIND_BN_BETA = 4 } hs_tensor_kind;
@@ -78,8 +79,11 @@ typedef struct hs_partitioner hs_partitioner;
  * accumulation; batch-norm statistics, loss, gradients and master weights
  * fp32).  The networks are CIFAR-shaped: MLP 784-256-10; small CNN
  * conv32-conv64-pool-conv128-GAP-FC10; ResNet-18 (3x3 stem, 4 stages of 2
- * basic blocks, widths 64..512); VGG-16 (13 conv-BN-ReLU, 5 pools, FC512,
- * FC10).  The paper's experiments use ResNet50 / VGG16 on CIFAR10 (Section 5). */
+ * basic blocks, widths 64..512); ResNet-50 (3x3 stem, stages of 3-4-6-3
+ * bottleneck blocks 1x1 / 3x3 / 1x1 at inner widths 64..512 and output
+ * widths 256..2048, stride 2 on the 3x3 of each later stage's first block);
+ * VGG-16 (13 conv-BN-ReLU, 5 pools, FC512, FC10).  The paper's experiments
+ * use ResNet50 / VGG16 on CIFAR10 (Section 5). */
 hs_status hs_model_create(int32_t arch, int32_t dtype, hs_model** out);
 hs_status hs_model_destroy(hs_model* model);
 

@@ -13,7 +13,7 @@ from typing import Optional, Tuple
 @dataclass(frozen=True)
 class Workload:
     name: str
-    arch: str                 # "mlp" | "small_cnn" | "resnet18" | "vgg16"
+    arch: str                 # "mlp" | "small_cnn" | "resnet18" | "resnet50" | "vgg16"
     dtype: str                # "fp32" | "bf16"
     total: int                # N, samples per step over all workers
     speeds: Tuple[float, ...] # initial simulated speed s_m of every worker
@@ -47,6 +47,12 @@ WORKLOADS = {
     # ResNet-18 (CIFAR), bf16 operands / fp32 master, N=2048 over 8 drifting
     # workers, repartition every 10 steps over 100 steps.
     "resnet18_bf16": Workload("resnet18_bf16", "resnet18", "bf16", 2048,
+                              (1.0, 1.0, 1.0, 2.0, 2.0, 4.0, 4.0, 8.0), 100, 10, True, 0.05,
+                              0.1, 0.9, 5e-4),
+    # ResNet-50 (CIFAR, bottleneck blocks), bf16 operands / fp32 master,
+    # N=1024 (128 per worker, as in Section 5) over 8 drifting workers,
+    # repartition every 10 steps over 100 steps.
+    "resnet50_bf16": Workload("resnet50_bf16", "resnet50", "bf16", 1024,
                               (1.0, 1.0, 1.0, 2.0, 2.0, 4.0, 4.0, 8.0), 100, 10, True, 0.05,
                               0.1, 0.9, 5e-4),
     # VGG-16 (CIFAR), bf16, N=4096 over 8 workers 1:1:1:2:2:4:4:8.

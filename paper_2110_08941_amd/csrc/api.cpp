@@ -83,7 +83,7 @@ const char* hs_last_error(void) { return g_err.c_str(); }
 hs_status hs_model_create(int32_t arch, int32_t dtype, hs_model** out) {
   if (!out) return fail(HS_ERR_INVALID, "hs_model_create: out is NULL");
   *out = nullptr;
-  if (arch < HS_MLP || arch > HS_VGG16) return fail(HS_ERR_INVALID, "unknown arch %d", arch);
+  if (arch < HS_MLP || arch > HS_RESNET50) return fail(HS_ERR_INVALID, "unknown arch %d", arch);
   if (dtype != HS_FP32 && dtype != HS_BF16) return fail(HS_ERR_INVALID, "unknown dtype %d", dtype);
   hs_model* m = new (std::nothrow) hs_model;
   if (!m) return fail(HS_ERR_OOM, "host allocation failed");

@@ -133,6 +133,37 @@ bool build_model(int arch, int dtype, Model& m) {
       }
     }
     m.fc2 = b.linear("fc", 512, 10, false);
+  } else if (arch == HS_RESNET50) {
+    m.in_numel = 3 * 32 * 32;
+    m.stem = b.conv("stem", 3, 64, 3, 1, 1, 32, 32, false, false);
+    m.stem_bn = b.bn("stem_bn", 64);
+    const int widths[4] = {64, 128, 256, 512}, nblocks[4] = {3, 4, 6, 3};
+    int cin = 64, H = 32;
+    for (int si = 0; si < 4; ++si) {
+      for (int bi = 0; bi < nblocks[si]; ++bi) {
+        const int stride = (si > 0 && bi == 0) ? 2 : 1;
+        const int mid = widths[si], cout = 4 * widths[si];
+        std::string nm = "layer" + std::to_string(si + 1) + "." + std::to_string(bi);
+        BlockL blk{};
+        blk.bottleneck = true;
+        blk.c1 = b.conv(nm + ".conv1", cin, mid, 1, 1, 0, H, H, false, false);
+        blk.b1 = b.bn(nm + ".bn1", mid);
+        blk.c2 = b.conv(nm + ".conv2", mid, mid, 3, stride, 1, H, H, false, false);
+        blk.b2 = b.bn(nm + ".bn2", mid);
+        const int Ho = blk.c2.Ho;
+        blk.c3 = b.conv(nm + ".conv3", mid, cout, 1, 1, 0, Ho, Ho, false, false);
+        blk.b3 = b.bn(nm + ".bn3", cout);
+        blk.proj = (stride != 1 || cin != cout);
+        if (blk.proj) {
+          blk.cp = b.conv(nm + ".proj", cin, cout, 1, stride, 0, H, H, false, false);
+          blk.bp = b.bn(nm + ".proj_bn", cout);
+        }
+        m.blocks.push_back(blk);
+        cin = cout;
+        H = Ho;
+      }
+    }
+    m.fc2 = b.linear("fc", 2048, 10, false);
   } else if (arch == HS_VGG16) {
     m.in_numel = 3 * 32 * 32;
     const int cfg[18] = {64, 64, -1, 128, 128, -1, 256, 256, 256, -1,
@@ -212,6 +243,23 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
       act(e);                // A_out
     }
     act(512);                // F
+  } else if (m.arch == HS_RESNET50) {
+    act(8 * 1024);           // 0: X0 (channels padded)
+    act(64 * 1024);          // 1: Zs
+    act(64 * 1024);          // 2: As
+    for (const BlockL& b : m.blocks) {
+      const int64_t ein = (int64_t)b.c1.Ho * b.c1.Wo * b.c1.cout;   // input grid, inner width
+      const int64_t emid = (int64_t)b.c2.Ho * b.c2.Wo * b.c2.cout;  // output grid, inner width
+      const int64_t eout = (int64_t)b.c3.Ho * b.c3.Wo * b.c3.cout;  // output grid, output width
+      act(ein);              // Z1
+      act(ein);              // H1
+      act(emid);             // Z2
+      act(emid);             // H2
+      act(eout);             // Z3
+      act(b.proj ? eout : 0);  // ZP
+      act(eout);             // A_out
+    }
+    act(2048);               // F
   } else {
     act(8 * 1024);           // 0: X0 (channels padded)
     for (const VggL& l : m.vgg) {
@@ -805,6 +853,93 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   return stem_wgrad(c, m.stem, dZs, S[0]);
 }
 
+// ---------------------------------------------------------- ResNet-50 ----
+// Bottleneck blocks: Z1 = conv1(in) (1x1), H1 = relu(bn1(Z1)); Z2 = conv2(H1)
+// (3x3, the block's stride), H2 = relu(bn2(Z2)); Z3 = conv3(H2) (1x1),
+// out = relu(bn3(Z3) + shortcut), the shortcut being the input or
+// bn_p(conv_p(in)) (1x1, the block's stride).
+hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, float* loss) {
+  const Model& m = c.m;
+  void** S = c.ws.slot.data();
+  void** G = c.ws.grad;
+  const int n = c.n;
+  constexpr int SLOTS = 7;
+  HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
+  HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
+  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2]));
+  const void* cur = S[2];
+  int si = 3;
+  for (const BlockL& b : m.blocks) {
+    void *Z1 = S[si], *H1 = S[si + 1], *Z2 = S[si + 2], *H2 = S[si + 3], *Z3 = S[si + 4],
+         *ZP = S[si + 5], *A = S[si + 6];
+    si += SLOTS;
+    const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
+    HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
+    HS_TRY(bn_stats(c, b.b1, Z1, rin));
+    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rin, H1));
+    HS_TRY(conv_fwd(c, b.c2, H1, Z2, false));
+    HS_TRY(bn_stats(c, b.b2, Z2, rout));
+    HS_TRY(bn_apply(c, b.b2, Z2, nullptr, 1, rout, H2));
+    HS_TRY(conv_fwd(c, b.c3, H2, Z3, false));
+    HS_TRY(bn_stats(c, b.b3, Z3, rout));
+    const void* res = cur;
+    if (b.proj) {
+      HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
+      HS_TRY(bn_stats(c, b.bp, ZP, rout));
+      HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rout, G[0]));
+      res = G[0];
+    }
+    HS_TRY(bn_apply(c, b.b3, Z3, res, 1, rout, A));
+    cur = A;
+  }
+  const int cfin = m.blocks.back().c3.cout;
+  const int hwfin = m.blocks.back().c3.Ho * m.blocks.back().c3.Wo;
+  void* F = S[si];
+  HS_TRY(launch_gap_fwd(c.bf, cur, n, hwfin, cfin, F, c.s));
+  HS_TRY(conv_fwd(c, m.fc2, F, c.ws.logits, true));
+  // ---- backward
+  const void* dz;
+  HS_TRY(loss_grad(c, y, loss, &dz));
+  HS_TRY(conv_wgrad(c, m.fc2, dz, F));
+  HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
+  HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
+  HS_TRY(launch_gap_bwd(c.bf, G[0], cur, n, hwfin, cfin, G[1], c.s));  // dA * [A > 0]
+  // G[gi]: gradient of the current block's output times its ReLU mask
+  int gi = 1;
+  for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
+    const BlockL& b = m.blocks[bi];
+    const int base = 3 + SLOTS * bi;
+    void *Z1 = S[base], *H1 = S[base + 1], *Z2 = S[base + 2], *H2 = S[base + 3],
+         *Z3 = S[base + 4], *ZP = S[base + 5];
+    const void* in = bi == 0 ? S[2] : S[3 + SLOTS * (bi - 1) + 6];   // post-ReLU input
+    int fr[4], k = 0;
+    for (int i = 0; i < 5; ++i)
+      if (i != gi) fr[k++] = i;
+    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]];
+    const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
+    HS_TRY(bn_bwd(c, b.b3, P1, nullptr, Z3, rout, P2));                     // dZ3
+    HS_TRY(conv_wgrad(c, b.c3, P2, H2));
+    HS_TRY(conv_dgrad(c, b.c3, P2, P3, nullptr, H2));                      // dH2 * [H2 > 0]
+    HS_TRY(bn_bwd(c, b.b2, P3, nullptr, Z2, rout, P2));                     // dZ2
+    HS_TRY(conv_wgrad(c, b.c2, P2, H1));
+    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, H1));                      // dH1 * [H1 > 0]
+    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rin, P2));                      // dZ1
+    HS_TRY(conv_wgrad(c, b.c1, P2, in));
+    if (b.proj) {
+      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rout, P3));                   // dZP
+      HS_TRY(conv_wgrad(c, b.cp, P3, in));
+      HS_TRY(conv_dgrad(c, b.cp, P3, P4, nullptr, nullptr));               // shortcut grad
+      HS_TRY(conv_dgrad(c, b.c1, P2, P1, P4, in));                         // dIn * [in > 0]
+    } else {
+      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in));                         // dIn * [in > 0]
+      gi = fr[1];
+    }
+  }
+  void* dZs = G[gi == 0 ? 1 : 0];
+  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], nullptr, S[1], 1024, dZs));
+  return stem_wgrad(c, m.stem, dZs, S[0]);
+}
+
 // -------------------------------------------------------------- VGG-16 ----
 hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const Model& m = c.m;
@@ -911,6 +1046,7 @@ hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
   if (m.arch == HS_MLP) return mlp(c, x, y, loss);
   if (m.arch == HS_SMALLCNN) return small_cnn(c, x, y, loss);
   if (m.arch == HS_RESNET18) return resnet(c, x, y, loss);
+  if (m.arch == HS_RESNET50) return resnet_bottleneck(c, x, y, loss);
   return vgg(c, x, y, loss);
 }
 

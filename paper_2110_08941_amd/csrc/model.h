@@ -29,10 +29,12 @@ struct BNL {
   int stat;                    // index of this layer's mean/rstd in the workspace
 };
 
+// Residual block: basic (c1 3x3, c2 3x3) or bottleneck (c1 1x1, c2 3x3
+// carrying the stride, c3 1x1 expansion); cp/bp the projection shortcut.
 struct BlockL {
-  ConvL c1, c2, cp;
-  BNL b1, b2, bp;
-  bool proj;
+  ConvL c1, c2, c3, cp;
+  BNL b1, b2, b3, bp;
+  bool proj, bottleneck;
 };
 
 struct VggL {
@@ -49,8 +51,8 @@ struct Model {
   int64_t in_numel = 0, fwd_macs = 0;
   int nbn = 0, max_c = 0;
   int64_t max_act = 0;         // largest activation, elements per sample
-  // MLP: fc1, fc2.  Small CNN: c1..c3, fc2.  ResNet: stem, stem_bn, blocks,
-  // fc2.  VGG: vgg, fc1, fc2.
+  // MLP: fc1, fc2.  Small CNN: c1..c3, fc2.  ResNet-18 / ResNet-50: stem,
+  // stem_bn, blocks, fc2.  VGG: vgg, fc1, fc2.
   ConvL fc1{}, fc2{}, c1{}, c2{}, c3{}, stem{};
   BNL stem_bn{};
   std::vector<BlockL> blocks;

@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhs.so")
 
 HS_OK, HS_ERR_INVALID, HS_ERR_HIP, HS_ERR_OOM, HS_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
-ARCH = {"mlp": 0, "small_cnn": 1, "resnet18": 2, "vgg16": 3}
+ARCH = {"mlp": 0, "small_cnn": 1, "resnet18": 2, "vgg16": 3, "resnet50": 4}
 DTYPE = {"fp32": 0, "bf16": 1}
 KIND = {0: "conv_w", 1: "lin_w", 2: "bias", 3: "bn_gamma", 4: "bn_beta"}
 

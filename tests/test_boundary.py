@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
     assert set(names) == set(hs.EXPORTED)
 
 
-@pytest.mark.parametrize("arch", ["mlp", "small_cnn", "resnet18", "vgg16"])
+@pytest.mark.parametrize("arch", ["mlp", "small_cnn", "resnet18", "resnet50", "vgg16"])
 def test_param_layout_matches_oracle(arch):
     for dtype in ("fp32", "bf16"):
         m = hs.model_create(arch, dtype)

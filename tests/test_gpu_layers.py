@@ -32,6 +32,19 @@ SHAPES = [
     (3, 16, 16, 64, 128, 3, 1, 1),
     (5, 4, 4, 256, 512, 3, 1, 1),
     (7, 1, 1, 512, 256, 1, 1, 0),     # linear with 128+ inputs
+    # ResNet-50 bottleneck layers: 1x1 to and from the inner width, the
+    # strided 3x3 at the inner width, strided 1x1 projections
+    (3, 32, 32, 64, 64, 1, 1, 0),
+    (2, 32, 32, 256, 64, 1, 1, 0),
+    (2, 32, 32, 64, 256, 1, 1, 0),
+    (3, 32, 32, 128, 128, 3, 2, 1),
+    (2, 32, 32, 256, 512, 1, 2, 0),
+    (3, 16, 16, 512, 128, 1, 1, 0),   # 1.5 tiles of 512 rows
+    (5, 8, 8, 1024, 256, 1, 1, 0),    # under one tile
+    (3, 4, 4, 512, 2048, 1, 1, 0),
+    (7, 4, 4, 2048, 512, 1, 1, 0),
+    (5, 8, 8, 512, 512, 3, 2, 1),
+    (3, 8, 8, 1024, 2048, 1, 2, 0),
 ]
 
 

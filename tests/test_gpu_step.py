@@ -40,6 +40,7 @@ def make_trainer(name, total=None, steps=None, clock="model", separated=False, s
     ("smallcnn_fp32", 40, False),
     ("resnet18_fp32", 24, True),
     ("resnet18_bf16", 32, True),
+    ("resnet50_bf16", 24, True),
     ("vgg16_bf16", 32, True)])
 def test_one_step(name, total, separated, grouped):
     """theta' - theta after one step (worker gradients -- on their own streams,

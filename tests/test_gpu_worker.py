@@ -112,14 +112,16 @@ def test_worker_grad_he_init(arch, dtype, n):
 SEPARATED = [("resnet18", "fp32", 4), ("resnet18", "fp32", 13),
              ("vgg16", "fp32", 4), ("vgg16", "fp32", 6),
              ("resnet18", "bf16", 4), ("resnet18", "bf16", 16),
-             ("vgg16", "bf16", 4), ("vgg16", "bf16", 12)]
+             ("vgg16", "bf16", 4), ("vgg16", "bf16", 12),
+             ("resnet50", "fp32", 3), ("resnet50", "fp32", 10),
+             ("resnet50", "bf16", 4), ("resnet50", "bf16", 9)]
 
 
 @pytest.mark.parametrize("arch,dtype,n", SEPARATED)
 def test_worker_grad_separated(arch, dtype, n):
     """Batch-norm networks with every ReLU decision far from zero: direct
-    comparison.  Max-pool decisions (VGG) are checked to be unambiguous in the
-    oracle; the first data seed whose pool margins exceed 1e-6 is used."""
+    comparison.  The first data seed whose ReLU margins exceed 1e-4 and whose
+    max-pool margins (VGG, fp32) exceed 1e-6 in the oracle is used."""
     log("worker_grad separated %s %s n=%d" % (arch, dtype, n))
     net = Mo.build(arch)
     table, P = Mo.param_table(net)
@@ -130,11 +132,10 @@ def test_worker_grad_separated(arch, dtype, n):
         ref_loss, ref = Mo.worker_grad(net, theta.astype(np.float64), x, y, ctx=ctx)
         relu = [m[1][0] for m in ctx.margins if m[0] == "relu" and m[1].size]
         pool = [m[1][0] for m in ctx.margins if m[0] == "maxpool" and m[1].size]
-        if min(pool, default=1.0) > AMBIGUOUS or dtype == "bf16":
+        if min(relu) > 1e-4 and (min(pool, default=1.0) > AMBIGUOUS or dtype == "bf16"):
             break
     else:
-        pytest.fail("no data seed with unambiguous max-pool decisions")
-    assert min(relu) > 1e-4
+        pytest.fail("no data seed with separated ReLU and unambiguous max-pool decisions")
     _, _, _, g, loss = run_worker(arch, dtype, n, theta=theta, data_seed=data_seed)
     assert np.all(np.isfinite(g))
     err = normwise(g, ref)
@@ -149,7 +150,11 @@ def test_bf16_he_init_error_is_that_of_bf16_storage(arch, n):
     """He-init batch-norm networks in bf16: the GPU gradient is as far from the
     exact gradient as the oracle's own bf16-storage gradient is (the spread
     comes from ReLU decisions that bf16 rounding flips), and the loss matches
-    the bf16-storage oracle."""
+    the bf16-storage oracle.  Not run for ResNet-50: through its 16 blocks at
+    He init the bf16 rounding order alone moves the loss by several percent
+    (GPU 4.70 against 4.87 for the bf16-storage oracle at n = 3, both gradients
+    about 110 % away from the exact one), so neither bound is a property of
+    correct code there; its bf16 parity is checked with separated decisions."""
     log("bf16 he-init spread %s n=%d" % (arch, n))
     theta, x, y, g, loss = run_worker(arch, "bf16", n, seed=n)
     net = Mo.build(arch)

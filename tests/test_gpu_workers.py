@@ -95,7 +95,8 @@ def test_workers_grad_he_init(arch, dtype, n):
 
 
 SEPARATED = [("resnet18", "fp32", [3, 1, 4]), ("resnet18", "bf16", [4, 2, 6, 1, 3]),
-             ("vgg16", "fp32", [2, 3]), ("vgg16", "bf16", [3, 5, 1])]
+             ("vgg16", "fp32", [2, 3]), ("vgg16", "bf16", [3, 5, 1]),
+             ("resnet50", "fp32", [2, 1, 3]), ("resnet50", "bf16", [3, 5, 1, 2])]
 
 
 def separated_problem(arch, dtype, n, seed):
@@ -139,7 +140,8 @@ def test_workers_grad_separated(arch, dtype, n):
 
 
 @pytest.mark.parametrize("arch,dtype,n", [("resnet18", "fp32", [2, 5, 3]),
-                                          ("vgg16", "bf16", [4, 1, 3])])
+                                          ("vgg16", "bf16", [4, 1, 3]),
+                                          ("resnet50", "bf16", [6, 2, 3])])
 def test_workers_grad_equals_separate_calls(arch, dtype, n):
     """One pass over all workers against one hs_worker_grad call per worker on
     the same rows (the two differ only in the order of fp32 sums)."""
@@ -170,19 +172,21 @@ def test_workers_grad_deterministic():
         assert np.array_equal(ga, gb)
 
 
-def test_workers_grad_full_size_bench_configuration():
-    """The benchmark's launch configuration: ResNet-18 bf16, N = 2048 over 8
-    workers with a skewed partition, in one pass.  The two smallest workers are
-    checked against the oracle (bf16 storage, separated decisions); every
-    worker is checked against its own separate hs_worker_grad call."""
-    n = [52, 48, 49, 113, 119, 247, 177, 1243]
-    log("workers_grad full size resnet18 bf16 n=%s" % n)
-    net = Mo.build("resnet18")
+@pytest.mark.parametrize("arch,n", [
+    ("resnet18", [52, 48, 49, 113, 119, 247, 177, 1243]),    # the benchmark, N = 2048
+    ("resnet50", [26, 24, 25, 56, 60, 123, 89, 621])])        # N = 1024
+def test_workers_grad_full_size_bench_configuration(arch, n):
+    """The full-size launch configurations: bf16, 8 workers with a skewed
+    partition, in one pass.  The two smallest workers are checked against the
+    oracle (bf16 storage, separated decisions); every worker is checked
+    against its own separate hs_worker_grad call."""
+    log("workers_grad full size %s bf16 n=%s" % (arch, n))
+    net = Mo.build(arch)
     table, P = Mo.param_table(net)
     theta = synth.separate_decisions(table, synth.he_normal(table, P, 11), 11)
     x, y = synth.batch((3, 32, 32), sum(n), 11, 1)
-    ga, la = run_workers("resnet18", "bf16", n, theta, x, y)
-    gb, lb = run_workers("resnet18", "bf16", n, theta, x, y, separate=True)
+    ga, la = run_workers(arch, "bf16", n, theta, x, y)
+    gb, lb = run_workers(arch, "bf16", n, theta, x, y, separate=True)
     for i in range(len(n)):
         assert np.all(np.isfinite(ga[i]))
         err = normwise(ga[i], gb[i])
