@@ -58,8 +58,9 @@ def separate_decisions(table, theta, seed, gamma=0.5, shift=3.0):
     and beta = +shift on every channel of a batch-norm that feeds a residual
     sum (in a residual block "layerS.B", the projection's batch-norm and the
     highest-numbered "bnK" of the block: bn2 of a basic block, bn3 of a
-    bottleneck), and beta = +shift or -shift on a random half of the channels
-    of every other batch-norm.  With |xhat| below shift / gamma, every
+    bottleneck) and on a batch-norm named "bn2" outside residual blocks
+    (VGG-16's second), and beta = +shift or -shift on a random half of the
+    channels of every other batch-norm.  With |xhat| below shift / gamma, every
     pre-activation is then >= shift - gamma |xhat| away from zero.  Returns a
     modified copy of theta."""
     th = np.array(theta, dtype=np.float32, copy=True)
@@ -72,8 +73,11 @@ def separate_decisions(table, theta, seed, gamma=0.5, shift=3.0):
     for name, kind, shape, off in table:
         numel = int(np.prod(shape))
         block, _, leaf = name.rpartition(".")[0].rpartition(".")
-        residual = "proj_bn" in name or (name.startswith("layer") and leaf.startswith("bn") and
-                                         int(leaf[2:]) == last_bn.get(block))
+        if name.startswith("layer"):
+            residual = "proj_bn" in name or (leaf.startswith("bn") and
+                                             int(leaf[2:]) == last_bn.get(block))
+        else:
+            residual = name.split(".")[0] == "bn2"
         if kind == "bn_gamma":
             th[off:off + numel] = gamma
         elif kind == "bn_beta":
