@@ -67,8 +67,9 @@ def parse():
     ap.add_argument("--workload", default="resnet18_bf16")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=576,
-                    help="samples of the CPU oracle's bounded step")
+    ap.add_argument("--cpu-samples", type=int, default=None,
+                    help="samples of the CPU oracle's bounded step (default: about 15 s of "
+                         "host work for the workload's network)")
     ap.add_argument("--streams", action="store_true",
                     help="one stream per worker, measured clock (default: one pass)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -77,6 +78,11 @@ def parse():
     ap.add_argument("--probe", default=None,
                     help="GEMM instantiation timed for the roofline, as mode,bm,bn")
     return ap.parse_args()
+
+
+# samples of the CPU oracle's bounded step per network (about 15 s of
+# float64 work on the host's cores)
+CPU_SAMPLES = {"resnet18": 576, "resnet50": 160, "vgg16": 2048, "small_cnn": 4096, "mlp": 65536}
 
 
 def cpu_baseline(wl, seed, samples):
@@ -269,7 +275,8 @@ def main():
     tr.close()
     result["wavg_sgd_standalone"] = standalone_wavg()
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_samples)
+        samples = args.cpu_samples or CPU_SAMPLES.get(wl.arch, 64)
+        result["cpu_baseline"] = cpu_baseline(wl, args.seed, samples)
     print(json.dumps(result), flush=True)
 
 
