@@ -41,6 +41,13 @@ class Trainer:
             raise ValueError("grouped workers have no per-worker device time: use clock='model'")
         if exchange not in ("edp", "mean"):
             raise ValueError("exchange must be 'edp' or 'mean'")
+        if estimator[0] not in ("window", "ema", "history"):
+            raise ValueError("unknown estimator %r" % (estimator,))
+        if lr_schedule is not None and (lr_schedule[0] != "cosine" or lr_schedule[1] <= 0):
+            raise ValueError("lr_schedule must be None or ('cosine', total_steps > 0, lr_min)")
+        if delays is not None and (len(delays) != wl.workers or
+                                   not all(math.isfinite(d) and d >= 0.0 for d in delays)):
+            raise ValueError("delays: one finite, non-negative delay per worker")
         self.clock = clock
         self.grouped = grouped
         # exchange: "edp" weights g_m by n_m / N (Section 4.2); "mean" is the
@@ -56,6 +63,17 @@ class Trainer:
         self.lr_schedule = lr_schedule
         self.dev = torch.device(device)
         self.M, self.N = wl.workers, wl.total
+        # the Dynamic Partitioning state first: its argument errors leave
+        # nothing allocated
+        self.part = hs.Partitioner(self.M, self.N, wl.window)
+        try:
+            if estimator[0] == "ema":
+                self.part.set_estimator("ema", alpha=estimator[1])
+            elif estimator[0] == "history":
+                self.part.set_estimator("history", history=estimator[1])
+        except Exception:
+            self.part.close()
+            raise
         self.steps = steps if steps is not None else wl.steps
         self.model = hs.model_create(wl.arch, wl.dtype)
         self.P = hs.num_params(self.model)
@@ -79,15 +97,6 @@ class Trainer:
         else:
             self.streams = [torch.cuda.Stream(device=self.dev) for _ in range(self.M)]
             self.ws = [hs.workspace_create(self.model, self.max_n) for _ in range(self.M)]
-        self.part = hs.Partitioner(self.M, self.N, wl.window)
-        if estimator[0] == "ema":
-            self.part.set_estimator("ema", alpha=estimator[1])
-        elif estimator[0] == "history":
-            self.part.set_estimator("history", history=estimator[1])
-        elif estimator[0] != "window":
-            raise ValueError("unknown estimator %r" % (estimator,))
-        if self.delays is not None and len(self.delays) != self.M:
-            raise ValueError("one delay per worker")
         if not wl.start_even:                       # fixed split in proportion to the speeds
             self.part.set_partition(hs.repartition(list(wl.speeds), self.N))
         self.speeds = synth.speed_schedule(wl.speeds, max(self.steps, 1), seed, wl.drift_sigma)
@@ -173,9 +182,7 @@ class Trainer:
         lr_min + (lr - lr_min) (1 + cos(pi t / total)) / 2."""
         if self.lr_schedule is None:
             return self.wl.lr
-        kind, total, lr_min = self.lr_schedule
-        if kind != "cosine":
-            raise ValueError("unknown lr schedule %r" % (kind,))
+        _, total, lr_min = self.lr_schedule
         return lr_min + (self.wl.lr - lr_min) * (1.0 + math.cos(math.pi * t / total)) / 2.0
 
     def flush(self):
