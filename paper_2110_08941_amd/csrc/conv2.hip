@@ -44,7 +44,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void* lds_ptr;          // LDS
 typedef __attribute__((address_space(1))) const void* gbl_cptr;   // global
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
 
 constexpr int C2_WAVES = 8;
 constexpr int C2_BM = 64 * C2_WAVES;   // rows per block
@@ -403,17 +403,20 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
     // written; rows past M re-read row M - 1 and are not stored.
     float* E = Ewave;
     constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
+    constexpr bool EBITS = (EPI & EPI_MBITS) != 0;   // the mask as bits: one byte per lane row
     auto epi_off = [&](int nb, int i) -> int64_t {
       const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
       const int m = m0 + row < p.M ? m0 + row : p.M - 1;
       return (int64_t)m * p.N + n0 + nb * 32 + c8;
     };
-    uint4 addv[2][EADD ? 4 : 1], maskv[2][EMASK ? 4 : 1];
+    uint4 addv[2][EADD ? 4 : 1], maskv[2][EMASK && !EBITS ? 4 : 1];
+    uint32_t maskb[2][EBITS ? 4 : 1];
     auto load_epi = [&](int nb, int slot) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if constexpr (EADD) addv[slot][i] = *(const uint4*)((const bf16_t*)p.addend + epi_off(nb, i));
-        if constexpr (EMASK) maskv[slot][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
+        if constexpr (EBITS) maskb[slot][i] = p.mbits[epi_off(nb, i) >> 3];
+        else if constexpr (EMASK) maskv[slot][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
       }
     };
     load_epi(0, 0);
@@ -444,7 +447,12 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
             v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
           }
         }
-        if constexpr (EMASK) {
+        if constexpr (EBITS) {
+          const uint32_t b = maskb[nb & 1][i];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (!((b >> e) & 1u)) v[e] = 0.f;
+        } else if constexpr (EMASK) {
           const uint4 u = maskv[nb & 1][i];
           const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -548,8 +556,10 @@ static void launch_epi2(const GemmParams& p, dim3 grid, hipStream_t s) {
     else if (relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_RELU, PATCH>), grid, dim3(512), 0, s, p);
     else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0, PATCH>), grid, dim3(512), 0, s, p);
   } else {
-    const bool add = p.addend != nullptr, mask = p.mask != nullptr;
-    if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
+    const bool add = p.addend != nullptr, mask = p.mask != nullptr || p.mbits != nullptr;
+    if (add && p.mbits) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK | EPI_MBITS, PATCH>), grid, dim3(512), 0, s, p);
+    else if (p.mbits) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK | EPI_MBITS, PATCH>), grid, dim3(512), 0, s, p);
+    else if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
     else if (add) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD, PATCH>), grid, dim3(512), 0, s, p);
     else if (mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
     else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0, PATCH>), grid, dim3(512), 0, s, p);

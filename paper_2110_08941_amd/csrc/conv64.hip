@@ -29,7 +29,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
 
 constexpr int P_W = 32;                     // map width
 constexpr int P_ROWS = 16;                  // output rows per tile
@@ -112,12 +112,15 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
       return (((int64_t)eb * H + y) * P_W + xx) * 64 + nb * 32 + c8;
     };
     constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
-    uint4 add_pre[2][EADD ? 4 : 1], mask_pre[2][EMASK ? 4 : 1];
+    constexpr bool EBITS = (EPI & EPI_MBITS) != 0;   // the mask as bits: one byte per lane row
+    uint4 add_pre[2][EADD ? 4 : 1], mask_pre[2][EMASK && !EBITS ? 4 : 1];
+    uint32_t maskb[2][EBITS ? 4 : 1];
     auto load_epi = [&](int nb) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if constexpr (EADD) add_pre[nb][i] = *(const uint4*)((const bf16_t*)p.addend + epi_off(nb, i));
-        if constexpr (EMASK) mask_pre[nb][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
+        if constexpr (EBITS) maskb[nb][i] = p.mbits[epi_off(nb, i) >> 3];
+        else if constexpr (EMASK) mask_pre[nb][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
       }
     };
     if constexpr (EADD || EMASK) load_epi(0);
@@ -212,7 +215,12 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
         }
-        if constexpr ((EPI & EPI_MASK) != 0) {
+        if constexpr (EBITS) {
+          const uint32_t b = maskb[nb][i];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (!((b >> e) & 1u)) v[e] = 0.f;
+        } else if constexpr ((EPI & EPI_MASK) != 0) {
           const uint4 u = mask_pre[nb][i];
           const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -246,8 +254,10 @@ static void launch64(const GemmParams& p, int ntiles, dim3 grid, hipStream_t s) 
     else if (relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
     else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);
   } else {
-    const bool add = p.addend != nullptr, mask = p.mask != nullptr;
-    if (add && mask) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD | EPI_MASK>), grid, dim3(512), 0, s, p, ntiles);
+    const bool add = p.addend != nullptr, mask = p.mask != nullptr || p.mbits != nullptr;
+    if (add && p.mbits) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD | EPI_MASK | EPI_MBITS>), grid, dim3(512), 0, s, p, ntiles);
+    else if (p.mbits) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_MASK | EPI_MBITS>), grid, dim3(512), 0, s, p, ntiles);
+    else if (add && mask) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD | EPI_MASK>), grid, dim3(512), 0, s, p, ntiles);
     else if (add) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_ADD>), grid, dim3(512), 0, s, p, ntiles);
     else if (mask) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_MASK>), grid, dim3(512), 0, s, p, ntiles);
     else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);

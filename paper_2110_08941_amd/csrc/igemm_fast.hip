@@ -29,7 +29,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_F32 = 4, EPI_ADD = 8, EPI_MASK = 16 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_F32 = 4, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
 
 __device__ inline int swz(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ inline int lds_off(int row, int chunk) { return row * 128 + ((chunk ^ swz(row)) << 4); }
@@ -446,6 +446,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
     constexpr int CW = 4 * WTM * (WTN + 4) * 4 <= SMEM ? WTN : WTN / 2;
     constexpr int EROW = CW + 4, LPR = CW / 8, RPP = 64 / LPR, NRI = WTM / RPP;
     constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
+    constexpr bool EBITS = (EPI & EPI_MBITS) != 0;   // the mask as bits: one byte per lane row
     static_assert(4 * WTM * EROW * 4 <= SMEM, "epilogue staging exceeds LDS");
     // The main loop ended with a barrier.  Each wave stages its sub-tile in
     // its own region and reads back only its own rows (one wave's LDS
@@ -468,7 +469,8 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
       __builtin_amdgcn_wave_barrier();
       int64_t offs[NRI];
       bool oks[NRI];
-      uint4 addv[EADD ? NRI : 1], maskv[EMASK ? NRI : 1];
+      uint4 addv[EADD ? NRI : 1], maskv[EMASK && !EBITS ? NRI : 1];
+      uint32_t maskb[EBITS ? NRI : 1];
 #pragma unroll
       for (int k = 0; k < NRI; ++k) {
         const int row = k * RPP + lane / LPR, c8 = 8 * (lane % LPR);
@@ -483,7 +485,8 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
         }
         offs[k] = oks[k] ? orow * p.N + n : 0;
         if constexpr (EADD) addv[k] = *(const uint4*)((const bf16_t*)p.addend + offs[k]);
-        if constexpr (EMASK) maskv[k] = *(const uint4*)((const bf16_t*)p.mask + offs[k]);
+        if constexpr (EBITS) maskb[k] = p.mbits[offs[k] >> 3];
+        else if constexpr (EMASK) maskv[k] = *(const uint4*)((const bf16_t*)p.mask + offs[k]);
       }
 #pragma unroll
       for (int k = 0; k < NRI; ++k) {
@@ -499,7 +502,11 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
             v[2 * e + 1] += bf2f((bf16_t)(w[e] >> 16));
           }
         }
-        if constexpr (EMASK) {
+        if constexpr (EBITS) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (!((maskb[k] >> e) & 1u)) v[e] = 0.f;
+        } else if constexpr (EMASK) {
           const uint32_t w[4] = {maskv[k].x, maskv[k].y, maskv[k].z, maskv[k].w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -607,6 +614,13 @@ static void launch_epi(const GemmParams& p, dim3 grid, hipStream_t s) {
     else launch_one<T, MODE, BM, BN, WGM, EPI_F32>(p, grid, s);
   } else if constexpr (MODE == MODE_DGRAD) {
     const bool add = p.addend != nullptr, mask = p.mask != nullptr;
+    if constexpr (sizeof(T) == 2) {
+      if (p.mbits) {   // bf16 data gradients stage their epilogue: the mask as bits
+        if (add) launch_one<T, MODE, BM, BN, WGM, EPI_ADD | EPI_MASK | EPI_MBITS>(p, grid, s);
+        else launch_one<T, MODE, BM, BN, WGM, EPI_MASK | EPI_MBITS>(p, grid, s);
+        return;
+      }
+    }
     if (add && mask) launch_one<T, MODE, BM, BN, WGM, EPI_ADD | EPI_MASK>(p, grid, s);
     else if (add) launch_one<T, MODE, BM, BN, WGM, EPI_ADD>(p, grid, s);
     else if (mask) launch_one<T, MODE, BM, BN, WGM, EPI_MASK>(p, grid, s);

@@ -35,6 +35,10 @@ struct GemmParams {
   const float* bias;    // FWD: [N] added to the output, or null
   const void* addend;   // DGRAD: [M][N] (activation type) added to the output, or null
   const void* mask;     // [M][N] (activation type): output zeroed where mask <= 0, or null
+  // the same mask as bits, 1 per element: bit e of byte (m N + n) / 8 is
+  // [mask[m][n + e] > 0] (N % 8 == 0).  Read instead of mask by the bf16
+  // data-gradient epilogues that stage 8 channels per lane; null: none
+  const uint8_t* mbits;
   int relu;             // FWD: clamp the output at zero
   int out_f32;          // FWD/DGRAD: output stored as fp32 (else activation type)
   int M, N, K;
@@ -174,10 +178,12 @@ hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy,
 // vectorised (C % 8 == 0) batch-norm apply / backward by segment: segment s
 // normalises with mean + s * mstride, rstd + s * mstride; the backward takes
 // its sums from sum_dy[s], sum_dyx[s]
+// ybits: also [y > 0] of every stored element as bits ([rows][C / 8] bytes,
+// the layout of GemmParams::mbits), or null
 hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const float* rstd,
                             int mstride, const float* gamma, const float* beta, const void* res,
                             int relu, const Segs& sg, int64_t rows_per_sample, int C, void* y,
-                            hipStream_t s);
+                            hipStream_t s, uint8_t* ybits = nullptr);
 hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const void* z,
                                const float* mean, const float* rstd, int mstride,
                                const float* gamma, float* const* sum_dy, float* const* sum_dyx,

@@ -219,7 +219,13 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   const int64_t es = m.dtype == HS_BF16 ? 2 : 4;
   Bump a{ws->arena};
   ws->slot.clear();
-  auto act = [&](int64_t per_sample) { ws->slot.push_back(a.take(per_sample * max_n * es)); };
+  ws->bits.clear();
+  // bits: the slot is a ReLU output that data gradients read as their mask;
+  // it also gets a copy of [value > 0] as bits (one byte per 8 channels)
+  auto act = [&](int64_t per_sample, bool bits = false) {
+    ws->slot.push_back(a.take(per_sample * max_n * es));
+    ws->bits.push_back(bits ? (uint8_t*)a.take(per_sample * max_n / 8) : nullptr);
+  };
   if (m.arch == HS_MLP) {
     act(784);    // 0: input in activation type
     act(256);    // 1: hidden (post ReLU)
@@ -233,31 +239,31 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   } else if (m.arch == HS_RESNET18) {
     act(8 * 1024);           // 0: X0 (channels padded)
     act(64 * 1024);          // 1: Zs
-    act(64 * 1024);          // 2: As
+    act(64 * 1024, true);    // 2: As
     for (const BlockL& b : m.blocks) {
       const int64_t e = (int64_t)b.c1.Ho * b.c1.Wo * b.c1.cout;
       act(e);                // Z1
-      act(e);                // H
+      act(e, true);          // H
       act(e);                // Z2
       act(b.proj ? e : 0);   // ZP
-      act(e);                // A_out
+      act(e, true);          // A_out
     }
     act(512);                // F
   } else if (m.arch == HS_RESNET50) {
     act(8 * 1024);           // 0: X0 (channels padded)
     act(64 * 1024);          // 1: Zs
-    act(64 * 1024);          // 2: As
+    act(64 * 1024, true);    // 2: As
     for (const BlockL& b : m.blocks) {
       const int64_t ein = (int64_t)b.c1.Ho * b.c1.Wo * b.c1.cout;   // input grid, inner width
       const int64_t emid = (int64_t)b.c2.Ho * b.c2.Wo * b.c2.cout;  // output grid, inner width
       const int64_t eout = (int64_t)b.c3.Ho * b.c3.Wo * b.c3.cout;  // output grid, output width
       act(ein);              // Z1
-      act(ein);              // H1
+      act(ein, true);        // H1
       act(emid);             // Z2
-      act(emid);             // H2
+      act(emid, true);       // H2
       act(eout);             // Z3
       act(b.proj ? eout : 0);  // ZP
-      act(eout);             // A_out
+      act(eout, true);       // A_out
     }
     act(2048);               // F
   } else {
@@ -457,7 +463,11 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   else if (w64) HS_TRY(launch_conv64(mode, q, c.s));
   else if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
   else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
-  else HS_TRY(launch_igemm(mode, c.bf, p, veca, vecb, bm, bn, splits, c.s));
+  else {
+    GemmParams r = p;
+    r.mbits = nullptr;   // the generic kernel reads the mask tensor
+    HS_TRY(launch_igemm(mode, c.bf, r, veca, vecb, bm, bn, splits, c.s));
+  }
   if (probe) {
     HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
     ws.probe_flops[ws.probe_used] = flops;
@@ -499,7 +509,8 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
 // stride-2 parity path, and when it is not available nothing is launched and
 // *fused is false (the caller then runs the two data gradients itself).
 hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, const void* addend,
-                      const void* mask, const ConvL* proj = nullptr, const void* dproj = nullptr,
+                      const void* mask, const uint8_t* mbits = nullptr,
+                      const ConvL* proj = nullptr, const void* dproj = nullptr,
                       bool* fused = nullptr) {
   if (fused) *fused = false;
   GemmParams p = base_params(L, c.n);
@@ -508,6 +519,7 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   p.out = dx;
   p.addend = addend;
   p.mask = mask;
+  p.mbits = c.bf && mask ? mbits : nullptr;   // bits of the same mask, where available
   p.out_f32 = c.bf ? 0 : 1;
   p.M = c.n * L.H * L.W;
   p.N = L.cin;
@@ -671,9 +683,9 @@ hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
 
 // y = relu?(batch-norm(z) + res) with every worker's own statistics
 hipError_t bn_apply(const Ctx& c, const BNL& b, const void* z, const void* res, int relu,
-                    int64_t rps, void* y) {
+                    int64_t rps, void* y, uint8_t* ybits = nullptr) {
   return launch_bn_apply8(c.bf, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
-                          c.theta + b.b, res, relu, c.sg, rps, b.c, y, c.s);
+                          c.theta + b.b, res, relu, c.sg, rps, b.c, y, c.s, ybits);
 }
 
 // dz = batch-norm backward of dy (masked by [act > 0] if act); writes every
@@ -774,20 +786,22 @@ hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss
 hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const Model& m = c.m;
   void** S = c.ws.slot.data();
+  uint8_t* const* Bt = c.ws.bits.data();   // bits of the ReLU outputs
   void** G = c.ws.grad;
   const int n = c.n;
   HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
   HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
-  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2]));
+  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
   const void* cur = S[2];
   int si = 3;
   for (const BlockL& b : m.blocks) {
     void *Z1 = S[si], *Hh = S[si + 1], *Z2 = S[si + 2], *ZP = S[si + 3], *A = S[si + 4];
+    uint8_t *Hb = Bt[si + 1], *Ab = Bt[si + 4];
     si += 5;
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
     HS_TRY(bn_stats(c, b.b1, Z1, rps));
-    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rps, Hh));
+    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rps, Hh, Hb));
     HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
     HS_TRY(bn_stats(c, b.b2, Z2, rps));
     const void* res = cur;
@@ -797,7 +811,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rps, G[0]));
       res = G[0];
     }
-    HS_TRY(bn_apply(c, b.b2, Z2, res, 1, rps, A));
+    HS_TRY(bn_apply(c, b.b2, Z2, res, 1, rps, A, Ab));
     cur = A;
   }
   void* F = S[si];
@@ -819,7 +833,9 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const BlockL& b = m.blocks[bi];
     const int base = 3 + 5 * bi;
     void *Z1 = S[base], *Hh = S[base + 1], *Z2 = S[base + 2], *ZP = S[base + 3];
-    const void* in = bi == 0 ? S[2] : S[3 + 5 * (bi - 1) + 4];   // post-ReLU input
+    const int in_slot = bi == 0 ? 2 : 3 + 5 * (bi - 1) + 4;      // post-ReLU input
+    const void* in = S[in_slot];
+    const uint8_t* inb = Bt[in_slot];
     int fr[4], k = 0;
     for (int i = 0; i < 5; ++i)
       if (i != gi) fr[k++] = i;
@@ -827,7 +843,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
-    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, Hh));                       // dH * [H > 0]
+    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, Hh, Bt[base + 1]));         // dH * [H > 0]
     HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rps, P2));                      // dZ1
     HS_TRY(conv_wgrad(c, b.c1, P2, in));
     if (b.proj) {
@@ -836,14 +852,14 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       // dIn * [in > 0], the shortcut's data gradient summed in the same pass
       // where the layer shapes allow it, else added from its own output
       bool fused = false;
-      HS_TRY(conv_dgrad(c, b.c1, P2, P4, nullptr, in, &b.cp, P3, &fused));
+      HS_TRY(conv_dgrad(c, b.c1, P2, P4, nullptr, in, inb, &b.cp, P3, &fused));
       if (!fused) {
         HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));              // shortcut grad
-        HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in));
+        HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in, inb));
       }
       gi = fr[2];
     } else {
-      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in));                          // dIn * [in > 0]
+      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in, inb));                     // dIn * [in > 0]
       gi = fr[1];
     }
   }
@@ -861,25 +877,27 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
 hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   const Model& m = c.m;
   void** S = c.ws.slot.data();
+  uint8_t* const* Bt = c.ws.bits.data();   // bits of the ReLU outputs
   void** G = c.ws.grad;
   const int n = c.n;
   constexpr int SLOTS = 7;
   HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
   HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
-  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2]));
+  HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
   const void* cur = S[2];
   int si = 3;
   for (const BlockL& b : m.blocks) {
     void *Z1 = S[si], *H1 = S[si + 1], *Z2 = S[si + 2], *H2 = S[si + 3], *Z3 = S[si + 4],
          *ZP = S[si + 5], *A = S[si + 6];
+    uint8_t *H1b = Bt[si + 1], *H2b = Bt[si + 3], *Ab = Bt[si + 6];
     si += SLOTS;
     const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
     HS_TRY(bn_stats(c, b.b1, Z1, rin));
-    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rin, H1));
+    HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rin, H1, H1b));
     HS_TRY(conv_fwd(c, b.c2, H1, Z2, false));
     HS_TRY(bn_stats(c, b.b2, Z2, rout));
-    HS_TRY(bn_apply(c, b.b2, Z2, nullptr, 1, rout, H2));
+    HS_TRY(bn_apply(c, b.b2, Z2, nullptr, 1, rout, H2, H2b));
     HS_TRY(conv_fwd(c, b.c3, H2, Z3, false));
     HS_TRY(bn_stats(c, b.b3, Z3, rout));
     const void* res = cur;
@@ -889,7 +907,7 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
       HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rout, G[0]));
       res = G[0];
     }
-    HS_TRY(bn_apply(c, b.b3, Z3, res, 1, rout, A));
+    HS_TRY(bn_apply(c, b.b3, Z3, res, 1, rout, A, Ab));
     cur = A;
   }
   const int cfin = m.blocks.back().c3.cout;
@@ -911,7 +929,9 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     const int base = 3 + SLOTS * bi;
     void *Z1 = S[base], *H1 = S[base + 1], *Z2 = S[base + 2], *H2 = S[base + 3],
          *Z3 = S[base + 4], *ZP = S[base + 5];
-    const void* in = bi == 0 ? S[2] : S[3 + SLOTS * (bi - 1) + 6];   // post-ReLU input
+    const int in_slot = bi == 0 ? 2 : 3 + SLOTS * (bi - 1) + 6;     // post-ReLU input
+    const void* in = S[in_slot];
+    const uint8_t* inb = Bt[in_slot];
     int fr[4], k = 0;
     for (int i = 0; i < 5; ++i)
       if (i != gi) fr[k++] = i;
@@ -919,19 +939,19 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
     HS_TRY(bn_bwd(c, b.b3, P1, nullptr, Z3, rout, P2));                     // dZ3
     HS_TRY(conv_wgrad(c, b.c3, P2, H2));
-    HS_TRY(conv_dgrad(c, b.c3, P2, P3, nullptr, H2));                      // dH2 * [H2 > 0]
+    HS_TRY(conv_dgrad(c, b.c3, P2, P3, nullptr, H2, Bt[base + 3]));        // dH2 * [H2 > 0]
     HS_TRY(bn_bwd(c, b.b2, P3, nullptr, Z2, rout, P2));                     // dZ2
     HS_TRY(conv_wgrad(c, b.c2, P2, H1));
-    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, H1));                      // dH1 * [H1 > 0]
+    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, H1, Bt[base + 1]));        // dH1 * [H1 > 0]
     HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rin, P2));                      // dZ1
     HS_TRY(conv_wgrad(c, b.c1, P2, in));
     if (b.proj) {
       HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rout, P3));                   // dZP
       HS_TRY(conv_wgrad(c, b.cp, P3, in));
       HS_TRY(conv_dgrad(c, b.cp, P3, P4, nullptr, nullptr));               // shortcut grad
-      HS_TRY(conv_dgrad(c, b.c1, P2, P1, P4, in));                         // dIn * [in > 0]
+      HS_TRY(conv_dgrad(c, b.c1, P2, P1, P4, in, inb));                    // dIn * [in > 0]
     } else {
-      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in));                         // dIn * [in > 0]
+      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in, inb));                    // dIn * [in > 0]
       gi = fr[1];
     }
   }

@@ -68,6 +68,7 @@ struct Workspace {
   char* arena = nullptr;
   int64_t bytes = 0;
   std::vector<void*> slot;     // forward activations, in plan order
+  std::vector<uint8_t*> bits;  // per slot: [slot > 0] as bits (ReLU outputs read as masks), or null
   void* grad[5] = {};          // gradient scratch buffers
   float* logits = nullptr;
   float* dz32 = nullptr;

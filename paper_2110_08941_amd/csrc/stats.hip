@@ -501,6 +501,7 @@ struct BnArgs {
   int relu;
   int C;
   void* out;
+  uint8_t* bits;        // apply: [y > 0] as bits, [rows][C / 8] bytes, or null
   SegRows sr;
   float* sum0[MAX_SEG]; // backward: per segment sum d and sum d * xhat
   float* sum1[MAX_SEG];
@@ -545,7 +546,29 @@ __global__ __launch_bounds__(256) void bn_apply8_kernel(BnArgs a) {
         if (res) o[j] += q[u][j];
         if (a.relu) o[j] = o[j] > 0.f ? o[j] : 0.f;
       }
-      store_vec8<T, NT>(y, rr * C + w.c0, o);
+      if constexpr (sizeof(T) == 2) {
+        // the bits test the stored (rounded) values
+        const uint32_t pk[4] = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])};
+        st16<NT>(y + rr * C + w.c0, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+        if (a.bits) {
+          uint32_t b = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            b |= (bf2f((bf16_t)(pk[e] & 0xffffu)) > 0.f ? 1u : 0u) << (2 * e);
+            b |= (bf2f((bf16_t)(pk[e] >> 16)) > 0.f ? 1u : 0u) << (2 * e + 1);
+          }
+          a.bits[(rr * C + w.c0) >> 3] = (uint8_t)b;
+        }
+      } else {
+        store_vec8<T, NT>(y, rr * C + w.c0, o);
+        if (a.bits) {
+          uint32_t b = 0;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) b |= (o[j] > 0.f ? 1u : 0u) << j;
+          a.bits[(rr * C + w.c0) >> 3] = (uint8_t)b;
+        }
+      }
     }
   }
 }
@@ -553,9 +576,10 @@ __global__ __launch_bounds__(256) void bn_apply8_kernel(BnArgs a) {
 hipError_t launch_bn_apply8(bool bf16, const void* z, const float* mean, const float* rstd,
                             int mstride, const float* gamma, const float* beta, const void* res,
                             int relu, const Segs& sg, int64_t rows_per_sample, int C, void* y,
-                            hipStream_t s) {
+                            hipStream_t s, uint8_t* ybits) {
   if (C % 8 || C / 8 > 256 || sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
   BnArgs a{};
+  a.bits = ybits;
   a.z = z;
   a.res = res;
   a.mean = mean;
