@@ -73,6 +73,19 @@ void probe_release(Workspace& w) {
   w.probe_mode = -1;
 }
 
+// the workspace's weight-gradient stream and events (tolerates a partial set)
+void release_side(Workspace& w) {
+  for (int i = 0; i < Workspace::kEvents; ++i)
+    if (w.ev[i]) {
+      (void)hipEventDestroy(w.ev[i]);
+      w.ev[i] = nullptr;
+    }
+  if (w.side) {
+    (void)hipStreamDestroy(w.side);
+    w.side = nullptr;
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -145,10 +158,21 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
   }
   w->ws.bytes = bytes;
   plan_workspace(model->m, max_n, &w->ws);
+  // the weight-gradient stream (default priority) and its ordering events
+  e = hipStreamCreateWithFlags(&w->ws.side, hipStreamNonBlocking);
+  for (int i = 0; e == hipSuccess && i < Workspace::kEvents; ++i)
+    e = hipEventCreateWithFlags(&w->ws.ev[i], hipEventDisableTiming);
+  if (e != hipSuccess) {
+    release_side(w->ws);
+    (void)hipFree(w->ws.arena);
+    delete w;
+    return hip_fail(e, "hs_workspace_create: stream/events");
+  }
   const std::vector<int64_t>& gaps = model->m.gaps;
   if (!gaps.empty()) {
     e = hipMemcpy(w->ws.gaps, gaps.data(), gaps.size() * sizeof(int64_t), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
+      release_side(w->ws);
       (void)hipFree(w->ws.arena);
       delete w;
       return hip_fail(e, "hs_workspace_create: upload");
@@ -161,6 +185,7 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
 hs_status hs_workspace_destroy(hs_workspace* ws) {
   if (!ws) return ok();
   probe_release(ws->ws);
+  release_side(ws->ws);
   if (ws->ws.arena) (void)hipFree(ws->ws.arena);
   delete ws;
   return ok();

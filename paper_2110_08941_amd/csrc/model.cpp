@@ -712,6 +712,26 @@ hipError_t loss_grad(const Ctx& c, const int32_t* y, float* loss, const void** d
   return hipSuccess;
 }
 
+// The weight gradients of the backward pass run on the workspace's second
+// stream, beside the batch-norm and data-gradient chain of the main stream:
+// fork() orders the second stream after the work enqueued so far on the
+// main one, join() the main stream after the second.  Without a second
+// stream (a temporary workspace) both are no-ops and side() is the main
+// stream.
+hipError_t order(Workspace& w, hipStream_t after, hipStream_t waiter) {
+  hipEvent_t e = w.ev[w.ev_next];
+  w.ev_next = (w.ev_next + 1) % Workspace::kEvents;
+  HS_TRY(hipEventRecord(e, after));
+  return hipStreamWaitEvent(waiter, e, 0);
+}
+hipError_t fork(const Ctx& c) { return c.ws.side ? order(c.ws, c.s, c.ws.side) : hipSuccess; }
+hipError_t join(const Ctx& c) { return c.ws.side ? order(c.ws, c.ws.side, c.s) : hipSuccess; }
+Ctx side(const Ctx& c) {
+  Ctx d = c;
+  if (c.ws.side) d.s = c.ws.side;
+  return d;
+}
+
 // ---------------------------------------------------------------- stem ----
 // The 3-channel first convolution runs on the fast kernel with its input and
 // weights zero-padded to 8 (bf16) or 4 (fp32) channels; its weight gradient
@@ -828,6 +848,12 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   // G[gi]: gradient of the current block's output, already multiplied by the
   // ReLU mask of that output: the data gradient that produces it applies
   // [input of the next block > 0] in its epilogue
+  // Weight gradients go to the second stream (cs).  Within a block each
+  // batch-norm backward writes a buffer of its own (dZ2 -> P2, dZ1 -> P4,
+  // dZP -> P3 after dH in P3 is consumed) and the block's output goes to a
+  // buffer the second stream does not read, so one join() per block -- before
+  // the next block reuses the buffers -- is enough.
+  const Ctx cs = side(c);
   int gi = 1;
   for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
     const BlockL& b = m.blocks[bi];
@@ -839,31 +865,37 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     int fr[4], k = 0;
     for (int i = 0; i < 5; ++i)
       if (i != gi) fr[k++] = i;
-    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]];
+    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]], *P5 = G[fr[3]];
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
+    HS_TRY(join(c));
     HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
-    HS_TRY(conv_wgrad(c, b.c2, P2, Hh));
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, b.c2, P2, Hh));
     HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, Hh, Bt[base + 1]));         // dH * [H > 0]
-    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rps, P2));                      // dZ1
-    HS_TRY(conv_wgrad(c, b.c1, P2, in));
+    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rps, P4));                      // dZ1
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, b.c1, P4, in));
     if (b.proj) {
       HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
-      HS_TRY(conv_wgrad(c, b.cp, P3, in));
+      HS_TRY(fork(c));
+      HS_TRY(conv_wgrad(cs, b.cp, P3, in));
       // dIn * [in > 0], the shortcut's data gradient summed in the same pass
       // where the layer shapes allow it, else added from its own output
       bool fused = false;
-      HS_TRY(conv_dgrad(c, b.c1, P2, P4, nullptr, in, inb, &b.cp, P3, &fused));
+      HS_TRY(conv_dgrad(c, b.c1, P4, P5, nullptr, in, inb, &b.cp, P3, &fused));
       if (!fused) {
         HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));              // shortcut grad
-        HS_TRY(conv_dgrad(c, b.c1, P2, P4, P1, in, inb));
+        HS_TRY(conv_dgrad(c, b.c1, P4, P5, P1, in, inb));
       }
-      gi = fr[2];
+      gi = fr[3];
     } else {
-      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in, inb));                     // dIn * [in > 0]
+      HS_TRY(conv_dgrad(c, b.c1, P4, P3, P1, in, inb));                     // dIn * [in > 0]
       gi = fr[1];
     }
   }
-  // stem (its ReLU mask is already applied)
+  // stem (its ReLU mask is already applied); every weight gradient is done
+  // when this returns
+  HS_TRY(join(c));
   void* dZs = G[gi == 0 ? 1 : 0];
   HS_TRY(bn_bwd(c, m.stem_bn, G[gi], nullptr, S[1], 1024, dZs));
   return stem_wgrad(c, m.stem, dZs, S[0]);

@@ -81,6 +81,12 @@ struct Workspace {
   void* wpack = nullptr;       // bf16 weights packed for the 32x32 MFMA kernel
   int64_t wpack_elems = 0;
   int64_t* gaps = nullptr;     // device copy of the padding ranges
+  // second stream for the weight gradients of the backward pass (null: all
+  // work on the caller's stream) and events that order the two streams
+  hipStream_t side = nullptr;
+  static constexpr int kEvents = 64;
+  hipEvent_t ev[kEvents] = {};
+  int ev_next = 0;
   // timing probe of one GEMM instantiation (mode, tile); see hs_probe_enable
   int probe_mode = -1, probe_bm = 0, probe_bn = 0;
   std::vector<hipEvent_t> probe_ev;   // 2 per launch
