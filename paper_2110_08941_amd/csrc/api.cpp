@@ -75,11 +75,16 @@ void probe_release(Workspace& w) {
 
 // the workspace's weight-gradient stream and events (tolerates a partial set)
 void release_side(Workspace& w) {
-  for (int i = 0; i < Workspace::kEvents; ++i)
+  for (int i = 0; i < Workspace::kEvents; ++i) {
     if (w.ev[i]) {
       (void)hipEventDestroy(w.ev[i]);
       w.ev[i] = nullptr;
     }
+    if (w.evr[i]) {
+      (void)hipEventDestroy(w.evr[i]);
+      w.evr[i] = nullptr;
+    }
+  }
   if (w.side) {
     (void)hipStreamDestroy(w.side);
     w.side = nullptr;
@@ -160,8 +165,10 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
   plan_workspace(model->m, max_n, &w->ws);
   // the weight-gradient stream (default priority) and its ordering events
   e = hipStreamCreateWithFlags(&w->ws.side, hipStreamNonBlocking);
-  for (int i = 0; e == hipSuccess && i < Workspace::kEvents; ++i)
+  for (int i = 0; e == hipSuccess && i < Workspace::kEvents; ++i) {
     e = hipEventCreateWithFlags(&w->ws.ev[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&w->ws.evr[i], hipEventDisableTiming);
+  }
   if (e != hipSuccess) {
     release_side(w->ws);
     (void)hipFree(w->ws.arena);

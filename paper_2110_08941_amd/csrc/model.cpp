@@ -276,7 +276,11 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     }
     act(512);                // Hf (fc1 output)
   }
-  for (int i = 0; i < 5; ++i) ws->grad[i] = a.take(m.max_act * max_n * es);
+  // the ResNet-18 backward rotates 8 buffers so that the weight-gradient
+  // stream can run a block behind (see GradPool); the others use 5
+  ws->ngrad = m.arch == HS_RESNET18 ? Workspace::kGrad : 5;
+  for (int i = 0; i < Workspace::kGrad; ++i)
+    ws->grad[i] = i < ws->ngrad ? a.take(m.max_act * max_n * es) : nullptr;
   ws->logits = (float*)a.take((int64_t)max_n * 10 * 4);
   ws->dz32 = (float*)a.take((int64_t)max_n * 10 * 4);
   ws->dzt = a.take((int64_t)max_n * 10 * es);
@@ -732,6 +736,62 @@ Ctx side(const Ctx& c) {
   return d;
 }
 
+// Gradient buffers of a backward pass whose weight gradients run on the
+// second stream: a buffer the second stream reads keeps the event recorded
+// after that read, and the main stream waits for it only when it writes the
+// buffer again.  Free buffers are handed out least recently released first,
+// those without a pending read before the others.
+struct GradPool {
+  Workspace& w;
+  hipStream_t main;
+  int n;
+  bool live[Workspace::kGrad] = {};
+  int pending[Workspace::kGrad];   // event slot of the last second-stream read, or -1
+  int64_t stamp[Workspace::kGrad] = {};
+  int64_t clock = 0;
+  GradPool(Workspace& ws, hipStream_t s) : w(ws), main(s), n(ws.ngrad) {
+    for (int i = 0; i < Workspace::kGrad; ++i) pending[i] = -1;
+  }
+  void* operator[](int i) const { return w.grad[i]; }
+  // a free buffer for the main stream to write
+  int take(int& out) {
+    int best = -1;
+    for (int i = 0; i < n; ++i) {
+      if (live[i]) continue;
+      if (best < 0 || (pending[i] < 0) > (pending[best] < 0) ||
+          ((pending[i] < 0) == (pending[best] < 0) && stamp[i] < stamp[best]))
+        best = i;
+    }
+    if (best < 0) return -1;
+    if (pending[best] >= 0 && w.side) {
+      if (hipStreamWaitEvent(main, w.evr[pending[best]], 0) != hipSuccess) return -1;
+    }
+    pending[best] = -1;
+    live[best] = true;
+    out = best;
+    return 0;
+  }
+  void drop(int i) {
+    live[i] = false;
+    stamp[i] = ++clock;
+  }
+  // the second stream has been given work that reads buffer i.  The slot's
+  // events are recorded on the second stream only, so if the ring reuses it
+  // before the wait, the wait covers a later point of that stream: later
+  // than needed, never earlier.
+  hipError_t read_on_side(int i) {
+    if (!w.side) return hipSuccess;
+    const int k = w.evr_next;
+    w.evr_next = (w.evr_next + 1) % Workspace::kEvents;
+    pending[i] = k;
+    return hipEventRecord(w.evr[k], w.side);
+  }
+};
+
+#define HS_TAKE(pool, var)                                 \
+  int var = -1;                                            \
+  if ((pool).take(var) != 0) return hipErrorInvalidValue;
+
 // ---------------------------------------------------------------- stem ----
 // The 3-channel first convolution runs on the fast kernel with its input and
 // weights zero-padded to 8 (bf16) or 4 (fp32) channels; its weight gradient
@@ -848,12 +908,11 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   // G[gi]: gradient of the current block's output, already multiplied by the
   // ReLU mask of that output: the data gradient that produces it applies
   // [input of the next block > 0] in its epilogue
-  // Weight gradients go to the second stream (cs).  Within a block each
-  // batch-norm backward writes a buffer of its own (dZ2 -> P2, dZ1 -> P4,
-  // dZP -> P3 after dH in P3 is consumed) and the block's output goes to a
-  // buffer the second stream does not read, so one join() per block -- before
-  // the next block reuses the buffers -- is enough.
+  // Weight gradients go to the second stream (cs); the buffers they read
+  // are only waited for when the main stream writes them again (GradPool).
   const Ctx cs = side(c);
+  GradPool gp(c.ws, c.s);
+  gp.live[1] = true;   // G[1]: gradient of the last block's output
   int gi = 1;
   for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
     const BlockL& b = m.blocks[bi];
@@ -862,43 +921,53 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const int in_slot = bi == 0 ? 2 : 3 + 5 * (bi - 1) + 4;      // post-ReLU input
     const void* in = S[in_slot];
     const uint8_t* inb = Bt[in_slot];
-    int fr[4], k = 0;
-    for (int i = 0; i < 5; ++i)
-      if (i != gi) fr[k++] = i;
-    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]], *P5 = G[fr[3]];
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
-    HS_TRY(join(c));
-    HS_TRY(bn_bwd(c, b.b2, P1, nullptr, Z2, rps, P2));                      // dZ2
+    const int p1 = gi;
+    HS_TAKE(gp, p2);
+    HS_TRY(bn_bwd(c, b.b2, gp[p1], nullptr, Z2, rps, gp[p2]));              // dZ2
     HS_TRY(fork(c));
-    HS_TRY(conv_wgrad(cs, b.c2, P2, Hh));
-    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, Hh, Bt[base + 1]));         // dH * [H > 0]
-    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rps, P4));                      // dZ1
+    HS_TRY(conv_wgrad(cs, b.c2, gp[p2], Hh));
+    HS_TRY(gp.read_on_side(p2));
+    HS_TAKE(gp, p3);
+    HS_TRY(conv_dgrad(c, b.c2, gp[p2], gp[p3], nullptr, Hh, Bt[base + 1])); // dH * [H > 0]
+    gp.drop(p2);
+    HS_TAKE(gp, p4);
+    HS_TRY(bn_bwd(c, b.b1, gp[p3], nullptr, Z1, rps, gp[p4]));              // dZ1
+    gp.drop(p3);
     HS_TRY(fork(c));
-    HS_TRY(conv_wgrad(cs, b.c1, P4, in));
+    HS_TRY(conv_wgrad(cs, b.c1, gp[p4], in));
+    HS_TRY(gp.read_on_side(p4));
+    HS_TAKE(gp, out);
     if (b.proj) {
-      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rps, P3));                    // dZP
+      HS_TAKE(gp, pz);
+      HS_TRY(bn_bwd(c, b.bp, gp[p1], nullptr, ZP, rps, gp[pz]));            // dZP
       HS_TRY(fork(c));
-      HS_TRY(conv_wgrad(cs, b.cp, P3, in));
+      HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
+      HS_TRY(gp.read_on_side(pz));
       // dIn * [in > 0], the shortcut's data gradient summed in the same pass
       // where the layer shapes allow it, else added from its own output
       bool fused = false;
-      HS_TRY(conv_dgrad(c, b.c1, P4, P5, nullptr, in, inb, &b.cp, P3, &fused));
+      HS_TRY(conv_dgrad(c, b.c1, gp[p4], gp[out], nullptr, in, inb, &b.cp, gp[pz], &fused));
       if (!fused) {
-        HS_TRY(conv_dgrad(c, b.cp, P3, P1, nullptr, nullptr));              // shortcut grad
-        HS_TRY(conv_dgrad(c, b.c1, P4, P5, P1, in, inb));
+        HS_TAKE(gp, sc);
+        HS_TRY(conv_dgrad(c, b.cp, gp[pz], gp[sc], nullptr, nullptr));      // shortcut grad
+        HS_TRY(conv_dgrad(c, b.c1, gp[p4], gp[out], gp[sc], in, inb));
+        gp.drop(sc);
       }
-      gi = fr[3];
+      gp.drop(pz);
     } else {
-      HS_TRY(conv_dgrad(c, b.c1, P4, P3, P1, in, inb));                     // dIn * [in > 0]
-      gi = fr[1];
+      HS_TRY(conv_dgrad(c, b.c1, gp[p4], gp[out], gp[p1], in, inb));        // dIn * [in > 0]
     }
+    gp.drop(p4);
+    gp.drop(p1);
+    gi = out;
   }
   // stem (its ReLU mask is already applied); every weight gradient is done
-  // when this returns
+  // when this returns (the stem's weight gradient shares the split-K buffer)
   HS_TRY(join(c));
-  void* dZs = G[gi == 0 ? 1 : 0];
-  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], nullptr, S[1], 1024, dZs));
-  return stem_wgrad(c, m.stem, dZs, S[0]);
+  HS_TAKE(gp, zs);
+  HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
+  return stem_wgrad(c, m.stem, gp[zs], S[0]);
 }
 
 // ---------------------------------------------------------- ResNet-50 ----

@@ -69,7 +69,9 @@ struct Workspace {
   int64_t bytes = 0;
   std::vector<void*> slot;     // forward activations, in plan order
   std::vector<uint8_t*> bits;  // per slot: [slot > 0] as bits (ReLU outputs read as masks), or null
-  void* grad[5] = {};          // gradient scratch buffers
+  static constexpr int kGrad = 8;
+  void* grad[kGrad] = {};      // gradient scratch buffers (5, or 8 for the ResNet-18 pool)
+  int ngrad = 5;
   float* logits = nullptr;
   float* dz32 = nullptr;
   void* dzt = nullptr;
@@ -85,8 +87,10 @@ struct Workspace {
   // work on the caller's stream) and events that order the two streams
   hipStream_t side = nullptr;
   static constexpr int kEvents = 64;
-  hipEvent_t ev[kEvents] = {};
+  hipEvent_t ev[kEvents] = {};     // fork / join points (either stream)
   int ev_next = 0;
+  hipEvent_t evr[kEvents] = {};    // points after second-stream reads (that stream only)
+  int evr_next = 0;
   // timing probe of one GEMM instantiation (mode, tile); see hs_probe_enable
   int probe_mode = -1, probe_bm = 0, probe_bn = 0;
   std::vector<hipEvent_t> probe_ev;   // 2 per launch
