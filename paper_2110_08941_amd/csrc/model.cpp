@@ -288,6 +288,7 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   const int64_t cmax = m.max_c > 512 ? m.max_c : 512;
   ws->stem_w = a.take((int64_t)64 * 9 * 8 * es);
   ws->stat_part = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
+  ws->stat_part_side = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
   // split-K partials: at least one split per worker of the largest weight
   // gradient (first layer counted with its padded channels)
   int64_t max_w = 64 * 9 * 8;
@@ -330,6 +331,8 @@ struct Ctx {
   int V;  // elements per 16 bytes
   Segs sg;
   float* g[MAX_SEG];
+  float* part = nullptr;   // statistics partials of this stream (null: ws.stat_part)
+  float* sp() const { return part ? part : ws.stat_part; }
   const void* W(int64_t off) const {
     return bf ? (const void*)(tbf + off) : (const void*)(theta + off);
   }
@@ -441,7 +444,7 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // there; with 64 channels or stride 2 the 128-byte K slices of the kernel
   // above use the cache lines of the gathered operand better)
   const int ctap = mode == MODE_FWD ? p.g.C : p.g.K;
-  const bool mfma32 = c.bf && mode != MODE_WGRAD && ws.wpack && p.g.stride == 1 && ctap >= 128 &&
+  bool mfma32 = c.bf && mode != MODE_WGRAD && ws.wpack && p.g.stride == 1 && ctap >= 128 &&
                       conv2_ok(mode, p) && conv2_packed_elems(p, mode) <= ws.wpack_elems;
   // bf16 3x3 stride-1 weight gradient: patch kernel (split table in slices)
   const bool wg3 = c.bf && mode == MODE_WGRAD && p.nseg > 0 && wgrad3_ok(p) &&
@@ -451,9 +454,12 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     bn = 64;
   }
   // 64 -> 64 channel 3x3 stride-1 on 32-wide maps: LDS patch kernel
-  const bool w64 = c.bf && mode != MODE_WGRAD && ws.wpack && conv64_ok(mode, p) &&
+  bool w64 = c.bf && mode != MODE_WGRAD && ws.wpack && conv64_ok(mode, p) &&
                    conv2_ok(mode, p) && conv2_packed_elems(p, mode) <= ws.wpack_elems;
   GemmParams q = p;
+  // the packed-weight buffer is the main stream's: launches on the second
+  // stream (c.part set) take the other kernels
+  if (c.part) mfma32 = w64 = false;
   if (mfma32 || w64) {
     HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
     q.b = ws.wpack;
@@ -671,7 +677,7 @@ hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64
   float* out[MAX_SEG];
   for (int i = 0; i < c.sg.count; ++i) out[i] = c.g[i] + boff;
   return launch_chan_stats(2, f32 ? false : c.bf, nullptr, dy, nullptr, nullptr, nullptr, 0, c.sg,
-                           rps, C, c.ws.stat_part, out, nullptr, 0.f, c.s);
+                           rps, C, c.sp(), out, nullptr, 0.f, c.s);
 }
 
 // per-worker batch-norm statistics of z (rps rows per sample)
@@ -682,7 +688,7 @@ hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
     o1[i] = c.rstd(b, i);
   }
   return launch_chan_stats(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, 0, c.sg, rps, b.c,
-                           c.ws.stat_part, o0, o1, 1e-5f, c.s);
+                           c.sp(), o0, o1, 1e-5f, c.s);
 }
 
 // y = relu?(batch-norm(z) + res) with every worker's own statistics
@@ -702,7 +708,7 @@ hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, c
     dg[i] = c.g[i] + b.g;
   }
   HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps, b.c,
-                           c.ws.stat_part, db, dg, 0.f, c.s));
+                           c.sp(), db, dg, 0.f, c.s));
   return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
                              db, dg, c.sg, rps, b.c, dz, c.s);
 }
@@ -732,8 +738,24 @@ hipError_t fork(const Ctx& c) { return c.ws.side ? order(c.ws, c.s, c.ws.side) :
 hipError_t join(const Ctx& c) { return c.ws.side ? order(c.ws, c.ws.side, c.s) : hipSuccess; }
 Ctx side(const Ctx& c) {
   Ctx d = c;
-  if (c.ws.side) d.s = c.ws.side;
+  if (c.ws.side) {
+    d.s = c.ws.side;
+    d.part = c.ws.stat_part_side;
+  }
   return d;
+}
+// a point of the second stream that the main stream waits for later: the
+// ring is recorded on the second stream only, so a reuse before the wait
+// makes the wait later than needed, never earlier
+int side_mark(const Ctx& c) {
+  if (!c.ws.side) return -1;
+  const int k = c.ws.evr_next;
+  c.ws.evr_next = (c.ws.evr_next + 1) % Workspace::kEvents;
+  return hipEventRecord(c.ws.evr[k], c.ws.side) == hipSuccess ? k : -2;
+}
+hipError_t wait_mark(const Ctx& c, int k) {
+  if (k == -2) return hipErrorUnknown;
+  return k >= 0 ? hipStreamWaitEvent(c.s, c.ws.evr[k], 0) : hipSuccess;
 }
 
 // Gradient buffers of a backward pass whose weight gradients run on the
@@ -869,6 +891,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   uint8_t* const* Bt = c.ws.bits.data();   // bits of the ReLU outputs
   void** G = c.ws.grad;
   const int n = c.n;
+  const Ctx cs = side(c);   // second stream: projection shortcuts, weight gradients
   HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
   HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
   HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
@@ -879,18 +902,23 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     uint8_t *Hb = Bt[si + 1], *Ab = Bt[si + 4];
     si += 5;
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
+    // the projection shortcut on the second stream, beside conv1 .. bn2
+    const void* res = cur;
+    int proj_done = -1;
+    if (b.proj) {
+      HS_TRY(fork(c));
+      HS_TRY(conv_fwd(cs, b.cp, cur, ZP, false));
+      HS_TRY(bn_stats(cs, b.bp, ZP, rps));
+      HS_TRY(bn_apply(cs, b.bp, ZP, nullptr, 0, rps, G[0]));
+      proj_done = side_mark(c);
+      res = G[0];
+    }
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
     HS_TRY(bn_stats(c, b.b1, Z1, rps));
     HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rps, Hh, Hb));
     HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
     HS_TRY(bn_stats(c, b.b2, Z2, rps));
-    const void* res = cur;
-    if (b.proj) {
-      HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
-      HS_TRY(bn_stats(c, b.bp, ZP, rps));
-      HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rps, G[0]));
-      res = G[0];
-    }
+    HS_TRY(wait_mark(c, proj_done));
     HS_TRY(bn_apply(c, b.b2, Z2, res, 1, rps, A, Ab));
     cur = A;
   }
@@ -908,9 +936,9 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   // G[gi]: gradient of the current block's output, already multiplied by the
   // ReLU mask of that output: the data gradient that produces it applies
   // [input of the next block > 0] in its epilogue
-  // Weight gradients go to the second stream (cs); the buffers they read
-  // are only waited for when the main stream writes them again (GradPool).
-  const Ctx cs = side(c);
+  // Weight gradients, and the projection's batch-norm backward, go to the
+  // second stream (cs); the buffers it reads are only waited for when the
+  // main stream writes them again (GradPool).
   GradPool gp(c.ws, c.s);
   gp.live[1] = true;   // G[1]: gradient of the last block's output
   int gi = 1;
@@ -923,6 +951,16 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const uint8_t* inb = Bt[in_slot];
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     const int p1 = gi;
+    int pz = -1, pz_done = -1;
+    if (b.proj) {   // dZP on the second stream, needed only by conv1's data gradient
+      if (gp.take(pz) != 0) return hipErrorInvalidValue;
+      HS_TRY(fork(c));
+      HS_TRY(bn_bwd(cs, b.bp, gp[p1], nullptr, ZP, rps, gp[pz]));          // dZP
+      pz_done = side_mark(c);
+      HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
+      HS_TRY(gp.read_on_side(pz));
+      HS_TRY(gp.read_on_side(p1));
+    }
     HS_TAKE(gp, p2);
     HS_TRY(bn_bwd(c, b.b2, gp[p1], nullptr, Z2, rps, gp[p2]));              // dZ2
     HS_TRY(fork(c));
@@ -939,11 +977,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     HS_TRY(gp.read_on_side(p4));
     HS_TAKE(gp, out);
     if (b.proj) {
-      HS_TAKE(gp, pz);
-      HS_TRY(bn_bwd(c, b.bp, gp[p1], nullptr, ZP, rps, gp[pz]));            // dZP
-      HS_TRY(fork(c));
-      HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
-      HS_TRY(gp.read_on_side(pz));
+      HS_TRY(wait_mark(c, pz_done));
       // dIn * [in > 0], the shortcut's data gradient summed in the same pass
       // where the layer shapes allow it, else added from its own output
       bool fused = false;

@@ -78,6 +78,7 @@ struct Workspace {
   float* stats = nullptr;      // per batch-norm and worker: mean[max_c], rstd[max_c]
   void* stem_w = nullptr;      // first-layer weights, channel-padded copy
   float* stat_part = nullptr;  // per-channel statistics: block partials
+  float* stat_part_side = nullptr;  // the same for statistics on the second stream
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
   void* wpack = nullptr;       // bf16 weights packed for the 32x32 MFMA kernel
