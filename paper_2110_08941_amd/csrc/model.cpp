@@ -276,9 +276,9 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     }
     act(512);                // Hf (fc1 output)
   }
-  // the ResNet-18 backward rotates 8 buffers so that the weight-gradient
+  // the ResNet backward passes rotate 8 buffers so that the weight-gradient
   // stream can run a block behind (see GradPool); the others use 5
-  ws->ngrad = m.arch == HS_RESNET18 ? Workspace::kGrad : 5;
+  ws->ngrad = (m.arch == HS_RESNET18 || m.arch == HS_RESNET50) ? Workspace::kGrad : 5;
   for (int i = 0; i < Workspace::kGrad; ++i)
     ws->grad[i] = i < ws->ngrad ? a.take(m.max_act * max_n * es) : nullptr;
   ws->logits = (float*)a.take((int64_t)max_n * 10 * 4);
@@ -1016,6 +1016,7 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
   void** G = c.ws.grad;
   const int n = c.n;
   constexpr int SLOTS = 7;
+  const Ctx cs = side(c);   // second stream: projection shortcuts, weight gradients
   HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
   HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
   HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
@@ -1027,6 +1028,17 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     uint8_t *H1b = Bt[si + 1], *H2b = Bt[si + 3], *Ab = Bt[si + 6];
     si += SLOTS;
     const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
+    // the projection shortcut on the second stream, beside conv1 .. bn3
+    const void* res = cur;
+    int proj_done = -1;
+    if (b.proj) {
+      HS_TRY(fork(c));
+      HS_TRY(conv_fwd(cs, b.cp, cur, ZP, false));
+      HS_TRY(bn_stats(cs, b.bp, ZP, rout));
+      HS_TRY(bn_apply(cs, b.bp, ZP, nullptr, 0, rout, G[0]));
+      proj_done = side_mark(c);
+      res = G[0];
+    }
     HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
     HS_TRY(bn_stats(c, b.b1, Z1, rin));
     HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rin, H1, H1b));
@@ -1035,13 +1047,7 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     HS_TRY(bn_apply(c, b.b2, Z2, nullptr, 1, rout, H2, H2b));
     HS_TRY(conv_fwd(c, b.c3, H2, Z3, false));
     HS_TRY(bn_stats(c, b.b3, Z3, rout));
-    const void* res = cur;
-    if (b.proj) {
-      HS_TRY(conv_fwd(c, b.cp, cur, ZP, false));
-      HS_TRY(bn_stats(c, b.bp, ZP, rout));
-      HS_TRY(bn_apply(c, b.bp, ZP, nullptr, 0, rout, G[0]));
-      res = G[0];
-    }
+    HS_TRY(wait_mark(c, proj_done));
     HS_TRY(bn_apply(c, b.b3, Z3, res, 1, rout, A, Ab));
     cur = A;
   }
@@ -1057,7 +1063,12 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
   HS_TRY(bias_grad(c, m.fc2.b, c.ws.dz32, true, 1, 10));
   HS_TRY(conv_dgrad(c, m.fc2, dz, G[0], nullptr, nullptr));           // dF
   HS_TRY(launch_gap_bwd(c.bf, G[0], cur, n, hwfin, cfin, G[1], c.s));  // dA * [A > 0]
-  // G[gi]: gradient of the current block's output times its ReLU mask
+  // G[gi]: gradient of the current block's output times its ReLU mask.
+  // Weight gradients, and the projection's batch-norm backward, go to the
+  // second stream; the buffers it reads are only waited for when the main
+  // stream writes them again (GradPool).
+  GradPool gp(c.ws, c.s);
+  gp.live[1] = true;
   int gi = 1;
   for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
     const BlockL& b = m.blocks[bi];
@@ -1067,32 +1078,62 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     const int in_slot = bi == 0 ? 2 : 3 + SLOTS * (bi - 1) + 6;     // post-ReLU input
     const void* in = S[in_slot];
     const uint8_t* inb = Bt[in_slot];
-    int fr[4], k = 0;
-    for (int i = 0; i < 5; ++i)
-      if (i != gi) fr[k++] = i;
-    void *P1 = G[gi], *P2 = G[fr[0]], *P3 = G[fr[1]], *P4 = G[fr[2]];
     const int64_t rin = (int64_t)b.c1.Ho * b.c1.Wo, rout = (int64_t)b.c2.Ho * b.c2.Wo;
-    HS_TRY(bn_bwd(c, b.b3, P1, nullptr, Z3, rout, P2));                     // dZ3
-    HS_TRY(conv_wgrad(c, b.c3, P2, H2));
-    HS_TRY(conv_dgrad(c, b.c3, P2, P3, nullptr, H2, Bt[base + 3]));        // dH2 * [H2 > 0]
-    HS_TRY(bn_bwd(c, b.b2, P3, nullptr, Z2, rout, P2));                     // dZ2
-    HS_TRY(conv_wgrad(c, b.c2, P2, H1));
-    HS_TRY(conv_dgrad(c, b.c2, P2, P3, nullptr, H1, Bt[base + 1]));        // dH1 * [H1 > 0]
-    HS_TRY(bn_bwd(c, b.b1, P3, nullptr, Z1, rin, P2));                      // dZ1
-    HS_TRY(conv_wgrad(c, b.c1, P2, in));
-    if (b.proj) {
-      HS_TRY(bn_bwd(c, b.bp, P1, nullptr, ZP, rout, P3));                   // dZP
-      HS_TRY(conv_wgrad(c, b.cp, P3, in));
-      HS_TRY(conv_dgrad(c, b.cp, P3, P4, nullptr, nullptr));               // shortcut grad
-      HS_TRY(conv_dgrad(c, b.c1, P2, P1, P4, in, inb));                    // dIn * [in > 0]
-    } else {
-      HS_TRY(conv_dgrad(c, b.c1, P2, P3, P1, in, inb));                    // dIn * [in > 0]
-      gi = fr[1];
+    const int p1 = gi;
+    int pz = -1, pz_done = -1;
+    if (b.proj) {   // dZP on the second stream, needed only by the shortcut's data gradient
+      if (gp.take(pz) != 0) return hipErrorInvalidValue;
+      HS_TRY(fork(c));
+      HS_TRY(bn_bwd(cs, b.bp, gp[p1], nullptr, ZP, rout, gp[pz]));         // dZP
+      pz_done = side_mark(c);
+      HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
+      HS_TRY(gp.read_on_side(pz));
+      HS_TRY(gp.read_on_side(p1));
     }
+    HS_TAKE(gp, p2);
+    HS_TRY(bn_bwd(c, b.b3, gp[p1], nullptr, Z3, rout, gp[p2]));             // dZ3
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, b.c3, gp[p2], H2));
+    HS_TRY(gp.read_on_side(p2));
+    HS_TAKE(gp, p3);
+    HS_TRY(conv_dgrad(c, b.c3, gp[p2], gp[p3], nullptr, H2, Bt[base + 3]));  // dH2 * [H2 > 0]
+    gp.drop(p2);
+    HS_TAKE(gp, p4);
+    HS_TRY(bn_bwd(c, b.b2, gp[p3], nullptr, Z2, rout, gp[p4]));             // dZ2
+    gp.drop(p3);
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, b.c2, gp[p4], H1));
+    HS_TRY(gp.read_on_side(p4));
+    HS_TAKE(gp, p5);
+    HS_TRY(conv_dgrad(c, b.c2, gp[p4], gp[p5], nullptr, H1, Bt[base + 1]));  // dH1 * [H1 > 0]
+    gp.drop(p4);
+    HS_TAKE(gp, p6);
+    HS_TRY(bn_bwd(c, b.b1, gp[p5], nullptr, Z1, rin, gp[p6]));              // dZ1
+    gp.drop(p5);
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, b.c1, gp[p6], in));
+    HS_TRY(gp.read_on_side(p6));
+    HS_TAKE(gp, out);
+    if (b.proj) {
+      HS_TRY(wait_mark(c, pz_done));
+      HS_TAKE(gp, sc);
+      HS_TRY(conv_dgrad(c, b.cp, gp[pz], gp[sc], nullptr, nullptr));        // shortcut grad
+      HS_TRY(conv_dgrad(c, b.c1, gp[p6], gp[out], gp[sc], in, inb));        // dIn * [in > 0]
+      gp.drop(sc);
+      gp.drop(pz);
+    } else {
+      HS_TRY(conv_dgrad(c, b.c1, gp[p6], gp[out], gp[p1], in, inb));        // dIn * [in > 0]
+    }
+    gp.drop(p6);
+    gp.drop(p1);
+    gi = out;
   }
-  void* dZs = G[gi == 0 ? 1 : 0];
-  HS_TRY(bn_bwd(c, m.stem_bn, G[gi], nullptr, S[1], 1024, dZs));
-  return stem_wgrad(c, m.stem, dZs, S[0]);
+  // every weight gradient is done when this returns (the stem's shares the
+  // split-K buffer)
+  HS_TRY(join(c));
+  HS_TAKE(gp, zs);
+  HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
+  return stem_wgrad(c, m.stem, gp[zs], S[0]);
 }
 
 // -------------------------------------------------------------- VGG-16 ----

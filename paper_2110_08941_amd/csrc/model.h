@@ -70,7 +70,7 @@ struct Workspace {
   std::vector<void*> slot;     // forward activations, in plan order
   std::vector<uint8_t*> bits;  // per slot: [slot > 0] as bits (ReLU outputs read as masks), or null
   static constexpr int kGrad = 8;
-  void* grad[kGrad] = {};      // gradient scratch buffers (5, or 8 for the ResNet-18 pool)
+  void* grad[kGrad] = {};      // gradient scratch buffers (5, or 8 for the ResNet pools)
   int ngrad = 5;
   float* logits = nullptr;
   float* dz32 = nullptr;
