@@ -35,13 +35,18 @@
  *     is allocated on the step path.
  *   - A model is read-only after creation and may be shared by threads.  A
  *     workspace serves one hs_worker_grad at a time: concurrent workers need
- *     one workspace each.
+ *     one workspace each.  A workspace also owns a second HIP stream (default
+ *     priority) on which the ResNet passes run their weight gradients and
+ *     projection shortcuts; a call orders all of its work before its end on
+ *     the caller's stream (that stream waits for the second one), so the
+ *     caller sees one stream.
  *
  * Flat parameter vector layout (theta, g_m, momentum, theta_bf16):
  *   tensors in forward order; conv weights OHWI [c_out][3][3][c_in] (1x1 for
  *   the ResNet projection); linear weights [out][in]; a layer's bias follows
  *   its weight; batch-norm stores gamma then beta; inside a residual block the
- *   order is conv1, bn1, conv2, bn2, projection conv, projection bn.  Every
+ *   order is conv1, bn1, conv2, bn2 (then conv3, bn3 in a bottleneck),
+ *   projection conv, projection bn.  Every
  *   tensor starts at a multiple of 64 elements; the gaps are zero in g_m.
  *   hs_num_params() is the padded length P.
  */
