@@ -301,6 +301,12 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   if (m.dtype == HS_BF16) {
     ws->wpack_elems = max_w;
     ws->wpack = a.take(max_w * 2);
+    // packed regions: at most two (forward, data gradient) per weight tensor
+    int64_t all_w = 0;
+    for (const ParamT& t : m.params)
+      if (t.kind == HS_KIND_CONV_W || t.kind == HS_KIND_LIN_W) all_w += (t.numel + 63) / 64 * 64;
+    ws->packed_cap = 2 * all_w;
+    ws->packed = (bf16_t*)a.take(ws->packed_cap * 2);
   }
   ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
   return a.off;
@@ -427,6 +433,8 @@ void pick_fast_tiles(int mode, int M, int N, int& bm, int& bn) {
   bn = cand[best < 0 ? 2 : best][1];
 }
 
+hipError_t wait_mark(const Ctx& c, int k);
+
 // Launch one GEMM (fast kernel when the shape allows, generic otherwise);
 // brackets it with probe events when it is the probed instantiation.
 hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
@@ -461,8 +469,33 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // stream (c.part set) take the other kernels
   if (c.part) mfma32 = w64 = false;
   if (mfma32 || w64) {
-    HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
-    q.b = ws.wpack;
+    // the layer's region of packed weights: packed on the second stream at
+    // the start of the call, or now (first call, or a workspace without one)
+    int64_t woff = c.tbf ? (const bf16_t*)p.b - c.tbf : -1;
+    if (woff >= c.m.P) woff = -1;   // not a tensor of theta
+    const int64_t key = woff * 2 + (mode == MODE_DGRAD ? 1 : 0);
+    const auto it = ws.packed && woff >= 0 ? ws.pack_of.find(key) : ws.pack_of.end();
+    if (it != ws.pack_of.end() && ws.pack_ready >= 0) {
+      if (!ws.pack_waited) {
+        HS_TRY(wait_mark(c, ws.pack_ready));
+        ws.pack_waited = true;
+      }
+      q.b = ws.packed + ws.packs[it->second].dst;
+    } else if (it != ws.pack_of.end()) {
+      q.b = ws.packed + ws.packs[it->second].dst;
+      HS_TRY(launch_pack_weights(p.b, (void*)q.b, mode, p, c.s));
+    } else if (ws.packed && woff >= 0 &&
+               ws.packed_used + conv2_packed_elems(p, mode) <= ws.packed_cap) {
+      Workspace::Pack e{woff, ws.packed_used, p, mode};
+      ws.packed_used += (conv2_packed_elems(p, mode) + 63) / 64 * 64;
+      ws.pack_of[key] = (int)ws.packs.size();
+      ws.packs.push_back(e);
+      q.b = ws.packed + e.dst;
+      HS_TRY(launch_pack_weights(p.b, (void*)q.b, mode, p, c.s));
+    } else {
+      HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
+      q.b = ws.wpack;
+    }
     bm = w64 ? 64 : 512;
     bn = w64 ? 64 : conv2_bn(p.N);
   }
@@ -1239,11 +1272,29 @@ hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
         {}};
   for (int i = 0; i < M; ++i) c.g[i] = g[i];
   HS_TRY(launch_zero_ranges(c.g, M, ws.gaps, (int)(m.gaps.size() / 2), s));
-  if (m.arch == HS_MLP) return mlp(c, x, y, loss);
-  if (m.arch == HS_SMALLCNN) return small_cnn(c, x, y, loss);
-  if (m.arch == HS_RESNET18) return resnet(c, x, y, loss);
-  if (m.arch == HS_RESNET50) return resnet_bottleneck(c, x, y, loss);
-  return vgg(c, x, y, loss);
+  // this call's packed weights, on the second stream: every region an
+  // earlier call listed, ordered after the work already on the caller's
+  // stream (the update of theta_bf16); the first packed launch waits for it
+  ws.pack_ready = -1;
+  ws.pack_waited = false;
+  if (c.bf && ws.side && !ws.packs.empty()) {
+    HS_TRY(fork(c));
+    for (const Workspace::Pack& e : ws.packs)
+      HS_TRY(launch_pack_weights(theta_bf16 + e.woff, ws.packed + e.dst, e.mode, e.p, ws.side));
+    ws.pack_ready = side_mark(c);
+    if (ws.pack_ready < 0) return hipErrorUnknown;
+  }
+  hipError_t e;
+  if (m.arch == HS_MLP) e = mlp(c, x, y, loss);
+  else if (m.arch == HS_SMALLCNN) e = small_cnn(c, x, y, loss);
+  else if (m.arch == HS_RESNET18) e = resnet(c, x, y, loss);
+  else if (m.arch == HS_RESNET50) e = resnet_bottleneck(c, x, y, loss);
+  else e = vgg(c, x, y, loss);
+  // the packing is ordered before the caller's stream continues even if no
+  // launch used it
+  if (e == hipSuccess && ws.pack_ready >= 0 && !ws.pack_waited) e = wait_mark(c, ws.pack_ready);
+  ws.pack_ready = -1;
+  return e;
 }
 
 }  // namespace hs

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "kernels.h"
@@ -83,6 +84,20 @@ struct Workspace {
   int64_t splitk_floats = 0;
   void* wpack = nullptr;       // bf16 weights packed for the 32x32 MFMA kernel
   int64_t wpack_elems = 0;
+  // every layer's packed weights, one region per (layer, mode), filled on the
+  // second stream at the start of a call (after the first call has listed
+  // the regions): the main stream then launches no packing
+  struct Pack {
+    int64_t woff, dst;           // weight offset in theta; region offset (elements)
+    GemmParams p;                // the contraction's shape
+    int mode;
+  };
+  bf16_t* packed = nullptr;
+  int64_t packed_cap = 0, packed_used = 0;
+  std::vector<Pack> packs;
+  std::unordered_map<int64_t, int> pack_of;   // (woff * 2 + mode) -> packs index
+  int pack_ready = -1;         // event slot after this call's packing, -1: not packed
+  bool pack_waited = false;
   int64_t* gaps = nullptr;     // device copy of the padding ranges
   // second stream for the weight gradients of the backward pass (null: all
   // work on the caller's stream) and events that order the two streams
