@@ -224,3 +224,51 @@ def test_workers_grad_rejects_bad_arguments():
         hs.workspace_destroy(ws)
     finally:
         hs.model_destroy(m)
+
+
+@pytest.mark.parametrize("arch,n", [("resnet18", [3, 5, 2]), ("resnet50", [2, 3]),
+                                    ("vgg16", [4, 1, 3])])
+def test_workers_grad_reused_workspace(arch, n):
+    """A workspace's later calls (packed weights prepared on its second stream
+    at the start of the call, from the current theta_bf16) give bit-identical
+    gradients to a fresh workspace's first call (which packs as it goes), also
+    after theta changed between the calls on the same stream."""
+    hs = require_gpu()
+    log("reused workspace %s bf16 n=%s" % (arch, n))
+    net = Mo.build(arch)
+    table, P = Mo.param_table(net)
+    th1 = synth.separate_decisions(table, synth.he_normal(table, P, 7), 7)
+    th2 = synth.separate_decisions(table, synth.he_normal(table, P, 8), 8)
+    x, y = synth.batch((3, 32, 32), sum(n), 7, 1)
+    m = hs.model_create(arch, "bf16")
+    try:
+        xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+
+        def call(ws, th):
+            t = torch.from_numpy(np.asarray(th, dtype=np.float32)).cuda()
+            tb = torch.empty(P, dtype=torch.int16, device="cuda")
+            hs.params_to_bf16(t.data_ptr(), tb.data_ptr(), P)
+            grads = [torch.full((P,), float("nan"), device="cuda") for _ in n]
+            loss = torch.zeros(len(n), device="cuda")
+            hs.workers_grad(m, ws, t.data_ptr(), tb.data_ptr(), xd.data_ptr(), yd.data_ptr(), n,
+                            [g.data_ptr() for g in grads], loss.data_ptr(), 0)
+            torch.cuda.synchronize()
+            return [g.cpu().numpy() for g in grads], loss.cpu().numpy()
+
+        ws = hs.workspace_create(m, sum(n))
+        first = call(ws, th1)
+        again = call(ws, th1)             # prepacked from the same theta
+        changed = call(ws, th2)           # prepacked after theta changed
+        hs.workspace_destroy(ws)
+        fresh = hs.workspace_create(m, sum(n))
+        ref2 = call(fresh, th2)
+        hs.workspace_destroy(fresh)
+    finally:
+        hs.model_destroy(m)
+    for a, b in zip(first[0], again[0]):
+        assert np.array_equal(a, b)
+    assert np.array_equal(first[1], again[1])
+    for a, b in zip(changed[0], ref2[0]):
+        assert np.array_equal(a, b)
+    assert np.array_equal(changed[1], ref2[1])
+    assert not np.array_equal(first[0][0], changed[0][0])
