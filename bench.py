@@ -45,7 +45,7 @@ HBM_PEAK_GBS = 8000.0
 # 2 the patch weight-gradient kernel).
 PROBE = {"resnet18_bf16": (0, 512, 128), "resnet18_fp32": (2, 128, 128),
          "resnet50_bf16": (0, 512, 128),
-         "vgg16_bf16": (0, 512, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 64, 64)}
+         "vgg16_bf16": (0, 512, 128), "smallcnn_fp32": (2, 128, 128), "mlp_fp32": (0, 128, 64)}
 MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
 # template instance of each probed kernel whose HBM traffic has been counted
 PROBE_KERNEL = {(0, 512, 128, "bf16"): "conv2_kernel<0, 128, 9, 0, true>"}
