@@ -153,6 +153,39 @@ def test_multistep_theta_small_cnn(grouped):
     assert err <= TOL["fp32"]
 
 
+@pytest.mark.parametrize("grouped", [False, True])
+@pytest.mark.parametrize("name", ["resnet18_bf16", "resnet50_bf16"])
+def test_multistep_theta_bf16_resnet(name, grouped):
+    """Four steps of a bf16 ResNet workload (N = 24 over its 8 workers,
+    separated decisions, lr 0.01 so that they stay separated, momentum and
+    weight decay) on one workspace per worker: the later calls take the
+    packed weights prepared on the second stream and run the weight
+    gradients there.  The update theta_4 - theta_0 against the oracle's
+    driver with bf16 storage, within the bf16 bar."""
+    log("multistep %s grouped=%s" % (name, grouped))
+    wl = dataclasses.replace(WORKLOADS[name], total=24, steps=4, drift_sigma=0.0, lr=0.01)
+    require_gpu()
+    from paper_2110_08941_amd.driver import Trainer
+    net = Mo.build(wl.arch)
+    table, P = Mo.param_table(net)
+    theta = synth.separate_decisions(table, synth.he_normal(table, P, 2), 2)
+    tr = Trainer(wl, seed=2, clock="model", steps=4, theta0=theta, n_batches=4, grouped=grouped)
+    try:
+        batches = [(x.cpu().numpy(), y.cpu().numpy()) for x, y in tr.batches]
+        tr.run(4)
+        got = tr.theta.cpu().numpy().astype(np.float64)
+        used = [e["n"] for e in tr.log]
+        speeds = tr.speeds
+    finally:
+        tr.close()
+    out = S.run(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym, storage="bf16"),
+                theta.astype(np.float64), batches, speeds, wl.window, wl.lr, wl.mu, wl.wd)
+    assert used == out["partitions"]
+    err = normwise(got - theta, out["theta"] - theta)
+    log("  partitions %s, normwise err of the update %.3e" % (used[0], err))
+    assert err <= TOL["bf16"]
+
+
 MODES = {
     # Sync-SGD: even split throughout, plain mean
     "sync": dict(window=0, exchange="mean"),
