@@ -276,9 +276,10 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     }
     act(512);                // Hf (fc1 output)
   }
-  // the ResNet backward passes rotate 8 buffers so that the weight-gradient
+  // the ResNet and VGG backward passes rotate 8 buffers so that the weight-gradient
   // stream can run a block behind (see GradPool); the others use 5
-  ws->ngrad = (m.arch == HS_RESNET18 || m.arch == HS_RESNET50) ? Workspace::kGrad : 5;
+  ws->ngrad = (m.arch == HS_RESNET18 || m.arch == HS_RESNET50 || m.arch == HS_VGG16)
+                  ? Workspace::kGrad : 5;
   for (int i = 0; i < Workspace::kGrad; ++i)
     ws->grad[i] = i < ws->ngrad ? a.take(m.max_act * max_n * es) : nullptr;
   ws->logits = (float*)a.take((int64_t)max_n * 10 * 4);
@@ -1203,27 +1204,39 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   HS_TRY(bias_grad(c, m.fc1.b, G[0], false, 1, 512));
   HS_TRY(conv_wgrad(c, m.fc1, G[0], F));
   HS_TRY(conv_dgrad(c, m.fc1, G[0], G[1], nullptr, nullptr));         // dF
+  // the conv layers' weight gradients on the second stream (GradPool), the
+  // pooling / batch-norm / data-gradient chain on the caller's
+  const Ctx cs = side(c);
+  GradPool gp(c.ws, c.s);
+  gp.live[1] = true;   // G[1]: dF
   int gi = 1;
   for (int i = L - 1; i >= 0; --i) {
     const VggL& l = m.vgg[i];
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i];
     const void* in = i == 0 ? S[0] : (m.vgg[i - 1].pool ? S[3 + 3 * (i - 1)] : S[2 + 3 * (i - 1)]);
     const int64_t rps = (int64_t)l.c.Ho * l.c.Wo;
-    const int a = (gi + 1) % 3, b2 = (gi + 2) % 3;
-    int dAi = gi;
+    int pa = gi;
     if (l.pool) {
-      HS_TRY(launch_maxpool_bwd(c.bf, A, G[gi], n, l.c.Ho, l.c.Wo, l.c.cout, 0, G[a], c.s));
-      dAi = a;
+      HS_TAKE(gp, q);
+      HS_TRY(launch_maxpool_bwd(c.bf, A, gp[pa], n, l.c.Ho, l.c.Wo, l.c.cout, 0, gp[q], c.s));
+      gp.drop(pa);
+      pa = q;
     }
-    const int dZi = dAi == a ? b2 : a;
-    HS_TRY(bn_bwd(c, l.bn, G[dAi], A, Z, rps, G[dZi]));
-    if (i == 0) HS_TRY(stem_wgrad(c, l.c, G[dZi], in));
-    else HS_TRY(conv_wgrad(c, l.c, G[dZi], in));
-    if (i > 0) {
-      const int out = (dZi + 1) % 3 == dAi ? (dZi + 2) % 3 : (dZi + 1) % 3;
-      HS_TRY(conv_dgrad(c, l.c, G[dZi], G[out], nullptr, nullptr));
-      gi = out;
+    HS_TAKE(gp, dz);
+    HS_TRY(bn_bwd(c, l.bn, gp[pa], A, Z, rps, gp[dz]));
+    gp.drop(pa);
+    if (i == 0) {   // the first layer's weight gradient shares the split-K buffer
+      HS_TRY(join(c));
+      HS_TRY(stem_wgrad(c, l.c, gp[dz], in));
+      break;
     }
+    HS_TRY(fork(c));
+    HS_TRY(conv_wgrad(cs, l.c, gp[dz], in));
+    HS_TRY(gp.read_on_side(dz));
+    HS_TAKE(gp, out);
+    HS_TRY(conv_dgrad(c, l.c, gp[dz], gp[out], nullptr, nullptr));
+    gp.drop(dz);
+    gi = out;
   }
   return hipSuccess;
 }
