@@ -36,7 +36,7 @@
  *   - A model is read-only after creation and may be shared by threads.  A
  *     workspace serves one hs_worker_grad at a time: concurrent workers need
  *     one workspace each.  A workspace also owns a second HIP stream (default
- *     priority) on which the ResNet passes run their weight gradients and
+ *     priority) on which the ResNet and VGG passes run their weight gradients and
  *     projection shortcuts; a call orders all of its work before its end on
  *     the caller's stream (that stream waits for the second one), so the
  *     caller sees one stream.
