@@ -18,6 +18,14 @@
 // (slot offset 2 - r, 2 - s) and the transposed weights.  The epilogue stages
 // each wave's 64 x 32 accumulator half-tiles in the patch area and writes
 // whole rows.
+//
+// Block b takes the consecutive tiles [ntiles b / blocks, ntiles (b + 1) /
+// blocks).  With stat_part set (forward), the epilogue also sums every stored
+// output value and its square per channel, each lane over its own rows; when
+// the next tile starts another worker segment (or the block's tiles end) the
+// block adds its lanes in a fixed order through the patch area and writes one
+// partial per channel for that segment: the batch-norm statistics of the
+// output without a second pass over it.
 #include "kernels.h"
 
 namespace hs {
@@ -29,7 +37,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32, EPI_STATS = 64 };
 
 constexpr int P_W = 32;                     // map width
 constexpr int P_ROWS = 16;                  // output rows per tile
@@ -92,13 +100,57 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
     }
   };
 
-  int t = blockIdx.x;
+  // the block's tiles, and (statistics) the worker segment of a tile
+  const int t_first = (int)((int64_t)ntiles * blockIdx.x / gridDim.x);
+  const int t_last = (int)((int64_t)ntiles * (blockIdx.x + 1) / gridDim.x);
+  constexpr bool ESTATS = (EPI & EPI_STATS) != 0;
+  auto seg_of = [&](int tile) {
+    const int img = tile / tiles_per_img;
+    int sg = 0;
+#pragma unroll
+    for (int i = 1; i < MAX_SEG; ++i) sg += (i < p.nseg && img >= p.seg_n0[i]) ? 1 : 0;
+    return sg;
+  };
+  // per lane: sums of y and y^2 over its rows, channels 32 nb + 8 (lane & 3) + e
+  float st0[2][8], st1[2][8];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) st0[nb][e] = st1[nb][e] = 0.f;
+  // Adds the lanes' sums (called by every thread after a block barrier that
+  // follows the last use of the patch area) and writes them as segment sg's
+  // partial of this block; leaves the patch area free and the sums zero.
+  auto flush = [&](int sg) {
+    float* R = (float*)Pl;   // [wave][lane / 4][k][64 channels]
+    const int j = lane >> 2, c8 = 8 * (lane & 3);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        float* r0 = R + ((wave * 16 + j) * 2 + 0) * 64 + nb * 32 + c8 + e;
+        float* r1 = R + ((wave * 16 + j) * 2 + 1) * 64 + nb * 32 + c8 + e;
+        *(float4*)r0 = make_float4(st0[nb][e], st0[nb][e + 1], st0[nb][e + 2], st0[nb][e + 3]);
+        *(float4*)r1 = make_float4(st1[nb][e], st1[nb][e + 1], st1[nb][e + 2], st1[nb][e + 3]);
+        st0[nb][e] = st0[nb][e + 1] = st0[nb][e + 2] = st0[nb][e + 3] = 0.f;
+        st1[nb][e] = st1[nb][e + 1] = st1[nb][e + 2] = st1[nb][e + 3] = 0.f;
+      }
+    __syncthreads();
+    if (tid < 128) {
+      const int k = tid >> 6, ch = tid & 63;
+      float sum = 0.f;
+      for (int r = 0; r < 8 * 16; ++r) sum += R[(r * 2 + k) * 64 + ch];
+      p.stat_part[((int64_t)(sg * (int)gridDim.x + (int)blockIdx.x) * 2 + k) * 64 + ch] = sum;
+    }
+    __syncthreads();
+  };
+
+  int t = t_first;
   uint4 pre[P_IT];
-  if (t < ntiles) load_patch(t, pre);
-  for (; t < ntiles; t += gridDim.x) {
+  if (t < t_last) load_patch(t, pre);
+  for (; t < t_last; ++t) {
     store_patch(pre);
     __syncthreads();
-    if (t + gridDim.x < ntiles) load_patch(t + gridDim.x, pre);
+    if (t + 1 < t_last) load_patch(t + 1, pre);
 
     // Epilogue operands (addend, mask) of this tile.  A lane's rows of the
     // epilogue are fixed: row 16 i + lane / 4 of the wave's 64 (mb * 32 +
@@ -229,12 +281,37 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
             if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
           }
         }
-        *(uint4*)((bf16_t*)p.out + off) =
-            make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+        const uint4 o = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+        *(uint4*)((bf16_t*)p.out + off) = o;
+        if constexpr (ESTATS) {   // the stored values, widened back from bf16
+          const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(w[e] << 16), hi = __uint_as_float(w[e] & 0xffff0000u);
+            st0[nb][2 * e] += lo;
+            st1[nb][2 * e] += lo * lo;
+            st0[nb][2 * e + 1] += hi;
+            st1[nb][2 * e + 1] += hi * hi;
+          }
+        }
       }
       __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();   // every wave is done with the patch area: the next tile's patch goes there
+    if constexpr (ESTATS) {
+      const int sg = seg_of(t);
+      if (t + 1 == t_last || seg_of(t + 1) != sg) flush(sg);
+    }
+  }
+  if constexpr (ESTATS) {
+    // segments without rows in this block: zero partials
+    const int s_lo = t_first < t_last ? seg_of(t_first) : p.nseg;
+    const int s_hi = t_first < t_last ? seg_of(t_last - 1) : -1;
+    if (tid < 128)
+      for (int sg = 0; sg < p.nseg; ++sg)
+        if (sg < s_lo || sg > s_hi)
+          p.stat_part[((int64_t)(sg * (int)gridDim.x + (int)blockIdx.x) * 2 + (tid >> 6)) * 64 +
+                      (tid & 63)] = 0.f;
   }
 }
 
@@ -249,7 +326,10 @@ template <int MODE>
 static void launch64(const GemmParams& p, int ntiles, dim3 grid, hipStream_t s) {
   if constexpr (MODE == MODE_FWD) {
     const bool bias = p.bias != nullptr, relu = p.relu != 0;
-    if (bias && relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
+    if (p.stat_part) {
+      if (bias || relu) return;   // statistics of a plain convolution only (rejected by the caller)
+      hipLaunchKernelGGL((conv64_kernel<MODE, EPI_STATS>), grid, dim3(512), 0, s, p, ntiles);
+    } else if (bias && relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
     else if (bias) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS>), grid, dim3(512), 0, s, p, ntiles);
     else if (relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
     else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);
@@ -264,14 +344,27 @@ static void launch64(const GemmParams& p, int ntiles, dim3 grid, hipStream_t s) 
   }
 }
 
-// p.b: packed weights (launch_pack_weights for the same mode); one block per CU
-hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s) {
-  if (!conv64_ok(mode, p)) return hipErrorInvalidValue;
+int conv64_blocks(const GemmParams& p) {
   const int ntiles = p.g.n * (p.g.H / P_ROWS);
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  const dim3 grid((unsigned)(ntiles < cus ? ntiles : cus));
+  return ntiles < cus ? ntiles : cus;
+}
+
+// p.b: packed weights (launch_pack_weights for the same mode); one block per CU
+hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s) {
+  if (!conv64_ok(mode, p)) return hipErrorInvalidValue;
+  const int ntiles = p.g.n * (p.g.H / P_ROWS);
+  if (p.stat_part) {
+    // forward sums of a plain convolution over whole-sample segments
+    if (mode != MODE_FWD || p.bias || p.relu || p.nseg < 1 || p.nseg > MAX_SEG ||
+        p.seg_n0[0] != 0 || p.seg_n0[p.nseg] != p.g.n)
+      return hipErrorInvalidValue;
+    for (int i = 0; i < p.nseg; ++i)
+      if (p.seg_n0[i + 1] <= p.seg_n0[i]) return hipErrorInvalidValue;
+  }
+  const dim3 grid((unsigned)conv64_blocks(p));
   if (mode == MODE_FWD) launch64<MODE_FWD>(p, ntiles, grid, s);
   else launch64<MODE_DGRAD>(p, ntiles, grid, s);
   return hipGetLastError();

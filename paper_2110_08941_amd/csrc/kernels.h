@@ -67,6 +67,13 @@ struct GemmParams {
   int nseg;
   int seg_split[MAX_SEG + 1];
   int seg_n0[MAX_SEG + 1];
+  // Batch-norm forward sums of the output, taken in the epilogue (conv64
+  // forward only; null: none): per segment s (samples seg_n0[s] ..
+  // seg_n0[s + 1] - 1, nseg segments) and block b of the launch,
+  // stat_part[((s * blocks + b) * 2 + k) * N + n] = sum over the block's
+  // output rows of segment s of y^(k + 1), y the stored (rounded) output;
+  // zero where the block has no rows of s.
+  float* stat_part;
 };
 
 // K range of weight-gradient split blockIdx.y over worker segments: the
@@ -114,6 +121,8 @@ hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
 // 32-wide maps (conv64.hip): packed weights resident in LDS, input patch of 16
 // output rows staged once per tile, taps as shifted LDS reads
 bool conv64_ok(int mode, const GemmParams& p);
+// blocks of a conv64 launch (one per CU, at most one per tile)
+int conv64_blocks(const GemmParams& p);
 hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s);
 // bf16 weight gradient of 3x3 stride-1 pad-1 layers (wgrad3.hip): the input
 // patch of a slice of output pixels staged once in LDS, the 9 taps as
@@ -171,6 +180,12 @@ hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, const S
 //   kind 2: out0[s] = sum d
 // part: float scratch [STAT_MAX_BLOCKS][2][C].
 constexpr int STAT_MAX_BLOCKS = 1024;
+// The finish alone, on block partials written elsewhere (GemmParams::
+// stat_part): segment s sums partials [s * blocks, (s + 1) * blocks) of
+// unshifted kind-0 sums over rows_per_sample rows per sample.
+hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, const Segs& sg,
+                                   int64_t rows_per_sample, int C, float* const* mean,
+                                   float* const* rstd, float eps, hipStream_t s);
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
                              const float* mean, const float* rstd, int mstride, const Segs& sg,
                              int64_t rows_per_sample, int C, float* part, float* const* out0,

@@ -439,8 +439,9 @@ hipError_t wait_mark(const Ctx& c, int k);
 // Launch one GEMM (fast kernel when the shape allows, generic otherwise);
 // brackets it with probe events when it is the probed instantiation.
 hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
-                int splits, double flops) {
+                int splits, double flops, bool* stats_fused = nullptr) {
   Workspace& ws = c.ws;
+  if (stats_fused) *stats_fused = false;
   int fbm = 0, fbn = 0;
   pick_fast_tiles(mode, p.M, p.N, fbm, fbn);
   const bool fast = p.par || (veca && vecb && igemm_fast_ok(mode, c.bf, p, fbm, fbn));
@@ -469,6 +470,15 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // the packed-weight buffer is the main stream's: launches on the second
   // stream (c.part set) take the other kernels
   if (c.part) mfma32 = w64 = false;
+  // epilogue statistics (GemmParams::stat_part) per worker: the 64-channel
+  // forward kernel only (nseg stays 0 for the others, where it means split-K
+  // over worker segments)
+  if (w64 && mode == MODE_FWD && q.stat_part) {
+    q.nseg = c.sg.count;
+    for (int i = 0; i <= MAX_SEG; ++i) q.seg_n0[i] = c.sg.n0[i < c.sg.count ? i : c.sg.count];
+  } else {
+    q.stat_part = nullptr;
+  }
   if (mfma32 || w64) {
     // the layer's region of packed weights: packed on the second stream at
     // the start of the call, or now (first call, or a workspace without one)
@@ -504,7 +514,10 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
                      (fast || mfma32 || wg3 || w64) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
   if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
   if (wg3) HS_TRY(launch_wgrad3(p, c.s));
-  else if (w64) HS_TRY(launch_conv64(mode, q, c.s));
+  else if (w64) {
+    HS_TRY(launch_conv64(mode, q, c.s));
+    if (stats_fused && q.stat_part) *stats_fused = true;
+  }
   else if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
   else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
   else {
@@ -526,9 +539,13 @@ double layer_flops(const ConvL& L, int n) {
 }
 
 // y = conv(x) (+ bias, ReLU); out_f32 forces an fp32 output
+// stat_part: request the batch-norm sums of y from the epilogue (see
+// GemmParams::stat_part); *stats_fused tells whether the kernel took them
 hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32,
-                    const void* wptr = nullptr, const float* bias = nullptr, double flops = 0.0) {
+                    const void* wptr = nullptr, const float* bias = nullptr, double flops = 0.0,
+                    float* stat_part = nullptr, bool* stats_fused = nullptr) {
   GemmParams p = base_params(L, c.n);
+  p.stat_part = stat_part;
   p.a = x;
   p.b = wptr ? wptr : c.W(L.w);
   p.out = y;
@@ -541,7 +558,8 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   const bool vec = (L.cin % c.V) == 0;
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
-  return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, flops > 0 ? flops : layer_flops(L, c.n));
+  return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, flops > 0 ? flops : layer_flops(L, c.n),
+              stats_fused);
 }
 
 // dx = dgrad(dy) (+ addend) (* [mask > 0]); a stride-2 layer is computed by
@@ -723,6 +741,31 @@ hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
   }
   return launch_chan_stats(0, c.bf, z, nullptr, nullptr, nullptr, nullptr, 0, c.sg, rps, b.c,
                            c.sp(), o0, o1, 1e-5f, c.s);
+}
+
+// z = conv(x) and the batch-norm statistics of z: summed in the
+// convolution's epilogue where its kernel takes them (the 64-channel 3x3
+// layers on 32-wide maps: partials per block and worker, then the finish),
+// else by a pass over z
+hipError_t conv_bn_fwd(const Ctx& c, const ConvL& L, const void* x, void* z, const BNL& b,
+                       int64_t rps) {
+  bool want = c.bf && !c.part && L.b < 0 && !L.relu && b.c == L.cout && c.sg.count >= 1 &&
+              c.sg.n0[0] == 0 && c.sg.n0[c.sg.count] == c.n;
+  for (int i = 0; want && i < c.sg.count; ++i) want = c.sg.n0[i + 1] > c.sg.n0[i];
+  int blocks = 0;
+  if (want) {
+    blocks = conv64_blocks(base_params(L, c.n));
+    want = (int64_t)c.sg.count * blocks * 2 * L.cout <= (int64_t)STAT_MAX_BLOCKS * 2 * 512;
+  }
+  bool fused = false;
+  HS_TRY(conv_fwd(c, L, x, z, false, nullptr, nullptr, 0.0, want ? c.sp() : nullptr, &fused));
+  if (!fused) return bn_stats(c, b, z, rps);
+  float *o0[MAX_SEG], *o1[MAX_SEG];
+  for (int i = 0; i < c.sg.count; ++i) {
+    o0[i] = c.mean(b, i);
+    o1[i] = c.rstd(b, i);
+  }
+  return launch_stats_finish_fwd(c.bf, c.sp(), blocks, c.sg, rps, b.c, o0, o1, 1e-5f, c.s);
 }
 
 // y = relu?(batch-norm(z) + res) with every worker's own statistics
@@ -947,11 +990,9 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       proj_done = side_mark(c);
       res = G[0];
     }
-    HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
-    HS_TRY(bn_stats(c, b.b1, Z1, rps));
+    HS_TRY(conv_bn_fwd(c, b.c1, cur, Z1, b.b1, rps));
     HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rps, Hh, Hb));
-    HS_TRY(conv_fwd(c, b.c2, Hh, Z2, false));
-    HS_TRY(bn_stats(c, b.b2, Z2, rps));
+    HS_TRY(conv_bn_fwd(c, b.c2, Hh, Z2, b.b2, rps));
     HS_TRY(wait_mark(c, proj_done));
     HS_TRY(bn_apply(c, b.b2, Z2, res, 1, rps, A, Ab));
     cur = A;

@@ -94,7 +94,7 @@ struct StatArgs {
 };
 
 struct FinishArgs {
-  const void* x;        // kind 0: the shift rows
+  const void* x;        // kind 0: the shift rows (null: unshifted sums)
   const float* part;
   int C;
   float eps;
@@ -351,13 +351,38 @@ __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
     const double m1 = t0 / cnt;
     double var = t1 / cnt - m1 * m1;
     if (var < 0.0) var = 0.0;
-    const float shift = ld<T>((const T*)a.x, seg0 * C + c);
+    const float shift = a.x ? ld<T>((const T*)a.x, seg0 * C + c) : 0.f;
     o0[c] = (float)((double)shift + m1);
     o1[c] = (float)(1.0 / sqrt(var + (double)a.eps));
   } else {
     if (o0) o0[c] = (float)t0;
     if (KIND == 1 && o1) o1[c] = (float)t1;
   }
+}
+
+hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, const Segs& sg,
+                                   int64_t rows_per_sample, int C, float* const* mean,
+                                   float* const* rstd, float eps, hipStream_t s) {
+  if (C < 1 || sg.count < 1 || sg.count > MAX_SEG || blocks < 1) return hipErrorInvalidValue;
+  FinishArgs f{};
+  f.x = nullptr;
+  f.part = part;
+  f.C = C;
+  f.eps = eps;
+  f.sr.count = sg.count;
+  for (int i = 0; i <= MAX_SEG; ++i) {
+    const int k = i < sg.count ? i : sg.count;
+    f.sr.blk[i] = k * blocks;
+    f.sr.row[i] = (int64_t)sg.n0[k] * rows_per_sample;
+  }
+  for (int i = 0; i < sg.count; ++i) {
+    f.out0[i] = mean[i];
+    f.out1[i] = rstd[i];
+  }
+  const dim3 fgrid((C + 7) / 8, sg.count);
+  if (bf16) hipLaunchKernelGGL((chan_finish_kernel<bf16_t, 0>), fgrid, dim3(256), 0, s, f);
+  else hipLaunchKernelGGL((chan_finish_kernel<float, 0>), fgrid, dim3(256), 0, s, f);
+  return hipGetLastError();
 }
 
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
