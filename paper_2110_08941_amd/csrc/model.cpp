@@ -1114,14 +1114,11 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
       proj_done = side_mark(c);
       res = G[0];
     }
-    HS_TRY(conv_fwd(c, b.c1, cur, Z1, false));
-    HS_TRY(bn_stats(c, b.b1, Z1, rin));
+    HS_TRY(conv_bn_fwd(c, b.c1, cur, Z1, b.b1, rin));
     HS_TRY(bn_apply(c, b.b1, Z1, nullptr, 1, rin, H1, H1b));
-    HS_TRY(conv_fwd(c, b.c2, H1, Z2, false));
-    HS_TRY(bn_stats(c, b.b2, Z2, rout));
+    HS_TRY(conv_bn_fwd(c, b.c2, H1, Z2, b.b2, rout));
     HS_TRY(bn_apply(c, b.b2, Z2, nullptr, 1, rout, H2, H2b));
-    HS_TRY(conv_fwd(c, b.c3, H2, Z3, false));
-    HS_TRY(bn_stats(c, b.b3, Z3, rout));
+    HS_TRY(conv_bn_fwd(c, b.c3, H2, Z3, b.b3, rout));
     HS_TRY(wait_mark(c, proj_done));
     HS_TRY(bn_apply(c, b.b3, Z3, res, 1, rout, A, Ab));
     cur = A;
@@ -1223,9 +1220,12 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const VggL& l = m.vgg[i];
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i], *P = S[3 + 3 * i];
     const int64_t rps = (int64_t)l.c.Ho * l.c.Wo;
-    if (i == 0) HS_TRY(stem_fwd(c, l.c, x, S[0], Z));
-    else HS_TRY(conv_fwd(c, l.c, cur, Z, false));
-    HS_TRY(bn_stats(c, l.bn, Z, rps));
+    if (i == 0) {
+      HS_TRY(stem_fwd(c, l.c, x, S[0], Z));
+      HS_TRY(bn_stats(c, l.bn, Z, rps));
+    } else {
+      HS_TRY(conv_bn_fwd(c, l.c, cur, Z, l.bn, rps));
+    }
     HS_TRY(bn_apply(c, l.bn, Z, nullptr, 1, rps, A));
     cur = A;
     if (l.pool) {
