@@ -29,7 +29,8 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_F32 = 4, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_F32 = 4, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32,
+       EPI_STAGE = 64 };
 
 __device__ inline int swz(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ inline int lds_off(int row, int chunk) { return row * 128 + ((chunk ^ swz(row)) << 4); }
@@ -440,7 +441,10 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   // stages its WTM x CW fp32 sub-tile (CW = WTN, or WTN / 2 when LDS is
   // short; row stride CW + 4 floats, conflict-free) and handles it row by
   // row, 8 channels per lane, so the loads and stores cover contiguous rows
-  constexpr bool STAGE_EPI = MODE == MODE_DGRAD && EB == 2 && (EPI & (EPI_ADD | EPI_MASK)) != 0;
+  // (also the bf16 forward outputs: 16-byte row stores instead of 8-byte
+  // pieces of 16 rows)
+  constexpr bool STAGE_EPI = (MODE == MODE_DGRAD && EB == 2 && (EPI & (EPI_ADD | EPI_MASK)) != 0) ||
+                             (MODE == MODE_FWD && EB == 2 && (EPI & EPI_STAGE) != 0);
   if constexpr (STAGE_EPI) {
     constexpr int SMEM = 2 * (BM + BN) * 128;
     constexpr int CW = 4 * WTM * (WTN + 4) * 4 <= SMEM ? WTN : WTN / 2;
@@ -494,6 +498,17 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
         const float4 lo = *(const float4*)(E + row * EROW + c8);
         const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
         float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if constexpr ((EPI & EPI_BIAS) != 0) {
+          const int n = n0 + wn * WTN + c0 + c8;
+          const float4 b0 = *(const float4*)(p.bias + (oks[k] ? n : 0));
+          const float4 b1 = *(const float4*)(p.bias + (oks[k] ? n : 0) + 4);
+          v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+          v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+        }
+        if constexpr ((EPI & EPI_RELU) != 0) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
+        }
         if constexpr (EADD) {
           const uint32_t w[4] = {addv[k].x, addv[k].y, addv[k].z, addv[k].w};
 #pragma unroll
@@ -606,6 +621,15 @@ template <typename T, int MODE, int BM, int BN, int WGM>
 static void launch_epi(const GemmParams& p, dim3 grid, hipStream_t s) {
   if constexpr (MODE == MODE_FWD) {
     const bool bias = p.bias != nullptr, relu = p.relu != 0, f32 = p.out_f32 != 0 || sizeof(T) == 4;
+    if constexpr (sizeof(T) == 2) {
+      if (!f32 && p.N % 8 == 0) {   // bf16 output: staged epilogue, 8 channels per lane row
+        if (bias && relu) launch_one<T, MODE, BM, BN, WGM, EPI_STAGE | EPI_BIAS | EPI_RELU>(p, grid, s);
+        else if (bias) launch_one<T, MODE, BM, BN, WGM, EPI_STAGE | EPI_BIAS>(p, grid, s);
+        else if (relu) launch_one<T, MODE, BM, BN, WGM, EPI_STAGE | EPI_RELU>(p, grid, s);
+        else launch_one<T, MODE, BM, BN, WGM, EPI_STAGE>(p, grid, s);
+        return;
+      }
+    }
     if (bias && relu && !f32) launch_one<T, MODE, BM, BN, WGM, EPI_BIAS | EPI_RELU>(p, grid, s);
     else if (bias && relu) launch_one<T, MODE, BM, BN, WGM, EPI_BIAS | EPI_RELU | EPI_F32>(p, grid, s);
     else if (bias && !f32) launch_one<T, MODE, BM, BN, WGM, EPI_BIAS>(p, grid, s);
