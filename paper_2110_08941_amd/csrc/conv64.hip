@@ -135,12 +135,18 @@ __global__ __launch_bounds__(512) void conv64_kernel(GemmParams p, int ntiles) {
         st1[nb][e] = st1[nb][e + 1] = st1[nb][e + 2] = st1[nb][e + 3] = 0.f;
       }
     __syncthreads();
-    if (tid < 128) {
-      const int k = tid >> 6, ch = tid & 63;
-      float sum = 0.f;
-      for (int r = 0; r < 8 * 16; ++r) sum += R[(r * 2 + k) * 64 + ch];
-      p.stat_part[((int64_t)(sg * (int)gridDim.x + (int)blockIdx.x) * 2 + k) * 64 + ch] = sum;
-    }
+    // four threads per (k, channel) add 32 of the 128 lane rows each, then
+    // the first adds the four in order
+    const int kc = tid & 127, part = tid >> 7;
+    float ps = 0.f;
+#pragma unroll 8
+    for (int r = 0; r < 32; ++r) ps += R[((part * 32 + r) * 2 + (kc >> 6)) * 64 + (kc & 63)];
+    float* Q = R + 128 * 2 * 64;   // [part][k * 64 + ch], after the lane rows
+    Q[part * 128 + kc] = ps;
+    __syncthreads();
+    if (tid < 128)
+      p.stat_part[((int64_t)(sg * (int)gridDim.x + (int)blockIdx.x) * 2 + (tid >> 6)) * 64 +
+                  (tid & 63)] = ((Q[tid] + Q[128 + tid]) + Q[256 + tid]) + Q[384 + tid];
     __syncthreads();
   };
 
