@@ -123,7 +123,21 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WGM, wn = wave / WGM;
-  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  // Weight gradients: the tiles of one split read the same dy rows and
+  // input pixels.  Workgroups are handed to the 8 XCDs (each with its own
+  // L2) in turn, so the block index is remapped to put the tiles of a split
+  // on one XCD, where they share those reads: the first 8 q blocks (q =
+  // blocks / 8) are dealt so that XCD k gets logical blocks [k q, (k + 1) q)
+  // in order; the rest keep their index.
+  int bx = blockIdx.x, split = blockIdx.y;
+  if constexpr (MODE == MODE_WGRAD) {
+    const int nblk = (int)(gridDim.x * gridDim.y), q8 = nblk / 8;
+    int lb = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+    if (lb < 8 * q8) lb = (lb % 8) * q8 + lb / 8;
+    bx = lb % (int)gridDim.x;
+    split = lb / (int)gridDim.x;
+  }
+  const int tm = bx / p.tiles_n, tn = bx - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int RS = g.R * g.S;
   const int Ctap = (MODE == MODE_FWD) ? g.C : g.K;   // channels per tap along K (A side)
@@ -135,10 +149,10 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
   // whose A is a2 at the class pixel's own grid point and whose B is b2
   const bool extra = par && cls == 0 && p.a2 != nullptr;
   const int ktiles = par ? (p.ntap[cls] + (extra ? 1 : 0)) * (g.K / BKE) : p.ktiles;
-  int kt0 = blockIdx.y * p.kt_per_split;
+  int kt0 = split * p.kt_per_split;
   int kt1 = min(kt0 + p.kt_per_split, ktiles);
   int koff = 0, kend = p.K;   // K range of this split (WGRAD: one worker segment)
-  if (MODE == MODE_WGRAD && p.nseg > 0) wgrad_split_range(p, BKE, koff, kend, kt0, kt1);
+  if (MODE == MODE_WGRAD && p.nseg > 0) wgrad_split_range(p, BKE, koff, kend, kt0, kt1, split);
   // the fused term reads the grid point (h / 2, w / 2): the centre tap (1, 1)
   // of the 3x3 filter (the term only exists for 3x3, pad 1, stride 2)
   auto tap_id = [&](int t) { return par ? (t < p.ntap[cls] ? p.taps[cls][t] : 4) : t; };
@@ -549,7 +563,7 @@ __global__ __launch_bounds__(256) void igemm_fast_kernel(GemmParams p) {
       if (n >= p.N) continue;
       float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
       if constexpr (MODE == MODE_WGRAD) {
-        float* out = (float*)p.out + (int64_t)blockIdx.y * p.split_stride + (int64_t)m * p.N + n;
+        float* out = (float*)p.out + (int64_t)split * p.split_stride + (int64_t)m * p.N + n;
         *(float4*)out = make_float4(v[0], v[1], v[2], v[3]);
       } else {
         int64_t row = m;

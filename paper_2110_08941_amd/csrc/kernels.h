@@ -76,12 +76,11 @@ struct GemmParams {
   float* stat_part;
 };
 
-// K range of weight-gradient split blockIdx.y over worker segments: the
+// K range of weight-gradient split y (default blockIdx.y) over worker segments: the
 // pixels [koff, kend) of its segment, and K tiles [kt0, kt1) of bke pixels
 // counted from koff.  Table indices are compile-time constants.
 __device__ inline void wgrad_split_range(const GemmParams& p, int bke, int& koff, int& kend,
-                                         int& kt0, int& kt1) {
-  const int y = blockIdx.y;
+                                         int& kt0, int& kt1, int y) {
   int s = 0;
 #pragma unroll
   for (int i = 1; i < MAX_SEG; ++i) s += (i < p.nseg && y >= p.seg_split[i]) ? 1 : 0;
@@ -99,6 +98,10 @@ __device__ inline void wgrad_split_range(const GemmParams& p, int bke, int& koff
   kt0 = (y - sp) * p.kt_per_split;
   const int nkt = (kend - koff + bke - 1) / bke;
   kt1 = kt0 + p.kt_per_split < nkt ? kt0 + p.kt_per_split : nkt;
+}
+__device__ inline void wgrad_split_range(const GemmParams& p, int bke, int& koff, int& kend,
+                                         int& kt0, int& kt1) {
+  wgrad_split_range(p, bke, koff, kend, kt0, kt1, (int)blockIdx.y);
 }
 
 hipError_t launch_igemm(int mode, bool bf16, const GemmParams& p, bool veca, bool vecb, int bm,
