@@ -332,10 +332,9 @@ template <int MODE>
 static void launch64(const GemmParams& p, int ntiles, dim3 grid, hipStream_t s) {
   if constexpr (MODE == MODE_FWD) {
     const bool bias = p.bias != nullptr, relu = p.relu != 0;
-    if (p.stat_part) {
-      if (bias || relu) return;   // statistics of a plain convolution only (rejected by the caller)
+    if (p.stat_part)   // a plain convolution (launch_conv64 rejects bias or ReLU with sums)
       hipLaunchKernelGGL((conv64_kernel<MODE, EPI_STATS>), grid, dim3(512), 0, s, p, ntiles);
-    } else if (bias && relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
+    else if (bias && relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS | EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
     else if (bias) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_BIAS>), grid, dim3(512), 0, s, p, ntiles);
     else if (relu) hipLaunchKernelGGL((conv64_kernel<MODE, EPI_RELU>), grid, dim3(512), 0, s, p, ntiles);
     else hipLaunchKernelGGL((conv64_kernel<MODE, 0>), grid, dim3(512), 0, s, p, ntiles);
