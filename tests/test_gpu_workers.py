@@ -141,10 +141,14 @@ def test_workers_grad_separated(arch, dtype, n):
 
 @pytest.mark.parametrize("arch,dtype,n", [("resnet18", "fp32", [2, 5, 3]),
                                           ("vgg16", "bf16", [4, 1, 3]),
-                                          ("resnet50", "bf16", [6, 2, 3])])
+                                          ("resnet50", "bf16", [6, 2, 3]),
+                                          ("resnet18", "bf16", [1, 1, 1, 1, 1, 1, 1, 761])])
 def test_workers_grad_equals_separate_calls(arch, dtype, n):
     """One pass over all workers against one hs_worker_grad call per worker on
-    the same rows (the two differ only in the order of fp32 sums)."""
+    the same rows (the two differ only in the order of fp32 sums).  The last
+    case puts several one-sample workers into one block of the 64-channel
+    forward kernel, whose epilogue sums the batch-norm statistics per worker
+    (N = 768: 1536 half-image tiles over 256 blocks)."""
     log("workers_grad vs worker_grad %s %s n=%s" % (arch, dtype, n))
     net = Mo.build(arch)
     table, P = Mo.param_table(net)
