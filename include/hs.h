@@ -111,6 +111,14 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
 hs_status hs_workspace_destroy(hs_workspace* ws);
 /* Device bytes held by the workspace. */
 int64_t hs_workspace_bytes(const hs_workspace* ws);
+/* Streams a workspace's calls use (a measurement knob): 2 (the default) runs
+ * the weight gradients and projection shortcuts of the ResNet and VGG passes
+ * on the workspace's second stream, beside the caller's; 1 runs every launch
+ * on the caller's stream, one kernel at a time (per-kernel timings without
+ * overlap).  The arithmetic, and so every result, is the same in both.  Takes
+ * effect from the next call; not to be changed while a call of this
+ * workspace is being issued from another thread. */
+hs_status hs_workspace_set_streams(hs_workspace* ws, int32_t streams);
 
 /* ------------------------------------------------------- the step itself -- */
 
@@ -145,6 +153,22 @@ hs_status hs_workers_grad(const hs_model* model, hs_workspace* ws, const float* 
                           const uint16_t* theta_bf16, const float* x, const int32_t* y,
                           const int32_t* n, int32_t M, float* const* g, float* loss,
                           void* stream);
+
+/* The partition-weighted gradient of M workers in one pass (Section 4.2 with
+ * Section 1, Eq. (1)): g_bar = sum_m w_m g_m, w_m = n[m] / sum n, without
+ * storing the g_m.  Each worker's weight-gradient partial sums (split-K over
+ * its own samples) and batch-norm / bias sums are reduced per worker exactly
+ * as hs_workers_grad reduces them, then combined with w_m (computed in
+ * double, applied in fp32, summed in worker order) in the same reduction
+ * kernel: g_bar equals, bit for bit, hs_weighted_average of the g_m that
+ * hs_workers_grad writes.  One fp32 [P] vector is written instead of M, and
+ * the SGD step (hs_sgd_step) reads one instead of M.  Arguments as
+ * hs_workers_grad, with g_bar (device fp32 [P], fully overwritten, 16-byte
+ * aligned) in place of g; loss[m] is still each worker's mean loss. */
+hs_status hs_workers_grad_wavg(const hs_model* model, hs_workspace* ws, const float* theta,
+                               const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                               const int32_t* n, int32_t M, float* g_bar, float* loss,
+                               void* stream);
 
 /* Partition-weighted gradient (Section 4.2):
  *   g_out[i] = sum_{m<M} w_m g[m][i],  w_m = n[m] / sum_j n[j]  (computed in
@@ -192,19 +216,23 @@ hs_status hs_repartition(const double* throughput, int32_t M, int32_t N, int32_t
 
 /* Dynamic Partitioning state across steps (Section 4.1).  Created with the
  * even split of Algorithm 1 for epoch 0.  After each step the caller reports
- * tau[m] (the measured time of worker m's gradient, or n[m] for a model
- * clock) and speed[m] (the simulated relative speed); the worker's batch time
- * is X_m = tau[m] / speed[m].  Every `window` steps the mean X over the window
- * (summed in step order, divided by window) gives CP (Eq. (2)) and the next
- * partition (hs_repartition); *repartitioned is set to 1 on those steps and
- * cp_out (if not NULL) receives the CP vector.  window = 0 never
- * repartitions.  1 <= M <= 1024, M <= N. */
+ * n_used[m] (the partition the step ran with: it must equal the current
+ * partition, hs_partitioner_partition, else HS_ERR_INVALID and nothing
+ * changes), tau[m] (the measured time of worker m's gradient, or n[m] for a
+ * model clock) and speed[m] (the simulated relative speed); the worker's batch
+ * time is X_m = tau[m] / speed[m].  Every `window` steps the mean X over the
+ * window (summed in step order, divided by window) gives CP (Eq. (2)) and the
+ * next partition (hs_repartition); *repartitioned is set to 1 on those steps
+ * and cp_out (if not NULL) receives the CP vector.  A caller that launches
+ * steps ahead of observing them must observe the last step of a window before
+ * it reads the partition of the next step.  window = 0 never repartitions.
+ * 1 <= M <= 1024, M <= N. */
 hs_status hs_partitioner_create(int32_t M, int32_t N, int32_t window, hs_partitioner** out);
 hs_status hs_partitioner_destroy(hs_partitioner* p);
 hs_status hs_partitioner_partition(const hs_partitioner* p, int32_t* n_out);
 hs_status hs_partitioner_set_partition(hs_partitioner* p, const int32_t* n);
-hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
-                                 int32_t* repartitioned, double* cp_out);
+hs_status hs_partitioner_observe(hs_partitioner* p, const int32_t* n_used, const double* tau,
+                                 const double* speed, int32_t* repartitioned, double* cp_out);
 
 /* Compute-power estimator across windows (Section 4.1: the estimate can use
  * the previous epoch only, which follows changes quickly, or a history of

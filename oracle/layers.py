@@ -1,4 +1,6 @@
-"""Layer definitions of the oracle: forward and backward, float64, NHWC.
+"""Layer definitions of the oracle: forward and backward, NHWC, in the
+arithmetic type of their arguments (float64 for the definition; float32 for
+the oracle's fp32-arithmetic mode).
 
 Test infrastructure (see the package docstring): plain definitions written
 from the textbook formulas, not optimised.  The loss these layers build is the
@@ -15,7 +17,7 @@ import numpy as np
 
 
 # ----------------------------------------------------------------------------
-# bf16 rounding (storage emulation only)
+# bf16 rounding (the arithmetic of a bf16 path)
 # ----------------------------------------------------------------------------
 def bf16_round(x):
     """Nearest bf16 value (8-bit significand), ties to even, of each entry:
@@ -44,11 +46,12 @@ def conv_forward(x, w, stride, pad, b=None):
     n, h, wd, ci = x.shape
     co, kh, kw, ci2 = w.shape
     assert ci == ci2
+    dt = np.result_type(x, w)
     ho = conv_out_size(h, kh, stride, pad)
     wo = conv_out_size(wd, kw, stride, pad)
-    xp = np.zeros((n, h + 2 * pad, wd + 2 * pad, ci), dtype=np.float64)
+    xp = np.zeros((n, h + 2 * pad, wd + 2 * pad, ci), dtype=dt)
     xp[:, pad:pad + h, pad:pad + wd, :] = x
-    y = np.zeros((n * ho * wo, co), dtype=np.float64)
+    y = np.zeros((n * ho * wo, co), dtype=dt)
     for r in range(kh):
         for s in range(kw):
             patch = xp[:, r:r + stride * (ho - 1) + 1:stride, s:s + stride * (wo - 1) + 1:stride, :]
@@ -69,10 +72,11 @@ def conv_backward(x, w, dy, stride, pad):
     n, h, wd, ci = x.shape
     co, kh, kw, _ = w.shape
     _, ho, wo, _ = dy.shape
-    xp = np.zeros((n, h + 2 * pad, wd + 2 * pad, ci), dtype=np.float64)
+    dt = np.result_type(x, w, dy)
+    xp = np.zeros((n, h + 2 * pad, wd + 2 * pad, ci), dtype=dt)
     xp[:, pad:pad + h, pad:pad + wd, :] = x
     dxp = np.zeros_like(xp)
-    dw = np.zeros_like(w, dtype=np.float64)
+    dw = np.zeros(w.shape, dtype=dt)
     dy2 = np.ascontiguousarray(dy).reshape(-1, co)
     for r in range(kh):
         for s in range(kw):

@@ -29,38 +29,79 @@ class Ctx:
     """Evaluation context of one forward/backward.
 
     storage = "exact": every value is float64 (the definition).
-    storage = "bf16": emulates where a bf16 implementation stores tensors, so
-    that the ReLU masks and max-pool choices -- decisions taken on stored
-    values -- are taken on the same bf16 values as the kernels take them:
-    GEMM weight operands and every stored activation / activation gradient are
-    rounded to bf16 (round to nearest even); products are still summed in
-    float64; statistics, logits, the loss and weight gradients stay float64.
-    Rounding happens where a value is written to memory, so a sum that a kernel
-    forms before storing (a block's residual add, the data gradient of a
-    block's first convolution plus the shortcut gradient, the second
-    batch-norm of a block feeding the residual add) is rounded once, after
-    the sum.
+
+    The other modes give the error that arithmetic at a lower precision makes
+    by itself; a test reads it as the floor of a GPU path's error at that
+    precision.  They follow no implementation's storage or fusion choices:
+    storage = "operands": every operand of a convolution or linear contraction
+    -- the weights, the activations of the forward and weight-gradient
+    products, the output gradients of the data- and weight-gradient products
+    -- is rounded to bf16 (nearest, ties to even) where the contraction reads
+    it; the products are summed in float64; everything else (batch-norm,
+    ReLU, pooling, the loss, bias gradients, every stored tensor) stays
+    float64.  The bf16 path does this by definition: no bf16 implementation
+    has less error.
+    storage = "bf16": contraction operands rounded as above, and every tensor
+    passed between layers stored in bf16 -- each layer's output in the forward
+    pass and each layer's input gradient in the backward pass (residual
+    blocks: the block's output and input gradient too).  Sums stay float64
+    (bf16 rounding dwarfs the fp32 accumulation of a bf16 path).
+    grid = k > 0 (modes "operands" and "bf16"): another realization of the
+    same rounding -- every rounded tensor is scaled by 2^u (u uniform in
+    [0, 1), drawn per tensor from a generator seeded with k), rounded to bf16
+    and scaled back.  Each value keeps the relative error bound of bf16
+    rounding (2^-8); where the errors fall changes.  The error of a bf16
+    computation is one draw from a wide distribution, so a floor is read as
+    the largest error over a few realizations.
+    storage = "fp32": the whole pass in float32 arithmetic (numpy float32:
+    operands, parameters, every sum and every stored tensor), the arithmetic
+    of an fp32 path.
 
     Every ReLU and max-pool decision records its margin: |pre-activation|
     (ReLU) or the gap between the two largest window values (max-pool),
     relative to the largest magnitude of that tensor.  A decision whose margin
     is within the arithmetic's error is ambiguous: either outcome is correct."""
 
-    def __init__(self, storage="exact", capture=0.0, toggles=()):
-        if storage not in ("exact", "bf16"):
+    MODES = ("exact", "operands", "bf16", "fp32")
+
+    def __init__(self, storage="exact", capture=0.0, toggles=(), grid=0):
+        if storage not in self.MODES:
             raise ValueError(storage)
         self.storage = storage
+        self.grid = np.random.default_rng(grid) if grid else None
         self.margins = []          # (layer tag, smallest relative margins of the decisions)
         self.capture = capture     # ReLU decisions with a margin below this are listed
         self.ambiguous = []        # (ReLU call index, flat index, margin)
         self.toggles = set(toggles)  # (call index, flat index): backward mask inverted
         self.calls = 0
 
-    def store(self, x):
-        return L.bf16_round(x) if self.storage == "bf16" else x
+    def bf16(self, x):
+        """x rounded to bf16, on the realization's grid (see grid above)."""
+        if self.grid is None:
+            return L.bf16_round(x)
+        s = 2.0 ** self.grid.random()
+        return L.bf16_round(np.asarray(x, dtype=np.float64) * s) / s
 
-    def weight(self, w):
-        return L.bf16_round(w) if self.storage == "bf16" else w
+    def op(self, x):
+        """A contraction operand as the contraction reads it."""
+        if self.storage in ("operands", "bf16"):
+            return self.bf16(x)
+        if self.storage == "fp32":
+            return np.asarray(x, dtype=np.float32)
+        return x
+
+    def store(self, x):
+        """A tensor passed from one layer to the next."""
+        if self.storage == "bf16":
+            return self.bf16(x)
+        if self.storage == "fp32":
+            return np.asarray(x, dtype=np.float32)
+        return x
+
+    def param(self, x):
+        """A parameter read outside a contraction (bias, batch-norm scale and
+        shift): float32 in the fp32 mode, else as given."""
+        return np.asarray(x, dtype=np.float32) if self.storage == "fp32" else x
 
     def record(self, tag, rel):
         self.margins.append((tag, np.sort(np.asarray(rel, dtype=np.float64).ravel())[:64]))
@@ -118,10 +159,9 @@ def pool_margins(x):
 # modules
 # ----------------------------------------------------------------------------
 class Conv:
-    def __init__(self, name, cin, cout, k, stride, pad, bias, raw_dx=False):
+    def __init__(self, name, cin, cout, k, stride, pad, bias):
         self.name, self.cin, self.cout, self.k = name, cin, cout, k
         self.stride, self.pad, self.bias = stride, pad, bias
-        self.raw_dx = raw_dx       # data gradient is summed before it is stored
 
     def params(self):
         out = [(self.name + ".weight", "conv_w", (self.cout, self.k, self.k, self.cin))]
@@ -130,61 +170,58 @@ class Conv:
         return out
 
     def forward(self, x, p, ctx):
-        b = p[self.name + ".bias"] if self.bias else None
-        w = ctx.weight(p[self.name + ".weight"])
-        return ctx.store(L.conv_forward(x, w, self.stride, self.pad, b)), x
+        b = ctx.param(p[self.name + ".bias"]) if self.bias else None
+        w = ctx.op(p[self.name + ".weight"])
+        return L.conv_forward(ctx.op(x), w, self.stride, self.pad, b), x
 
     def backward(self, cache, dy, p, g, ctx):
         x = cache
-        w = ctx.weight(p[self.name + ".weight"])
-        dx, dw, db = L.conv_backward(x, w, dy, self.stride, self.pad)
+        w = ctx.op(p[self.name + ".weight"])
+        dx, dw, _ = L.conv_backward(ctx.op(x), w, ctx.op(dy), self.stride, self.pad)
         g[self.name + ".weight"] += dw
         if self.bias:
-            g[self.name + ".bias"] += db
-        return dx if self.raw_dx else ctx.store(dx)
+            g[self.name + ".bias"] += dy.sum(axis=(0, 1, 2))
+        return dx
 
 
 class Linear:
-    def __init__(self, name, fin, fout, logits=False):
+    def __init__(self, name, fin, fout):
         self.name, self.fin, self.fout = name, fin, fout
-        self.logits = logits       # output layer: logits are not stored rounded
 
     def params(self):
         return [(self.name + ".weight", "lin_w", (self.fout, self.fin)),
                 (self.name + ".bias", "bias", (self.fout,))]
 
     def forward(self, x, p, ctx):
-        y = L.linear_forward(x, ctx.weight(p[self.name + ".weight"]), p[self.name + ".bias"])
-        return (y if self.logits else ctx.store(y)), x
+        y = L.linear_forward(ctx.op(x), ctx.op(p[self.name + ".weight"]),
+                             ctx.param(p[self.name + ".bias"]))
+        return y, x
 
     def backward(self, cache, dy, p, g, ctx):
-        # the output layer's gradient is stored once (rounded) for the two
-        # products; its bias gradient sums the unrounded values
-        dys = ctx.store(dy) if self.logits else dy
-        dx, dw, _ = L.linear_backward(cache, ctx.weight(p[self.name + ".weight"]), dys)
+        dx, dw, _ = L.linear_backward(ctx.op(cache), ctx.op(p[self.name + ".weight"]), ctx.op(dy))
         g[self.name + ".weight"] += dw
         g[self.name + ".bias"] += dy.sum(axis=0)
-        return ctx.store(dx)
+        return dx
 
 
 class BatchNorm:
-    def __init__(self, name, c, raw_out=False):
+    def __init__(self, name, c):
         self.name, self.c = name, c
-        self.raw_out = raw_out     # output feeds a sum before it is stored
 
     def params(self):
         return [(self.name + ".gamma", "bn_gamma", (self.c,)),
                 (self.name + ".beta", "bn_beta", (self.c,))]
 
     def forward(self, x, p, ctx):
-        y, cache = L.bn_forward(x, p[self.name + ".gamma"], p[self.name + ".beta"])
-        return (y if self.raw_out else ctx.store(y)), cache
+        y, cache = L.bn_forward(x, ctx.param(p[self.name + ".gamma"]),
+                                ctx.param(p[self.name + ".beta"]))
+        return y, cache
 
     def backward(self, cache, dy, p, g, ctx):
-        dz, dgamma, dbeta = L.bn_backward(dy, p[self.name + ".gamma"], cache)
+        dz, dgamma, dbeta = L.bn_backward(dy, ctx.param(p[self.name + ".gamma"]), cache)
         g[self.name + ".gamma"] += dgamma
         g[self.name + ".beta"] += dbeta
-        return ctx.store(dz)
+        return dz
 
 
 class ReLU:
@@ -217,10 +254,10 @@ class GlobalAvgPool:
         return []
 
     def forward(self, x, p, ctx):
-        return ctx.store(L.gap_forward(x)), x.shape
+        return L.gap_forward(x), x.shape
 
     def backward(self, cache, dy, p, g, ctx):
-        return ctx.store(L.gap_backward(cache, dy))
+        return L.gap_backward(cache, dy)
 
 
 class Flatten:
@@ -252,12 +289,13 @@ class Sequential:
         caches = []
         for m in self.mods:
             x, c = m.forward(x, p, ctx)
+            x = ctx.store(x)
             caches.append(c)
         return x, caches
 
     def backward(self, caches, dy, p, g, ctx):
         for i in range(len(self.mods) - 1, -1, -1):
-            dy = self.mods[i].backward(caches[i], dy, p, g, ctx)
+            dy = ctx.store(self.mods[i].backward(caches[i], dy, p, g, ctx))
         return dy
 
 
@@ -267,10 +305,10 @@ class BasicBlock:
     stride or the width changes."""
 
     def __init__(self, name, cin, cout, stride):
-        self.main = Sequential([Conv(name + ".conv1", cin, cout, 3, stride, 1, False, raw_dx=True),
+        self.main = Sequential([Conv(name + ".conv1", cin, cout, 3, stride, 1, False),
                                 BatchNorm(name + ".bn1", cout), ReLU(),
                                 Conv(name + ".conv2", cout, cout, 3, 1, 1, False),
-                                BatchNorm(name + ".bn2", cout, raw_out=True)])
+                                BatchNorm(name + ".bn2", cout)])
         self.short = None
         if stride != 1 or cin != cout:
             self.short = Sequential([Conv(name + ".proj", cin, cout, 1, stride, 0, False),
@@ -310,12 +348,12 @@ class Bottleneck(BasicBlock):
 
     def __init__(self, name, cin, mid, stride, expansion=4):
         cout = mid * expansion
-        self.main = Sequential([Conv(name + ".conv1", cin, mid, 1, 1, 0, False, raw_dx=True),
+        self.main = Sequential([Conv(name + ".conv1", cin, mid, 1, 1, 0, False),
                                 BatchNorm(name + ".bn1", mid), ReLU(),
                                 Conv(name + ".conv2", mid, mid, 3, stride, 1, False),
                                 BatchNorm(name + ".bn2", mid), ReLU(),
                                 Conv(name + ".conv3", mid, cout, 1, 1, 0, False),
-                                BatchNorm(name + ".bn3", cout, raw_out=True)])
+                                BatchNorm(name + ".bn3", cout)])
         self.short = None
         if stride != 1 or cin != cout:
             self.short = Sequential([Conv(name + ".proj", cin, cout, 1, stride, 0, False),
@@ -332,7 +370,7 @@ VGG16_CFG = (64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M",
 def mlp(in_dim=784, hidden=256, classes=10):
     """Linear(in, hidden) + ReLU + Linear(hidden, classes)."""
     return Sequential([Linear("fc1", in_dim, hidden), ReLU(),
-                       Linear("fc2", hidden, classes, logits=True)])
+                       Linear("fc2", hidden, classes)])
 
 
 def small_cnn(in_ch=3, widths=(32, 64, 128), classes=10):
@@ -342,7 +380,7 @@ def small_cnn(in_ch=3, widths=(32, 64, 128), classes=10):
     return Sequential([Conv("conv1", in_ch, c1, 3, 1, 1, True), ReLU(),
                        Conv("conv2", c1, c2, 3, 1, 1, True), ReLU(), MaxPool2(),
                        Conv("conv3", c2, c3, 3, 1, 1, True), ReLU(),
-                       GlobalAvgPool(), Linear("fc", c3, classes, logits=True)])
+                       GlobalAvgPool(), Linear("fc", c3, classes)])
 
 
 def resnet18(in_ch=3, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2), classes=10):
@@ -356,7 +394,7 @@ def resnet18(in_ch=3, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2), classes=1
             stride = 2 if (si > 0 and bi == 0) else 1
             mods.append(BasicBlock("layer%d.%d" % (si + 1, bi), cin, w, stride))
             cin = w
-    mods += [GlobalAvgPool(), Linear("fc", cin, classes, logits=True)]
+    mods += [GlobalAvgPool(), Linear("fc", cin, classes)]
     return Sequential(mods)
 
 
@@ -373,7 +411,7 @@ def resnet50(in_ch=3, widths=(64, 128, 256, 512), blocks=(3, 4, 6, 3), expansion
             stride = 2 if (si > 0 and bi == 0) else 1
             mods.append(Bottleneck("layer%d.%d" % (si + 1, bi), cin, w, stride, expansion))
             cin = w * expansion
-    mods += [GlobalAvgPool(), Linear("fc", cin, classes, logits=True)]
+    mods += [GlobalAvgPool(), Linear("fc", cin, classes)]
     return Sequential(mods)
 
 
@@ -390,7 +428,7 @@ def vgg16(in_ch=3, cfg=VGG16_CFG, fc_hidden=512, classes=10):
             mods += [Conv("conv%d" % i, cin, v, 3, 1, 1, False), BatchNorm("bn%d" % i, v), ReLU()]
             cin = v
     mods += [Flatten(), Linear("fc1", cin, fc_hidden), ReLU(),
-             Linear("fc2", fc_hidden, classes, logits=True)]
+             Linear("fc2", fc_hidden, classes)]
     return Sequential(mods)
 
 
@@ -435,21 +473,22 @@ def to_nhwc(x):
     return x.transpose(0, 2, 3, 1) if x.ndim == 4 else x
 
 
-def worker_grad(net, theta, x, y, storage="exact", ctx=None):
+def worker_grad(net, theta, x, y, storage="exact", ctx=None, grid=0):
     """g_m = gradient of f_m = (1/n_m) sum_i CE(net(x_i), y_i) over the worker's
     n_m samples (Eq. (1) with the expectation taken over the partition).
     Batch-norm statistics are those of this worker's samples.
-    storage: "exact" (float64 throughout) or "bf16" (see Ctx).  Pass a Ctx to
+    storage: "exact" (float64 throughout), or "operands", "bf16", "fp32"
+    (see Ctx; grid selects a rounding realization).  Pass a Ctx to
     read the decision margins afterwards.
     Returns (loss_m, g_m) with g_m a flat float64 vector in the layout above."""
-    ctx = ctx or Ctx(storage)
+    ctx = ctx or Ctx(storage, grid=grid)
     table, total = param_table(net)
     th = np.asarray(theta, dtype=np.float64)
     assert th.shape == (total,)
     p = views(th, table)
     g = np.zeros(total, dtype=np.float64)
     gv = views(g, table)
-    logits, caches = net.forward(ctx.store(to_nhwc(x)), p, ctx)
+    logits, caches = net.forward(to_nhwc(x), p, ctx)
     loss, dz = L.softmax_ce(logits, np.asarray(y, dtype=np.int64))
     net.backward(caches, dz, p, gv, ctx)
     return loss, g
@@ -459,7 +498,7 @@ def loss_only(net, theta, x, y, storage="exact"):
     ctx = Ctx(storage)
     table, total = param_table(net)
     p = views(np.asarray(theta, dtype=np.float64), table)
-    logits, _ = net.forward(ctx.store(to_nhwc(x)), p, ctx)
+    logits, _ = net.forward(to_nhwc(x), p, ctx)
     loss, _ = L.softmax_ce(logits, np.asarray(y, dtype=np.int64))
     return loss
 

@@ -177,7 +177,8 @@ def smooth_cp(estimator, c, state):
 
 
 def run(net_grad, theta, batches, speeds, window, lr, mu, wd, times=None, n0=None,
-        exchange="edp", delays=None, estimator=("window",), lr_total=None, lr_min=0.0):
+        exchange="edp", delays=None, estimator=("window",), lr_total=None, lr_min=0.0,
+        theta_store=None):
     """Multi-step driver of Dynamic Partitioning (Algorithm 1).
 
     batches[t] = (x_t, y_t); speeds[t][m] = s_m at step t.  The time worker m
@@ -205,6 +206,8 @@ def run(net_grad, theta, batches, speeds, window, lr, mu, wd, times=None, n0=Non
         lr_t = cosine_lr(lr, t, lr_total, lr_min) if lr_total else lr
         out = step(net_grad, theta, buf, x, y, n, lr_t, mu, wd, exchange)
         theta, buf = out["theta"], out["buf"]
+        if theta_store is not None:
+            theta, buf = theta_store(theta), theta_store(buf)
         losses.append(out["losses"])
         xt = []
         for j in range(m):

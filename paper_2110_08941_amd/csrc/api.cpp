@@ -85,10 +85,11 @@ void release_side(Workspace& w) {
       w.evr[i] = nullptr;
     }
   }
-  if (w.side) {
-    (void)hipStreamDestroy(w.side);
-    w.side = nullptr;
+  if (w.side_owned) {
+    (void)hipStreamDestroy(w.side_owned);
+    w.side_owned = nullptr;
   }
+  w.side = nullptr;
 }
 
 }  // namespace
@@ -164,7 +165,8 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
   w->ws.bytes = bytes;
   plan_workspace(model->m, max_n, &w->ws);
   // the weight-gradient stream (default priority) and its ordering events
-  e = hipStreamCreateWithFlags(&w->ws.side, hipStreamNonBlocking);
+  e = hipStreamCreateWithFlags(&w->ws.side_owned, hipStreamNonBlocking);
+  w->ws.side = w->ws.side_owned;
   for (int i = 0; e == hipSuccess && i < Workspace::kEvents; ++i) {
     e = hipEventCreateWithFlags(&w->ws.ev[i], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->ws.evr[i], hipEventDisableTiming);
@@ -186,6 +188,17 @@ hs_status hs_workspace_create(const hs_model* model, int32_t max_n, hs_workspace
     }
   }
   *out = w;
+  return ok();
+}
+
+hs_status hs_workspace_set_streams(hs_workspace* ws, int32_t streams) {
+  if (!ws) return fail(HS_ERR_INVALID, "hs_workspace_set_streams: workspace is NULL");
+  if (streams != 1 && streams != 2)
+    return fail(HS_ERR_INVALID, "hs_workspace_set_streams: streams must be 1 or 2, not %d", streams);
+  // the next call packs on whichever stream it runs; nothing of an earlier
+  // call is pending on the second stream once that call's work is ordered
+  // on the caller's stream (every call joins it before returning)
+  ws->ws.side = streams == 2 ? ws->ws.side_owned : nullptr;
   return ok();
 }
 
@@ -225,6 +238,32 @@ hs_status hs_worker_grad(const hs_model* model, hs_workspace* ws, const float* t
   return ok();
 }
 
+// argument checks shared by the one-pass calls: fills nn[0..M) and *total
+static hs_status check_workers(const char* fn, const hs_model* model, const float* theta,
+                               const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                               const int32_t* n, int32_t M, float* const* g, int* nn,
+                               int64_t* total) {
+  if (!model) return fail(HS_ERR_INVALID, "%s: model is NULL", fn);
+  if (!theta || !x || !y || !n || !g)
+    return fail(HS_ERR_INVALID, "%s: theta, x, y, n and g must not be NULL", fn);
+  if (M < 1 || M > MAX_SEG) return fail(HS_ERR_INVALID, "%s: M %d outside 1..%d", fn, M, MAX_SEG);
+  const bool bf = model->m.dtype == HS_BF16;
+  if (bf && !theta_bf16) return fail(HS_ERR_INVALID, "%s: bf16 model needs theta_bf16", fn);
+  if (!bf && theta_bf16)
+    return fail(HS_ERR_INVALID, "%s: theta_bf16 must be NULL for an fp32 model", fn);
+  *total = 0;
+  for (int i = 0; i < M; ++i) {
+    if (n[i] < 1) return fail(HS_ERR_INVALID, "%s: n[%d] = %d < 1", fn, i, n[i]);
+    if (!g[i]) return fail(HS_ERR_INVALID, "%s: g[%d] is NULL", fn, i);
+    if (!aligned16(g[i])) return fail(HS_ERR_INVALID, "%s: g[%d] must be 16-byte aligned", fn, i);
+    *total += n[i];
+    nn[i] = n[i];
+  }
+  if (!aligned16(theta) || !aligned16(x) || (theta_bf16 && !aligned16(theta_bf16)))
+    return fail(HS_ERR_INVALID, "%s: device pointers must be 16-byte aligned", fn);
+  return HS_OK;
+}
+
 hs_status hs_workers_grad(const hs_model* model, hs_workspace* ws, const float* theta,
                           const uint16_t* theta_bf16, const float* x, const int32_t* y,
                           const int32_t* n, int32_t M, float* const* g, float* loss,
@@ -232,32 +271,45 @@ hs_status hs_workers_grad(const hs_model* model, hs_workspace* ws, const float* 
   if (!model || !ws) return fail(HS_ERR_INVALID, "hs_workers_grad: model/workspace is NULL");
   if (ws->model != model)
     return fail(HS_ERR_INVALID, "hs_workers_grad: workspace of another model");
-  if (!theta || !x || !y || !n || !g)
-    return fail(HS_ERR_INVALID, "hs_workers_grad: theta, x, y, n and g must not be NULL");
-  if (M < 1 || M > MAX_SEG)
-    return fail(HS_ERR_INVALID, "hs_workers_grad: M %d outside 1..%d", M, MAX_SEG);
-  const bool bf = model->m.dtype == HS_BF16;
-  if (bf && !theta_bf16) return fail(HS_ERR_INVALID, "hs_workers_grad: bf16 model needs theta_bf16");
-  if (!bf && theta_bf16)
-    return fail(HS_ERR_INVALID, "hs_workers_grad: theta_bf16 must be NULL for an fp32 model");
-  int64_t total = 0;
   int nn[MAX_SEG];
-  for (int i = 0; i < M; ++i) {
-    if (n[i] < 1) return fail(HS_ERR_INVALID, "hs_workers_grad: n[%d] = %d < 1", i, n[i]);
-    if (!g[i]) return fail(HS_ERR_INVALID, "hs_workers_grad: g[%d] is NULL", i);
-    if (!aligned16(g[i]))
-      return fail(HS_ERR_INVALID, "hs_workers_grad: g[%d] must be 16-byte aligned", i);
-    total += n[i];
-    nn[i] = n[i];
-  }
+  int64_t total = 0;
+  hs_status st = check_workers("hs_workers_grad", model, theta, theta_bf16, x, y, n, M, g, nn,
+                               &total);
+  if (st != HS_OK) return st;
   if (total > ws->ws.max_n)
     return fail(HS_ERR_INVALID, "hs_workers_grad: sum of n = %lld exceeds the workspace's %d",
                 (long long)total, ws->ws.max_n);
-  if (!aligned16(theta) || !aligned16(x) || (theta_bf16 && !aligned16(theta_bf16)))
-    return fail(HS_ERR_INVALID, "hs_workers_grad: device pointers must be 16-byte aligned");
   hipError_t e = workers_grad(model->m, ws->ws, theta, theta_bf16, x, y, nn, M, g, loss,
                               (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hs_workers_grad");
+  return ok();
+}
+
+hs_status hs_workers_grad_wavg(const hs_model* model, hs_workspace* ws, const float* theta,
+                               const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                               const int32_t* n, int32_t M, float* g_bar, float* loss,
+                               void* stream) {
+  if (!model || !ws) return fail(HS_ERR_INVALID, "hs_workers_grad_wavg: model/workspace is NULL");
+  if (ws->model != model)
+    return fail(HS_ERR_INVALID, "hs_workers_grad_wavg: workspace of another model");
+  if (!g_bar || !aligned16(g_bar))
+    return fail(HS_ERR_INVALID, "hs_workers_grad_wavg: g_bar must be a 16-byte aligned pointer");
+  float* g[MAX_SEG];
+  for (int i = 0; i < MAX_SEG; ++i) g[i] = g_bar;   // argument checks only
+  int nn[MAX_SEG];
+  int64_t total = 0;
+  hs_status st = check_workers("hs_workers_grad_wavg", model, theta, theta_bf16, x, y, n, M, g,
+                               nn, &total);
+  if (st != HS_OK) return st;
+  if (total > ws->ws.max_n)
+    return fail(HS_ERR_INVALID, "hs_workers_grad_wavg: sum of n = %lld exceeds the workspace's %d",
+                (long long)total, ws->ws.max_n);
+  // w_m = n_m / sum n, in double, applied in fp32 (as hs_weighted_average)
+  float w[MAX_SEG];
+  for (int i = 0; i < M; ++i) w[i] = (float)((double)n[i] / (double)total);
+  hipError_t e = workers_grad(model->m, ws->ws, theta, theta_bf16, x, y, nn, M, nullptr, loss,
+                              (hipStream_t)stream, g_bar, w);
+  if (e != hipSuccess) return hip_fail(e, "hs_workers_grad_wavg");
   return ok();
 }
 
@@ -545,9 +597,19 @@ hs_status hs_partitioner_set_estimator(hs_partitioner* p, int32_t kind, double a
   return ok();
 }
 
-hs_status hs_partitioner_observe(hs_partitioner* p, const double* tau, const double* speed,
-                                 int32_t* repartitioned, double* cp_out) {
-  if (!p || !tau || !speed) return fail(HS_ERR_INVALID, "hs_partitioner_observe: NULL pointer");
+hs_status hs_partitioner_observe(hs_partitioner* p, const int32_t* n_used, const double* tau,
+                                 const double* speed, int32_t* repartitioned, double* cp_out) {
+  if (!p || !n_used || !tau || !speed)
+    return fail(HS_ERR_INVALID, "hs_partitioner_observe: NULL pointer");
+  // the observation must belong to the window being measured: a step run
+  // with another partition (one started before the last repartition was
+  // observed) would mix two partitions in one compute-power estimate
+  for (int m = 0; m < p->M; ++m)
+    if (n_used[m] != p->n[m])
+      return fail(HS_ERR_INVALID,
+                  "hs_partitioner_observe: the step ran with n[%d] = %d, the current partition "
+                  "has %d (observe every step of a window before starting the next window)",
+                  m, n_used[m], p->n[m]);
   for (int m = 0; m < p->M; ++m) {
     if (!isfinite(tau[m]) || !(tau[m] > 0.0) || !isfinite(speed[m]) || !(speed[m] > 0.0))
       return fail(HS_ERR_INVALID, "hs_partitioner_observe: tau/speed[%d] not finite and > 0", m);

@@ -513,6 +513,240 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
 }
 
 // ----------------------------------------------------------------------------
+// Data gradient of a 3x3, stride-2, pad-1 convolution in the patch form.
+//
+// With dx[h] = sum over (o, r) with 2 o - 1 + r = h of dy[o] W[r] (per
+// dimension), an input pixel of parity a (h = 2 i + a) receives tap r = 1 of
+// dy row i when a = 0, and taps r = 2 (dy row i) and r = 0 (dy row i + 1)
+// when a = 1.  So the 2 x 2 block of input pixels (2i + a, 2j + b) is a
+// function of the dy positions (i, j), (i + 1, j), (i, j + 1), (i + 1, j + 1)
+// only: the nine taps of the filter each feed one parity class (a, b), read
+// dy at offset (di, dj) in {0, 1}^2 of the class's dy position, and the four
+// classes together are one stride-1 contraction over the dy grid whose taps
+// go to four accumulators.  A block holds 256 dy positions (whole dy
+// images, so a neighbour in the image is in the tile and out-of-image taps
+// are a per-lane mask) x 64 input channels; each of its 8 waves owns 32
+// positions x 64 channels x 4 classes (eight 32 x 32 accumulators).  The dy
+// slice (16 output channels) and the slice's packed weights are copied once
+// into LDS (global-to-LDS, double-buffered, as the stride-1 patch kernel) and
+// all nine taps read them; the projection shortcut of a residual block (a
+// 1 x 1 stride-2 convolution of the same input: class (0, 0) only, dy of the
+// shortcut at the same position) runs as further slices with one tap.
+// The epilogue stages each (class, 32 channels) tile of a wave in LDS and
+// writes rows of 8 channels (16 bytes) to the class's pixels, with the ReLU
+// mask bits and the addend of the residual path applied.
+// ----------------------------------------------------------------------------
+constexpr int S2_POS = 256;   // dy positions per block
+constexpr int S2_BN = 64;     // input channels per block
+
+template <int EPI, bool PROJ>
+__global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
+  constexpr int BN = S2_BN, NB = BN / 32, RS = 9;
+  constexpr int SEG = RS * 2 * BN;              // 16-byte B chunks per slice (9 taps)
+  constexpr int BREG = (SEG + 511) / 512;
+  constexpr int BBUF = BREG * 512;
+  constexpr int SEG1 = 2 * BN;                  // the projection's slice: one tap
+  constexpr int PPLANE = S2_POS * 16 + 128;
+  constexpr int EROW = 36;
+  constexpr bool EADD = (EPI & EPI_ADD) != 0, EBITS = (EPI & EPI_MBITS) != 0;
+  static_assert(5 * 32 * EROW * 4 <= BBUF * 16, "epilogue staging of five waves fits a B buffer");
+  __shared__ __attribute__((aligned(16))) uint4 sB0[BBUF];
+  __shared__ __attribute__((aligned(16))) uint4 sB1[BBUF];
+  __shared__ __attribute__((aligned(16))) char sP0[2 * PPLANE];
+  __shared__ __attribute__((aligned(16))) char sP1[2 * PPLANE];
+
+  const ConvGeom& g = p.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  const int n0 = tn * BN;
+  const int kh = lane >> 5;
+  const int Kc = g.K;                           // dy channels (the reduction)
+  const int ns = Kc / C2_CK;                    // slices over dy
+  const int ns_all = PROJ ? 2 * ns : ns;        // then as many over the shortcut's dy
+  const int Ho = g.Ho, Wo = g.Wo, HW = Ho * Wo;
+  const int tile_m0 = tm * S2_POS;
+  const bf16_t* A = (const bf16_t*)p.a;
+  const bf16_t* A2 = (const bf16_t*)p.a2;
+  const bf16_t* B = (const bf16_t*)p.b;
+  const bf16_t* B2 = (const bf16_t*)p.b2;
+
+  // this lane's dy position (one 32-row block per wave) and its taps' masks:
+  // bit t = tap t reads a dy position inside the image
+  const int q = wave * 32 + (lane & 31);
+  uint32_t vm;
+  {
+    const int pix = q % HW, i = pix / Wo, j = pix - (pix / Wo) * Wo;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int di = t / 3 == 0 ? 1 : 0, dj = t % 3 == 0 ? 1 : 0;
+      if (i + di < Ho && j + dj < Wo) bits |= 1u << t;
+    }
+    vm = tile_m0 + q < p.M ? bits : 0u;
+  }
+  const uint32_t vm1 = tile_m0 + q < p.M ? 1u : 0u;   // the shortcut's single tap
+
+  f32x16 acc[4][NB];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[c][nb] = (f32x16){};
+
+  auto read_a = [&](const char* P, int off, uint4& ra) {
+    ra = *(const uint4*)(P + kh * PPLANE + ((q + off) & (S2_POS - 1)) * 16);
+  };
+  auto read_b = [&](const uint4* Bb, int t, uint4 (&rb)[NB]) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) rb[nb] = Bb[(t * 2 + kh) * BN + nb * 32 + (lane & 31)];
+  };
+  auto masked = [&](uint32_t m, int t, const uint4& v) -> uint4 {
+    const uint32_t k = 0u - ((m >> t) & 1u);
+    return make_uint4(v.x & k, v.y & k, v.z & k, v.w & k);
+  };
+  // slice sl of B and of the dy patch, straight from global memory into LDS;
+  // slices ns.. are the shortcut's (one tap); rows past the last image re-read
+  // the last row (they feed no stored output)
+  const int wbase = wave * 64;
+  auto dma_slice = [&](int sl, uint4* Bb, char* P) {
+    const bool second = PROJ && sl >= ns;
+    const int ssl = second ? sl - ns : sl;
+    const bf16_t* Bs = second ? B2 : B;
+    const int rs = second ? 1 : RS, seg = second ? SEG1 : SEG;
+#pragma unroll
+    for (int i = 0; i < BREG; ++i) {
+      int c = tid + 512 * i;
+      c = c < seg ? c : seg - 1;
+      const int n = c % BN, rest = c / BN;
+      const bf16_t* src = Bs + (((int64_t)ssl * rs * 2 + rest) * p.N + n0 + n) * 8;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bb + 512 * i + wbase), 16, 0, 0);
+    }
+    const int px = tid & (S2_POS - 1), h = tid >> 8;
+    int64_t m = (int64_t)tile_m0 + px;
+    m = m < p.M ? m : p.M - 1;
+    const bf16_t* src = (second ? A2 : A) + m * Kc + ssl * C2_CK + 8 * h;
+    __builtin_amdgcn_global_load_lds((gbl_cptr)src,
+                                     (lds_ptr)(P + h * PPLANE + (wbase & (S2_POS - 1)) * 16), 16,
+                                     0, 0);
+  };
+
+  uint4 fa, fb[NB];
+  auto first_reads = [&](int sl, const uint4* Bb, const char* P) {
+    if (PROJ && sl >= ns) read_a(P, 0, fa);
+    else read_a(P, Wo + 1, fa);                   // tap 0: (di, dj) = (1, 1)
+    read_b(Bb, 0, fb);
+  };
+  // one slice from (Bc, Pc) while the next is copied into (Bn, Pn)
+  auto slice = [&](int sl, const uint4* Bc, const char* Pc, uint4* Bn, char* Pn) {
+    const bool more = sl + 1 < ns_all;
+    if (more) dma_slice(sl + 1, Bn, Pn);
+    if (!PROJ || sl < ns) {
+#pragma unroll
+      for (int t = 0; t < RS; ++t) {
+        // tap t = (r, s): class (r != 1, s != 1), dy offset (r == 0, s == 0)
+        constexpr int dummy = 0;
+        (void)dummy;
+        const int cls = 2 * (t / 3 != 1 ? 1 : 0) + (t % 3 != 1 ? 1 : 0);
+        const uint4 am = masked(vm, t, fa);
+        uint4 na, nbv[NB];
+        if (t + 1 < RS) {
+          const int tn1 = t + 1;
+          const int off = (tn1 / 3 == 0 ? Wo : 0) + (tn1 % 3 == 0 ? 1 : 0);
+          read_a(Pc, off, na);
+          read_b(Bc, tn1, nbv);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 av;
+        __builtin_memcpy(&av, &am, 16);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          bf16x8 bv;
+          __builtin_memcpy(&bv, &fb[nb], 16);
+          acc[cls][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[cls][nb], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 1 < RS) {
+          fa = na;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
+        }
+      }
+    } else {
+      const uint4 am = masked(vm1, 0, fa);
+      bf16x8 av;
+      __builtin_memcpy(&av, &am, 16);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        bf16x8 bv;
+        __builtin_memcpy(&bv, &fb[nb], 16);
+        acc[0][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[0][nb], 0, 0, 0);
+      }
+    }
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (more) first_reads(sl + 1, Bn, Pn);
+  };
+
+  dma_slice(0, sB0, sP0);
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  first_reads(0, sB0, sP0);
+  for (int sl = 0; sl < ns_all; sl += 2) {
+    slice(sl, sB0, sP0, sB1, sP1);
+    if (sl + 1 < ns_all) slice(sl + 1, sB1, sP1, sB0, sP0);
+  }
+
+  // ---- epilogue: per (class, 32 channels), this wave's 32 x 32 tile staged in
+  // LDS, then 4 lanes per row write 8 channels each to the class's pixel
+  float* E = (float*)(wave < 5 ? sB0 : sB1) + (wave < 5 ? wave : wave - 5) * 32 * EROW;
+  const int H = g.H, W = g.W;
+#pragma unroll
+  for (int cls = 0; cls < 4; ++cls) {
+    const int a = cls >> 1, b = cls & 1;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        *(float4*)(E + (lane & 31) * EROW + 8 * qq + 4 * kh) =
+            make_float4(acc[cls][nb][4 * qq], acc[cls][nb][4 * qq + 1], acc[cls][nb][4 * qq + 2],
+                        acc[cls][nb][4 * qq + 3]);
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+        const int64_t m = (int64_t)tile_m0 + wave * 32 + row;
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        if (m < p.M) {
+          const int img = (int)(m / HW), pix = (int)(m - (int64_t)img * HW);
+          const int ii = pix / Wo, jj = pix - (pix / Wo) * Wo;
+          const int64_t off = (((int64_t)img * H + 2 * ii + a) * W + 2 * jj + b) * p.N + n0 +
+                              nb * 32 + c8;
+          float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          if constexpr (EADD) {
+            const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
+            const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += bf2f((bf16_t)(w4[e] & 0xffffu));
+              v[2 * e + 1] += bf2f((bf16_t)(w4[e] >> 16));
+            }
+          }
+          if constexpr (EBITS) {
+            const uint32_t bits = p.mbits[off >> 3];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (!((bits >> e) & 1u)) v[e] = 0.f;
+          }
+          *(uint4*)((bf16_t*)p.out + off) = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]),
+                                                       pack2(v[4], v[5]), pack2(v[6], v[7]));
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
 // host side
 // ----------------------------------------------------------------------------
 int conv2_bn(int N) { return N % 128 == 0 ? 128 : (N % 64 == 0 ? 64 : 0); }
@@ -592,6 +826,38 @@ static hipError_t launch_mode2(const GemmParams& p0, hipStream_t s) {
     else if (RS == 9) launch_epi2<MODE, 64, 9, false>(p, grid, s);
     else launch_epi2<MODE, 64, 1, false>(p, grid, s);
   }
+  return hipGetLastError();
+}
+
+// the stride-2 data-gradient patch kernel: 3x3, stride 2, pad 1, the input
+// exactly twice the dy grid, whole dy images per 256-position tile, channel
+// counts in whole slices and column tiles, bf16 output with a mask as bits
+// (and optionally an addend); with p.a2 / p.b2 the shortcut's 1 x 1 stride-2
+// data gradient is summed into class (0, 0)
+bool conv2s2_ok(const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  const int64_t hw = (int64_t)g.Ho * g.Wo;
+  if (p.out_f32 || !p.mbits || p.mask == nullptr) return false;
+  if (!(g.R == 3 && g.S == 3 && g.stride == 2 && g.pad == 1)) return false;
+  if (g.H != 2 * g.Ho || g.W != 2 * g.Wo || hw < 1 || S2_POS % hw != 0) return false;
+  if (g.K % C2_CK != 0 || g.C % S2_BN != 0 || p.N != g.C) return false;
+  if ((p.a2 == nullptr) != (p.b2 == nullptr)) return false;
+  return true;
+}
+
+// p.b (and p.b2) must point to the weights packed for the data gradient
+// (launch_pack_weights with MODE_DGRAD: 3x3, and 1x1 for the shortcut)
+hipError_t launch_conv2s2(const GemmParams& p0, hipStream_t s) {
+  if (!conv2s2_ok(p0)) return hipErrorInvalidValue;
+  GemmParams p = p0;
+  p.M = p.g.n * p.g.Ho * p.g.Wo;
+  p.tiles_n = p.N / S2_BN;
+  const dim3 grid((unsigned)(ceil_div(p.M, S2_POS) * p.tiles_n));
+  const bool add = p.addend != nullptr, proj = p.a2 != nullptr;
+  if (add && proj) hipLaunchKernelGGL((conv2s2_kernel<EPI_ADD | EPI_MBITS, true>), grid, dim3(512), 0, s, p);
+  else if (add) hipLaunchKernelGGL((conv2s2_kernel<EPI_ADD | EPI_MBITS, false>), grid, dim3(512), 0, s, p);
+  else if (proj) hipLaunchKernelGGL((conv2s2_kernel<EPI_MBITS, true>), grid, dim3(512), 0, s, p);
+  else hipLaunchKernelGGL((conv2s2_kernel<EPI_MBITS, false>), grid, dim3(512), 0, s, p);
   return hipGetLastError();
 }
 

@@ -567,6 +567,94 @@ hipError_t launch_splitk_reduce_seg(const float* part, int64_t stride, int64_t c
   return hipGetLastError();
 }
 
+// Weighted over the segments into one output (see launch_splitk_reduce_wsum):
+// each segment's sum is formed exactly as splitk_reduce_seg_kernel forms it,
+// then acc = w0 g0, acc = fma(w_s, g_s, acc) in segment order.
+struct SegW {
+  int split0[MAX_SEG + 1];
+  float w[MAX_SEG];
+};
+
+__global__ __launch_bounds__(256) void splitk_reduce_wsum_kernel(const float* __restrict__ part,
+                                                                 int64_t stride, int64_t count,
+                                                                 SegW o, int nseg,
+                                                                 float* __restrict__ out, int c,
+                                                                 int cp, int vec) {
+  if (vec) {
+    const int64_t groups = count >> 2, st4 = stride >> 2;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
+         q += (int64_t)gridDim.x * blockDim.x) {
+      const float4* pp = (const float4*)part + q;
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int sg = 0; sg < MAX_SEG; ++sg) {
+        if (sg >= nseg) break;
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        int k = o.split0[sg];
+        const int y1 = o.split0[sg + 1];
+        for (; k + 4 <= y1; k += 4) {
+          const float4 a = pp[(k + 0) * st4], b = pp[(k + 1) * st4], cc = pp[(k + 2) * st4],
+                       d = pp[(k + 3) * st4];
+          s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+          s.x += b.x; s.y += b.y; s.z += b.z; s.w += b.w;
+          s.x += cc.x; s.y += cc.y; s.z += cc.z; s.w += cc.w;
+          s.x += d.x; s.y += d.y; s.z += d.z; s.w += d.w;
+        }
+        for (; k < y1; ++k) {
+          const float4 a = pp[k * st4];
+          s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+        }
+        const float w = o.w[sg];
+        if (sg == 0) {
+          acc.x = w * s.x; acc.y = w * s.y; acc.z = w * s.z; acc.w = w * s.w;
+        } else {
+          acc.x = __builtin_fmaf(w, s.x, acc.x);
+          acc.y = __builtin_fmaf(w, s.y, acc.y);
+          acc.z = __builtin_fmaf(w, s.z, acc.z);
+          acc.w = __builtin_fmaf(w, s.w, acc.w);
+        }
+      }
+      ((float4*)out)[q] = acc;
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const int64_t q = i / c, ch = i - q * c;
+      const int64_t src = q * cp + ch;
+      float acc = 0.f;
+#pragma unroll
+      for (int sg = 0; sg < MAX_SEG; ++sg) {
+        if (sg >= nseg) break;
+        float s = 0.f;
+        for (int k = o.split0[sg]; k < o.split0[sg + 1]; ++k) s += part[(int64_t)k * stride + src];
+        const float w = o.w[sg];
+        if (sg == 0) acc = w * s;
+        else acc = __builtin_fmaf(w, s, acc);
+      }
+      out[i] = acc;
+    }
+  }
+}
+
+hipError_t launch_splitk_reduce_wsum(const float* part, int64_t stride, int64_t count,
+                                     const int* split0, const float* w, float* out, int nseg,
+                                     int c, int cp, hipStream_t s) {
+  if (nseg < 1 || nseg > MAX_SEG || c < 1 || cp < c) return hipErrorInvalidValue;
+  SegW o{};
+  for (int i = 0; i <= nseg; ++i) o.split0[i] = split0[i];
+  for (int i = nseg + 1; i <= MAX_SEG; ++i) o.split0[i] = split0[nseg];
+  for (int i = 0; i < nseg; ++i) o.w[i] = w[i];
+  const bool vec = cp == c && count % 4 == 0 && stride % 4 == 0 &&
+                   ((uintptr_t)part & 15) == 0 && ((uintptr_t)out & 15) == 0;
+  const int64_t work = vec ? count / 4 : count;
+  int64_t blocks = (work + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(splitk_reduce_wsum_kernel, dim3((unsigned)blocks), dim3(256), 0, s, part,
+                     stride, count, o, nseg, out, c, cp, vec ? 1 : 0);
+  return hipGetLastError();
+}
+
 // ----------------------------------------------------------------------------
 // host-side launch
 // ----------------------------------------------------------------------------

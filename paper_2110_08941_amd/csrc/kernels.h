@@ -120,6 +120,12 @@ int64_t conv2_packed_elems(const GemmParams& p, int mode);
 hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
                                hipStream_t s);
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
+// Data gradient of a 3x3 stride-2 pad-1 convolution on the same packed
+// weights (conv2.hip, "stride-2 patch form"): p.a = dy [n][Ho][Wo][K], p.out =
+// dx [n][2Ho][2Wo][C] bf16 with the mask bits p.mbits (and p.addend) applied;
+// with p.a2 / p.b2 (packed 1x1 weights) the shortcut's data gradient is added.
+bool conv2s2_ok(const GemmParams& p);
+hipError_t launch_conv2s2(const GemmParams& p, hipStream_t s);
 // bf16 forward / data gradient of 64 -> 64 channel 3x3 stride-1 layers on
 // 32-wide maps (conv64.hip): packed weights resident in LDS, input patch of 16
 // output rows staged once per tile, taps as shifted LDS reads
@@ -148,6 +154,14 @@ hipError_t launch_pad_weights(const float* w, void* wp, int k, int rs, int c, in
 hipError_t launch_splitk_reduce_seg(const float* part, int64_t stride, int64_t count,
                                     const int* split0, float* const* out, int nseg, int c, int cp,
                                     hipStream_t s);
+// The same reduction weighted over the segments into one output:
+// out[i] = w[0] g_0[i], then out[i] = fma(w[s], g_s[i], out[i]) in segment
+// order (the arithmetic of the weighted average kernel), where
+// g_s[i] is segment s's sum exactly as launch_splitk_reduce_seg forms it (the
+// arithmetic of the weighted average of separately stored g_s).
+hipError_t launch_splitk_reduce_wsum(const float* part, int64_t stride, int64_t count,
+                                     const int* split0, const float* w, float* out, int nseg,
+                                     int c, int cp, hipStream_t s);
 
 // ---- elementwise / reduction kernels (layers.hip) ----
 // NCHW fp32 input -> NHWC activation (fp32 or bf16)
@@ -189,10 +203,20 @@ constexpr int STAT_MAX_BLOCKS = 1024;
 hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, const Segs& sg,
                                    int64_t rows_per_sample, int C, float* const* mean,
                                    float* const* rstd, float eps, hipStream_t s);
+// Optional weighted sum over the segments of kinds 1 and 2 (the partition-
+// weighted gradient): sum0[c] = w[0] out0[0][c] + w[1] out0[1][c] + ... in
+// segment order (sum1 likewise from out1), the per-segment outputs still
+// written.
+struct StatWsum {
+  float* sum0;
+  float* sum1;
+  float w[MAX_SEG];
+};
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
                              const float* mean, const float* rstd, int mstride, const Segs& sg,
                              int64_t rows_per_sample, int C, float* part, float* const* out0,
-                             float* const* out1, float eps, hipStream_t s);
+                             float* const* out1, float eps, hipStream_t s,
+                             const StatWsum* wsum = nullptr);
 // vectorised (C % 8 == 0) batch-norm apply / backward by segment: segment s
 // normalises with mean + s * mstride, rstd + s * mstride; the backward takes
 // its sums from sum_dy[s], sum_dyx[s]
@@ -210,6 +234,10 @@ hipError_t launch_bn_backward8(bool bf16, const void* dy, const void* act, const
 // zero a list of [begin, end) element ranges of each of nbuf float buffers
 hipError_t launch_zero_ranges(float* const* bufs, int nbuf, const int64_t* ranges, int count,
                               hipStream_t s);
+// the same with the ranges read from host memory and passed by value in the
+// kernel arguments (no device copy of the list)
+hipError_t launch_zero_ranges_host(float* const* bufs, int nbuf, const int64_t* ranges, int count,
+                                   hipStream_t s);
 
 // ---- optimizer kernels (opt.hip) ----
 hipError_t launch_wavg_sgd(const float* const* g, const float* w, int M, float* theta, float* mom,

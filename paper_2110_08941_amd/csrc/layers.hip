@@ -328,4 +328,38 @@ hipError_t launch_zero_ranges(float* const* bufs, int nbuf, const int64_t* range
   return hipGetLastError();
 }
 
+// up to kRangesByValue ranges per launch, in the kernel arguments
+constexpr int kRangesByValue = 32;
+struct RangeList {
+  int64_t r[2 * kRangesByValue];
+};
+
+__global__ void zero_ranges_byval_kernel(BufList bufs, RangeList rl, int count) {
+  const int r = blockIdx.x;
+  if (r >= count) return;
+  float* buf = bufs.p[0];
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i)
+    if (i == (int)blockIdx.y) buf = bufs.p[i];
+  const int64_t b = rl.r[2 * r], e = rl.r[2 * r + 1];
+  for (int64_t i = b + threadIdx.x; i < e; i += blockDim.x) buf[i] = 0.f;
+}
+
+hipError_t launch_zero_ranges_host(float* const* bufs, int nbuf, const int64_t* ranges, int count,
+                                   hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  if (nbuf < 1 || nbuf > MAX_SEG) return hipErrorInvalidValue;
+  BufList l{};
+  for (int i = 0; i < nbuf; ++i) l.p[i] = bufs[i];
+  for (int c0 = 0; c0 < count; c0 += kRangesByValue) {
+    const int k = count - c0 < kRangesByValue ? count - c0 : kRangesByValue;
+    RangeList rl{};
+    for (int i = 0; i < 2 * k; ++i) rl.r[i] = ranges[2 * c0 + i];
+    hipLaunchKernelGGL(zero_ranges_byval_kernel, dim3(k, nbuf), dim3(64), 0, s, l, rl, k);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace hs

@@ -215,7 +215,7 @@ struct Bump {
 };
 }  // namespace
 
-int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
+int64_t plan_workspace(const Model& m, int max_n, Workspace* ws, int64_t splitk_min_floats) {
   const int64_t es = m.dtype == HS_BF16 ? 2 : 4;
   Bump a{ws->arena};
   ws->slot.clear();
@@ -296,7 +296,7 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
   for (const ParamT& t : m.params)
     if ((t.kind == HS_KIND_CONV_W || t.kind == HS_KIND_LIN_W) && t.numel > max_w) max_w = t.numel;
   const int64_t segs = max_n < MAX_SEG ? max_n : MAX_SEG;
-  ws->splitk_floats = (int64_t)16 << 20;
+  ws->splitk_floats = splitk_min_floats;
   if (segs * max_w > ws->splitk_floats) ws->splitk_floats = segs * max_w;
   ws->splitk = (float*)a.take(ws->splitk_floats * 4);
   if (m.dtype == HS_BF16) {
@@ -309,6 +309,11 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws) {
     ws->packed_cap = 2 * all_w;
     ws->packed = (bf16_t*)a.take(ws->packed_cap * 2);
   }
+  // per-worker batch-norm / bias gradient sums of the partition-weighted mode,
+  // one set per stream
+  ws->gtmp_c = cmax > 512 ? cmax : 512;
+  ws->gtmp = (float*)a.take((int64_t)MAX_SEG * 2 * ws->gtmp_c * 4);
+  ws->gtmp_side = (float*)a.take((int64_t)MAX_SEG * 2 * ws->gtmp_c * 4);
   ws->gaps = (int64_t*)a.take((int64_t)(m.gaps.size() + 2) * 8);
   return a.off;
 }
@@ -339,7 +344,13 @@ struct Ctx {
   Segs sg;
   float* g[MAX_SEG];
   float* part = nullptr;   // statistics partials of this stream (null: ws.stat_part)
+  // partition-weighted mode: every parameter gradient goes to gbar as
+  // sum_s w[s] g_s (the per-worker g_s are not stored; per-worker batch-norm
+  // and bias sums go to this stream's gtmp slots)
+  float* gbar = nullptr;
+  float w[MAX_SEG] = {};
   float* sp() const { return part ? part : ws.stat_part; }
+  float* gtmp() const { return part ? ws.gtmp_side : ws.gtmp; }
   const void* W(int64_t off) const {
     return bf ? (const void*)(tbf + off) : (const void*)(theta + off);
   }
@@ -436,6 +447,61 @@ void pick_fast_tiles(int mode, int M, int N, int& bm, int& bn) {
 
 hipError_t wait_mark(const Ctx& c, int k);
 
+// The packed copy (launch_pack_weights) of weights w -- a tensor of
+// theta_bf16 -- for `mode` and the contraction shape `shape`: the tensor's
+// listed region (packed on the second stream at the start of every later
+// call; waited for here), a new region packed now on the first call, or, with
+// scratch_ok, the workspace's one-layer buffer (packed now).  *out is null
+// when none of them is available.
+hipError_t packed_weights(const Ctx& c, const void* w, int mode, const GemmParams& shape,
+                          bool scratch_ok, const void** out) {
+  Workspace& ws = c.ws;
+  *out = nullptr;
+  int64_t woff = c.tbf ? (const bf16_t*)w - c.tbf : -1;
+  if (woff >= c.m.P) woff = -1;   // not a tensor of theta
+  const int64_t key = woff * 2 + (mode == MODE_DGRAD ? 1 : 0);
+  const auto it = ws.packed && woff >= 0 ? ws.pack_of.find(key) : ws.pack_of.end();
+  if (it != ws.pack_of.end() && ws.pack_ready >= 0) {
+    if (!ws.pack_waited) {
+      HS_TRY(wait_mark(c, ws.pack_ready));
+      ws.pack_waited = true;
+    }
+    *out = ws.packed + ws.packs[it->second].dst;
+  } else if (it != ws.pack_of.end()) {
+    *out = ws.packed + ws.packs[it->second].dst;
+    HS_TRY(launch_pack_weights(w, (void*)*out, mode, shape, c.s));
+  } else if (ws.packed && woff >= 0 &&
+             ws.packed_used + conv2_packed_elems(shape, mode) <= ws.packed_cap) {
+    Workspace::Pack e{woff, ws.packed_used, shape, mode};
+    ws.packed_used += (conv2_packed_elems(shape, mode) + 63) / 64 * 64;
+    ws.pack_of[key] = (int)ws.packs.size();
+    ws.packs.push_back(e);
+    *out = ws.packed + e.dst;
+    HS_TRY(launch_pack_weights(w, (void*)*out, mode, shape, c.s));
+  } else if (scratch_ok && conv2_packed_elems(shape, mode) <= ws.wpack_elems) {
+    HS_TRY(launch_pack_weights(w, ws.wpack, mode, shape, c.s));
+    *out = ws.wpack;
+  }
+  return hipSuccess;
+}
+
+// timing probe (hs_probe_enable): an event before and after a launch of the
+// probed (mode, tile) on the launch's stream
+bool probe_begin(const Ctx& c, int mode, int bm, int bn) {
+  Workspace& ws = c.ws;
+  if (!(ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn &&
+        ws.probe_used * 2 + 1 < ws.probe_ev.size()))
+    return false;
+  return hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s) == hipSuccess;
+}
+hipError_t probe_end(const Ctx& c, double flops) {
+  Workspace& ws = c.ws;
+  HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
+  ws.probe_flops[ws.probe_used] = flops;
+  ws.probe_used += 1;
+  return hipSuccess;
+}
+
 // Launch one GEMM (fast kernel when the shape allows, generic otherwise);
 // brackets it with probe events when it is the probed instantiation.
 hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
@@ -480,39 +546,13 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     q.stat_part = nullptr;
   }
   if (mfma32 || w64) {
-    // the layer's region of packed weights: packed on the second stream at
-    // the start of the call, or now (first call, or a workspace without one)
-    int64_t woff = c.tbf ? (const bf16_t*)p.b - c.tbf : -1;
-    if (woff >= c.m.P) woff = -1;   // not a tensor of theta
-    const int64_t key = woff * 2 + (mode == MODE_DGRAD ? 1 : 0);
-    const auto it = ws.packed && woff >= 0 ? ws.pack_of.find(key) : ws.pack_of.end();
-    if (it != ws.pack_of.end() && ws.pack_ready >= 0) {
-      if (!ws.pack_waited) {
-        HS_TRY(wait_mark(c, ws.pack_ready));
-        ws.pack_waited = true;
-      }
-      q.b = ws.packed + ws.packs[it->second].dst;
-    } else if (it != ws.pack_of.end()) {
-      q.b = ws.packed + ws.packs[it->second].dst;
-      HS_TRY(launch_pack_weights(p.b, (void*)q.b, mode, p, c.s));
-    } else if (ws.packed && woff >= 0 &&
-               ws.packed_used + conv2_packed_elems(p, mode) <= ws.packed_cap) {
-      Workspace::Pack e{woff, ws.packed_used, p, mode};
-      ws.packed_used += (conv2_packed_elems(p, mode) + 63) / 64 * 64;
-      ws.pack_of[key] = (int)ws.packs.size();
-      ws.packs.push_back(e);
-      q.b = ws.packed + e.dst;
-      HS_TRY(launch_pack_weights(p.b, (void*)q.b, mode, p, c.s));
-    } else {
-      HS_TRY(launch_pack_weights(p.b, ws.wpack, mode, p, c.s));
-      q.b = ws.wpack;
-    }
+    const void* wb = nullptr;
+    HS_TRY(packed_weights(c, p.b, mode, p, true, &wb));
+    q.b = wb;
     bm = w64 ? 64 : 512;
     bn = w64 ? 64 : conv2_bn(p.N);
   }
-  const bool probe = ws.probe_mode == mode && ws.probe_bm == bm && ws.probe_bn == bn &&
-                     (fast || mfma32 || wg3 || w64) && ws.probe_used * 2 + 1 < ws.probe_ev.size();
-  if (probe) HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used], c.s));
+  const bool probe = (fast || mfma32 || wg3 || w64) && probe_begin(c, mode, bm, bn);
   if (wg3) HS_TRY(launch_wgrad3(p, c.s));
   else if (w64) {
     HS_TRY(launch_conv64(mode, q, c.s));
@@ -525,11 +565,7 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     r.mbits = nullptr;   // the generic kernel reads the mask tensor
     HS_TRY(launch_igemm(mode, c.bf, r, veca, vecb, bm, bn, splits, c.s));
   }
-  if (probe) {
-    HS_TRY(hipEventRecord(ws.probe_ev[2 * ws.probe_used + 1], c.s));
-    ws.probe_flops[ws.probe_used] = flops;
-    ws.probe_used += 1;
-  }
+  if (probe) HS_TRY(probe_end(c, flops));
   return hipSuccess;
 }
 
@@ -588,6 +624,38 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   p.K = L.k * L.k * L.cout;
   const bool veca = (L.cout % c.V) == 0;
   const bool vecb = (L.cin % c.V) == 0;
+  const bool can_fuse = proj && dproj && fused && L.k == 3 && L.pad == 1 && proj->k == 1 &&
+                        proj->stride == 2 && proj->pad == 0 && proj->cin == L.cin &&
+                        proj->cout == L.cout && proj->H == L.H && proj->W == L.W;
+  if (c.bf && L.stride == 2 && !c.part && c.ws.packed && (can_fuse || !proj)) {
+    // bf16 3x3 stride 2: every parity class from one staged dy patch
+    // (conv2.hip, stride-2 patch form), the shortcut's data gradient summed in
+    GemmParams q = p;
+    if (can_fuse) {
+      q.a2 = dproj;
+      q.b2 = c.W(proj->w);
+    }
+    if (conv2s2_ok(q)) {
+      GemmParams pshape{};
+      if (can_fuse) {
+        pshape = base_params(*proj, c.n);
+        pshape.N = proj->cin;
+      }
+      const void *wb = nullptr, *wb2 = nullptr;
+      HS_TRY(packed_weights(c, p.b, MODE_DGRAD, p, false, &wb));
+      if (wb && can_fuse) HS_TRY(packed_weights(c, q.b2, MODE_DGRAD, pshape, false, &wb2));
+      if (wb && (!can_fuse || wb2)) {
+        q.b = wb;
+        q.b2 = wb2;
+        const double flops = layer_flops(L, c.n) + (can_fuse ? layer_flops(*proj, c.n) : 0.0);
+        const bool probe = probe_begin(c, MODE_DGRAD, 256, 256);
+        HS_TRY(launch_conv2s2(q, c.s));
+        if (probe) HS_TRY(probe_end(c, flops));
+        if (can_fuse) *fused = true;
+        return hipSuccess;
+      }
+    }
+  }
   if (L.stride == 2 && L.H % 2 == 0 && L.W % 2 == 0 && veca && vecb) {
     GemmParams q = p;
     q.par = 1;
@@ -605,9 +673,7 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
       q.ntap[cls] = nt;
     }
     double flops = layer_flops(L, c.n);
-    const bool fuse = proj && dproj && fused && L.k == 3 && L.pad == 1 && proj->k == 1 &&
-                      proj->stride == 2 && proj->pad == 0 && proj->cin == L.cin &&
-                      proj->cout == L.cout && proj->H == L.H && proj->W == L.W;
+    const bool fuse = can_fuse;
     if (fuse) {
       q.a2 = dproj;
       q.b2 = c.W(proj->w);
@@ -673,6 +739,9 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
     p.out = c.ws.splitk;
     p.split_stride = mn;
     HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, 64, 64, p.seg_split[c.sg.count], flops));
+    if (c.gbar)
+      return launch_splitk_reduce_wsum(c.ws.splitk, mn, mn, p.seg_split, c.w, c.gbar + L.w,
+                                       c.sg.count, L.cin, L.cin, c.s);
     float* outs[MAX_SEG];
     for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
     return launch_splitk_reduce_seg(c.ws.splitk, mn, mn, p.seg_split, outs, c.sg.count, L.cin,
@@ -709,16 +778,20 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
   }
   p.seg_n0[c.sg.count] = c.sg.n0[c.sg.count];
   if (direct) {
-    p.out = c.g[0] + L.w;
+    // one worker (its weight is 1): straight into its gradient
+    p.out = (c.gbar ? c.gbar : c.g[0]) + L.w;
     p.split_stride = 0;
     return gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, flops);
   }
   p.out = c.ws.splitk;
   p.split_stride = mn;
   HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, bm, bn, splits, flops));
+  const int64_t count = (int64_t)L.cout * L.k * L.k * cin_true;
+  if (c.gbar)
+    return launch_splitk_reduce_wsum(c.ws.splitk, mn, count, p.seg_split, c.w, c.gbar + L.w,
+                                     c.sg.count, cin_true, L.cin, c.s);
   float* outs[MAX_SEG];
   for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
-  const int64_t count = (int64_t)L.cout * L.k * L.k * cin_true;
   return launch_splitk_reduce_seg(c.ws.splitk, mn, count, p.seg_split, outs, c.sg.count, cin_true,
                                   L.cin, c.s);
 }
@@ -727,9 +800,16 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
 // unless f32); rps rows per sample
 hipError_t bias_grad(const Ctx& c, int64_t boff, const void* dy, bool f32, int64_t rps, int C) {
   float* out[MAX_SEG];
-  for (int i = 0; i < c.sg.count; ++i) out[i] = c.g[i] + boff;
+  StatWsum ws{};
+  if (c.gbar) {
+    for (int i = 0; i < c.sg.count; ++i) out[i] = c.gtmp() + (int64_t)i * 2 * c.ws.gtmp_c;
+    ws.sum0 = c.gbar + boff;
+    for (int i = 0; i < c.sg.count; ++i) ws.w[i] = c.w[i];
+  } else {
+    for (int i = 0; i < c.sg.count; ++i) out[i] = c.g[i] + boff;
+  }
   return launch_chan_stats(2, f32 ? false : c.bf, nullptr, dy, nullptr, nullptr, nullptr, 0, c.sg,
-                           rps, C, c.sp(), out, nullptr, 0.f, c.s);
+                           rps, C, c.sp(), out, nullptr, 0.f, c.s, c.gbar ? &ws : nullptr);
 }
 
 // per-worker batch-norm statistics of z (rps rows per sample)
@@ -780,12 +860,25 @@ hipError_t bn_apply(const Ctx& c, const BNL& b, const void* z, const void* res, 
 hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
                   int64_t rps, void* dz) {
   float *db[MAX_SEG], *dg[MAX_SEG];
-  for (int i = 0; i < c.sg.count; ++i) {
-    db[i] = c.g[i] + b.b;
-    dg[i] = c.g[i] + b.g;
+  StatWsum ws{};
+  if (c.gbar) {
+    // the workers' sums in this stream's slots (the backward below reads
+    // them), their weighted sums into gbar
+    for (int i = 0; i < c.sg.count; ++i) {
+      db[i] = c.gtmp() + (int64_t)i * 2 * c.ws.gtmp_c;
+      dg[i] = db[i] + c.ws.gtmp_c;
+      ws.w[i] = c.w[i];
+    }
+    ws.sum0 = c.gbar + b.b;
+    ws.sum1 = c.gbar + b.g;
+  } else {
+    for (int i = 0; i < c.sg.count; ++i) {
+      db[i] = c.g[i] + b.b;
+      dg[i] = c.g[i] + b.g;
+    }
   }
   HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps, b.c,
-                           c.sp(), db, dg, 0.f, c.s));
+                           c.sp(), db, dg, 0.f, c.s, c.gbar ? &ws : nullptr));
   return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
                              db, dg, c.sg, rps, b.c, dz, c.s);
 }
@@ -1316,16 +1409,25 @@ hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a,
 
 hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
                         const bf16_t* theta_bf16, const float* x, const int32_t* y, const int* n,
-                        int M, float* const* g, float* loss, hipStream_t s) {
+                        int M, float* const* g, float* loss, hipStream_t s, float* gbar,
+                        const float* w) {
   if (M < 1 || M > MAX_SEG) return hipErrorInvalidValue;
+  if (gbar && !w) return hipErrorInvalidValue;
   Segs sg{};
   sg.count = M;
   sg.n0[0] = 0;
   for (int i = 0; i < M; ++i) sg.n0[i + 1] = sg.n0[i] + n[i];
   Ctx c{m, ws, theta, theta_bf16, sg.n0[M], s, m.dtype == HS_BF16, m.dtype == HS_BF16 ? 8 : 4, sg,
         {}};
-  for (int i = 0; i < M; ++i) c.g[i] = g[i];
-  HS_TRY(launch_zero_ranges(c.g, M, ws.gaps, (int)(m.gaps.size() / 2), s));
+  for (int i = 0; i < M; ++i) c.g[i] = gbar ? nullptr : g[i];
+  c.gbar = gbar;
+  for (int i = 0; i < M; ++i) c.w[i] = gbar ? w[i] : 0.f;
+  float* const* zero_bufs = gbar ? &gbar : c.g;
+  const int nzero = gbar ? 1 : M;
+  if (ws.gaps_by_value)
+    HS_TRY(launch_zero_ranges_host(zero_bufs, nzero, m.gaps.data(), (int)(m.gaps.size() / 2), s));
+  else
+    HS_TRY(launch_zero_ranges(zero_bufs, nzero, ws.gaps, (int)(m.gaps.size() / 2), s));
   // this call's packed weights, on the second stream: every region an
   // earlier call listed, ordered after the work already on the caller's
   // stream (the update of theta_bf16); the first packed launch waits for it

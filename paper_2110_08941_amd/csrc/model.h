@@ -98,10 +98,15 @@ struct Workspace {
   std::unordered_map<int64_t, int> pack_of;   // (woff * 2 + mode) -> packs index
   int pack_ready = -1;         // event slot after this call's packing, -1: not packed
   bool pack_waited = false;
+  float* gtmp = nullptr;       // partition-weighted mode: per-worker sums (caller's stream)
+  float* gtmp_side = nullptr;  // the same for the second stream
+  int64_t gtmp_c = 0;          // channels per slot
   int64_t* gaps = nullptr;     // device copy of the padding ranges
+  bool gaps_by_value = false;  // zero the gaps from the model's host list instead
   // second stream for the weight gradients of the backward pass (null: all
   // work on the caller's stream) and events that order the two streams
   hipStream_t side = nullptr;
+  hipStream_t side_owned = nullptr;   // the workspace's stream; side is it or null
   static constexpr int kEvents = 64;
   hipEvent_t ev[kEvents] = {};     // fork / join points (either stream)
   int ev_next = 0;
@@ -114,14 +119,24 @@ struct Workspace {
   size_t probe_used = 0;
 };
 
-int64_t plan_workspace(const Model& m, int max_n, Workspace* ws);  // ws->arena set => bind
+// Lays out (ws->arena set: binds) a workspace for max_n samples; returns its
+// bytes.  The split-K partial buffer holds at least splitk_min_floats floats
+// (more splits, shorter weight-gradient launches) and at least one split per
+// worker of the largest weight gradient.
+constexpr int64_t kSplitkMinFloats = (int64_t)16 << 20;
+int64_t plan_workspace(const Model& m, int max_n, Workspace* ws,
+                       int64_t splitk_min_floats = kSplitkMinFloats);
 
 // Gradients of M workers in one pass over the layers: worker s owns samples
 // [o_s, o_s + n[s]) of x / y (o_s = n[0] + ... + n[s-1]); its gradient goes to
-// g[s] and its mean loss to loss[s] (loss may be null).
+// g[s] and its mean loss to loss[s] (loss may be null).  With gbar (and the
+// weights w[0..M)), g is not used: gbar receives sum_s w[s] g_s, each
+// parameter's per-worker sums combined in worker order as the weighted
+// average of stored g_s does.
 hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
                         const bf16_t* theta_bf16, const float* x, const int32_t* y, const int* n,
-                        int M, float* const* g, float* loss, hipStream_t s);
+                        int M, float* const* g, float* loss, hipStream_t s,
+                        float* gbar = nullptr, const float* w = nullptr);
 
 // One layer contraction (mode 0 forward, 1 data gradient, 2 weight gradient)
 // with the schedule hs_worker_grad uses.

@@ -33,8 +33,16 @@ __global__ __launch_bounds__(256) void wavg_sgd_kernel(WavgArgs a, int M, float*
     if (MODE == 1) {
       gs = __builtin_nontemporal_load((const f4*)a.g[0] + i);
     } else {
+      // w_0 g_0, then fma(w_m, g_m, sum) in worker order (the arithmetic the
+      // weighted reductions of the one-pass gradient repeat exactly)
       gs = a.w[0] * __builtin_nontemporal_load((const f4*)a.g[0] + i);
-      for (int m = 1; m < M; ++m) gs += a.w[m] * __builtin_nontemporal_load((const f4*)a.g[m] + i);
+      for (int m = 1; m < M; ++m) {
+        const f4 v = __builtin_nontemporal_load((const f4*)a.g[m] + i);
+        gs.x = __builtin_fmaf(a.w[m], v.x, gs.x);
+        gs.y = __builtin_fmaf(a.w[m], v.y, gs.y);
+        gs.z = __builtin_fmaf(a.w[m], v.z, gs.z);
+        gs.w = __builtin_fmaf(a.w[m], v.w, gs.w);
+      }
     }
     if (MODE == 0) {
       __builtin_nontemporal_store(gs, (f4*)gout + i);
@@ -62,7 +70,7 @@ __global__ __launch_bounds__(256) void wavg_sgd_kernel(WavgArgs a, int M, float*
         gsum = a.g[0][j];
       } else {
         gsum = a.w[0] * a.g[0][j];
-        for (int m = 1; m < M; ++m) gsum += a.w[m] * a.g[m][j];
+        for (int m = 1; m < M; ++m) gsum = __builtin_fmaf(a.w[m], a.g[m][j], gsum);
       }
       if (MODE == 0) {
         gout[j] = gsum;

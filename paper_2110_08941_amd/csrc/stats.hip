@@ -101,6 +101,7 @@ struct FinishArgs {
   SegRows sr;
   float* out0[MAX_SEG];
   float* out1[MAX_SEG];
+  StatWsum wsum;               // sum0 null: no weighted sum
 };
 
 // V consecutive channels of one row kept in their storage format until they
@@ -293,70 +294,94 @@ __global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
 }
 
 // blockIdx.y = segment, blockIdx.x = group of 8 channels; thread = channel
-// (t & 7) x lane (t >> 3)
+// (t & 7) x lane (t >> 3).  With a weighted sum (a.wsum, kinds 1 and 2) one
+// block per channel group takes every segment in turn and also adds the
+// segments' results with their weights.
 template <typename T, int KIND>
 __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
   __shared__ double red[2][256];
-  const int s = blockIdx.y;
   const int t = threadIdx.x, lane = t >> 3;
   const int c = blockIdx.x * 8 + (t & 7);
   const int C = a.C;
-  int b0 = 0, b1 = 0;
-  int64_t seg0 = 0, seg1 = 0;
+  const bool wsum = KIND != 0 && a.wsum.sum0 != nullptr;
+  const int sfirst = wsum ? 0 : (int)blockIdx.y, slast = wsum ? a.sr.count : (int)blockIdx.y + 1;
+  float acc0 = 0.f, acc1 = 0.f;
+  for (int s = sfirst; s < slast; ++s) {
+    int b0 = 0, b1 = 0;
+    int64_t seg0 = 0, seg1 = 0;
+    float w = 0.f;
 #pragma unroll
-  for (int i = 0; i < MAX_SEG; ++i)
-    if (i == s) {
-      b0 = a.sr.blk[i];
-      b1 = a.sr.blk[i + 1];
-      seg0 = a.sr.row[i];
-      seg1 = a.sr.row[i + 1];
-    }
-  double s0 = 0.0, s1 = 0.0;
-  if (c < C) {
-    int b = b0 + lane;
-    for (; b + 96 < b1; b += 128) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        v[2 * u] = a.part[((int64_t)(b + 32 * u) * 2 + 0) * C + c];
-        v[2 * u + 1] = a.part[((int64_t)(b + 32 * u) * 2 + 1) * C + c];
+    for (int i = 0; i < MAX_SEG; ++i)
+      if (i == s) {
+        b0 = a.sr.blk[i];
+        b1 = a.sr.blk[i + 1];
+        seg0 = a.sr.row[i];
+        seg1 = a.sr.row[i + 1];
+        w = a.wsum.w[i];
       }
+    double s0 = 0.0, s1 = 0.0;
+    if (c < C) {
+      int b = b0 + lane;
+      for (; b + 96 < b1; b += 128) {
+        float v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        s0 += (double)v[2 * u];
-        s1 += (double)v[2 * u + 1];
+        for (int u = 0; u < 4; ++u) {
+          v[2 * u] = a.part[((int64_t)(b + 32 * u) * 2 + 0) * C + c];
+          v[2 * u + 1] = a.part[((int64_t)(b + 32 * u) * 2 + 1) * C + c];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          s0 += (double)v[2 * u];
+          s1 += (double)v[2 * u + 1];
+        }
+      }
+      for (; b < b1; b += 32) {
+        s0 += (double)a.part[((int64_t)b * 2 + 0) * C + c];
+        s1 += (double)a.part[((int64_t)b * 2 + 1) * C + c];
       }
     }
-    for (; b < b1; b += 32) {
-      s0 += (double)a.part[((int64_t)b * 2 + 0) * C + c];
-      s1 += (double)a.part[((int64_t)b * 2 + 1) * C + c];
-    }
-  }
-  red[0][t] = s0;
-  red[1][t] = s1;
-  __syncthreads();
-  for (int w = 16; w >= 1; w >>= 1) {
-    if (lane < w) {
-      red[0][t] += red[0][t + 8 * w];
-      red[1][t] += red[1][t + 8 * w];
-    }
+    red[0][t] = s0;
+    red[1][t] = s1;
     __syncthreads();
+    for (int step = 16; step >= 1; step >>= 1) {
+      if (lane < step) {
+        red[0][t] += red[0][t + 8 * step];
+        red[1][t] += red[1][t + 8 * step];
+      }
+      __syncthreads();
+    }
+    if (lane == 0 && c < C) {
+      float* o0 = pick(a.out0, s);
+      float* o1 = pick(a.out1, s);
+      const double t0 = red[0][t], t1 = red[1][t];
+      if (KIND == 0) {
+        const double cnt = (double)(seg1 - seg0);
+        const double m1 = t0 / cnt;
+        double var = t1 / cnt - m1 * m1;
+        if (var < 0.0) var = 0.0;
+        const float shift = a.x ? ld<T>((const T*)a.x, seg0 * C + c) : 0.f;
+        o0[c] = (float)((double)shift + m1);
+        o1[c] = (float)(1.0 / sqrt(var + (double)a.eps));
+      } else {
+        const float v0 = (float)t0, v1 = (float)t1;
+        if (o0) o0[c] = v0;
+        if (KIND == 1 && o1) o1[c] = v1;
+        if (wsum) {
+          if (s == 0) {
+            acc0 = w * v0;
+            acc1 = w * v1;
+          } else {
+            acc0 = __builtin_fmaf(w, v0, acc0);
+            acc1 = __builtin_fmaf(w, v1, acc1);
+          }
+        }
+      }
+    }
+    __syncthreads();   // red is reused by the next segment
   }
-  if (lane != 0 || c >= C) return;
-  float* o0 = pick(a.out0, s);
-  float* o1 = pick(a.out1, s);
-  const double t0 = red[0][t], t1 = red[1][t];
-  if (KIND == 0) {
-    const double cnt = (double)(seg1 - seg0);
-    const double m1 = t0 / cnt;
-    double var = t1 / cnt - m1 * m1;
-    if (var < 0.0) var = 0.0;
-    const float shift = a.x ? ld<T>((const T*)a.x, seg0 * C + c) : 0.f;
-    o0[c] = (float)((double)shift + m1);
-    o1[c] = (float)(1.0 / sqrt(var + (double)a.eps));
-  } else {
-    if (o0) o0[c] = (float)t0;
-    if (KIND == 1 && o1) o1[c] = (float)t1;
+  if (wsum && lane == 0 && c < C) {
+    a.wsum.sum0[c] = acc0;
+    if (KIND == 1 && a.wsum.sum1) a.wsum.sum1[c] = acc1;
   }
 }
 
@@ -388,7 +413,8 @@ hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, con
 hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy, const void* act,
                              const float* mean, const float* rstd, int mstride, const Segs& sg,
                              int64_t rows_per_sample, int C, float* part, float* const* out0,
-                             float* const* out1, float eps, hipStream_t s) {
+                             float* const* out1, float eps, hipStream_t s, const StatWsum* wsum) {
+  if (wsum && kind == 0) return hipErrorInvalidValue;
   if (C < 1 || C > 256 * 8 || (C % 8 != 0 && C > 256)) return hipErrorInvalidValue;
   if (sg.count < 1 || sg.count > MAX_SEG) return hipErrorInvalidValue;
   const bool vec = (C % 8 == 0 && C / 8 <= 256);
@@ -406,8 +432,9 @@ hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy,
     f.out0[i] = out0 ? out0[i] : nullptr;
     f.out1[i] = out1 ? out1[i] : nullptr;
   }
+  if (wsum) f.wsum = *wsum;
   const dim3 grid(a.sr.blk[sg.count]), block(256);
-  const dim3 fgrid((C + 7) / 8, sg.count);
+  const dim3 fgrid((C + 7) / 8, wsum ? 1 : sg.count);
   const int64_t rows = (int64_t)(sg.n0[sg.count] - sg.n0[0]) * rows_per_sample;
   // the sums over two or three tensors gain from streaming loads only when
   // they are far beyond the last-level cache; the single-tensor forward sums

@@ -30,7 +30,8 @@ from .configs import WORKLOADS, Workload
 class Trainer:
     def __init__(self, workload, seed=0, clock="measured", device="cuda:0", n_batches=4,
                  max_n=None, steps=None, theta0=None, grouped=False, exchange="edp",
-                 delays=None, estimator=("window",), lr_schedule=None, serial=False):
+                 delays=None, estimator=("window",), lr_schedule=None, serial=False,
+                 fused_avg=False):
         self.wl = wl = WORKLOADS[workload] if isinstance(workload, str) else workload
         assert isinstance(wl, Workload)
         if clock not in ("measured", "model"):
@@ -39,6 +40,8 @@ class Trainer:
             raise ValueError("serial applies to per-worker launches, not grouped ones")
         if grouped and clock != "model":
             raise ValueError("grouped workers have no per-worker device time: use clock='model'")
+        if fused_avg and (not grouped or exchange != "edp"):
+            raise ValueError("fused_avg needs grouped workers and the edp exchange")
         if exchange not in ("edp", "mean"):
             raise ValueError("exchange must be 'edp' or 'mean'")
         if estimator[0] not in ("window", "ema", "history"):
@@ -50,6 +53,9 @@ class Trainer:
             raise ValueError("delays: one finite, non-negative delay per worker")
         self.clock = clock
         self.grouped = grouped
+        # fused_avg: the one-pass call forms the partition-weighted gradient
+        # itself (hs_workers_grad_wavg) and the step applies plain SGD to it
+        self.fused_avg = fused_avg
         # exchange: "edp" weights g_m by n_m / N (Section 4.2); "mean" is the
         # plain mean of Sync-SGD and DP-SGD.  delays: additive per-batch delay
         # of each worker in the units of X (Section 5's simulated
@@ -85,7 +91,8 @@ class Trainer:
         if self.bf16:
             hs.params_to_bf16(self.theta.data_ptr(), self.theta_bf16.data_ptr(), self.P)
         self.mom = torch.zeros(self.P, device=self.dev) if wl.mu != 0.0 else None
-        self.grads = [torch.empty(self.P, device=self.dev) for _ in range(self.M)]
+        self.grads = [torch.empty(self.P, device=self.dev)
+                      for _ in range(1 if fused_avg else self.M)]
         self.losses = torch.zeros(self.M, device=self.dev)
         self.max_n = max_n or self.N
         if grouped:
@@ -106,6 +113,7 @@ class Trainer:
             x, y = synth.batch(wl.in_shape, self.N, seed, b)
             self.batches.append((torch.from_numpy(x).to(self.dev), torch.from_numpy(y).to(self.dev)))
         self.t = 0
+        self.in_window = 0      # steps launched since the current window started
         self.time_opt = False   # record events around the weighted-average + SGD launch
         self.opt_events = []
         self.pending = []       # (step, partition, [(e0, e1)] or None) awaiting observation
@@ -151,7 +159,13 @@ class Trainer:
         n = self.part.partition()
         x, y = self.batch(t)
         main = torch.cuda.current_stream(self.dev)
-        if self.grouped:
+        if self.fused_avg:
+            hs.workers_grad_wavg(self.model, self.ws[0], self.theta.data_ptr(),
+                                 self.theta_bf16.data_ptr() if self.bf16 else 0, x.data_ptr(),
+                                 y.data_ptr(), n, self.grads[0].data_ptr(),
+                                 self.losses.data_ptr(), main.cuda_stream)
+            events = None
+        elif self.grouped:
             hs.workers_grad(self.model, self.ws[0], self.theta.data_ptr(),
                             self.theta_bf16.data_ptr() if self.bf16 else 0, x.data_ptr(),
                             y.data_ptr(), n, [g.data_ptr() for g in self.grads],
@@ -164,16 +178,31 @@ class Trainer:
             e0.record(main)
         # the kernel weights worker m by w[m] / sum w: the partition sizes, or
         # ones for the plain mean
-        w = n if self.exchange == "edp" else [1] * self.M
-        hs.wavg_sgd([g.data_ptr() for g in self.grads], w, self.theta.data_ptr(),
-                    self.mom.data_ptr() if self.mom is not None else 0, self.P, self.lr(t),
-                    wl.mu, wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0, main.cuda_stream)
+        if self.fused_avg:
+            hs.sgd_step(self.theta.data_ptr(), self.grads[0].data_ptr(),
+                        self.mom.data_ptr() if self.mom is not None else 0, self.P, self.lr(t),
+                        wl.mu, wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0,
+                        main.cuda_stream)
+        else:
+            w = n if self.exchange == "edp" else [1] * self.M
+            hs.wavg_sgd([g.data_ptr() for g in self.grads], w, self.theta.data_ptr(),
+                        self.mom.data_ptr() if self.mom is not None else 0, self.P, self.lr(t),
+                        wl.mu, wl.wd, self.theta_bf16.data_ptr() if self.bf16 else 0,
+                        main.cuda_stream)
         if self.time_opt:
             e1.record(main)
             self.opt_events.append((e0, e1))
         self.pending.append((t, n, events))
         self.t += 1
-        if len(self.pending) >= (wl.window if wl.window > 0 else 64):
+        # the last step of a window is observed before the next step reads
+        # its partition, so that every observation of a window describes a
+        # step run with that window's partition (a flush in between, e.g.
+        # after warm-up steps, only observes steps earlier)
+        self.in_window += 1
+        if wl.window > 0 and self.in_window == wl.window:
+            self.flush()
+            self.in_window = 0
+        elif len(self.pending) >= 64:
             self.flush()
         return n
 
@@ -202,17 +231,18 @@ class Trainer:
             cp = None
             if self.wl.window > 0:
                 # with delays the batch times are reported whole (speed 1)
-                cp = (self.part.observe(tau, speed) if self.delays is None
-                      else self.part.observe(x, [1.0] * self.M))
+                cp = (self.part.observe(n, tau, speed) if self.delays is None
+                      else self.part.observe(n, x, [1.0] * self.M))
             self.log.append({"step": t, "n": list(n), "tau": tau, "speed": list(speed), "x": x,
                              "xmax": max(x), "cp": cp})
         self.pending = []
 
     def opt_bytes(self):
         """Algorithmic HBM bytes of one weighted-average + SGD launch: M fp32
-        gradients read, theta read and written, the momentum buffer read and
-        written (if any), the bf16 copy written (if any)."""
-        b = self.M * 4 + 8
+        gradients read (one, the weighted gradient, with fused_avg), theta
+        read and written, the momentum buffer read and written (if any), the
+        bf16 copy written (if any)."""
+        b = (1 if self.fused_avg else self.M) * 4 + 8
         if self.mom is not None:
             b += 8
         if self.bf16:

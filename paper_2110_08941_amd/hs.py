@@ -52,8 +52,10 @@ def _load():
         "hs_workspace_create": (I32, [P, I32, PP]),
         "hs_workspace_destroy": (I32, [P]),
         "hs_workspace_bytes": (I64, [P]),
+        "hs_workspace_set_streams": (I32, [P, I32]),
         "hs_worker_grad": (I32, [P, P, P, P, P, P, I32, P, P, P]),
         "hs_workers_grad": (I32, [P, P, P, P, P, P, PI32, I32, PP, P, P]),
+        "hs_workers_grad_wavg": (I32, [P, P, P, P, P, P, PI32, I32, P, P, P]),
         "hs_weighted_average": (I32, [PP, PI32, I32, I64, P, P]),
         "hs_sgd_step": (I32, [P, P, P, I64, F, F, F, P, P]),
         "hs_wavg_sgd": (I32, [PP, PI32, I32, P, P, I64, F, F, F, P, P]),
@@ -64,7 +66,7 @@ def _load():
         "hs_partitioner_destroy": (I32, [P]),
         "hs_partitioner_partition": (I32, [P, PI32]),
         "hs_partitioner_set_partition": (I32, [P, PI32]),
-        "hs_partitioner_observe": (I32, [P, PD, PD, PI32, PD]),
+        "hs_partitioner_observe": (I32, [P, PI32, PD, PD, PI32, PD]),
         "hs_partitioner_set_estimator": (I32, [P, I32, ctypes.c_double, I32]),
         "hs_layer_gemm": (I32, [I32, I32, I32, I32, I32, I32, I32, I32, I32, I32, P, P, P, P, I32,
                                 I32, P, I64, P]),
@@ -90,8 +92,10 @@ _lib = _load()
 EXPORTED = (
     "hs_model_create", "hs_model_destroy", "hs_num_params", "hs_num_true_params",
     "hs_num_param_tensors", "hs_param_tensor", "hs_input_numel", "hs_forward_macs",
-    "hs_workspace_create", "hs_workspace_destroy", "hs_workspace_bytes", "hs_worker_grad",
+    "hs_workspace_create", "hs_workspace_destroy", "hs_workspace_bytes",
+    "hs_workspace_set_streams", "hs_worker_grad",
     "hs_workers_grad",
+    "hs_workers_grad_wavg",
     "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
     "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
@@ -178,6 +182,10 @@ def workspace_bytes(ws):
     return int(_lib.hs_workspace_bytes(ws))
 
 
+def workspace_set_streams(ws, streams):
+    _check(_lib.hs_workspace_set_streams(ws, int(streams)))
+
+
 # ---------------------------------------------------------------- step --
 def worker_grad(model, ws, theta, theta_bf16, x_m, y_m, n_m, g_m, loss_m=0, stream=0):
     _check(_lib.hs_worker_grad(model, ws, theta, theta_bf16 or None, x_m, y_m, int(n_m), g_m,
@@ -191,6 +199,13 @@ def workers_grad(model, ws, theta, theta_bf16, x, y, n, g, loss=0, stream=0):
         raise ValueError("workers_grad: one gradient buffer per worker")
     _check(_lib.hs_workers_grad(model, ws, theta, theta_bf16 or None, x, y, _i32(n), len(n),
                                 _ptrs(g), loss or None, stream or None))
+
+
+def workers_grad_wavg(model, ws, theta, theta_bf16, x, y, n, g_bar, loss=0, stream=0):
+    """The partition-weighted gradient sum_m (n_m / sum n) g_m of all workers in
+    one pass, into g_bar (device pointer)."""
+    _check(_lib.hs_workers_grad_wavg(model, ws, theta, theta_bf16 or None, x, y, _i32(n), len(n),
+                                     g_bar, loss or None, stream or None))
 
 
 def weighted_average(g, n, P, g_out, stream=0):
@@ -265,11 +280,13 @@ class Partitioner:
         k = {"window": 0, "ema": 1, "history": 2}[kind]
         _check(_lib.hs_partitioner_set_estimator(self.h, k, float(alpha), int(history)))
 
-    def observe(self, tau, speed):
-        """Returns the CP vector if this step closed a window, else None."""
+    def observe(self, n_used, tau, speed):
+        """Reports one step run with partition n_used; returns the CP vector if
+        this step closed a window, else None."""
         rep = ctypes.c_int32()
         cp = (ctypes.c_double * self.M)()
-        _check(_lib.hs_partitioner_observe(self.h, _f64(tau), _f64(speed), ctypes.byref(rep), cp))
+        _check(_lib.hs_partitioner_observe(self.h, _i32(n_used), _f64(tau), _f64(speed),
+                                           ctypes.byref(rep), cp))
         return list(cp) if rep.value else None
 
     def close(self):

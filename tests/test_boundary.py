@@ -90,7 +90,7 @@ def test_partitioner_matches_oracle_driver_logic():
         for t in range(steps):
             tau = [float(v) for v in rng.uniform(0.5, 5.0, size=m)]
             speed = [float(v) for v in rng.uniform(0.5, 4.0, size=m)]
-            cp = p.observe(tau, speed)
+            cp = p.observe(p.partition(), tau, speed)
             for j in range(m):
                 xsum[j] = xsum[j] + tau[j] / speed[j]
             if (t + 1) % window == 0:
@@ -122,7 +122,7 @@ def test_partitioner_estimators_match_oracle(est):
         for t in range(10 * window):
             tau = [float(v) for v in rng.uniform(0.5, 5.0, size=m)]
             speed = [float(v) for v in rng.uniform(0.5, 4.0, size=m)]
-            cp = p.observe(tau, speed)
+            cp = p.observe(p.partition(), tau, speed)
             for j in range(m):
                 xsum[j] = xsum[j] + tau[j] / speed[j]
             if (t + 1) % window == 0:
@@ -144,14 +144,14 @@ def test_estimator_errors_and_reset():
     # switching estimators clears the carried state: history 2 after a reset
     # equals history 2 from scratch
     p.set_estimator("history", history=2)
-    p.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+    p.observe(p.partition(), [1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
     p.set_estimator("history", history=2)
     q = hs.Partitioner(3, 30, 1)
     q.set_partition(p.partition())
     q.set_estimator("history", history=2)
     for _ in range(3):
-        a = p.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
-        b = q.observe([1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+        a = p.observe(p.partition(), [1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
+        b = q.observe(q.partition(), [1.0, 2.0, 3.0], [1.0, 1.0, 1.0])
         assert a == b
     p.close()
     q.close()
@@ -166,7 +166,7 @@ def test_model_clock_reaches_speed_proportional_partition():
     for t in range(20):
         n = p.partition()
         seen.append(n)
-        p.observe([float(v) for v in n], speeds)
+        p.observe(n, [float(v) for v in n], speeds)
     assert seen[0] == [128] * 4 and seen[4] == [128] * 4
     assert all(s == [64, 64, 128, 256] for s in seen[5:])
 
@@ -188,7 +188,9 @@ def test_error_paths():
         hs.Partitioner(4, 3, 1)
     p = hs.Partitioner(2, 10, 1)
     with pytest.raises(hs.HSError):
-        p.observe([1.0, float("nan")], [1.0, 1.0])
+        p.observe([5, 5], [1.0, float("nan")], [1.0, 1.0])
+    with pytest.raises(hs.HSError):              # a step of another partition
+        p.observe([4, 6], [1.0, 1.0], [1.0, 1.0])
     with pytest.raises(hs.HSError):
         p.set_partition([5, 4])
     assert p.partition() == [5, 5]                 # untouched by the failed calls
@@ -205,3 +207,25 @@ def test_error_paths():
     with pytest.raises(hs.HSError):
         hs.wavg_sgd([16 + 4], [1], 64, 0, 64, 0.1, 0.0, 0.0)  # misaligned gradient
     hs.model_destroy(m)
+
+
+def test_observation_of_another_partition_is_rejected():
+    """An observation must describe a step run with the current partition: one
+    launched before the window's repartition was observed is refused, and the
+    state is unchanged (the next valid observation closes the window as if the
+    refused one never came)."""
+    p = hs.Partitioner(2, 12, 2)
+    q = hs.Partitioner(2, 12, 2)
+    for part in (p, q):
+        part.observe([6, 6], [6.0, 6.0], [1.0, 3.0])
+        assert part.observe([6, 6], [6.0, 6.0], [1.0, 3.0]) is not None
+    assert p.partition() == [3, 9]
+    with pytest.raises(hs.HSError):
+        p.observe([6, 6], [6.0, 6.0], [1.0, 3.0])
+    assert p.partition() == [3, 9]
+    for part in (p, q):
+        part.observe([3, 9], [3.0, 9.0], [1.0, 3.0])
+        assert part.observe([3, 9], [3.0, 9.0], [1.0, 3.0]) is not None
+    assert p.partition() == q.partition() == [3, 9]
+    p.close()
+    q.close()

@@ -11,12 +11,10 @@ from oracle import models as Mo
 from oracle import step as S
 from paper_2110_08941_amd import synth
 from paper_2110_08941_amd.configs import WORKLOADS
-from tests.gpu_util import require_gpu, normwise, log
+from tests.gpu_util import (require_gpu, log, TOL, pertensor, check_pertensor, separate_by_bias,
+                            REALIZATIONS, floor_max)
 
 pytestmark = pytest.mark.gpu
-
-TOL = {"fp32": 1e-4, "bf16": 2e-2}
-STORAGE = {"fp32": "exact", "bf16": "bf16"}
 
 
 def make_trainer(name, total=None, steps=None, clock="model", separated=False, seed=0, **kw):
@@ -34,7 +32,7 @@ def make_trainer(name, total=None, steps=None, clock="model", separated=False, s
     return tr, net, theta
 
 
-@pytest.mark.parametrize("grouped", [False, True])
+@pytest.mark.parametrize("grouped", [False, True, "fused"])
 @pytest.mark.parametrize("name,total,separated", [
     ("mlp_fp32", 256, False),            # the full MLP workload
     ("smallcnn_fp32", 40, False),
@@ -44,11 +42,14 @@ def make_trainer(name, total=None, steps=None, clock="model", separated=False, s
     ("vgg16_bf16", 32, True)])
 def test_one_step(name, total, separated, grouped):
     """theta' - theta after one step (worker gradients -- on their own streams,
-    or all in one pass -- weighted average, momentum SGD) against the oracle's
-    step on the same partition."""
+    all in one pass, or all in one pass forming the weighted gradient itself
+    ("fused") -- weighted average, momentum SGD) against the exact
+    oracle's step on the same partition, per tensor: the bar, or 3 x the
+    error of the oracle's own arithmetic at the workload's precision (theta'
+    stored in fp32) where that exceeds it."""
     log("one step %s N=%d grouped=%s" % (name, total, grouped))
     tr, net, theta = make_trainer(name, total=total, steps=1, separated=separated,
-                                  grouped=grouped)
+                                  grouped=bool(grouped), fused_avg=grouped == "fused")
     try:
         n = tr.part.partition()
         x, y = tr.batch(0)
@@ -60,15 +61,37 @@ def test_one_step(name, total, separated, grouped):
     finally:
         tr.close()
     wl = tr.wl
-    st = STORAGE[wl.dtype]
-    out = S.step(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym, storage=st),
+    table, _ = Mo.param_table(net)
+    out = S.step(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym),
                  theta.astype(np.float64), None, xs, ys, n, wl.lr, wl.mu, wl.wd)
     d_ref = out["theta"] - theta
-    err = normwise(got - theta, d_ref)
-    log("  partition %s  normwise update err %.3e" % (n, err))
-    assert err <= TOL[wl.dtype]
-    assert normwise(got, out["theta"]) <= TOL[wl.dtype]
+    floors = []
+    for k in REALIZATIONS[wl.dtype]:
+        op = S.step(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym, storage=wl.dtype, grid=k),
+                    theta.astype(np.float64), None, xs, ys, n, wl.lr, wl.mu, wl.wd)
+        th32 = op["theta"].astype(np.float32).astype(np.float64)    # fp32 master weights
+        floors.append(pertensor(th32 - theta, d_ref, table))
+    floor = floor_max(floors)
+    log("  partition %s" % n)
+    check_pertensor(got - theta, d_ref, table, TOL[wl.dtype], floor=floor, what="update")
+    check_pertensor(got, out["theta"], table, TOL[wl.dtype], what="theta'")
     np.testing.assert_allclose(gpu_losses, out["losses"], rtol=TOL[wl.dtype], atol=0)
+
+
+def run_floor(net, theta, batches, speeds, wl, d_ref, table, **kw):
+    """Per-tensor error of theta_K - theta_0 that the oracle's driver makes in
+    its own arithmetic at the workload's precision, each step's theta stored
+    in fp32 as the caller's master weights are (the largest over the
+    precision's rounding realizations)."""
+    floors = []
+    for k in REALIZATIONS[wl.dtype]:
+        def worker(th, xm, ym):
+            return Mo.worker_grad(net, th, xm, ym, storage=wl.dtype, grid=k)
+
+        out = S.run(worker, theta.astype(np.float64), batches, speeds, wl.window, wl.lr, wl.mu,
+                    wl.wd, theta_store=lambda t: t.astype(np.float32).astype(np.float64), **kw)
+        floors.append(pertensor(out["theta"] - theta, d_ref, table))
+    return floor_max(floors)
 
 
 def replay(log_entries, M, N, window):
@@ -127,14 +150,22 @@ def test_model_clock_partitions(grouped):
 @pytest.mark.parametrize("grouped", [False, True])
 def test_multistep_theta_small_cnn(grouped):
     """Ten steps of the small CNN workload (reduced to N = 32, repartition
-    every 5 steps with the model clock) against the oracle's driver."""
+    every 5 steps with the model clock) against the oracle's driver.  Over
+    ten steps at He init some ReLU decision lands within fp32 rounding of
+    zero, and either of its outcomes is correct; the biases therefore keep
+    every ReLU input of the ten batches away from zero.  Those biases make
+    the activations and gradients large (tens), where the workload's lr 0.1
+    diverges and 1e-3 moves inputs across zero within a step; at lr 3e-5
+    every decision of the oracle's run keeps a margin above 1e-4 (asserted)."""
     log("multistep small cnn grouped=%s" % grouped)
-    wl = dataclasses.replace(WORKLOADS["smallcnn_fp32"], total=32, window=5, steps=10)
+    wl = dataclasses.replace(WORKLOADS["smallcnn_fp32"], total=32, window=5, steps=10, lr=3e-5)
     require_gpu()
     from paper_2110_08941_amd.driver import Trainer
     net = Mo.build(wl.arch)
     table, P = Mo.param_table(net)
     theta = synth.he_normal(table, P, 0)
+    xs = np.concatenate([synth.batch(wl.in_shape, wl.total, 0, b)[0] for b in range(10)])
+    theta = separate_by_bias(net, theta, xs, table, 0)
     tr = Trainer(wl, seed=0, clock="model", steps=10, theta0=theta, n_batches=10,
                  grouped=grouped)
     try:
@@ -145,12 +176,21 @@ def test_multistep_theta_small_cnn(grouped):
         speeds = tr.speeds
     finally:
         tr.close()
-    out = S.run(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym), theta.astype(np.float64),
-                batches, speeds, wl.window, wl.lr, wl.mu, wl.wd)
+    margins = []
+
+    def worker(th, xm, ym):
+        ctx = Mo.Ctx("exact")
+        r = Mo.worker_grad(net, th, xm, ym, ctx=ctx)
+        margins.append(min(m[1][0] for m in ctx.margins if m[0] == "relu" and m[1].size))
+        return r
+
+    out = S.run(worker, theta.astype(np.float64), batches, speeds, wl.window, wl.lr, wl.mu, wl.wd)
     assert used == out["partitions"]
-    err = normwise(got - theta, out["theta"] - theta)
-    log("  partitions %s ... %s, normwise err %.3e" % (used[0], used[-1], err))
-    assert err <= TOL["fp32"]
+    log("  partitions %s ... %s; min relu margin %.1e" % (used[0], used[-1], min(margins)))
+    assert min(margins) > 1e-4
+    check_pertensor(got - theta, out["theta"] - theta, table, TOL["fp32"],
+                    floor=run_floor(net, theta, batches, speeds, wl, out["theta"] - theta, table),
+                    what="update over 10 steps")
 
 
 @pytest.mark.parametrize("grouped", [False, True])
@@ -160,8 +200,9 @@ def test_multistep_theta_bf16_resnet(name, grouped):
     separated decisions, lr 0.01 so that they stay separated, momentum and
     weight decay) on one workspace per worker: the later calls take the
     packed weights prepared on the second stream and run the weight
-    gradients there.  The update theta_4 - theta_0 against the oracle's
-    driver with bf16 storage, within the bf16 bar."""
+    gradients there.  The update theta_4 - theta_0 against the exact oracle's
+    driver, per tensor: the bf16 bar, or 3 x the error of the oracle's own
+    bf16 arithmetic over the same steps where that exceeds it."""
     log("multistep %s grouped=%s" % (name, grouped))
     wl = dataclasses.replace(WORKLOADS[name], total=24, steps=4, drift_sigma=0.0, lr=0.01)
     require_gpu()
@@ -178,12 +219,13 @@ def test_multistep_theta_bf16_resnet(name, grouped):
         speeds = tr.speeds
     finally:
         tr.close()
-    out = S.run(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym, storage="bf16"),
+    out = S.run(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym),
                 theta.astype(np.float64), batches, speeds, wl.window, wl.lr, wl.mu, wl.wd)
     assert used == out["partitions"]
-    err = normwise(got - theta, out["theta"] - theta)
-    log("  partitions %s, normwise err of the update %.3e" % (used[0], err))
-    assert err <= TOL["bf16"]
+    log("  partitions %s" % used[0])
+    check_pertensor(got - theta, out["theta"] - theta, table, TOL["bf16"],
+                    floor=run_floor(net, theta, batches, speeds, wl, out["theta"] - theta, table),
+                    what="update over 4 steps")
 
 
 MODES = {
@@ -239,9 +281,13 @@ def test_multistep_modes_small_cnn(mode, grouped):
         assert used == [[8, 8, 8, 8]] * 10
     else:
         assert used[-1] != [8, 8, 8, 8]
-    err = normwise(got - theta, out["theta"] - theta)
-    log("  partitions %s ... %s, normwise err %.3e" % (used[0], used[-1], err))
-    assert err <= TOL["fp32"]
+    log("  partitions %s ... %s" % (used[0], used[-1]))
+    floor = run_floor(net, theta, batches, speeds, wl, out["theta"] - theta, table,
+                      exchange=cfg["exchange"], delays=delays,
+                      estimator=cfg.get("estimator", ("window",)),
+                      lr_total=sched[1] if sched else None, lr_min=sched[2] if sched else 0.0)
+    check_pertensor(got - theta, out["theta"] - theta, table, TOL["fp32"], floor=floor,
+                    what="update over 10 steps")
 
 
 def test_full_size_weighted_average_invariant():
@@ -264,8 +310,42 @@ def test_full_size_weighted_average_invariant():
                        full.data_ptr(), 0, 0)
         torch.cuda.synchronize()
         hs.workspace_destroy(ws)
-        err = normwise(gbar.cpu().numpy(), full.cpu().numpy())
+        gb, gf = gbar.cpu().numpy(), full.cpu().numpy()
     finally:
         tr.close()
-    log("  partition %s normwise err %.3e" % (n, err))
-    assert err <= TOL["fp32"]
+    log("  partition %s" % n)
+    check_pertensor(gb, gf, Mo.param_table(Mo.build("small_cnn"))[0], TOL["fp32"],
+                    what="weighted average vs full batch")
+
+
+@pytest.mark.parametrize("grouped", [False, True])
+def test_model_clock_partitions_with_flush_mid_window(grouped):
+    """The benchmark's order of calls -- 5 warm-up steps, a flush of the
+    pending observations in the middle of a 10-step window, then 20 steps --
+    with the drifting speeds of the ResNet-18 bf16 workload (8 workers, sigma
+    0.05) on the small CNN at N = 64, model clock: the partition of every step
+    equals Algorithm 1 run by the oracle on the same speeds (the first
+    repartition applies from step 10, each window's estimate uses only steps
+    run with that window's partition)."""
+    require_gpu()
+    from paper_2110_08941_amd.driver import Trainer
+    log("model clock with a mid-window flush grouped=%s" % grouped)
+    wl = dataclasses.replace(WORKLOADS["resnet18_bf16"], arch="small_cnn", dtype="fp32",
+                             total=64, steps=25)
+    tr = Trainer(wl, seed=3, clock="model", steps=25, n_batches=1, grouped=grouped)
+    try:
+        for _ in range(5):
+            tr.step()
+        tr.flush()
+        for _ in range(20):
+            tr.step()
+        tr.flush()
+        used = [e["n"] for e in tr.log]
+        speeds = tr.speeds
+    finally:
+        tr.close()
+    zeros = lambda th, xm, ym: (0.0, np.zeros(1))
+    out = S.run(zeros, np.zeros(1), [(np.zeros((64, 1)), np.zeros(64, dtype=np.int32))] * 25,
+                speeds[:25], wl.window, wl.lr, 0.0, 0.0)
+    assert used == out["partitions"]
+    assert used[9] == [8] * 8 and used[10] != used[9]

@@ -69,21 +69,62 @@ def test_finite_differences(arch):
 # ----------------------------------------------------------------------------
 # independent float64 implementation with torch autograd
 # ----------------------------------------------------------------------------
-def torch_forward(net, p, x):
-    """Run `net` with torch ops; p maps names to torch tensors."""
-    def run(mod, h):
-        if isinstance(mod, Mo.Sequential):
-            for m in mod.mods:
-                h = run(m, h)
-            return h
-        if isinstance(mod, Mo.BasicBlock):
-            a = run(mod.main, h)
-            s = run(mod.short, h) if mod.short else h
-            return F.relu(a + s)
+def _rounder(kind):
+    """Rounding to bf16 (via float32, ties to even) or float32, in float64."""
+    if kind == "bf16":
+        return lambda t: t.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    return lambda t: t.to(torch.float32).to(torch.float64)
+
+
+def _rounding_functions(kind):
+    """Three autograd functions rounding to `kind`: the forward value only,
+    the gradient only, or neither (kind None)."""
+    if kind is None:
+        ident = lambda t: t
+        return ident, ident
+    rnd = _rounder(kind)
+
+    class ForwardOnly(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, x):
+            return rnd(x)
+
+        @staticmethod
+        def backward(ctx, g):
+            return g
+
+    class GradientOnly(torch.autograd.Function):
+        @staticmethod
+        def forward(ctx, x):
+            return x.view_as(x)
+
+        @staticmethod
+        def backward(ctx, g):
+            return rnd(g)
+
+    return ForwardOnly.apply, GradientOnly.apply
+
+
+def torch_forward(net, p, x, mode=None):
+    """Run `net` with torch ops; p maps names to torch tensors.  mode (the
+    oracle's bf16 modes, written independently): "operands" -- every
+    convolution and linear contraction reads bf16-rounded operands (inputs and
+    weights forward, the output gradient backward; the bias is added after the
+    contraction, so its gradient is the unrounded one); "bf16" -- the same,
+    and every layer's output (forward) and input gradient (backward) rounded
+    to bf16, residual blocks included."""
+    op_kind = {"operands": "bf16", "bf16": "bf16"}.get(mode)
+    st_kind = mode if mode == "bf16" else None
+    R, G = _rounding_functions(op_kind)          # contraction operands
+    SF, SG = _rounding_functions(st_kind)        # tensors between layers
+
+    def leaf(mod, h):
         if isinstance(mod, Mo.Conv):
-            w = p[mod.name + ".weight"].permute(0, 3, 1, 2)      # OHWI -> OIHW
-            b = p[mod.name + ".bias"] if mod.bias else None
-            return F.conv2d(h, w, b, stride=mod.stride, padding=mod.pad)
+            w = R(p[mod.name + ".weight"]).permute(0, 3, 1, 2)      # OHWI -> OIHW
+            out = G(F.conv2d(R(h), w, None, stride=mod.stride, padding=mod.pad))
+            if mod.bias:
+                out = out + p[mod.name + ".bias"].view(1, -1, 1, 1)
+            return out
         if isinstance(mod, Mo.BatchNorm):
             return F.batch_norm(h, None, None, p[mod.name + ".gamma"], p[mod.name + ".beta"],
                                 training=True, eps=1e-5)
@@ -96,23 +137,36 @@ def torch_forward(net, p, x):
         if isinstance(mod, Mo.Flatten):
             return h.reshape(h.shape[0], -1)
         if isinstance(mod, Mo.Linear):
-            return F.linear(h, p[mod.name + ".weight"], p[mod.name + ".bias"])
+            return G(F.linear(R(h), R(p[mod.name + ".weight"]))) + p[mod.name + ".bias"]
         raise TypeError(mod)
+
+    def run(mod, h):
+        if isinstance(mod, Mo.Sequential):
+            for m in mod.mods:
+                h = run(m, h)
+            return h
+        h = SG(h)          # this layer's input gradient is stored
+        if isinstance(mod, Mo.BasicBlock):
+            a = run(mod.main, h)
+            s = run(mod.short, h) if mod.short else h
+            return SF(F.relu(a + s))
+        return SF(leaf(mod, h))
+
     return run(net, x)
 
 
-def torch_grad(net, table, total, theta, x, y):
+def torch_grad(net, table, total, theta, x, y, mode=None, dtype=torch.float64):
     p = {}
     for name, kind, shape, off in table:
         p[name] = torch.tensor(theta[off:off + int(np.prod(shape))].reshape(shape),
-                               dtype=torch.float64, requires_grad=True)
-    logits = torch_forward(net, p, torch.tensor(x, dtype=torch.float64))
+                               dtype=dtype, requires_grad=True)
+    logits = torch_forward(net, p, torch.tensor(x, dtype=dtype), mode)
     loss = F.cross_entropy(logits, torch.tensor(y, dtype=torch.int64))
     loss.backward()
     loss = loss.detach()
     g = np.zeros(total)
     for name, kind, shape, off in table:
-        g[off:off + int(np.prod(shape))] = p[name].grad.numpy().ravel()
+        g[off:off + int(np.prod(shape))] = p[name].grad.double().numpy().ravel()
     return float(loss), g
 
 
@@ -271,7 +325,7 @@ def test_pins_catch_planted_mistakes(monkeypatch, mutation):
 
 
 def test_bf16_round_matches_torch():
-    """Round-to-nearest-even bf16 of the storage emulation against torch's
+    """Round-to-nearest-even bf16 of the operand rounding against torch's
     float32 -> bfloat16 conversion (ties, subnormals, large values)."""
     from oracle import layers as L
     rng = np.random.default_rng(12)
@@ -282,16 +336,76 @@ def test_bf16_round_matches_torch():
     np.testing.assert_array_equal(L.bf16_round(x), ref)
 
 
-def test_storage_emulation_and_decision_toggles():
-    """bf16 storage stays close to the exact gradient on a network without
-    batch-norm; toggling a listed ambiguous ReLU decision changes the gradient
-    only along that decision's direction; exact storage lists no decision with
-    a margin above the capture threshold."""
+@pytest.mark.parametrize("arch", sorted(TINY))
+def test_fp32_mode_against_torch_float32(arch):
+    """The oracle's fp32 mode is float32 arithmetic: it agrees with torch's
+    float32 autograd of the same network, and with the exact gradient, to
+    float32 accuracy, and differs from the exact one."""
+    kw, in_shape, n = TINY[arch]
+    net, table, total, theta, x, y = rand_problem(arch, kw, in_shape, n, seed=23)
+    loss, g = Mo.worker_grad(net, theta, x, y, storage="fp32")
+    tl, tg = torch_grad(net, table, total, theta, x, y, dtype=torch.float32)
+    _, ge = Mo.worker_grad(net, theta, x, y)
+    scale = np.max(np.abs(ge))
+    assert abs(loss - tl) < 1e-5 * max(1.0, abs(tl))
+    assert np.max(np.abs(g - tg)) <= 1e-5 * scale
+    assert 0 < np.max(np.abs(g - ge)) <= 1e-5 * scale
+
+
+def test_rounding_realizations():
+    """Another realization of the bf16 rounding (Ctx grid = k > 0) keeps
+    bf16's relative error bound (2^-8) on every value and places the errors
+    elsewhere: a different result from the same inputs, reproducible per k;
+    grid 0 is plain round-to-nearest-even."""
+    from oracle import layers as L
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(200000) * 10.0 ** rng.integers(-8, 8, 200000)
+    np.testing.assert_array_equal(Mo.Ctx("bf16").bf16(x), L.bf16_round(x))
+    a = Mo.Ctx("bf16", grid=3).bf16(x)
+    b = Mo.Ctx("bf16", grid=3).bf16(x)
+    c = Mo.Ctx("bf16", grid=4).bf16(x)
+    np.testing.assert_array_equal(a, b)
+    assert np.all(np.abs(a - x) <= 2.0 ** -8 * np.abs(x))
+    assert np.mean(a != L.bf16_round(x)) > 0.2 and np.mean(a != c) > 0.2
+    # error statistics of a realization match plain rounding's
+    e0 = np.abs(L.bf16_round(x) - x) / np.abs(x)
+    e1 = np.abs(a - x) / np.abs(x)
+    assert 0.7 < np.mean(e1) / np.mean(e0) < 1.3
+    kw, in_shape, n = TINY["small_cnn"]
+    net, table, total, theta, x, y = rand_problem("small_cnn", kw, in_shape, n, seed=23)
+    _, ge = Mo.worker_grad(net, theta, x, y)
+    _, g0 = Mo.worker_grad(net, theta, x, y, storage="bf16")
+    _, g1 = Mo.worker_grad(net, theta, x, y, storage="bf16", grid=1)
+    scale = np.max(np.abs(ge))
+    assert np.max(np.abs(g0 - g1)) > 0
+    assert np.max(np.abs(g1 - ge)) < 20 * max(np.max(np.abs(g0 - ge)), 1e-6 * scale)
+
+
+@pytest.mark.parametrize("mode", ["operands", "bf16"])
+@pytest.mark.parametrize("arch", sorted(TINY))
+def test_rounding_modes_against_torch(arch, mode):
+    """The oracle's bf16 modes against an independent torch autograd
+    implementation that rounds the same values with autograd functions
+    (forward value only, gradient only) around each contraction and each
+    layer."""
+    kw, in_shape, n = TINY[arch]
+    net, table, total, theta, x, y = rand_problem(arch, kw, in_shape, n, seed=23)
+    loss, g = Mo.worker_grad(net, theta, x, y, storage=mode)
+    tl, tg = torch_grad(net, table, total, theta, x, y, mode=mode)
+    assert abs(loss - tl) < 1e-12 * max(1.0, abs(tl))
+    assert np.max(np.abs(g - tg)) <= 1e-11 * np.max(np.abs(tg))
+    # the rounding is really applied: the exact gradient differs
+    _, ge = Mo.worker_grad(net, theta, x, y)
+    assert np.max(np.abs(g - ge)) > 1e-6 * np.max(np.abs(ge))
+
+
+def test_decision_toggles():
+    """Toggling a listed ambiguous ReLU decision changes the gradient only
+    along that decision's direction; toggles are a set; every listed decision
+    has a margin below the capture threshold."""
     kw, in_shape, n = TINY["small_cnn"]
     net, table, total, theta, x, y = rand_problem("small_cnn", kw, in_shape, 6, seed=61)
     _, ge = Mo.worker_grad(net, theta, x, y)
-    _, gb = Mo.worker_grad(net, theta, x, y, storage="bf16")
-    assert 0 < np.max(np.abs(gb - ge)) <= 5e-2 * np.max(np.abs(ge))
     ctx = Mo.Ctx("exact", capture=0.05)
     _, g0 = Mo.worker_grad(net, theta, x, y, ctx=ctx)
     assert np.array_equal(g0, ge)
@@ -419,3 +533,35 @@ def test_resnet50_matches_independent_torch_modules():
         gt = gt.transpose(0, 2, 3, 1) if gt.ndim == 4 else gt
         np.testing.assert_allclose(g[off:off + int(np.prod(shape))].reshape(shape), gt,
                                    rtol=0, atol=1e-11 * scale, err_msg=nm)
+
+
+def test_bf16_operand_floor():
+    """How far bf16 arithmetic alone moves the gradient from the exact one
+    (the reason the bf16 GPU tests bound a tensor by 3 x this floor where it
+    exceeds 2e-2).  Rounding only the contraction operands to bf16 keeps every
+    tensor of the small CNN within 2e-2 of the exact gradient, but moves most
+    tensors of the full-width ResNet-18 by more than that, with every ReLU
+    decision far from zero (separated batch-norm parameters): through the deep
+    batch-norm chain the rounding of the always-on channels' large-mean
+    activations is amplified, and batch-norm shift gradients are small residues
+    of cancelling sums."""
+    from paper_2110_08941_amd import synth
+    from tests.gpu_util import pertensor, separate_by_bias
+    out = {}
+    for arch, n in (("small_cnn", 8), ("resnet18", 4)):
+        net = Mo.build(arch)
+        table, total = Mo.param_table(net)
+        theta = synth.he_normal(table, total, n)
+        x, y = synth.batch((3, 32, 32), n, n, 1)
+        if arch == "small_cnn":
+            theta = separate_by_bias(net, theta, x, table, n)
+        else:
+            theta = synth.separate_decisions(table, theta, n)
+        th = theta.astype(np.float64)
+        ctx = Mo.Ctx("exact")
+        _, ge = Mo.worker_grad(net, th, x, y, ctx=ctx)
+        assert min(m[1][0] for m in ctx.margins if m[0] == "relu" and m[1].size) > 1e-4
+        _, go = Mo.worker_grad(net, th, x, y, storage="operands")
+        out[arch] = [e for _, e, _ in pertensor(go, ge, table)]
+    assert max(out["small_cnn"]) <= 2e-2
+    assert sum(e > 2e-2 for e in out["resnet18"]) > len(out["resnet18"]) // 2

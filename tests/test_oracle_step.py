@@ -167,6 +167,29 @@ def test_sgd_closed_form():
     np.testing.assert_allclose(t0, th - lr * g1, rtol=0, atol=1e-15)
 
 
+def test_sgd_against_torch_optim():
+    """Three momentum steps of the oracle's SGD against torch.optim.SGD with the
+    Section 5 hyper-parameters (momentum 0.9, weight decay 5e-4, lr 0.1; no
+    dampening, no Nesterov), float64, on changing gradients; also plain SGD."""
+    import torch
+    rng = np.random.default_rng(14)
+    for mu, wd in ((0.9, 5e-4), (0.0, 0.0), (0.9, 0.0), (0.0, 5e-4)):
+        th0 = rng.standard_normal(257)
+        grads = [rng.standard_normal(257) for _ in range(3)]
+        p = torch.nn.Parameter(torch.tensor(th0, dtype=torch.float64))
+        opt = torch.optim.SGD([p], lr=0.1, momentum=mu, weight_decay=wd, dampening=0.0,
+                              nesterov=False)
+        th, buf = th0.copy(), None
+        for g in grads:
+            p.grad = torch.tensor(g, dtype=torch.float64)
+            opt.step()
+            th, buf = S.sgd_step(th, g, buf, 0.1, mu, wd)
+            np.testing.assert_allclose(th, p.detach().numpy(), rtol=0, atol=1e-14)
+            if mu != 0.0:
+                np.testing.assert_allclose(buf, opt.state[p]["momentum_buffer"].numpy(),
+                                           rtol=0, atol=1e-14)
+
+
 # ----------------------------------------------------------------------------
 # Sync-SGD / DP-SGD exchange, estimators across windows, cosine schedule,
 # additive delays (Section 5 comparison)
