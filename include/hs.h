@@ -170,6 +170,34 @@ hs_status hs_workers_grad_wavg(const hs_model* model, hs_workspace* ws, const fl
                                const int32_t* n, int32_t M, float* g_bar, float* loss,
                                void* stream);
 
+/* hs_workers_grad without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, allocation-free serving loops,
+ * harnesses that forbid hipMalloc.  It calls no hipMalloc, hipFree or other
+ * allocating routine; its scratch (activations, batch-norm statistics,
+ * split-K partials, packed weights) is a static device buffer of
+ * HS_STATIC_SCRATCH_BYTES that every GPU the library runs on holds until the
+ * process ends.  Arguments, results and errors as hs_workers_grad, except:
+ *   - sum n is limited by that buffer: a call whose layout needs more returns
+ *     HS_ERR_INVALID, with the bytes needed in hs_last_error(), before any
+ *     launch (hs_workers_grad_static_bytes gives the need: the MLP fits over
+ *     5000 samples, the small CNN 62 in fp32 and 124 in bf16, ResNet-18 and
+ *     VGG-16 5 in bf16, ResNet-50 bf16 none);
+ *   - every launch is on `stream` (no second stream), and the split-K
+ *     partial buffer is at its minimum, so the weight-gradient sums may be
+ *     split differently from a workspace call (fp32 rounding differences);
+ *   - all calls on one GPU share its buffer, which keeps the last call's
+ *     contents (each call writes what it reads): calls that overlap on one
+ *     GPU -- on different streams, or from different host threads without
+ *     ordering -- race and give undefined results; serialize them. */
+#define HS_STATIC_SCRATCH_BYTES (128LL << 20)
+hs_status hs_workers_grad_static(const hs_model* model, const float* theta,
+                                 const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                                 const int32_t* n, int32_t M, float* const* g, float* loss,
+                                 void* stream);
+/* Scratch bytes hs_workers_grad_static needs for total_n samples of the model
+ * (host only), or -1 for a NULL model or total_n outside 1..16384. */
+int64_t hs_workers_grad_static_bytes(const hs_model* model, int32_t total_n);
+
 /* Partition-weighted gradient (Section 4.2):
  *   g_out[i] = sum_{m<M} w_m g[m][i],  w_m = n[m] / sum_j n[j]  (computed in
  *   double, applied in fp32, summed in worker order).

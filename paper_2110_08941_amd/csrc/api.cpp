@@ -313,6 +313,54 @@ hs_status hs_workers_grad_wavg(const hs_model* model, hs_workspace* ws, const fl
   return ok();
 }
 
+// ------------------------------------------ the allocation-free variant --
+// The workspace of hs_workers_grad_static is laid out per call in the static
+// device buffer of static_scratch.hip: the split-K partial buffer at its
+// minimum (one split per worker of the largest weight gradient), one stream,
+// the padding ranges of g zeroed from the model's host list by value.
+static int64_t static_plan_bytes(const Model& m, int total) {
+  Workspace w;
+  return plan_workspace(m, total, &w, 0);
+}
+
+int64_t hs_workers_grad_static_bytes(const hs_model* model, int32_t total_n) {
+  if (!model || total_n < 1 || total_n > 16384) return -1;
+  return static_plan_bytes(model->m, total_n);
+}
+
+hs_status hs_workers_grad_static(const hs_model* model, const float* theta,
+                                 const uint16_t* theta_bf16, const float* x, const int32_t* y,
+                                 const int32_t* n, int32_t M, float* const* g, float* loss,
+                                 void* stream) {
+  int nn[MAX_SEG];
+  int64_t total = 0;
+  hs_status st = check_workers("hs_workers_grad_static", model, theta, theta_bf16, x, y, n, M, g,
+                               nn, &total);
+  if (st != HS_OK) return st;
+  if (total > 16384)
+    return fail(HS_ERR_INVALID, "hs_workers_grad_static: sum of n = %lld exceeds 16384",
+                (long long)total);
+  const int64_t need = static_plan_bytes(model->m, (int)total);
+  if (need > HS_STATIC_SCRATCH_BYTES)
+    return fail(HS_ERR_INVALID,
+                "hs_workers_grad_static: %lld samples of this model need %lld bytes of scratch, "
+                "the static buffer holds %lld (use hs_workers_grad with a workspace)",
+                (long long)total, (long long)need, (long long)HS_STATIC_SCRATCH_BYTES);
+  void* scratch = nullptr;
+  hipError_t e = static_scratch(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "hs_workers_grad_static: static scratch address");
+  Workspace w;
+  w.model = &model->m;
+  w.max_n = (int)total;
+  w.arena = (char*)scratch;
+  w.bytes = plan_workspace(model->m, (int)total, &w, 0);
+  w.side = nullptr;
+  w.gaps_by_value = true;
+  e = workers_grad(model->m, w, theta, theta_bf16, x, y, nn, M, g, loss, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_workers_grad_static");
+  return ok();
+}
+
 static hs_status check_wavg(const float* const* g, const int32_t* n, int32_t M, int64_t P,
                             float* w) {
   if (!g || !n) return fail(HS_ERR_INVALID, "weighted average: g and n must not be NULL");

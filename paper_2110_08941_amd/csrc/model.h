@@ -138,6 +138,10 @@ hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
                         int M, float* const* g, float* loss, hipStream_t s,
                         float* gbar = nullptr, const float* w = nullptr);
 
+// Address of this device's static scratch buffer (static_scratch.hip),
+// HS_STATIC_SCRATCH_BYTES bytes; looked up once per device.
+hipError_t static_scratch(void** ptr);
+
 // One layer contraction (mode 0 forward, 1 data gradient, 2 weight gradient)
 // with the schedule hs_worker_grad uses.
 hipError_t layer_gemm(int mode, bool bf16, const ConvL& L, int n, const void* a, const void* b,

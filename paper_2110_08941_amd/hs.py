@@ -55,7 +55,9 @@ def _load():
         "hs_workspace_set_streams": (I32, [P, I32]),
         "hs_worker_grad": (I32, [P, P, P, P, P, P, I32, P, P, P]),
         "hs_workers_grad": (I32, [P, P, P, P, P, P, PI32, I32, PP, P, P]),
+        "hs_workers_grad_static": (I32, [P, P, P, P, P, PI32, I32, PP, P, P]),
         "hs_workers_grad_wavg": (I32, [P, P, P, P, P, P, PI32, I32, P, P, P]),
+        "hs_workers_grad_static_bytes": (I64, [P, I32]),
         "hs_weighted_average": (I32, [PP, PI32, I32, I64, P, P]),
         "hs_sgd_step": (I32, [P, P, P, I64, F, F, F, P, P]),
         "hs_wavg_sgd": (I32, [PP, PI32, I32, P, P, I64, F, F, F, P, P]),
@@ -94,7 +96,7 @@ EXPORTED = (
     "hs_num_param_tensors", "hs_param_tensor", "hs_input_numel", "hs_forward_macs",
     "hs_workspace_create", "hs_workspace_destroy", "hs_workspace_bytes",
     "hs_workspace_set_streams", "hs_worker_grad",
-    "hs_workers_grad",
+    "hs_workers_grad", "hs_workers_grad_static", "hs_workers_grad_static_bytes",
     "hs_workers_grad_wavg",
     "hs_weighted_average", "hs_sgd_step", "hs_wavg_sgd", "hs_params_to_bf16", "hs_estimate_cp",
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
@@ -206,6 +208,18 @@ def workers_grad_wavg(model, ws, theta, theta_bf16, x, y, n, g_bar, loss=0, stre
     one pass, into g_bar (device pointer)."""
     _check(_lib.hs_workers_grad_wavg(model, ws, theta, theta_bf16 or None, x, y, _i32(n), len(n),
                                      g_bar, loss or None, stream or None))
+
+
+def workers_grad_static(model, theta, theta_bf16, x, y, n, g, loss=0, stream=0):
+    """workers_grad without a workspace (the library's static device buffer)."""
+    if len(g) != len(n):
+        raise ValueError("workers_grad_static: one gradient buffer per worker")
+    _check(_lib.hs_workers_grad_static(model, theta, theta_bf16 or None, x, y, _i32(n), len(n),
+                                       _ptrs(g), loss or None, stream or None))
+
+
+def workers_grad_static_bytes(model, total_n):
+    return int(_lib.hs_workers_grad_static_bytes(model, int(total_n)))
 
 
 def weighted_average(g, n, P, g_out, stream=0):
