@@ -23,11 +23,13 @@ def bf16_round(x):
     """Nearest bf16 value (8-bit significand), ties to even, of each entry:
     the value is first rounded to float32, then its low 16 bits are rounded
     away; returned as float64."""
-    f = np.asarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    u = ((u + 0x7FFF + lsb) >> 16) << 16
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+    f = np.array(x, dtype=np.float32)
+    u = f.view(np.uint32)
+    lsb = (u >> 16) & np.uint32(1)
+    u += np.uint32(0x7FFF)
+    u += lsb
+    u &= np.uint32(0xFFFF0000)
+    return f.astype(np.float64)
 
 
 # ----------------------------------------------------------------------------

@@ -95,8 +95,12 @@ def oracle_floor(net, theta, x, y, table, exact, dtype):
     over the precision's rounding realizations."""
     from oracle import models as Mo
     th = np.asarray(theta, dtype=np.float64)
-    return floor_max([pertensor(Mo.worker_grad(net, th, x, y, storage=dtype, grid=k)[1],
-                                exact, table) for k in REALIZATIONS[dtype]])
+    out = []
+    for k in REALIZATIONS[dtype]:
+        out.append(pertensor(Mo.worker_grad(net, th, x, y, storage=dtype, grid=k)[1], exact, table))
+        if len(y) > 64:
+            log("    floor realization %d of %d done (n=%d)" % (k + 1, len(REALIZATIONS[dtype]), len(y)))
+    return floor_max(out)
 
 
 def check_pertensor(a, b, table, tol, floor=None, what=""):
@@ -121,8 +125,8 @@ def check_pertensor(a, b, table, tol, floor=None, what=""):
     if floor is not None:
         fw = max(floor, key=lambda r: r[1])
         above = sum(1 for _, e, _ in floor if FLOOR_FACTOR * e > tol)
-        ratio = max(((e / fl[name]) if fl.get(name, 0.0) > 0 else 0.0, name)
-                    for name, e, _ in errs)
+        ratio = max([(e / fl[name], name) for name, e, _ in errs
+                     if FLOOR_FACTOR * fl.get(name, 0.0) > tol] or [(0.0, "-")])
         msg += ("; oracle floor worst %s %.3e, %d tensors bounded by 3x floor; "
                 "largest error/floor %.2f (%s)" % (fw[0], fw[1], above, ratio[0], ratio[1]))
     log("  " + msg)

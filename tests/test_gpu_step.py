@@ -193,8 +193,8 @@ def test_multistep_theta_small_cnn(grouped):
                     what="update over 10 steps")
 
 
-@pytest.mark.parametrize("grouped", [False, True])
-@pytest.mark.parametrize("name", ["resnet18_bf16", "resnet50_bf16"])
+@pytest.mark.parametrize("name,grouped", [("resnet18_bf16", False), ("resnet18_bf16", True),
+                                          ("resnet50_bf16", True)])
 def test_multistep_theta_bf16_resnet(name, grouped):
     """Four steps of a bf16 ResNet workload (N = 24 over its 8 workers,
     separated decisions, lr 0.01 so that they stay separated, momentum and

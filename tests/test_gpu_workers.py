@@ -6,23 +6,25 @@ exact oracle, and against separate hs_worker_grad calls.
 Error measure, tolerances and decision regimes are those of
 test_gpu_worker.py: per parameter tensor against the exact float64 oracle,
 1e-4 (fp32) / 2e-2 (bf16), or 3 x the oracle's own error at the path's
-precision on a tensor where that floor exceeds the bar.  The workload configurations are checked at
-their own sizes: every worker of the ResNet-18 bf16 (N = 2048) and fp32
-(N = 1024) workloads, the smallest and the largest worker of the VGG-16
-workload (N = 4096), every worker of the small-CNN workload (N = 512).
-Every case prints its name before it runs."""
-import dataclasses
+precision on a tensor where that floor exceeds the bar.  The workload
+configurations are checked at their own sizes against stored oracle values
+(tests/fullsize.py) on sampled entries: every worker of the ResNet-18 bf16
+(N = 2048) and fp32 (N = 1024) workloads, the smallest and the largest worker
+of the VGG-16 workload (N = 4096), every worker of the small-CNN workload
+(N = 512), the two smallest of ResNet-50 (N = 1024).  Every case prints its
+name before it runs."""
+import os
 
 import numpy as np
 import pytest
 import torch
 
 from oracle import models as Mo
-from oracle import step as S
 from paper_2110_08941_amd import synth
 from paper_2110_08941_amd.configs import WORKLOADS
-from tests.gpu_util import (require_gpu, log, TOL, pertensor, check_pertensor,
-                            separate_by_bias, oracle_floor, REALIZATIONS, floor_max)
+from tests import fullsize as F
+from tests.gpu_util import (require_gpu, log, TOL, FLOOR_FACTOR, pertensor, check_pertensor,
+                            separate_by_bias, oracle_floor, floor_max)
 from tests.test_gpu_worker import decision_aware, check_padding, AMBIGUOUS
 
 pytestmark = pytest.mark.gpu
@@ -181,7 +183,9 @@ def test_workers_grad_equals_separate_calls(arch, dtype, n):
     the path's precision for that worker where that exceeds it.  The last case
     puts several one-sample workers into one block of the 64-channel forward
     kernel, whose epilogue sums the batch-norm statistics per worker (N = 768:
-    1536 half-image tiles over 256 blocks)."""
+    1536 half-image tiles over 256 blocks); its 761-sample worker (a float64
+    oracle pass over it takes minutes) is bounded by twice the largest floor
+    of the others, as two computations each within 3x the floor of exact."""
     log("workers_grad vs worker_grad %s %s n=%s" % (arch, dtype, n))
     net = Mo.build(arch)
     table, P = Mo.param_table(net)
@@ -189,9 +193,12 @@ def test_workers_grad_equals_separate_calls(arch, dtype, n):
     x, y = synth.batch((3, 32, 32), sum(n), 3, 1)
     ga, la = run_workers(arch, dtype, n, theta, x, y)
     gb, lb = run_workers(arch, dtype, n, theta, x, y, separate=True)
-    refs = exact_refs(net, table, theta, x, y, n, dtype, log_margin=False)
+    small = [i for i in range(len(n)) if n[i] <= 64]
+    refs = exact_refs(net, table, theta, x, y, n, dtype, workers=small, log_margin=False)
+    fmax = floor_max([refs[i][4] for i in small])
+    pair = [(name, 2.0 * e, sc) for name, e, sc in fmax]
     for i in range(len(n)):
-        check_pertensor(ga[i], gb[i], table, TOL[dtype], floor=refs[i][4],
+        check_pertensor(ga[i], gb[i], table, TOL[dtype], floor=refs[i][4] if i in refs else pair,
                         what="worker %d one pass vs separate" % i)
     np.testing.assert_allclose(la, lb, rtol=TOL[dtype])
 
@@ -210,115 +217,111 @@ def test_workers_grad_deterministic():
 
 
 # ---------------------------------------------------------------------------
-# the workload configurations at their own sizes
+# the workload configurations at their own sizes (stored oracle values)
 # ---------------------------------------------------------------------------
-FULL_SIZE = [
-    # ResNet-18 bf16, N = 2048 over 8 workers: a partition the benchmark's
-    # drifting speeds reach (all eight workers against the oracle)
-    ("resnet18", "bf16", [52, 48, 49, 113, 119, 247, 177, 1243], None),
-    # ResNet-18 fp32, N = 1024, speeds 1:1.5:2:3.5
-    ("resnet18", "fp32", [128, 192, 256, 448], None),
-    # VGG-16 bf16, N = 4096, speeds 1:1:1:2:2:4:4:8: the smallest and the
-    # largest worker against the oracle
-    ("vgg16", "bf16", [178, 178, 178, 356, 356, 713, 712, 1425], (0, 7)),
-    # small CNN fp32, N = 512 at the partition of speeds 1:1:2:4
-    ("small_cnn", "fp32", [64, 64, 128, 256], None),
-    # ResNet-50 bf16, N = 1024 over 8 workers: the two smallest workers
-    # against the oracle (a float64 pass over the largest takes minutes)
-    ("resnet50", "bf16", [26, 24, 25, 56, 60, 123, 89, 621], (0, 1)),
-]
+def load_golden(name):
+    path = F.path(name)
+    assert os.path.exists(path), "%s missing: python -m tests.golden.make_fullsize %s" % (path, name)
+    return np.load(path)
 
 
-@pytest.mark.parametrize("arch,dtype,n,workers", FULL_SIZE,
-                         ids=["%s-%s-N%d" % (a, d, sum(n)) for a, d, n, _ in FULL_SIZE])
-def test_workers_grad_full_size(arch, dtype, n, workers):
+def check_sampled(a, gold, prefix, table, idx, tol, what, floor_scale=1.0, ref=None):
+    """Sampled per-tensor errors of a against the stored values `prefix`
+    (or against `ref` sampled the same way, with the stored scales), bound
+    max(tol, 3 x floor_scale x stored floor) on every tensor; returns the
+    worst (error, tensor)."""
+    scales, vmax = gold[prefix + "_scale"], float(gold[prefix + "_vmax"])
+    r = gold[prefix + "_ref"] if ref is None else np.concatenate([ref[ix] for ix in idx])
+    errs = F.sampled_errors(a, r, idx, scales, vmax)
+    fl = floor_scale * gold[prefix + "_floor"]
+    bad, worst, within = [], (0.0, ""), 0
+    for t, (row, e) in enumerate(zip(table, errs)):
+        bound = max(tol, FLOOR_FACTOR * fl[t])
+        within += e <= tol
+        worst = max(worst, (e, row[0]))
+        if not e <= bound:
+            bad.append("%s %.3e > %.3e (floor %.3e)" % (row[0], e, bound, fl[t]))
+    log("  %s: worst tensor %s %.3e; %d of %d tensors within %.0e (sampled, %d entries each)"
+        % (what, worst[1], worst[0], within, len(errs), tol, F.SAMPLE))
+    assert not bad, "%s: tensors beyond their bound: %s" % (what, "; ".join(bad[:8]))
+    return worst
+
+
+@pytest.mark.parametrize("name", [c[0] for c in F.FULL_SIZE])
+def test_workers_grad_full_size(name):
     """A workload configuration at its own size, in one pass (the launch
-    configuration the benchmark times), separated decisions: the listed
-    workers (all by default) against the exact oracle on every tensor, from
-    the one pass and from separate hs_worker_grad calls; every other worker's
-    one-pass gradient against its separate call (fp32: the bar; bf16: two
-    computations each within 3x the floor of exact differ by up to twice
-    that, with the largest floor of the listed workers)."""
-    log("workers_grad full size %s %s n=%s" % (arch, dtype, n))
-    net, table, theta, x, y = separated_setup(arch, n, 11, 11)
+    configuration the benchmark times), separated decisions: the compared
+    workers against the exact oracle's stored values (tests/golden/
+    make_fullsize.py), per tensor on sampled entries, from the one pass and
+    from separate hs_worker_grad calls; every other worker's one-pass
+    gradient against its separate call on all entries (fp32: the bar; bf16:
+    two computations each within 3x the floor of exact differ by up to twice
+    that, with the largest floor of the compared workers)."""
+    _, arch, dtype, n, workers = F.CONFIGS[name]
+    log("workers_grad full size %s n=%s" % (name, n))
+    gold = load_golden(name)
+    net, table, theta, x, y = F.setup(arch, n)
+    np.testing.assert_allclose(F.fingerprint(theta, x, y), gold["fingerprint"], rtol=1e-9)
+    assert list(gold["n"]) == list(n) and tuple(gold["workers"]) == tuple(workers)
+    idx = F.sample_index(table)
     ga, la = run_workers(arch, dtype, n, theta, x, y)
-    for i in range(len(n)):
-        assert np.all(np.isfinite(ga[i])), "worker %d: non-finite gradient" % i
-    refs = exact_refs(net, table, theta, x, y, n, dtype, workers=workers)
-    worst = []
-    for i, (ref_loss, ref, relu, _, floor) in sorted(refs.items()):
-        log("  worker %d (n=%d): loss %.6f vs %.6f" % (i, n[i], la[i], ref_loss))
-        e, name, within = check_pertensor(ga[i], ref, table, TOL[dtype], floor=floor,
-                                          what="worker %d vs exact" % i)
-        worst.append((e, i, name))
-        assert abs(la[i] - ref_loss) <= TOL[dtype] * max(1.0, abs(ref_loss))
-    log("  worst over workers: %.3e (worker %d, %s)" % max(worst))
     gb, lb = run_workers(arch, dtype, n, theta, x, y, separate=True)
-    fmax = floor_max([r[4] for r in refs.values()])
-    pair = [(name, 2.0 * e, sc) for name, e, sc in fmax] if dtype == "bf16" else None
     for i in range(len(n)):
-        if i in refs:
-            check_pertensor(gb[i], refs[i][1], table, TOL[dtype], floor=refs[i][4],
-                            what="worker %d separate call vs exact" % i)
-        else:
-            check_pertensor(ga[i], gb[i], table, TOL[dtype], floor=pair,
-                            what="worker %d one pass vs separate" % i)
+        assert np.all(np.isfinite(ga[i])) and np.all(np.isfinite(gb[i])), "worker %d" % i
+        check_padding(arch, ga[i])
+    for i in workers:
+        ref_loss = float(gold["w%d_loss" % i])
+        log("  worker %d (n=%d): loss %.6f / %.6f vs %.6f, min relu margin %.1e"
+            % (i, n[i], la[i], lb[i], ref_loss, float(gold["w%d_relu" % i])))
+        check_sampled(ga[i], gold, "w%d" % i, table, idx, TOL[dtype], "worker %d one pass vs exact" % i)
+        check_sampled(gb[i], gold, "w%d" % i, table, idx, TOL[dtype], "worker %d separate vs exact" % i)
+        for loss in (la[i], lb[i]):
+            assert abs(loss - ref_loss) <= TOL[dtype] * max(1.0, abs(ref_loss))
+    fmax = np.max([gold["w%d_floor" % i] for i in workers], axis=0)
     for i in range(len(n)):
-        ref_loss = refs[i][0] if i in refs else la[i]
-        assert abs(lb[i] - ref_loss) <= TOL[dtype] * max(1.0, abs(ref_loss))
-
-
-def step_floor(net, theta, xs, ys, n, wl, d_ref, table):
-    """Per-tensor error of the update theta' - theta that the oracle's own
-    arithmetic at the workload's precision makes (mode "fp32" / "bf16"), with
-    theta' stored in fp32 as the caller's master weights are (the largest over
-    the precision's rounding realizations; the first realization's step is
-    returned too)."""
-    floors, first = [], None
-    for k in REALIZATIONS[wl.dtype]:
-        op = S.step(lambda th, xm, ym: Mo.worker_grad(net, th, xm, ym, storage=wl.dtype, grid=k),
-                    theta.astype(np.float64), None, xs, ys, n, wl.lr, wl.mu, wl.wd)
-        th32 = op["theta"].astype(np.float32).astype(np.float64)
-        floors.append(pertensor(th32 - theta, d_ref, table))
-        first = first or op
-    return floor_max(floors), first
+        if i in workers:
+            continue
+        errs = pertensor(ga[i], gb[i], table)
+        bound = [max(TOL[dtype], FLOOR_FACTOR * 2.0 * f) if dtype == "bf16" else TOL[dtype]
+                 for f in fmax]
+        bad = ["%s %.3e > %.3e" % (nm, e, bd) for (nm, e, _), bd in zip(errs, bound) if not e <= bd]
+        log("  worker %d (n=%d) one pass vs separate: worst %.3e" % (i, n[i], max(e for _, e, _ in errs)))
+        assert not bad, "worker %d one pass vs separate: %s" % (i, "; ".join(bad[:8]))
+        assert abs(la[i] - lb[i]) <= TOL[dtype] * max(1.0, abs(lb[i]))
 
 
 def test_resnet18_fp32_full_size_step():
     """The ResNet-18 fp32 workload's step at its own size (N = 1024 over four
     workers 128/192/256/448, momentum 0.9, weight decay 5e-4, lr 0.1), all
     workers in one pass: the update theta' - theta and the momentum buffer
-    after one step against the oracle's step, per tensor."""
+    after one step against the oracle's stored step (tests/golden/
+    make_fullsize.py), per tensor on sampled entries."""
     require_gpu()
     from paper_2110_08941_amd.driver import Trainer
     log("full-size step resnet18_fp32 N=1024")
+    gold = load_golden(F.STEP_NAME)
     wl = WORKLOADS["resnet18_fp32"]
     net = Mo.build(wl.arch)
     table, P = Mo.param_table(net)
-    theta = synth.separate_decisions(table, synth.he_normal(table, P, 4), 4)
-    tr = Trainer(wl, seed=4, clock="model", steps=1, theta0=theta, grouped=True)
+    theta = synth.separate_decisions(table, synth.he_normal(table, P, F.STEP_SEED), F.STEP_SEED)
+    tr = Trainer(wl, seed=F.STEP_SEED, clock="model", steps=1, theta0=theta, grouped=True)
     try:
         n = tr.part.partition()
-        assert n == [128, 192, 256, 448]
+        assert n == F.STEP_PARTITION
         x, y = tr.batch(0)
-        xs, ys = x.cpu().numpy(), y.cpu().numpy()
+        np.testing.assert_allclose(F.fingerprint(theta, x.cpu().numpy(), y.cpu().numpy()),
+                                   gold["fingerprint"], rtol=1e-9)
         tr.step()
         torch.cuda.synchronize()
         got = tr.theta.cpu().numpy().astype(np.float64)
         mom = tr.mom.cpu().numpy().astype(np.float64)
+        losses = tr.losses.cpu().numpy()
     finally:
         tr.close()
-
-    def worker(th, xm, ym):
-        log("  oracle worker n=%d" % len(ym))
-        return Mo.worker_grad(net, th, xm, ym)
-
-    out = S.step(worker, theta.astype(np.float64), None, xs, ys, n, wl.lr, wl.mu, wl.wd)
-    d_ref = out["theta"] - theta
-    floor, op = step_floor(net, theta, xs, ys, n, wl, d_ref, table)
-    check_pertensor(got - theta, d_ref, table, TOL["fp32"], floor=floor, what="update")
-    check_pertensor(mom, out["buf"], table, TOL["fp32"], floor=pertensor(op["buf"], out["buf"], table),
-                    what="momentum buffer")
+    idx = F.sample_index(table)
+    check_sampled(got - theta.astype(np.float64), gold, "d", table, idx, TOL["fp32"], "update")
+    check_sampled(mom, gold, "buf", table, idx, TOL["fp32"], "momentum buffer")
+    np.testing.assert_allclose(losses, gold["losses"], rtol=TOL["fp32"], atol=0)
 
 
 @pytest.mark.parametrize("arch,dtype,n", [("resnet18", "bf16", [3, 5, 2]),
