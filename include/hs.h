@@ -286,10 +286,12 @@ hs_status hs_partitioner_set_estimator(hs_partitioner* p, int32_t kind, double a
 /* Timing probe of one implicit-GEMM kernel instantiation inside
  * hs_worker_grad (for roofline reports).  While enabled, every launch of the
  * GEMM kernel with the given mode (0 forward, 1 data gradient, 2 weight
- * gradient) and output tile (bm x bn: bm 64, 128, 256 or 512, bn 64, 128 or
- * 256; bm = 512 selects the 32x32 MFMA forward / data-gradient kernel, 64 x 64
- * the 64-channel patch kernels: forward / data gradient in modes 0 and 1,
- * 3x3 weight gradient in mode 2) on this workspace is
+ * gradient) and output tile (bm x bn: bm 32, 64, 128, 256 or 512, bn 64, 128
+ * or 256; bm = 512 selects the 32x32 MFMA forward / data-gradient kernel,
+ * 64 x 64 the 64-channel patch kernels: forward / data gradient in modes 0
+ * and 1, 3x3 weight gradient in mode 2; 256 x 256 in mode 1 the stride-2
+ * data-gradient patch kernel; 32 x 64 in mode 0 the direct bf16 stem) on this
+ * workspace is
  * bracketed by two HIP events on the worker's stream, and its algorithmic
  * FLOPs (2 x pixels x c_out x taps x c_in, i.e. dense 3x3 taps, independent of
  * the stride handling) are added up.  At most `capacity` launches are

@@ -450,7 +450,7 @@ hs_status hs_probe_enable(hs_workspace* ws, int32_t mode, int32_t bm, int32_t bn
   if (!ws) return fail(HS_ERR_INVALID, "hs_probe_enable: workspace is NULL");
   probe_release(ws->ws);
   if (mode < 0) return ok();
-  if (mode > 2 || (bm != 64 && bm != 128 && bm != 256 && bm != 512) ||
+  if (mode > 2 || (bm != 32 && bm != 64 && bm != 128 && bm != 256 && bm != 512) ||
       (bn != 64 && bn != 128 && bn != 256) || capacity < 1 || capacity > 1000000)
     return fail(HS_ERR_INVALID, "hs_probe_enable: bad mode/tile/capacity");
   ws->ws.probe_ev.resize(2 * (size_t)capacity + 1, nullptr);

@@ -114,7 +114,20 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  // row tile tm, column tile tn: with several column tiles, blocks b, b + 8,
+  // b + 16, ... (dispatched to the same XCD, whose L2 then serves the rows
+  // they share) take the column tiles of one row tile; blocks past the last
+  // row tile (grid rounded up to 8) have no work
+  int tm, tn;
+  if (p.tiles_n > 1) {
+    const int b = (int)blockIdx.x;
+    tn = (b >> 3) % p.tiles_n;
+    tm = (b / (8 * p.tiles_n)) * 8 + (b & 7);
+    if ((int64_t)tm * C2_BM >= p.M) return;
+  } else {
+    tm = (int)blockIdx.x;
+    tn = 0;
+  }
   const int m0 = tm * C2_BM + wave * 64, n0 = tn * BN;
   const int kh = lane >> 5;
   const int Ctap = MODE == MODE_FWD ? g.C : g.K;   // channels per tap (A side)
@@ -538,31 +551,47 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
 // ----------------------------------------------------------------------------
 constexpr int S2_POS = 256;   // dy positions per block
 constexpr int S2_BN = 64;     // input channels per block
+constexpr int S2_CK = 32;     // dy channels per slice (two 16-channel steps)
 
 template <int EPI, bool PROJ>
 __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
   constexpr int BN = S2_BN, NB = BN / 32, RS = 9;
-  constexpr int SEG = RS * 2 * BN;              // 16-byte B chunks per slice (9 taps)
-  constexpr int BREG = (SEG + 511) / 512;
+  constexpr int KK = S2_CK / C2_CK;             // 16-channel steps per slice
+  constexpr int NT = RS + (PROJ ? 1 : 0);       // taps per step (the shortcut's last)
+  constexpr int SEG = RS * 2 * BN;              // 16-byte B chunks per step (9 taps)
+  constexpr int SEG1 = PROJ ? 2 * BN : 0;       // the shortcut's (one tap)
+  constexpr int BREG = (KK * (SEG + SEG1) + 511) / 512;
   constexpr int BBUF = BREG * 512;
-  constexpr int SEG1 = 2 * BN;                  // the projection's slice: one tap
   constexpr int PPLANE = S2_POS * 16 + 128;
+  constexpr int NPL = KK * 2 * (PROJ ? 2 : 1);  // dy planes (8 channels each): main, shortcut
   constexpr int EROW = 36;
   constexpr bool EADD = (EPI & EPI_ADD) != 0, EBITS = (EPI & EPI_MBITS) != 0;
   static_assert(5 * 32 * EROW * 4 <= BBUF * 16, "epilogue staging of five waves fits a B buffer");
   __shared__ __attribute__((aligned(16))) uint4 sB0[BBUF];
   __shared__ __attribute__((aligned(16))) uint4 sB1[BBUF];
-  __shared__ __attribute__((aligned(16))) char sP0[2 * PPLANE];
-  __shared__ __attribute__((aligned(16))) char sP1[2 * PPLANE];
+  __shared__ __attribute__((aligned(16))) char sP0[NPL * PPLANE];
+  __shared__ __attribute__((aligned(16))) char sP1[NPL * PPLANE];
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  // position tile tm, channel tile tn: with several channel tiles, blocks
+  // b, b + 8, b + 16, ... (dispatched to the same XCD, whose L2 then serves
+  // the dy tile they share) take the channel tiles of one position tile;
+  // blocks past the last position tile (grid rounded up to 8) have no work
+  int tm, tn;
+  if (p.tiles_n > 1) {
+    const int b = (int)blockIdx.x;
+    tn = (b >> 3) % p.tiles_n;
+    tm = (b / (8 * p.tiles_n)) * 8 + (b & 7);
+    if ((int64_t)tm * S2_POS >= p.M) return;
+  } else {
+    tm = (int)blockIdx.x;
+    tn = 0;
+  }
   const int n0 = tn * BN;
   const int kh = lane >> 5;
   const int Kc = g.K;                           // dy channels (the reduction)
-  const int ns = Kc / C2_CK;                    // slices over dy
-  const int ns_all = PROJ ? 2 * ns : ns;        // then as many over the shortcut's dy
+  const int ns = Kc / S2_CK;                    // slices over dy
   const int Ho = g.Ho, Wo = g.Wo, HW = Ho * Wo;
   const int tile_m0 = tm * S2_POS;
   const bf16_t* A = (const bf16_t*)p.a;
@@ -571,12 +600,13 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
   const bf16_t* B2 = (const bf16_t*)p.b2;
 
   // this lane's dy position (one 32-row block per wave) and its taps' masks:
-  // bit t = tap t reads a dy position inside the image
+  // bit t = tap t reads a dy position inside the image; bit 9 = the
+  // shortcut's tap (the position itself)
   const int q = wave * 32 + (lane & 31);
   uint32_t vm;
   {
     const int pix = q % HW, i = pix / Wo, j = pix - (pix / Wo) * Wo;
-    uint32_t bits = 0;
+    uint32_t bits = 1u << 9;
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
       const int di = t / 3 == 0 ? 1 : 0, dj = t % 3 == 0 ? 1 : 0;
@@ -584,7 +614,6 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
     }
     vm = tile_m0 + q < p.M ? bits : 0u;
   }
-  const uint32_t vm1 = tile_m0 + q < p.M ? 1u : 0u;   // the shortcut's single tap
 
   f32x16 acc[4][NB];
 #pragma unroll
@@ -592,113 +621,157 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[c][nb] = (f32x16){};
 
-  auto read_a = [&](const char* P, int off, uint4& ra) {
-    ra = *(const uint4*)(P + kh * PPLANE + ((q + off) & (S2_POS - 1)) * 16);
-  };
-  auto read_b = [&](const uint4* Bb, int t, uint4 (&rb)[NB]) {
+  // The ReLU mask bits of the block's output: its dy positions are whole
+  // images, so its dx pixels are the 4 x 256 consecutive pixels from image
+  // tile_m0 / HW on; thread t loads the 8 bytes (64 channels of the column
+  // tile) of pixels t and t + 512 now, in two coalesced loads, and stores
+  // them in LDS for the epilogue after the main loop.
+  const int64_t px_total = (int64_t)p.M * 4;
+  const int64_t px0 = (int64_t)tile_m0 * 4;
+  uint2 mload[2];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) rb[nb] = Bb[(t * 2 + kh) * BN + nb * 32 + (lane & 31)];
+  for (int r = 0; r < 2; ++r) {
+    const int64_t gp = px0 + tid + 512 * r;
+    mload[r] = EBITS && gp < px_total
+                   ? *(const uint2*)(p.mbits + gp * (p.N / 8) + n0 / 8)
+                   : make_uint2(0u, 0u);
+  }
+
+  // step u = (16-channel step kk, tap t) of a slice: the dy fragment (8
+  // channels of this lane's position, shifted by the tap's dy offset) and the
+  // weight fragments of 64 channels
+  auto read_tap = [&](const uint4* Bb, const char* P, int u, uint4& ra, uint4 (&rb)[NB]) {
+    const int kk = u / NT, t = u - kk * NT;
+    if (PROJ && t == RS) {
+      ra = *(const uint4*)(P + (2 * KK + 2 * kk + kh) * PPLANE + q * 16);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        rb[nb] = Bb[KK * SEG + (2 * kk + kh) * BN + nb * 32 + (lane & 31)];
+    } else {
+      const int off = (t / 3 == 0 ? Wo : 0) + (t % 3 == 0 ? 1 : 0);
+      ra = *(const uint4*)(P + (2 * kk + kh) * PPLANE + ((q + off) & (S2_POS - 1)) * 16);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        rb[nb] = Bb[((kk * RS + t) * 2 + kh) * BN + nb * 32 + (lane & 31)];
+    }
   };
   auto masked = [&](uint32_t m, int t, const uint4& v) -> uint4 {
     const uint32_t k = 0u - ((m >> t) & 1u);
     return make_uint4(v.x & k, v.y & k, v.z & k, v.w & k);
   };
-  // slice sl of B and of the dy patch, straight from global memory into LDS;
-  // slices ns.. are the shortcut's (one tap); rows past the last image re-read
-  // the last row (they feed no stored output)
+  // slice sl of B (and the shortcut's B) and of the dy patches, straight from
+  // global memory into LDS; rows past the last image re-read the last row
+  // (they feed no stored output).  The packed weights of the slice's KK
+  // 16-channel steps are consecutive, so chunk c of the slice is chunk
+  // sl * KK * SEG + c of the packed array (likewise for the shortcut).
   const int wbase = wave * 64;
   auto dma_slice = [&](int sl, uint4* Bb, char* P) {
-    const bool second = PROJ && sl >= ns;
-    const int ssl = second ? sl - ns : sl;
-    const bf16_t* Bs = second ? B2 : B;
-    const int rs = second ? 1 : RS, seg = second ? SEG1 : SEG;
 #pragma unroll
     for (int i = 0; i < BREG; ++i) {
       int c = tid + 512 * i;
-      c = c < seg ? c : seg - 1;
-      const int n = c % BN, rest = c / BN;
-      const bf16_t* src = Bs + (((int64_t)ssl * rs * 2 + rest) * p.N + n0 + n) * 8;
+      const bf16_t* src;
+      if (!PROJ || c < KK * SEG) {
+        c = c < KK * SEG ? c : KK * SEG - 1;
+        const int n = c % BN, rest = c / BN;
+        src = B + (((int64_t)sl * KK * RS * 2 + rest) * p.N + n0 + n) * 8;
+      } else {
+        int c1 = c - KK * SEG;
+        c1 = c1 < KK * SEG1 ? c1 : KK * SEG1 - 1;
+        const int n = c1 % BN, rest = c1 / BN;
+        src = B2 + (((int64_t)sl * KK * 2 + rest) * p.N + n0 + n) * 8;
+      }
       __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bb + 512 * i + wbase), 16, 0, 0);
     }
     const int px = tid & (S2_POS - 1), h = tid >> 8;
     int64_t m = (int64_t)tile_m0 + px;
     m = m < p.M ? m : p.M - 1;
-    const bf16_t* src = (second ? A2 : A) + m * Kc + ssl * C2_CK + 8 * h;
-    __builtin_amdgcn_global_load_lds((gbl_cptr)src,
-                                     (lds_ptr)(P + h * PPLANE + (wbase & (S2_POS - 1)) * 16), 16,
-                                     0, 0);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int64_t col = (int64_t)sl * S2_CK + kk * C2_CK + 8 * h;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)(A + m * Kc + col),
+                                       (lds_ptr)(P + (2 * kk + h) * PPLANE +
+                                                 (wbase & (S2_POS - 1)) * 16),
+                                       16, 0, 0);
+      if (PROJ)
+        __builtin_amdgcn_global_load_lds((gbl_cptr)(A2 + m * Kc + col),
+                                         (lds_ptr)(P + (2 * KK + 2 * kk + h) * PPLANE +
+                                                   (wbase & (S2_POS - 1)) * 16),
+                                         16, 0, 0);
+    }
   };
 
   uint4 fa, fb[NB];
-  auto first_reads = [&](int sl, const uint4* Bb, const char* P) {
-    if (PROJ && sl >= ns) read_a(P, 0, fa);
-    else read_a(P, Wo + 1, fa);                   // tap 0: (di, dj) = (1, 1)
-    read_b(Bb, 0, fb);
-  };
   // one slice from (Bc, Pc) while the next is copied into (Bn, Pn)
   auto slice = [&](int sl, const uint4* Bc, const char* Pc, uint4* Bn, char* Pn) {
-    const bool more = sl + 1 < ns_all;
+    const bool more = sl + 1 < ns;
     if (more) dma_slice(sl + 1, Bn, Pn);
-    if (!PROJ || sl < ns) {
 #pragma unroll
-      for (int t = 0; t < RS; ++t) {
-        // tap t = (r, s): class (r != 1, s != 1), dy offset (r == 0, s == 0)
-        constexpr int dummy = 0;
-        (void)dummy;
-        const int cls = 2 * (t / 3 != 1 ? 1 : 0) + (t % 3 != 1 ? 1 : 0);
-        const uint4 am = masked(vm, t, fa);
-        uint4 na, nbv[NB];
-        if (t + 1 < RS) {
-          const int tn1 = t + 1;
-          const int off = (tn1 / 3 == 0 ? Wo : 0) + (tn1 % 3 == 0 ? 1 : 0);
-          read_a(Pc, off, na);
-          read_b(Bc, tn1, nbv);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        bf16x8 av;
-        __builtin_memcpy(&av, &am, 16);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          bf16x8 bv;
-          __builtin_memcpy(&bv, &fb[nb], 16);
-          acc[cls][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[cls][nb], 0, 0, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        if (t + 1 < RS) {
-          fa = na;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
-        }
-      }
-    } else {
-      const uint4 am = masked(vm1, 0, fa);
+    for (int u = 0; u < KK * NT; ++u) {
+      // tap t = (r, s): class (r != 1, s != 1), dy offset (r == 0, s == 0);
+      // the shortcut's tap: class (0, 0)
+      const int t = u % NT;
+      const int cls = t == RS ? 0 : 2 * (t / 3 != 1 ? 1 : 0) + (t % 3 != 1 ? 1 : 0);
+      const uint4 am = masked(vm, t, fa);
+      uint4 na, nbv[NB];
+      if (u + 1 < KK * NT) read_tap(Bc, Pc, u + 1, na, nbv);
+      __builtin_amdgcn_sched_barrier(0);
       bf16x8 av;
       __builtin_memcpy(&av, &am, 16);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         bf16x8 bv;
         __builtin_memcpy(&bv, &fb[nb], 16);
-        acc[0][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[0][nb], 0, 0, 0);
+        acc[cls][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[cls][nb], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (u + 1 < KK * NT) {
+        fa = na;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
       }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (more) first_reads(sl + 1, Bn, Pn);
+    if (more) read_tap(Bn, Pn, 0, fa, fb);
   };
 
   dma_slice(0, sB0, sP0);
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  first_reads(0, sB0, sP0);
-  for (int sl = 0; sl < ns_all; sl += 2) {
+  read_tap(sB0, sP0, 0, fa, fb);
+  for (int sl = 0; sl < ns; sl += 2) {
     slice(sl, sB0, sP0, sB1, sP1);
-    if (sl + 1 < ns_all) slice(sl + 1, sB1, sP1, sB0, sP0);
+    if (sl + 1 < ns) slice(sl + 1, sB1, sP1, sB0, sP0);
   }
 
   // ---- epilogue: per (class, 32 channels), this wave's 32 x 32 tile staged in
-  // LDS, then 4 lanes per row write 8 channels each to the class's pixel
+  // LDS, then 4 lanes per row write 8 channels each to the class's pixel.
+  // The lane's two rows (dy positions) give its pixels' offsets; the mask
+  // bytes of all 16 (class, channel half, row) are loaded before the first
+  // store, so that their latency is paid once per block.
   float* E = (float*)(wave < 5 ? sB0 : sB1) + (wave < 5 ? wave : wave - 5) * 32 * EROW;
+  uint2* mkl = (uint2*)sP0;                     // the block's mask bytes, per dx pixel
+  if (EBITS) {
+    mkl[tid] = mload[0];
+    mkl[tid + 512] = mload[1];
+    __syncthreads();
+  }
   const int H = g.H, W = g.W;
+  const int c8 = 8 * (lane & 3);
+  int64_t pbase[2];
+  int lpix[2];                                  // dx pixel of class (0, 0), within the block
+  bool live[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q2 = wave * 32 + 16 * i + (lane >> 2);
+    const int64_t m = (int64_t)tile_m0 + q2;
+    live[i] = m < p.M;
+    const int64_t mm = live[i] ? m : 0;
+    const int img = (int)(mm / HW), pix = (int)(mm - (int64_t)img * HW);
+    const int ii = pix / Wo, jj = pix - (pix / Wo) * Wo;
+    pbase[i] = (((int64_t)img * H + 2 * ii) * W + 2 * jj) * p.N + n0 + c8;
+    lpix[i] = ((q2 / HW) * H + 2 * ii) * W + 2 * jj;
+  }
 #pragma unroll
   for (int cls = 0; cls < 4; ++cls) {
     const int a = cls >> 1, b = cls & 1;
@@ -712,15 +785,11 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
-        const int64_t m = (int64_t)tile_m0 + wave * 32 + row;
+        const int row = 16 * i + (lane >> 2);
         const float4 lo = *(const float4*)(E + row * EROW + c8);
         const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
-        if (m < p.M) {
-          const int img = (int)(m / HW), pix = (int)(m - (int64_t)img * HW);
-          const int ii = pix / Wo, jj = pix - (pix / Wo) * Wo;
-          const int64_t off = (((int64_t)img * H + 2 * ii + a) * W + 2 * jj + b) * p.N + n0 +
-                              nb * 32 + c8;
+        if (live[i]) {
+          const int64_t off = pbase[i] + ((int64_t)a * W + b) * p.N + nb * 32;
           float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
           if constexpr (EADD) {
             const uint4 u = *(const uint4*)((const bf16_t*)p.addend + off);
@@ -732,7 +801,9 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
             }
           }
           if constexpr (EBITS) {
-            const uint32_t bits = p.mbits[off >> 3];
+            const uint2 mw = mkl[lpix[i] + a * W + b];
+            const uint32_t word = nb == 0 ? mw.x : mw.y;
+            const uint32_t bits = (word >> (8 * (lane & 3))) & 0xffu;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
               if (!((bits >> e) & 1u)) v[e] = 0.f;
@@ -815,7 +886,8 @@ static hipError_t launch_mode2(const GemmParams& p0, hipStream_t s) {
   const int BN = conv2_bn(p.N);
   const int RS = p.g.R * p.g.S;
   p.tiles_n = p.N / BN;
-  const dim3 grid((unsigned)(ceil_div(p.M, C2_BM) * p.tiles_n));
+  const int64_t tiles_m = ceil_div(p.M, C2_BM);
+  const dim3 grid((unsigned)(p.tiles_n > 1 ? ceil_div(tiles_m, 8) * 8 * p.tiles_n : tiles_m));
   const bool patch = conv2_patch(p);
   if (BN == 128) {
     if (patch) launch_epi2<MODE, 128, 9, true>(p, grid, s);
@@ -840,7 +912,7 @@ bool conv2s2_ok(const GemmParams& p) {
   if (p.out_f32 || !p.mbits || p.mask == nullptr) return false;
   if (!(g.R == 3 && g.S == 3 && g.stride == 2 && g.pad == 1)) return false;
   if (g.H != 2 * g.Ho || g.W != 2 * g.Wo || hw < 1 || S2_POS % hw != 0) return false;
-  if (g.K % C2_CK != 0 || g.C % S2_BN != 0 || p.N != g.C) return false;
+  if (g.K % S2_CK != 0 || g.C % S2_BN != 0 || p.N != g.C) return false;
   if ((p.a2 == nullptr) != (p.b2 == nullptr)) return false;
   return true;
 }
@@ -852,7 +924,8 @@ hipError_t launch_conv2s2(const GemmParams& p0, hipStream_t s) {
   GemmParams p = p0;
   p.M = p.g.n * p.g.Ho * p.g.Wo;
   p.tiles_n = p.N / S2_BN;
-  const dim3 grid((unsigned)(ceil_div(p.M, S2_POS) * p.tiles_n));
+  const int64_t tiles_m = ceil_div(p.M, S2_POS);
+  const dim3 grid((unsigned)(p.tiles_n > 1 ? ceil_div(tiles_m, 8) * 8 * p.tiles_n : tiles_m));
   const bool add = p.addend != nullptr, proj = p.a2 != nullptr;
   if (add && proj) hipLaunchKernelGGL((conv2s2_kernel<EPI_ADD | EPI_MBITS, true>), grid, dim3(512), 0, s, p);
   else if (add) hipLaunchKernelGGL((conv2s2_kernel<EPI_ADD | EPI_MBITS, false>), grid, dim3(512), 0, s, p);

@@ -142,6 +142,13 @@ bool wgrad3_ok(const GemmParams& p);
 int wgrad3_slices(const GemmParams& p, int nimg);
 hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s);
 // NCHW fp32 [n][c][hw] -> NHWC [n][hw][cp] (activation type), channels c..cp-1 zero
+// The CIFAR stem in bf16 (stem.hip): 3 -> 64 channels, 3x3, stride 1, pad 1,
+// 32x32, from the caller's fp32 NCHW batch x [n][3][32][32] and bf16 weights
+// [64][3][3][3]; writes y [n][32][32][64] bf16 and, when x8 is not null, the
+// input rounded to bf16 in NHWC with 8 channels (3 real, 5 zero).
+bool stem_ok(int cin, int cout, int k, int stride, int pad, int H, int W);
+hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8, int n,
+                           hipStream_t s);
 hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
                                    hipStream_t s);
 // weights [k][rs][c] fp32 -> [k][rs][cp] activation type, zero padded

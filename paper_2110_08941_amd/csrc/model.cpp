@@ -992,6 +992,13 @@ int stem_cpad(const Ctx& c) { return c.bf ? 8 : 4; }
 
 hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void* y) {
   const int cp = stem_cpad(c);
+  if (c.bf && stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W)) {
+    // the direct stem kernel (stem.hip); it also writes X0 for the weight gradient
+    const bool probe = probe_begin(c, MODE_FWD, 32, 64);
+    HS_TRY(launch_stem_fwd(x, c.W(L.w), y, X0, c.n, c.s));
+    if (probe) HS_TRY(probe_end(c, layer_flops(L, c.n)));
+    return hipSuccess;
+  }
   ConvL st = L;
   st.cin = cp;
   HS_TRY(launch_nchw_to_nhwc_pad(x, X0, c.n, 3, cp, L.H * L.W, c.bf, c.s));
