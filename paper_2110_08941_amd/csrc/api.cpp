@@ -455,7 +455,9 @@ hs_status hs_probe_enable(hs_workspace* ws, int32_t mode, int32_t bm, int32_t bn
     return fail(HS_ERR_INVALID, "hs_probe_enable: bad mode/tile/capacity");
   ws->ws.probe_ev.resize(2 * (size_t)capacity + 1, nullptr);
   for (size_t i = 0; i < ws->ws.probe_ev.size(); ++i) {
-    hipError_t e = hipEventCreate(&ws->ws.probe_ev[i]);
+    // timing only: no system-scope fence (no cache writeback between the
+    // launches it brackets, which would add to the measured time)
+    hipError_t e = hipEventCreateWithFlags(&ws->ws.probe_ev[i], hipEventDisableSystemFence);
     if (e != hipSuccess) {
       ws->ws.probe_ev.resize(i);
       probe_release(ws->ws);

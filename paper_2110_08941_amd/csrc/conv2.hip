@@ -818,6 +818,181 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
 }
 
 // ----------------------------------------------------------------------------
+// Forward of a 3x3, stride-2, pad-1 convolution in the patch form.
+//
+// Output position (i, j) reads input pixels (2i + r - 1, 2j + s - 1).  A block
+// holds 256 output positions -- whole output images, so their input pixels
+// are the 4 x 256 pixels of the same whole input images -- x 128 output
+// channels; each of its 8 waves owns 32 positions x 128 channels (four 32 x
+// 32 accumulators).  Per 16-channel slice the block copies those 1024 input
+// pixels and the slice's packed weights into LDS (global-to-LDS,
+// double-buffered); tap (r, s) is a shifted read of the pixel plane.  Only
+// r = 0 on output row 0 and s = 0 on output column 0 read outside the image
+// (a per-lane mask); the plane offset wraps within the block's pixels there.
+// The epilogue stages each 32 x 32 tile in LDS and writes 8-channel rows.
+// ----------------------------------------------------------------------------
+constexpr int F2_POS = 256;   // output positions per block
+constexpr int F2_BN = 128;    // output channels per block
+
+__global__ __launch_bounds__(512) void conv2s2f_kernel(GemmParams p) {
+  constexpr int BN = F2_BN, NB = BN / 32, RS = 9;
+  constexpr int SEG = RS * 2 * BN;              // 16-byte B chunks per slice
+  constexpr int BREG = (SEG + 511) / 512;
+  constexpr int BBUF = BREG * 512;
+  constexpr int NPIX = 4 * F2_POS;              // input pixels per block
+  constexpr int PPLANE = NPIX * 16 + 128;       // one 8-channel half of the slice
+  constexpr int EROW = 36;
+  static_assert(8 * 32 * EROW * 4 <= BBUF * 16, "epilogue staging fits a B buffer");
+  __shared__ __attribute__((aligned(16))) uint4 sB0[BBUF];
+  __shared__ __attribute__((aligned(16))) uint4 sB1[BBUF];
+  __shared__ __attribute__((aligned(16))) char sP0[2 * PPLANE];
+  __shared__ __attribute__((aligned(16))) char sP1[2 * PPLANE];
+
+  const ConvGeom& g = p.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int tm, tn;
+  if (p.tiles_n > 1) {
+    const int b = (int)blockIdx.x;
+    tn = (b >> 3) % p.tiles_n;
+    tm = (b / (8 * p.tiles_n)) * 8 + (b & 7);
+    if ((int64_t)tm * F2_POS >= p.M) return;
+  } else {
+    tm = (int)blockIdx.x;
+    tn = 0;
+  }
+  const int n0 = tn * BN;
+  const int kh = lane >> 5;
+  const int C = g.C;
+  const int ns = C / C2_CK;
+  const int Wo = g.Wo, HWo = g.Ho * Wo, W = g.W, HW = g.H * W;
+  const int tile_m0 = tm * F2_POS;
+  const int64_t px0 = (int64_t)(tile_m0 / HWo) * HW;   // first input pixel of the block
+  const int64_t px_total = (int64_t)g.n * HW;
+  const bf16_t* A = (const bf16_t*)p.a;
+  const bf16_t* B = (const bf16_t*)p.b;
+
+  // this lane's output position, its pixel base (input pixel (2i - 1, 2j - 1)
+  // within the block) and its taps' masks
+  const int q = wave * 32 + (lane & 31);
+  int pbase;
+  uint32_t vm;
+  {
+    const int pix = q % HWo, i = pix / Wo, j = pix - (pix / Wo) * Wo;
+    pbase = (q / HWo) * HW + (2 * i - 1) * W + (2 * j - 1);
+    uint32_t bits = 0;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int r = t / 3, s = t % 3;
+      if ((i > 0 || r > 0) && (j > 0 || s > 0)) bits |= 1u << t;
+    }
+    vm = tile_m0 + q < p.M ? bits : 0u;
+  }
+
+  f32x16 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = (f32x16){};
+
+  auto read_tap = [&](const uint4* Bb, const char* P, int t, uint4& ra, uint4 (&rb)[NB]) {
+    const int off = (t / 3) * W + (t % 3);
+    ra = *(const uint4*)(P + kh * PPLANE + ((pbase + off) & (NPIX - 1)) * 16);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) rb[nb] = Bb[(t * 2 + kh) * BN + nb * 32 + (lane & 31)];
+  };
+  auto masked = [&](int t, const uint4& v) -> uint4 {
+    const uint32_t k = 0u - ((vm >> t) & 1u);
+    return make_uint4(v.x & k, v.y & k, v.z & k, v.w & k);
+  };
+  // slice sl: the packed weights, and the block's input pixels (two 8-channel
+  // halves); pixels past the last image re-read the last pixel
+  const int wbase = wave * 64;
+  auto dma_slice = [&](int sl, uint4* Bb, char* P) {
+#pragma unroll
+    for (int i = 0; i < BREG; ++i) {
+      int c = tid + 512 * i;
+      c = c < SEG ? c : SEG - 1;
+      const int n = c % BN, rest = c / BN;
+      const bf16_t* src = B + (((int64_t)sl * RS * 2 + rest) * p.N + n0 + n) * 8;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bb + 512 * i + wbase), 16, 0, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int c = tid + 512 * it;                // chunk: half c / NPIX, pixel c % NPIX
+      const int px = c & (NPIX - 1), h = c / NPIX;
+      int64_t gp = px0 + px;
+      gp = gp < px_total ? gp : px_total - 1;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)(A + gp * C + sl * C2_CK + 8 * h),
+                                       (lds_ptr)(P + h * PPLANE +
+                                                 ((wbase + 512 * it) & (NPIX - 1)) * 16),
+                                       16, 0, 0);
+    }
+  };
+
+  uint4 fa, fb[NB];
+  auto slice = [&](int sl, const uint4* Bc, const char* Pc, uint4* Bn, char* Pn) {
+    const bool more = sl + 1 < ns;
+    if (more) dma_slice(sl + 1, Bn, Pn);
+#pragma unroll
+    for (int t = 0; t < RS; ++t) {
+      const uint4 am = masked(t, fa);
+      uint4 na, nbv[NB];
+      if (t + 1 < RS) read_tap(Bc, Pc, t + 1, na, nbv);
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8 av;
+      __builtin_memcpy(&av, &am, 16);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        bf16x8 bv;
+        __builtin_memcpy(&bv, &fb[nb], 16);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv, av, acc[nb], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < RS) {
+        fa = na;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) fb[nb] = nbv[nb];
+      }
+    }
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (more) read_tap(Bn, Pn, 0, fa, fb);
+  };
+
+  dma_slice(0, sB0, sP0);
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  read_tap(sB0, sP0, 0, fa, fb);
+  for (int sl = 0; sl < ns; sl += 2) {
+    slice(sl, sB0, sP0, sB1, sP1);
+    if (sl + 1 < ns) slice(sl + 1, sB1, sP1, sB0, sP0);
+  }
+
+  // ---- epilogue: per 32 channels, this wave's 32 x 32 tile staged in LDS
+  // (a B buffer, free after the last barrier), then 4 lanes per row write 8
+  // channels each
+  float* E = (float*)sB0 + wave * 32 * EROW;
+  const int c8 = 8 * (lane & 3);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq)
+      *(float4*)(E + (lane & 31) * EROW + 8 * qq + 4 * kh) =
+          make_float4(acc[nb][4 * qq], acc[nb][4 * qq + 1], acc[nb][4 * qq + 2], acc[nb][4 * qq + 3]);
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = 16 * i + (lane >> 2);
+      const int64_t m = (int64_t)tile_m0 + wave * 32 + row;
+      const float4 lo = *(const float4*)(E + row * EROW + c8);
+      const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+      if (m < p.M)
+        *(uint4*)((bf16_t*)p.out + m * p.N + n0 + nb * 32 + c8) =
+            make_uint4(pack2(lo.x, lo.y), pack2(lo.z, lo.w), pack2(hi.x, hi.y), pack2(hi.z, hi.w));
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// ----------------------------------------------------------------------------
 // host side
 // ----------------------------------------------------------------------------
 int conv2_bn(int N) { return N % 128 == 0 ? 128 : (N % 64 == 0 ? 64 : 0); }
@@ -931,6 +1106,32 @@ hipError_t launch_conv2s2(const GemmParams& p0, hipStream_t s) {
   else if (add) hipLaunchKernelGGL((conv2s2_kernel<EPI_ADD | EPI_MBITS, false>), grid, dim3(512), 0, s, p);
   else if (proj) hipLaunchKernelGGL((conv2s2_kernel<EPI_MBITS, true>), grid, dim3(512), 0, s, p);
   else hipLaunchKernelGGL((conv2s2_kernel<EPI_MBITS, false>), grid, dim3(512), 0, s, p);
+  return hipGetLastError();
+}
+
+// the stride-2 forward patch kernel: 3x3, stride 2, pad 1, the input exactly
+// twice the output, whole output images per 256-position tile, input
+// channels in whole slices, output channels in 128-wide tiles, a plain bf16
+// output (no bias, ReLU or shortcut)
+bool conv2s2f_ok(const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  const int64_t hw = (int64_t)g.Ho * g.Wo;
+  if (p.out_f32 || p.bias || p.relu || p.addend || p.mask || p.mbits || p.a2) return false;
+  if (!(g.R == 3 && g.S == 3 && g.stride == 2 && g.pad == 1)) return false;
+  if (g.H != 2 * g.Ho || g.W != 2 * g.Wo || hw < 1 || F2_POS % hw != 0) return false;
+  return g.C % C2_CK == 0 && g.C > 0 && p.N == g.K && g.K % F2_BN == 0;
+}
+
+// p.b must point to the weights packed for the forward (launch_pack_weights
+// with MODE_FWD and the same p)
+hipError_t launch_conv2s2f(const GemmParams& p0, hipStream_t s) {
+  if (!conv2s2f_ok(p0)) return hipErrorInvalidValue;
+  GemmParams p = p0;
+  p.M = p.g.n * p.g.Ho * p.g.Wo;
+  p.tiles_n = p.N / F2_BN;
+  const int64_t tiles_m = ceil_div(p.M, F2_POS);
+  const dim3 grid((unsigned)(p.tiles_n > 1 ? ceil_div(tiles_m, 8) * 8 * p.tiles_n : tiles_m));
+  hipLaunchKernelGGL(conv2s2f_kernel, grid, dim3(512), 0, s, p);
   return hipGetLastError();
 }
 

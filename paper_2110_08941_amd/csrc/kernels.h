@@ -126,6 +126,11 @@ hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
 // with p.a2 / p.b2 (packed 1x1 weights) the shortcut's data gradient is added.
 bool conv2s2_ok(const GemmParams& p);
 hipError_t launch_conv2s2(const GemmParams& p, hipStream_t s);
+// Forward of a 3x3 stride-2 pad-1 convolution in the patch form (conv2.hip):
+// p.a = x [n][2Ho][2Wo][C], p.b = weights packed for MODE_FWD, p.out = y
+// [n][Ho][Wo][K] bf16, no epilogue operations.
+bool conv2s2f_ok(const GemmParams& p);
+hipError_t launch_conv2s2f(const GemmParams& p, hipStream_t s);
 // bf16 forward / data gradient of 64 -> 64 channel 3x3 stride-1 layers on
 // 32-wide maps (conv64.hip): packed weights resident in LDS, input patch of 16
 // output rows staged once per tile, taps as shifted LDS reads

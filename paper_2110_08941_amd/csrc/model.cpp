@@ -592,6 +592,21 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   p.N = L.cout;
   p.K = L.k * L.k * L.cin;
   const bool vec = (L.cin % c.V) == 0;
+  if (c.bf && L.stride == 2 && !c.part && c.ws.packed && !wptr && conv2s2f_ok(p)) {
+    // bf16 3x3 stride 2: the patch form over whole input images (conv2.hip);
+    // it takes no batch-norm sums (*stats_fused stays false)
+    const void* wb = nullptr;
+    HS_TRY(packed_weights(c, p.b, MODE_FWD, p, false, &wb));
+    if (wb) {
+      GemmParams q = p;
+      q.b = wb;
+      const bool probe = probe_begin(c, MODE_FWD, 256, 128);
+      HS_TRY(launch_conv2s2f(q, c.s));
+      if (probe) HS_TRY(probe_end(c, flops > 0 ? flops : layer_flops(L, c.n)));
+      if (stats_fused) *stats_fused = false;
+      return hipSuccess;
+    }
+  }
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
   return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, flops > 0 ? flops : layer_flops(L, c.n),
