@@ -91,6 +91,38 @@ __global__ void pack_weights_kernel(const bf16_t* __restrict__ W, bf16_t* __rest
   }
 }
 
+// Several packings in one launch: job blockIdx.y packs theta_bf16 + woff
+// into Bp + dst as pack_weights_kernel does.
+__global__ void pack_batch_kernel(const bf16_t* __restrict__ W, bf16_t* __restrict__ Bp,
+                                  PackBatch b) {
+  const PackJob jb = b.job[blockIdx.y];
+  const int N = jb.N, RS = jb.RS, C = jb.C;
+  const bf16_t* w = W + jb.woff;
+  bf16_t* bp = Bp + jb.dst;
+  const int64_t chunks = (int64_t)(C / C2_CK) * RS * 2 * N;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < chunks;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int n = (int)(q % N);
+    int64_t r = q / N;
+    const int kh = (int)(r & 1);
+    r >>= 1;
+    const int tap = (int)(r % RS);
+    const int s = (int)(r / RS);
+    const int c0 = s * C2_CK + kh * 8;
+    uint4 v;
+    if (!jb.transpose) {
+      v = *(const uint4*)(w + ((int64_t)n * RS + tap) * C + c0);
+    } else {
+      uint16_t e[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = w[((int64_t)(c0 + j) * RS + tap) * N + n];
+      v = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
+                     e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
+    }
+    *(uint4*)(bp + q * 8) = v;
+  }
+}
+
 template <int MODE, int BN, int RS, int EPI, bool PATCH>
 __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   constexpr int NB = BN / 32;
@@ -1024,6 +1056,24 @@ hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmPara
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
                      (const bf16_t*)W, (bf16_t*)Bp, p.N, RS, C, mode == MODE_DGRAD ? 1 : 0);
+  return hipGetLastError();
+}
+
+PackJob pack_job(int64_t woff, int64_t dst, int mode, const GemmParams& p) {
+  PackJob j{};
+  j.woff = woff;
+  j.dst = dst;
+  j.N = p.N;
+  j.RS = p.g.R * p.g.S;
+  j.C = mode == MODE_FWD ? p.g.C : p.g.K;
+  j.transpose = mode == MODE_DGRAD ? 1 : 0;
+  return j;
+}
+
+hipError_t launch_pack_batch(const void* W, void* Bp, const PackBatch& b, hipStream_t s) {
+  if (b.count < 1 || b.count > PACK_BATCH) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_batch_kernel, dim3(64, (unsigned)b.count), dim3(256), 0, s,
+                     (const bf16_t*)W, (bf16_t*)Bp, b);
   return hipGetLastError();
 }
 

@@ -120,6 +120,19 @@ int64_t conv2_packed_elems(const GemmParams& p, int mode);
 hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
                                hipStream_t s);
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
+// Up to PACK_BATCH packings (launch_pack_weights of theta_bf16 + woff into
+// Bp + dst, offsets in elements) in one launch, passed by value.
+struct PackJob {
+  int64_t woff, dst;
+  int N, RS, C, transpose;
+};
+constexpr int PACK_BATCH = 64;
+struct PackBatch {
+  PackJob job[PACK_BATCH];
+  int count;
+};
+PackJob pack_job(int64_t woff, int64_t dst, int mode, const GemmParams& p);
+hipError_t launch_pack_batch(const void* W, void* Bp, const PackBatch& b, hipStream_t s);
 // Data gradient of a 3x3 stride-2 pad-1 convolution on the same packed
 // weights (conv2.hip, "stride-2 patch form"): p.a = dy [n][Ho][Wo][K], p.out =
 // dx [n][2Ho][2Wo][C] bf16 with the mask bits p.mbits (and p.addend) applied;

@@ -1457,8 +1457,15 @@ hipError_t workers_grad(const Model& m, Workspace& ws, const float* theta,
   ws.pack_waited = false;
   if (c.bf && ws.side && !ws.packs.empty()) {
     HS_TRY(fork(c));
-    for (const Workspace::Pack& e : ws.packs)
-      HS_TRY(launch_pack_weights(theta_bf16 + e.woff, ws.packed + e.dst, e.mode, e.p, ws.side));
+    PackBatch pb{};
+    for (const Workspace::Pack& e : ws.packs) {
+      pb.job[pb.count++] = pack_job(e.woff, e.dst, e.mode, e.p);
+      if (pb.count == PACK_BATCH) {
+        HS_TRY(launch_pack_batch(theta_bf16, ws.packed, pb, ws.side));
+        pb.count = 0;
+      }
+    }
+    if (pb.count > 0) HS_TRY(launch_pack_batch(theta_bf16, ws.packed, pb, ws.side));
     ws.pack_ready = side_mark(c);
     if (ws.pack_ready < 0) return hipErrorUnknown;
   }
