@@ -12,6 +12,23 @@
 
 namespace hs {
 
+// Target block counts of the weight-gradient launches (split-K over pixels):
+// about this many blocks per launch of the 3x3 patch kernel and of the fast
+// kernel, and at most this many splits of the fast kernel's reduction (its
+// per-worker reduce sums the splits of an output in sequence).
+#ifndef HS_WGRAD3_BLOCKS
+#define HS_WGRAD3_BLOCKS 512
+#endif
+#ifndef HS_WGRAD_FAST_TILES
+#define HS_WGRAD_FAST_TILES 1024
+#endif
+#ifndef HS_WGRAD_FAST_MAX_SPLITS
+#define HS_WGRAD_FAST_MAX_SPLITS 256
+#endif
+constexpr int kWgrad3Blocks = HS_WGRAD3_BLOCKS;
+constexpr int kWgradFastMaxSplits = HS_WGRAD_FAST_MAX_SPLITS;
+constexpr int kWgradFastTiles = HS_WGRAD_FAST_TILES;
+
 // ----------------------------------------------------------------------------
 // model construction
 // ----------------------------------------------------------------------------
@@ -733,7 +750,7 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
       total += ns[i];
     }
     const int tiles = (L.cout / 64) * (L.cin / 64);
-    const int want = tiles >= 512 ? 1 : 512 / tiles;
+    const int want = tiles >= kWgrad3Blocks ? 1 : kWgrad3Blocks / tiles;
     int per = ceil_div(total, want);
     if (per < 1) per = 1;
     auto count = [&](int q) {
@@ -771,7 +788,8 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
     kt[i] = ceil_div((c.sg.n0[i + 1] - c.sg.n0[i]) * hw, bke);
     total_kt += kt[i];
   }
-  int want = ceil_div(1024, tiles);
+  int want = ceil_div(kWgradFastTiles, tiles);
+  if (want > kWgradFastMaxSplits) want = kWgradFastMaxSplits;
   int per = ceil_div(total_kt, want > 0 ? want : 1);
   if (per < 4) per = 4;
   auto count_splits = [&](int q) {
@@ -1186,11 +1204,13 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     gp.drop(p1);
     gi = out;
   }
-  // stem (its ReLU mask is already applied); every weight gradient is done
-  // when this returns (the stem's weight gradient shares the split-K buffer)
-  HS_TRY(join(c));
+  // stem (its ReLU mask is already applied): its batch-norm backward beside
+  // the second stream's last weight gradients, then the join; every weight
+  // gradient is done when this returns (the stem's weight gradient shares
+  // the split-K buffer)
   HS_TAKE(gp, zs);
   HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
+  HS_TRY(join(c));
   return stem_wgrad(c, m.stem, gp[zs], S[0]);
 }
 
@@ -1315,11 +1335,12 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     gp.drop(p1);
     gi = out;
   }
-  // every weight gradient is done when this returns (the stem's shares the
-  // split-K buffer)
-  HS_TRY(join(c));
+  // the stem's batch-norm backward beside the second stream's last weight
+  // gradients, then the join; every weight gradient is done when this
+  // returns (the stem's shares the split-K buffer)
   HS_TAKE(gp, zs);
   HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
+  HS_TRY(join(c));
   return stem_wgrad(c, m.stem, gp[zs], S[0]);
 }
 
