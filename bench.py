@@ -54,8 +54,9 @@ MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
 # 2) on the bf16 path, bm = bn = 256 the stride-2 3x3 data-gradient patch
 # kernel (256 output-gradient positions x 64 channels per block, all four
 # parity classes, the shortcut's data gradient summed in); the others are
-# tiles of the fast implicit-GEMM kernel; (32, 64) is the direct bf16 stem
-# kernel (3 -> 64 channels from the fp32 NCHW batch); (256, 128) in mode 0
+# tiles of the fast implicit-GEMM kernel; (32, 64) the direct bf16 stem
+# kernels (3 -> 64 channels from the fp32 NCHW batch: forward in mode 0,
+# weight gradient in mode 2); (256, 128) in mode 0
 # the stride-2 3x3 forward patch kernel
 PROBE_TILES = [(512, 64), (512, 128), (512, 256), (64, 64), (128, 128), (128, 64), (64, 128),
                (256, 64), (256, 256), (32, 64), (256, 128)]
@@ -75,6 +76,8 @@ def kernel_name(mode, bm, bn, dtype):
     if bm == 256 and bn == 128 and mode == 0:
         return "conv2s2f_kernel<3x3 stride-2 forward, 256 positions x 128 channels, bf16>"
     if bm == 32 and bn == 64:
+        if mode == 2:
+            return "stem_wgrad_kernel<3->64 channels 3x3 weight gradient from fp32 NCHW, bf16>"
         return "stem_fwd_kernel<3->64 channels 3x3 from fp32 NCHW, bf16>"
     return "igemm_fast_kernel<%s, %s, %dx%d tile>" % (dtype, MODE_NAME[mode], bm, bn)
 

@@ -290,7 +290,9 @@ hs_status hs_partitioner_set_estimator(hs_partitioner* p, int32_t kind, double a
  * or 256; bm = 512 selects the 32x32 MFMA forward / data-gradient kernel,
  * 64 x 64 the 64-channel patch kernels: forward / data gradient in modes 0
  * and 1, 3x3 weight gradient in mode 2; 256 x 256 in mode 1 the stride-2
- * data-gradient patch kernel; 32 x 64 in mode 0 the direct bf16 stem) on this
+ * data-gradient patch kernel, in mode 0 the stride-2 forward patch kernel
+ * (256 x 128); 32 x 64 the direct bf16 stem, forward in mode 0 and weight
+ * gradient in mode 2) on this
  * workspace is
  * bracketed by two HIP events on the worker's stream, and its algorithmic
  * FLOPs (2 x pixels x c_out x taps x c_in, i.e. dense 3x3 taps, independent of

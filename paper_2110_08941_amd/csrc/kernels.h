@@ -167,6 +167,14 @@ hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s);
 bool stem_ok(int cin, int cout, int k, int stride, int pad, int H, int W);
 hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8, int n,
                            hipStream_t s);
+// The stem's weight gradient in bf16 (stem.hip), split-K per worker segment:
+// stem_wgrad_splits fills seg_split (blocks of each segment) from the
+// segments' sample counts and returns the split count; launch_stem_wgrad
+// writes split y's partial gW [64][27] (fp32) at part + 1728 y, from x (fp32
+// NCHW) and dy [n][32][32][64] bf16.
+int stem_wgrad_splits(const int* n, int nseg, int* seg_split);
+hipError_t launch_stem_wgrad(const float* x, const void* dy, float* part, const int* seg_n0,
+                             const int* seg_split, int nseg, hipStream_t s);
 hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
                                    hipStream_t s);
 // weights [k][rs][c] fp32 -> [k][rs][cp] activation type, zero padded

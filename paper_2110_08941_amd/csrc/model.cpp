@@ -1026,9 +1026,9 @@ int stem_cpad(const Ctx& c) { return c.bf ? 8 : 4; }
 hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void* y) {
   const int cp = stem_cpad(c);
   if (c.bf && stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W)) {
-    // the direct stem kernel (stem.hip); it also writes X0 for the weight gradient
+    // the direct stem kernel (stem.hip); the weight gradient reads x too
     const bool probe = probe_begin(c, MODE_FWD, 32, 64);
-    HS_TRY(launch_stem_fwd(x, c.W(L.w), y, X0, c.n, c.s));
+    HS_TRY(launch_stem_fwd(x, c.W(L.w), y, nullptr, c.n, c.s));
     if (probe) HS_TRY(probe_end(c, layer_flops(L, c.n)));
     return hipSuccess;
   }
@@ -1039,7 +1039,27 @@ hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void
   return conv_fwd(c, st, X0, y, false, c.ws.stem_w, nullptr, layer_flops(L, c.n));
 }
 
-hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0) {
+hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0,
+                      const float* x) {
+  if (c.bf && stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W)) {
+    // the direct stem weight gradient (stem.hip): split-K partials per worker
+    // from x and dz, then the per-worker reduce
+    int nseg_n[MAX_SEG], split[MAX_SEG + 1];
+    for (int i = 0; i < c.sg.count; ++i) nseg_n[i] = c.sg.n0[i + 1] - c.sg.n0[i];
+    const int splits = stem_wgrad_splits(nseg_n, c.sg.count, split);
+    const int64_t mn = (int64_t)L.cout * L.k * L.k * L.cin;
+    if ((int64_t)splits * mn > c.ws.splitk_floats) return hipErrorInvalidValue;
+    const bool probe = probe_begin(c, MODE_WGRAD, 32, 64);
+    HS_TRY(launch_stem_wgrad(x, dz, c.ws.splitk, c.sg.n0, split, c.sg.count, c.s));
+    if (probe) HS_TRY(probe_end(c, layer_flops(L, c.n)));
+    if (c.gbar)
+      return launch_splitk_reduce_wsum(c.ws.splitk, mn, mn, split, c.w, c.gbar + L.w, c.sg.count,
+                                       (int)mn, (int)mn, c.s);
+    float* outs[MAX_SEG];
+    for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
+    return launch_splitk_reduce_seg(c.ws.splitk, mn, mn, split, outs, c.sg.count, (int)mn,
+                                    (int)mn, c.s);
+  }
   ConvL st = L;
   st.cin = stem_cpad(c);
   return conv_wgrad(c, st, dz, X0, L.cin, layer_flops(L, c.n));
@@ -1091,7 +1111,7 @@ hipError_t small_cnn(const Ctx& c, const float* x, const int32_t* y, float* loss
   HS_TRY(conv_wgrad(c, m.c2, G[2], S[1]));
   HS_TRY(conv_dgrad(c, m.c2, G[2], G[0], nullptr, S[1]));             // dA1 * [A1 > 0]
   HS_TRY(bias_grad(c, m.c1.b, G[0], false, 1024, 32));
-  return stem_wgrad(c, m.c1, G[0], S[0]);
+  return stem_wgrad(c, m.c1, G[0], S[0], x);
 }
 
 // ---------------------------------------------------------- ResNet-18 ----
@@ -1211,7 +1231,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   HS_TAKE(gp, zs);
   HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
   HS_TRY(join(c));
-  return stem_wgrad(c, m.stem, gp[zs], S[0]);
+  return stem_wgrad(c, m.stem, gp[zs], S[0], x);
 }
 
 // ---------------------------------------------------------- ResNet-50 ----
@@ -1341,7 +1361,7 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
   HS_TAKE(gp, zs);
   HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
   HS_TRY(join(c));
-  return stem_wgrad(c, m.stem, gp[zs], S[0]);
+  return stem_wgrad(c, m.stem, gp[zs], S[0], x);
 }
 
 // -------------------------------------------------------------- VGG-16 ----
@@ -1404,7 +1424,7 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     gp.drop(pa);
     if (i == 0) {   // the first layer's weight gradient shares the split-K buffer
       HS_TRY(join(c));
-      HS_TRY(stem_wgrad(c, l.c, gp[dz], in));
+      HS_TRY(stem_wgrad(c, l.c, gp[dz], in, x));
       break;
     }
     HS_TRY(fork(c));

@@ -11,8 +11,8 @@
 // gathered per lane from the framed image (8 values of k for one output
 // pixel).  A wave computes 8 output rows of 32 pixels x 64 channels, one row
 // at a time: 4 MFMAs, then the row is staged in LDS and written as whole
-// 128-byte pixel rows.  The block also writes the image in the padded NHWC
-// layout (8 channels, 5 of them zero) that the weight gradient reads.
+// 128-byte pixel rows.  With x8 set, the block also writes the image in the
+// padded NHWC layout (8 channels, 5 of them zero).
 #include "kernels.h"
 
 namespace hs {
@@ -143,6 +143,164 @@ __global__ __launch_bounds__(256) void stem_fwd_kernel(const float* __restrict__
   }
 }
 
+// Weight gradient of the stem: gW[co][k] = sum over the pixels p of a worker's
+// images of dy[p][co] x patch[p][k], k = (3 r + s) 3 + ci, in split-K form.
+//
+// A block takes STW_IMG consecutive images of one worker (split y of the
+// launch; segment s owns splits seg_split[s] .. seg_split[s + 1] - 1) and
+// writes its partial [64][27] (fp32) at part + y * 1728.  Per image: the fp32
+// NCHW image goes to LDS in bf16 as three column-shifted copies
+// (img[ci][s][row + 1][c] = x[ci][row][c + s - 1], zero outside), so that the
+// 8 consecutive pixels of a tap are one aligned 16-byte read; dy goes to LDS
+// a quarter image (8 rows) at a time, transposed to [co][pixel] by the
+// copying threads, so that 8 consecutive pixels of a channel are one aligned
+// read too; each quarter's inputs are loaded into registers while the
+// previous one is computed.  The 32x32x16 MFMA runs with the taps as rows (27 of 32
+// used), the output channels as columns (two tiles) and 16 pixels per step;
+// the 4 waves take the steps in turn and their accumulators are added in a
+// fixed order at the end.
+constexpr int STW_IMG = 4;              // images per block
+constexpr int STW_ROWP = 32;            // shifted image copy: 32 columns per row
+constexpr int STW_COPY = 34 * STW_ROWP; // one shifted copy of one channel
+constexpr int STW_QPIX = 256;           // dy pixels per quarter
+constexpr int STW_TP = STW_QPIX + 8;    // transposed dy row pitch (bf16)
+
+struct StemWgradArgs {
+  const float* x;     // [n][3][32][32]
+  const bf16_t* dy;   // [n][32][32][64]
+  float* part;        // [splits][64][27]
+  int nseg;
+  int seg_split[MAX_SEG + 1];
+  int seg_n0[MAX_SEG + 1];
+};
+
+__global__ __launch_bounds__(256) void stem_wgrad_kernel(StemWgradArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t img[9 * STW_COPY];
+  // the transposed dy quarter; after the loop, the waves' accumulators
+  __shared__ __attribute__((aligned(16))) bf16_t dyt[ST_CO * STW_TP];
+  static_assert(3 * 2 * 16 * 64 * 4 <= ST_CO * STW_TP * 2, "accumulators fit the dy buffer");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kh = lane >> 5;
+  const int y = (int)blockIdx.x;
+  int sg = 0;
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i) sg += (i < a.nseg && y >= a.seg_split[i]) ? 1 : 0;
+  int sp = 0, n0 = 0, n1 = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == sg) {
+      sp = a.seg_split[i];
+      n0 = a.seg_n0[i];
+      n1 = a.seg_n0[i + 1];
+    }
+  const int i0 = n0 + (y - sp) * STW_IMG;
+  const int i1 = min(n1, i0 + STW_IMG);
+  const int nq = i1 > i0 ? 4 * (i1 - i0) : 0;   // quarters of this block
+
+  // the lane's tap row k and its offset in the shifted copies (-1: k >= 27)
+  const int k = lane & 31;
+  const int koff = k < ST_K ? (((k % 3) * 3 + (k / 3) % 3) * 34 + k / 9) * STW_ROWP : -1;
+  f32x16 acc[2];
+  acc[0] = acc[1] = (f32x16){};
+
+  // quarter q's inputs go to registers one quarter ahead
+  float4 xv[3];
+  uint4 dv[8];
+  auto load_x = [&](int im) {
+    const float* xb = a.x + (int64_t)im * 3 * ST_W * ST_W;
+#pragma unroll
+    for (int it = 0; it < 3; ++it) xv[it] = *(const float4*)(xb + 4 * (tid + 256 * it));
+  };
+  auto load_dy = [&](int im, int qt) {
+    const bf16_t* db = a.dy + ((int64_t)im * ST_W * ST_W + qt * STW_QPIX) * ST_CO;
+#pragma unroll
+    for (int it = 0; it < 8; ++it) dv[it] = *(const uint4*)(db + (int64_t)(tid + 256 * it) * 8);
+  };
+  if (nq > 0) {
+    load_x(i0);
+    load_dy(i0, 0);
+  }
+  // the copies' zero borders (never written below)
+  for (int i = tid; i < 9 * STW_COPY / 2; i += 256) ((uint32_t*)img)[i] = 0u;
+
+  for (int q = 0; q < nq; ++q) {
+    const int qt = q & 3;
+    __syncthreads();   // the previous quarter's reads are done
+    if (qt == 0) {
+      // the image at its three column shifts, rounded to bf16
+#pragma unroll
+      for (int it = 0; it < 3; ++it) {
+        const int e = 4 * (tid + 256 * it);
+        const int ci = e >> 10, row = (e >> 5) & 31, col = e & 31;
+        const float vv[4] = {xv[it].x, xv[it].y, xv[it].z, xv[it].w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int s2 = 0; s2 < 3; ++s2) {
+            const int c = col + u + 1 - s2;
+            if (c >= 0 && c < 32) img[((ci * 3 + s2) * 34 + row + 1) * STW_ROWP + c] = f2bf(vv[u]);
+          }
+      }
+    }
+    // the dy quarter (rows 8 qt .. 8 qt + 7), transposed into [co][pixel]
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int c = tid + 256 * it;               // 16-byte chunk: pixel c / 8, channels 8 (c % 8)
+      const int px = c >> 3, co = (c & 7) * 8;
+      const uint32_t w[4] = {dv[it].x, dv[it].y, dv[it].z, dv[it].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dyt[(co + 2 * e) * STW_TP + px] = (bf16_t)(w[e] & 0xffffu);
+        dyt[(co + 2 * e + 1) * STW_TP + px] = (bf16_t)(w[e] >> 16);
+      }
+    }
+    if (q + 1 < nq) {
+      const int im1 = i0 + ((q + 1) >> 2);
+      if (((q + 1) & 3) == 0) load_x(im1);
+      load_dy(im1, (q + 1) & 3);
+    }
+    __syncthreads();
+    // steps of 16 pixels: wave w takes steps w, w + 4, w + 8, w + 12
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int step = wave + 4 * st;             // pixels 16 step .. + 15 of the quarter
+      const int row = qt * 8 + step / 2, col0 = (step & 1) * 16 + 8 * kh;
+      uint4 pv = make_uint4(0u, 0u, 0u, 0u);
+      if (koff >= 0) pv = *(const uint4*)(img + koff + row * STW_ROWP + col0);
+      bf16x8 pa;
+      __builtin_memcpy(&pa, &pv, 16);
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const uint4 dd = *(const uint4*)(dyt + (32 * ct + (lane & 31)) * STW_TP + 16 * step + 8 * kh);
+        bf16x8 db8;
+        __builtin_memcpy(&db8, &dd, 16);
+        acc[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, db8, acc[ct], 0, 0, 0);
+      }
+    }
+  }
+  // acc[ct]: lane holds co = 32 ct + (lane & 31), taps k = 8 q + 4 kh + e;
+  // waves 1..3 hand theirs to LDS, wave 0 adds them in order and writes
+  float (*red)[2][16][64] = (float (*)[2][16][64])dyt;
+  __syncthreads();
+  if (wave > 0) {
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) red[wave - 1][ct][e][lane] = acc[ct][e];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float* out = a.part + (int64_t)y * (ST_CO * ST_K);
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float v = ((acc[ct][e] + red[0][ct][e][lane]) + red[1][ct][e][lane]) + red[2][ct][e][lane];
+        const int kk = 8 * (e >> 2) + 4 * kh + (e & 3);
+        if (kk < ST_K) out[(32 * ct + (lane & 31)) * ST_K + kk] = v;
+      }
+  }
+}
+
 }  // namespace
 
 bool stem_ok(int cin, int cout, int k, int stride, int pad, int H, int W) {
@@ -154,6 +312,35 @@ hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8
   if (n < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stem_fwd_kernel, dim3((unsigned)n), dim3(256), 0, s, x,
                      (const bf16_t*)w_bf16, (bf16_t*)y, (bf16_t*)x8);
+  return hipGetLastError();
+}
+
+int stem_wgrad_splits(const int* n, int nseg, int* seg_split) {
+  seg_split[0] = 0;
+  for (int i = 0; i < nseg; ++i) {
+    const int b = n[i] > 0 ? (n[i] + STW_IMG - 1) / STW_IMG : 1;
+    seg_split[i + 1] = seg_split[i] + b;
+  }
+  return seg_split[nseg];
+}
+
+hipError_t launch_stem_wgrad(const float* x, const void* dy, float* part, const int* seg_n0,
+                             const int* seg_split, int nseg, hipStream_t s) {
+  if (nseg < 1 || nseg > MAX_SEG || seg_split[nseg] < 1) return hipErrorInvalidValue;
+  StemWgradArgs a{};
+  a.x = x;
+  a.dy = (const bf16_t*)dy;
+  a.part = part;
+  a.nseg = nseg;
+  for (int i = 0; i <= nseg; ++i) {
+    a.seg_split[i] = seg_split[i];
+    a.seg_n0[i] = seg_n0[i];
+  }
+  for (int i = nseg + 1; i <= MAX_SEG; ++i) {
+    a.seg_split[i] = seg_split[nseg];
+    a.seg_n0[i] = seg_n0[nseg];
+  }
+  hipLaunchKernelGGL(stem_wgrad_kernel, dim3((unsigned)seg_split[nseg]), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
