@@ -192,9 +192,14 @@ def copy_calibration(mib, reps=4):
 # committed HBM-traffic counter summaries, per workload
 TRAFFIC_PROFILE = {"resnet18_bf16": os.path.join(ROOT, "profiles",
                                                  "hbm_traffic_resnet18_bf16_n2048_m8.md")}
-# template instance of each probed kernel whose HBM traffic has been counted
-PROBE_KERNEL = {(0, 512, 128, "bf16"): "conv2_kernel<0, 128, 9, 0, true>",
-                (2, 64, 64, "bf16"): "wgrad3_kernel<32>"}
+# the HBM-traffic summary's entry for each probed kernel family (counted bytes per launch)
+PROBE_KERNEL = {(0, 512, 128, "bf16"): "conv2 forward",
+                (2, 64, 64, "bf16"): "wgrad3 (every width)",
+                (1, 256, 256, "bf16"): "conv2s2 data gradient",
+                (0, 256, 128, "bf16"): "conv2s2f forward",
+                (0, 64, 64, "bf16"): "conv64 forward",
+                (0, 32, 64, "bf16"): "stem forward",
+                (2, 32, 64, "bf16"): "stem weight gradient"}
 
 
 def measured_traffic(workload, kernel):
@@ -423,6 +428,9 @@ def main():
             "flops_per_launch": top["flops_per_step"] / max(top["launches_per_step"], 1),
             "selection": "the GEMM family with the largest time per step (HIP events "
                          "around its launches in the step)"}
+        for k in kernels:   # counted HBM bytes per launch, where the summary has the family
+            k["traffic"] = measured_traffic(args.workload, PROBE_KERNEL.get(
+                (k["mode"], k["tile"][0], k["tile"][1], wl.dtype)))
         result["kernels"] = kernels
     result["hbm_roofline"] = r["hbm_roofline"]
     result["sim_step"] = r["sim_step"]
