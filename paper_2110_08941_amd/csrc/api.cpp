@@ -1,4 +1,5 @@
-// C ABI of libhs (declared in include/hs.h): argument checking, object
+// C ABI of libhs (declared in include/hs.h; the measurement and test entry
+// points in include/hs_testing.h): argument checking, object
 // lifetime, and the host-side parts of the method (compute-power estimate,
 // repartition, the Dynamic Partitioning window).
 //
@@ -15,6 +16,7 @@
 #include <vector>
 
 #include "../../include/hs.h"
+#include "../../include/hs_testing.h"
 #include "model.h"
 
 using namespace hs;

@@ -1,5 +1,5 @@
 """The C-ABI library on the host (no GPU needed): it loads, exports every
-symbol include/hs.h declares, and its host-side parts (parameter layout,
+symbol include/*.h declares (hs.h, the step; hs_testing.h, measurement and tests), and its host-side parts (parameter layout,
 compute-power estimate, repartition, Dynamic Partitioning window) agree with
 the oracle exactly."""
 import math
@@ -18,7 +18,8 @@ hs = pytest.importorskip("paper_2110_08941_amd.hs", reason="libhs.so not built")
 
 
 def declared_symbols():
-    text = open(os.path.join(ROOT, "include", "hs.h")).read()
+    text = "".join(open(os.path.join(ROOT, "include", f)).read()
+                   for f in sorted(os.listdir(os.path.join(ROOT, "include"))) if f.endswith(".h"))
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(hs_[a-z0-9_]+)\s*\(", text)))
 
