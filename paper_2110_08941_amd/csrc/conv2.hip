@@ -596,6 +596,12 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
   constexpr int BBUF = BREG * 512;
   constexpr int PPLANE = S2_POS * 16 + 128;
   constexpr int NPL = KK * 2 * (PROJ ? 2 : 1);  // dy planes (8 channels each): main, shortcut
+  // dy patch of a slice: [position / 32][piece (8 channels)][position % 32]
+  // 16-byte slots, the shortcut's after the main one
+  constexpr int AREG = S2_POS * 4 * 16;
+  static_assert(KK == 2, "four 8-channel pieces per slice");
+  static_assert((PROJ ? 2 : 1) * AREG <= NPL * PPLANE, "dy patches fit their buffers");
+  auto aslot = [](int pos, int piece) { return ((pos >> 5) * 4 + piece) * 32 + (pos & 31); };
   constexpr int EROW = 36;
   constexpr bool EADD = (EPI & EPI_ADD) != 0, EBITS = (EPI & EPI_MBITS) != 0;
   static_assert(5 * 32 * EROW * 4 <= BBUF * 16, "epilogue staging of five waves fits a B buffer");
@@ -675,13 +681,13 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
   auto read_tap = [&](const uint4* Bb, const char* P, int u, uint4& ra, uint4 (&rb)[NB]) {
     const int kk = u / NT, t = u - kk * NT;
     if (PROJ && t == RS) {
-      ra = *(const uint4*)(P + (2 * KK + 2 * kk + kh) * PPLANE + q * 16);
+      ra = *(const uint4*)(P + AREG + aslot(q, 2 * kk + kh) * 16);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
         rb[nb] = Bb[KK * SEG + (2 * kk + kh) * BN + nb * 32 + (lane & 31)];
     } else {
       const int off = (t / 3 == 0 ? Wo : 0) + (t % 3 == 0 ? 1 : 0);
-      ra = *(const uint4*)(P + (2 * kk + kh) * PPLANE + ((q + off) & (S2_POS - 1)) * 16);
+      ra = *(const uint4*)(P + aslot((q + off) & (S2_POS - 1), 2 * kk + kh) * 16);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
         rb[nb] = Bb[((kk * RS + t) * 2 + kh) * BN + nb * 32 + (lane & 31)];
@@ -714,20 +720,19 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
       }
       __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bb + 512 * i + wbase), 16, 0, 0);
     }
-    const int px = tid & (S2_POS - 1), h = tid >> 8;
-    int64_t m = (int64_t)tile_m0 + px;
+    // wave w copies the 4 pieces of 8 channels of its 32 positions, two
+    // pieces per copy: lanes 0-31 one piece, lanes 32-63 the next, so that
+    // a position's 64 bytes of the slice are requested together
+    int64_t m = (int64_t)tile_m0 + 32 * wave + (lane & 31);
     m = m < p.M ? m : p.M - 1;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int64_t col = (int64_t)sl * S2_CK + kk * C2_CK + 8 * h;
-      __builtin_amdgcn_global_load_lds((gbl_cptr)(A + m * Kc + col),
-                                       (lds_ptr)(P + (2 * kk + h) * PPLANE +
-                                                 (wbase & (S2_POS - 1)) * 16),
-                                       16, 0, 0);
+    for (int inst = 0; inst < 2; ++inst) {
+      const int piece = 2 * inst + (lane >> 5);
+      const int64_t col = (int64_t)sl * S2_CK + 8 * piece;
+      const int dst = aslot(32 * wave, 2 * inst) * 16;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)(A + m * Kc + col), (lds_ptr)(P + dst), 16, 0, 0);
       if (PROJ)
-        __builtin_amdgcn_global_load_lds((gbl_cptr)(A2 + m * Kc + col),
-                                         (lds_ptr)(P + (2 * KK + 2 * kk + h) * PPLANE +
-                                                   (wbase & (S2_POS - 1)) * 16),
+        __builtin_amdgcn_global_load_lds((gbl_cptr)(A2 + m * Kc + col), (lds_ptr)(P + AREG + dst),
                                          16, 0, 0);
     }
   };
