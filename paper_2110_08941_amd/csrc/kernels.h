@@ -151,9 +151,9 @@ bool conv64_ok(int mode, const GemmParams& p);
 // blocks of a conv64 launch (one per CU, at most one per tile)
 int conv64_blocks(const GemmParams& p);
 hipError_t launch_conv64(int mode, const GemmParams& p, hipStream_t s);
-// bf16 weight gradient of 3x3 stride-1 pad-1 layers (wgrad3.hip): the input
-// patch of a slice of output pixels staged once in LDS, the 9 taps as
-// shifted transposing reads.  kt_per_split counts slices (wgrad3_slices per
+// bf16 weight gradient of 3x3 pad-1 layers, stride 1 or 2 (wgrad3.hip): the
+// input patch of a slice of output pixels staged once in LDS (stride 2: as
+// four parity planes), the 9 taps as shifted transposing reads.  kt_per_split counts slices (wgrad3_slices per
 // worker segment); the split table (nseg, seg_split, seg_n0) is the caller's;
 // out / split_stride as WGRAD.
 bool wgrad3_ok(const GemmParams& p);

@@ -32,6 +32,20 @@
 // compile-time offset: no address arithmetic and no branches in the loop.
 // The next k step's fragments are read while the current step's MFMAs run.  The reduction is split over slices (split-K, per worker segment):
 // split y writes its partial gW at out + y * split_stride.
+//
+// Stride 2 (wgrad3s2_kernel, output width WO, input width 2 WO): an output
+// pixel o reads input rows 2 o - 1, 2 o, 2 o + 1 (and the same columns), so
+// consecutive output pixels are two input pixels apart.  The patch is kept
+// as four parity planes of the input, plane (a, b) holding the pixels of
+// row parity a and column parity b with one zero row on top and one zero
+// column on the left: in plane coordinates tap r = 0 is row o of the odd
+// plane, r = 1 row o + 1 of the even one, r = 2 row o + 1 of the odd one
+// (likewise for columns).  A tap is again a row offset into one plane, and
+// the lane's 8 consecutive output pixels are 8 consecutive plane slots:
+// taps s = 0 and s = 2 are the odd-column plane at shifts 0 and 1 (three
+// reads, one byte-aligned), s = 1 the even-column plane at shift 1 (two
+// reads).  A slice is 64 output pixels (four planes of its input take four
+// times the slots of a stride-1 patch).
 #include "kernels.h"
 
 namespace hs {
@@ -357,16 +371,306 @@ __global__ __launch_bounds__(768) void wgrad3_kernel(GemmParams p) {
     }
 }
 
+namespace {
+
+// Geometry of a stride-2 slice for output width WO (square images, input
+// width 2 WO).  Slot of plane pl = 2 a + b (row parity a, column parity b),
+// plane row fy, plane column fx in frame f: f FS + pl PS + fy FW + fx; plane
+// row fy of a slice whose first output row is y0 holds input row
+// 2 (y0 + fy - 1) + a, plane column fx input column 2 (fx - 1) + b.
+template <int WO>
+struct Slice2 {
+  static constexpr int PIX = 64;                        // output pixels per slice
+  static constexpr int WI = 2 * WO;                     // input width
+  static constexpr int HWO = WO * WO, HWI = WI * WI;
+  static constexpr bool ROWS = HWO >= PIX;              // slice = rows of one image
+  static constexpr int RG = ROWS ? PIX / WO : WO;       // output rows per frame
+  static constexpr int NF = ROWS ? 1 : PIX / HWO;       // frames (images) per slice
+  static constexpr int FW = WO + 1, FR = RG + 1;        // plane with its zero row / column
+  static constexpr int PS = FR * FW;                    // slots per plane
+  static constexpr int FS = 4 * PS;                     // slots per frame
+  static constexpr int SLOTS = NF * FS;
+  static constexpr int SPI = ROWS ? WO / RG : 1;        // slices per image (ROWS)
+  __device__ static int frame(int p) { return p / (RG * WO); }
+  __device__ static int prow(int p) { return (p % (RG * WO)) / WO; }
+  __device__ static int pcol(int p) { return p % WO; }
+  // slot of output pixel p in plane 0 at plane row / column offset 0: the
+  // plane, the filter row's row offset and the tap's column offset are added
+  __device__ static int slot(int p) { return frame(p) * FS + prow(p) * FW + pcol(p); }
+  // the lane's first fragment pixel is 16 kk + kb + 4 h (kb = 0 or 8)
+  __device__ static int lane_slot(int kb) {
+    if (WO >= 16) return kb;               // same output row
+    if (WO == 8) return (kb / 8) * FW;     // next output row
+    return (kb / 4) * FW;                  // WO = 4: two rows down
+  }
+};
+
+}  // namespace
+
+template <int WO>
+__global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
+  typedef Slice2<WO> S;
+  constexpr int NT = 768;
+  constexpr int AROWS = S::PIX;
+  constexpr int ACH = AROWS * 8, BCH = S::SLOTS * 8;   // 16-byte chunks
+  constexpr int AIT = (ACH + NT - 1) / NT, BIT = (BCH + NT - 1) / NT;
+  static_assert(ACH % 64 == 0, "dy rows: whole waves per copy round");
+  // plane rows: the 4-row reads at +8 may pass the last slot by up to 3 rows
+  // (values unused)
+  constexpr int BR8 = (S::SLOTS + 7) / 8 * 8;
+  constexpr int BROWS = BR8 > S::SLOTS + 4 ? BR8 : S::SLOTS + 4;
+  __shared__ __attribute__((aligned(16))) char sA0[AROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sA1[AROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sB0[BROWS * ROWB];
+  __shared__ __attribute__((aligned(16))) char sB1[BROWS * ROWB];
+
+  const ConvGeom& g = p.g;
+  const int C = g.C, K = g.K;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 2, wk = (wave >> 1) & 1, wc = wave & 1;
+  // all tiles of a split on one XCD, as in the stride-1 kernel
+  const int nblk = (int)(gridDim.x * gridDim.y), q8 = nblk / 8;
+  int lb = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+  if (lb < 8 * q8) lb = (lb % 8) * q8 + lb / 8;
+  const int bx = lb % (int)gridDim.x, by = lb / (int)gridDim.x;
+  const int tiles_c = C / 64;
+  const int k0 = (bx / tiles_c) * 64, c0 = (bx % tiles_c) * 64;
+
+  int sg = 0;
+#pragma unroll
+  for (int i = 1; i < MAX_SEG; ++i) sg += (i < p.nseg && by >= p.seg_split[i]) ? 1 : 0;
+  int sp = 0, s_n0 = 0, s_n1 = 0;
+#pragma unroll
+  for (int i = 0; i < MAX_SEG; ++i)
+    if (i == sg) {
+      sp = p.seg_split[i];
+      s_n0 = p.seg_n0[i];
+      s_n1 = p.seg_n0[i + 1];
+    }
+  const int nimg = s_n1 - s_n0;
+  const int nsl = S::ROWS ? nimg * S::SPI : (nimg + S::NF - 1) / S::NF;
+  const int j0 = (by - sp) * p.kt_per_split;
+  const int cnt = max(0, min(p.kt_per_split, nsl - j0));
+
+  const bf16_t* X = (const bf16_t*)p.b;    // x  [n][2 WO][2 WO][C]
+  const bf16_t* DY = (const bf16_t*)p.a;   // dy [n][WO][WO][K]
+  const void* zero16 = &g_zero16;
+  __asm__ volatile("" : "+s"(zero16));
+
+  // Copy slice j into (As, Bs), as the stride-1 kernel: chunk NT i + 64 w +
+  // lane of copy round i; the lane parts of the source offsets are computed
+  // once.  Plane slots: element offset boff relative to input row 2 y0 of
+  // the frame, the relative input row bfy for the image-row check, the
+  // frame bfr; zero-column slots and chunks past the last get NEVER.
+  constexpr int NEVER = 1 << 28;
+  int aoff[AIT], afr[AIT], boff[BIT], bfy[BIT], bfr[BIT];
+#pragma unroll
+  for (int i = 0; i < AIT; ++i) {
+    const int d = tid + NT * i, row = d >> 3;
+    const int ch = (d & 7) ^ (((row >> 1) & 1) << 2);
+    afr[i] = S::frame(row);
+    aoff[i] = ((afr[i] * S::HWO * (S::ROWS ? 0 : 1)) + S::prow(row) * WO + S::pcol(row)) * K + ch * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < BIT; ++i) {
+    const int d = tid + NT * i, sl = d >> 3;
+    const int ch = (d & 7) ^ (((sl >> 1) & 1) << 2);
+    const int f = sl / S::FS, rem = sl - f * S::FS;
+    const int pl = rem / S::PS, r2 = rem - pl * S::PS;
+    const int fy = r2 / S::FW, fx = r2 - fy * S::FW;
+    const int iy = 2 * (fy - 1) + (pl >> 1), ix = 2 * (fx - 1) + (pl & 1);
+    const bool colok = d < BCH && (unsigned)ix < (unsigned)S::WI;
+    boff[i] = ((S::ROWS ? 0 : f * S::HWI) + iy * S::WI + ix) * C + ch * 8;
+    bfy[i] = colok ? iy : NEVER;
+    bfr[i] = colok ? f : NEVER;
+  }
+  auto copy_slice = [&](int j, char* As, char* Bs) {
+    int img0, y0, nfr;
+    if (S::ROWS) {
+      img0 = s_n0 + j / S::SPI;
+      y0 = (j % S::SPI) * S::RG;
+      nfr = 1;
+    } else {
+      img0 = s_n0 + j * S::NF;
+      y0 = 0;
+      nfr = s_n1 - img0;
+    }
+    const bf16_t* dyb = DY + ((int64_t)(img0 * WO + y0) * WO) * K + k0;
+    const bf16_t* xb = X + ((int64_t)(img0 * S::WI + 2 * y0) * S::WI) * C + c0;
+#pragma unroll
+    for (int i = 0; i < AIT; ++i) {
+      if (NT * i + 64 * wave >= ACH) continue;              // wave-uniform
+      const void* src = afr[i] < nfr || S::ROWS ? (const void*)(dyb + aoff[i]) : zero16;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(As + (NT * i + 64 * wave) * 16), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < BIT; ++i) {
+      if (NT * i + 64 * wave >= BCH) continue;              // wave-uniform
+      const bool ok = bfr[i] < nfr && (unsigned)(2 * y0 + bfy[i]) < (unsigned)S::WI;
+      const void* src = ok ? (const void*)(xb + boff[i]) : zero16;
+      __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(Bs + (NT * i + 64 * wave) * 16), 16, 0, 0);
+    }
+  };
+  auto tr_read = [&](const char* lane_base, int off) -> i16x4 {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(lds_i16p)(short*)(lane_base + off));
+  };
+  f32x16 acc[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) acc[t] = (f32x16){};
+
+  const int grp = lane >> 4, q = lane & 15;
+  const int colA = wk * 32 + 16 * (grp & 1);
+  const int colB = wc * 32 + 16 * (grp & 1);
+  const int kb = 8 * (lane >> 5);
+  // filter row wr: plane row parity and row offset (r = 0: odd, +0;
+  // r = 1: even, +1; r = 2: odd, +1); the odd-column plane at column offset
+  // 0 (taps s = 0, 2) and the even-column plane at offset 1 (tap s = 1)
+  const int pa = wr == 1 ? 0 : 1, dr = wr == 0 ? 0 : 1;
+  const int rowB = dr * S::FW + S::lane_slot(kb) + (q >> 2);
+  int baseA[4], baseO[4], baseE[4];
+#pragma unroll
+  for (int ph = 0; ph < 4; ++ph) {
+    baseA[ph] = swz_off(ph + kb + (q >> 2), (colA + 4 * (q & 3)) * 2);
+    baseO[ph] = swz_off(ph + (2 * pa + 1) * S::PS + rowB, (colB + 4 * (q & 3)) * 2);
+    baseE[ph] = swz_off(ph + 2 * pa * S::PS + 1 + rowB, (colB + 4 * (q & 3)) * 2);
+  }
+  auto rd = [&](const char* base, const int (&lbase)[4], int row0) {
+    return tr_read(base + lbase[row0 & 3], (row0 & ~3) * ROWB);
+  };
+  // fragments of k step kk: dy (2 reads), the odd-column plane (3 reads; WO
+  // = 4: 2 per image-row half) and the even-column plane (2; WO = 4: 1 per
+  // half)
+  constexpr int NBO = WO >= 8 ? 3 : 4;
+  constexpr int NBE = 2;
+  auto read_k = [&](const char* pa_, const char* pb_, int kk, i16x4 (&fa)[2], i16x4 (&fo)[NBO],
+                    i16x4 (&fe)[NBE]) {
+    fa[0] = rd(pa_, baseA, 16 * kk);
+    fa[1] = rd(pa_, baseA, 16 * kk + 4);
+    if constexpr (WO >= 8) {
+      const int r0 = S::slot(16 * kk);
+      fo[0] = rd(pb_, baseO, r0);
+      fo[1] = rd(pb_, baseO, r0 + 4);
+      fo[2] = rd(pb_, baseO, r0 + 8);
+      fe[0] = rd(pb_, baseE, r0);
+      fe[1] = rd(pb_, baseE, r0 + 4);
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r0 = S::slot(16 * kk + 4 * h);
+        fo[2 * h] = rd(pb_, baseO, r0);
+        fo[2 * h + 1] = rd(pb_, baseO, r0 + 4);
+        fe[h] = rd(pb_, baseE, r0);
+      }
+    }
+  };
+  // operands: bv[0] odd plane at shift 0, bv[2] at shift 1 (byte align),
+  // bv[1] the even plane as read
+  auto prep_k = [&](const i16x4 (&fa)[2], const i16x4 (&fo)[NBO], const i16x4 (&fe)[NBE],
+                    bf16x8& av, bf16x8 (&bv)[3]) {
+    __builtin_memcpy(&av, &fa[0], 8);
+    __builtin_memcpy((char*)&av + 8, &fa[1], 8);
+    __builtin_memcpy(&bv[1], &fe[0], 8);
+    __builtin_memcpy((char*)&bv[1] + 8, &fe[1], 8);
+    if constexpr (WO >= 8) {
+      uint32_t w[6];
+      __builtin_memcpy(&w[0], &fo[0], 8);
+      __builtin_memcpy(&w[2], &fo[1], 8);
+      __builtin_memcpy(&w[4], &fo[2], 8);
+      uint32_t f0[4], f2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f0[i] = w[i];
+        f2[i] = __builtin_amdgcn_alignbyte(w[i + 1], w[i], 2);
+      }
+      __builtin_memcpy(&bv[0], f0, 16);
+      __builtin_memcpy(&bv[2], f2, 16);
+    } else {
+      uint32_t d[2][4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        __builtin_memcpy(&d[h][0], &fo[2 * h], 8);
+        __builtin_memcpy(&d[h][2], &fo[2 * h + 1], 8);
+      }
+      uint32_t f0[4], f2[4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          f0[2 * h + i] = d[h][i];
+          f2[2 * h + i] = __builtin_amdgcn_alignbyte(d[h][i + 1], d[h][i], 2);
+        }
+      __builtin_memcpy(&bv[0], f0, 16);
+      __builtin_memcpy(&bv[2], f2, 16);
+    }
+  };
+
+  constexpr int KK = S::PIX / 16;
+  i16x4 fa[2], fo[NBO], fe[NBE];
+  auto slice = [&](int i, const char* pa_, const char* pb_, char* na, char* nb) {
+    const bool more = i + 1 < cnt;
+    if (more) copy_slice(j0 + i + 1, na, nb);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      bf16x8 av, bv[3];
+      prep_k(fa, fo, fe, av, bv);
+      __builtin_amdgcn_sched_barrier(0);
+      i16x4 ga[2], go[NBO], ge[NBE];
+      if (kk + 1 < KK) read_k(pa_, pb_, kk + 1, ga, go, ge);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[s], av, acc[s], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kk + 1 < KK) {
+        fa[0] = ga[0];
+        fa[1] = ga[1];
+#pragma unroll
+        for (int u = 0; u < NBO; ++u) fo[u] = go[u];
+#pragma unroll
+        for (int u = 0; u < NBE; ++u) fe[u] = ge[u];
+      }
+    }
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (more) read_k(na, nb, 0, fa, fo, fe);
+  };
+  if (cnt > 0) {
+    copy_slice(j0, sA0, sB0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    read_k(sA0, sB0, 0, fa, fo, fe);
+  }
+  for (int i = 0; i < cnt; i += 2) {
+    slice(i, sA0, sB0, sA1, sB1);
+    if (i + 1 < cnt) slice(i + 1, sA1, sB1, sA0, sB0);
+  }
+
+  // ---- epilogue as the stride-1 kernel
+  const int co = k0 + wk * 32 + (lane & 31);
+  float* out = (float*)p.out + (int64_t)by * p.split_stride;
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int ci = c0 + wc * 32 + 8 * r4 + 4 * (lane >> 5);
+      *(float4*)(out + ((int64_t)co * 9 + 3 * wr + s) * C + ci) =
+          make_float4(acc[s][4 * r4], acc[s][4 * r4 + 1], acc[s][4 * r4 + 2], acc[s][4 * r4 + 3]);
+    }
+}
+
 bool wgrad3_ok(const GemmParams& p) {
   const ConvGeom& g = p.g;
-  if (g.R != 3 || g.S != 3 || g.stride != 1 || g.pad != 1) return false;
-  if (g.H != g.W || (g.W != 32 && g.W != 16 && g.W != 8 && g.W != 4)) return false;
-  return g.C % 64 == 0 && g.K % 64 == 0;
+  if (g.R != 3 || g.S != 3 || g.pad != 1 || g.C % 64 != 0 || g.K % 64 != 0) return false;
+  if (g.stride == 2)   // output 16, 8 or 4 wide, input exactly twice that
+    return g.Ho == g.Wo && (g.Wo == 16 || g.Wo == 8 || g.Wo == 4) && g.H == 2 * g.Ho &&
+           g.W == 2 * g.Wo;
+  if (g.stride != 1) return false;
+  return g.H == g.W && (g.W == 32 || g.W == 16 || g.W == 8 || g.W == 4);
 }
 
 // slices of one worker segment of nimg images
 int wgrad3_slices(const GemmParams& p, int nimg) {
-  const int W = p.g.W, HW = W * W, pix = W >= 16 ? 256 : 128;
+  const int W = p.g.Wo, HW = W * W;
+  const int pix = p.g.stride == 2 ? 64 : (W >= 16 ? 256 : 128);
   if (HW >= pix) return nimg * (HW / pix);
   return (nimg + pix / HW - 1) / (pix / HW);
 }
@@ -376,6 +680,14 @@ int wgrad3_slices(const GemmParams& p, int nimg) {
 hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s) {
   if (!wgrad3_ok(p) || p.nseg < 1) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((p.g.K / 64) * (p.g.C / 64)), (unsigned)p.seg_split[p.nseg]);
+  if (p.g.stride == 2) {
+    switch (p.g.Wo) {
+      case 16: hipLaunchKernelGGL(wgrad3s2_kernel<16>, grid, dim3(768), 0, s, p); break;
+      case 8: hipLaunchKernelGGL(wgrad3s2_kernel<8>, grid, dim3(768), 0, s, p); break;
+      default: hipLaunchKernelGGL(wgrad3s2_kernel<4>, grid, dim3(768), 0, s, p); break;
+    }
+    return hipGetLastError();
+  }
   switch (p.g.W) {
     case 32: hipLaunchKernelGGL(wgrad3_kernel<32>, grid, dim3(768), 0, s, p); break;
     case 16: hipLaunchKernelGGL(wgrad3_kernel<16>, grid, dim3(768), 0, s, p); break;

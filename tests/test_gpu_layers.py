@@ -80,6 +80,23 @@ PATCH_SHAPES = [
 ]
 
 
+# bf16 weight gradients of 3x3 stride-2 layers (the parity-plane patch
+# kernel for 16-, 8- and 4-wide outputs): several slices per image, whole-
+# image slices, and slices of four images with a ragged last one
+WGRAD_S2_SHAPES = [
+    (9, 32, 32, 64, 128, 3, 2, 1),
+    (4, 32, 32, 128, 64, 3, 2, 1),
+    (13, 16, 16, 128, 256, 3, 2, 1),
+    (7, 8, 8, 256, 128, 3, 2, 1),
+    (18, 8, 8, 64, 64, 3, 2, 1),
+]
+
+
+@pytest.mark.parametrize("shape", WGRAD_S2_SHAPES, ids=[str(s) for s in WGRAD_S2_SHAPES])
+def test_layer_wgrad_stride2(shape):
+    check_layer_gemm(2, shape, "bf16", packed=False)
+
+
 # bf16 forward (bf16 output) and data gradient given a scratch buffer: the
 # 32x32 MFMA kernel on packed weights wherever the shape allows it
 @pytest.mark.parametrize("shape", SHAPES + PATCH_SHAPES, ids=[str(s) for s in SHAPES + PATCH_SHAPES])
