@@ -57,9 +57,10 @@ MODE_NAME = {0: "forward", 1: "data gradient", 2: "weight gradient"}
 # tiles of the fast implicit-GEMM kernel; (32, 64) the direct bf16 stem
 # kernels (3 -> 64 channels from the fp32 NCHW batch: forward in mode 0,
 # weight gradient in mode 2); (256, 128) in mode 0
-# the stride-2 3x3 forward patch kernel
+# the stride-2 3x3 forward patch kernel; (64, 256) in mode 2 the stride-2
+# 3x3 weight-gradient patch kernel (input as four parity planes)
 PROBE_TILES = [(512, 64), (512, 128), (512, 256), (64, 64), (128, 128), (128, 64), (64, 128),
-               (256, 64), (256, 256), (32, 64), (256, 128)]
+               (256, 64), (256, 256), (32, 64), (256, 128), (64, 256)]
 # sub-objects of the JSON line: the other large single-GPU workloads
 EXTRA = ("resnet18_fp32", "vgg16_bf16")
 
@@ -67,6 +68,8 @@ EXTRA = ("resnet18_fp32", "vgg16_bf16")
 def kernel_name(mode, bm, bn, dtype):
     if bm == 512:
         return "conv2_kernel<%s, %dx%d tile, 32x32x16 MFMA, %s>" % (MODE_NAME[mode], bm, bn, dtype)
+    if bm == 64 and bn == 256 and mode == 2:
+        return "wgrad3s2_kernel<3x3 stride-2 weight gradient, 64x64x9 tile, parity planes, bf16>"
     if bm == 64 and bn == 64 and dtype == "bf16":
         if mode == 2:
             return "wgrad3_kernel<3x3 weight gradient, 64x64x9 tile, bf16>"
@@ -195,6 +198,7 @@ TRAFFIC_PROFILE = {"resnet18_bf16": os.path.join(ROOT, "profiles",
 # the HBM-traffic summary's entry for each probed kernel family (counted bytes per launch)
 PROBE_KERNEL = {(0, 512, 128, "bf16"): "conv2 forward",
                 (2, 64, 64, "bf16"): "wgrad3 (every width)",
+                (2, 64, 256, "bf16"): "wgrad3s2 (stride 2)",
                 (1, 256, 256, "bf16"): "conv2s2 data gradient",
                 (0, 256, 128, "bf16"): "conv2s2f forward",
                 (0, 64, 64, "bf16"): "conv64 forward",

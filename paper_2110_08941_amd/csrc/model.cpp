@@ -542,9 +542,9 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // bf16 3x3 stride-1 weight gradient: patch kernel (split table in slices)
   const bool wg3 = c.bf && mode == MODE_WGRAD && p.nseg > 0 && wgrad3_ok(p) &&
                    p.split_stride > 0;
-  if (wg3) {
+  if (wg3) {   // probe label: (64, 64) stride 1, (64, 256) stride 2
     bm = 64;
-    bn = 64;
+    bn = p.g.stride == 2 ? 256 : 64;
   }
   // 64 -> 64 channel 3x3 stride-1 on 32-wide maps: LDS patch kernel
   bool w64 = c.bf && mode != MODE_WGRAD && ws.wpack && conv64_ok(mode, p) &&
@@ -724,15 +724,33 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
 }
 
+// Whether the weight gradient of a residual block's 1x1 stride-2 projection
+// P can be taken in the same launch as that of the block's first 3x3
+// stride-2 convolution L (same input): the stride-2 patch kernel, and room in
+// the split-K buffer for one split per worker of both partials.
+bool wgrad_fuses_proj(const Ctx& c, const ConvL& L, const ConvL& P) {
+  if (!c.bf || L.k != 3 || L.stride != 2 || P.k != 1 || P.stride != 2 || P.pad != 0 ||
+      P.cin != L.cin || P.cout != L.cout || P.Ho != L.Ho || P.Wo != L.Wo)
+    return false;
+  GemmParams p = base_params(L, c.n);
+  if (!wgrad3_ok(p)) return false;
+  const int64_t mn = (int64_t)L.cout * 9 * L.cin + (int64_t)P.cout * P.cin;
+  return (int64_t)c.sg.count * mn <= c.ws.splitk_floats;
+}
+
 // Weight gradient of every worker: worker s reduces over the pixels of its own
 // samples and writes g[s] + L.w.  The reduction is split (split-K) so that
 // the launch has about 1024 blocks; the partial sums are added per worker in
 // split order.  With cin_true < L.cin the layer's input channels are padded
-// and the padded columns of the gradient are dropped.
+// and the padded columns of the gradient are dropped.  With proj (see
+// wgrad_fuses_proj) the same launch also takes the projection's weight
+// gradient from its output gradient dy_proj (same input x).
 hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* x,
-                      int cin_true = 0, double flops = 0.0) {
+                      int cin_true = 0, double flops = 0.0, const ConvL* proj = nullptr,
+                      const void* dy_proj = nullptr) {
   if (flops <= 0) flops = layer_flops(L, c.n);
   if (cin_true <= 0) cin_true = L.cin;
+  if (proj && !wgrad_fuses_proj(c, L, *proj)) return hipErrorInvalidValue;
   GemmParams p = base_params(L, c.n);
   p.a = dy;
   p.b = x;
@@ -741,9 +759,16 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
   p.K = c.n * L.Ho * L.Wo;
   const bool veca = (L.cout % c.V) == 0;
   const bool vecb = (L.cin % c.V) == 0;
-  const int64_t mn = (int64_t)p.M * p.N;
+  const int64_t mn1 = (int64_t)p.M * p.N;
   if (c.bf && cin_true == L.cin && wgrad3_ok(p)) {
-    // patch kernel: splits of 64-pixel slices, about 512 blocks in all
+    // patch kernel: splits of 64-pixel slices, about 512 blocks in all; a
+    // split's output holds the layer's partial and then the projection's
+    const int64_t mnp = proj ? (int64_t)proj->cout * proj->cin : 0;
+    const int64_t mn = mn1 + mnp;
+    if (proj) {
+      p.a2 = dy_proj;
+      flops += layer_flops(*proj, c.n);
+    }
     int ns[MAX_SEG], total = 0;
     for (int i = 0; i < c.sg.count; ++i) {
       ns[i] = wgrad3_slices(p, c.sg.n0[i + 1] - c.sg.n0[i]);
@@ -771,14 +796,24 @@ hipError_t conv_wgrad(const Ctx& c, const ConvL& L, const void* dy, const void* 
     p.out = c.ws.splitk;
     p.split_stride = mn;
     HS_TRY(gemm(c, MODE_WGRAD, p, veca, vecb, 64, 64, p.seg_split[c.sg.count], flops));
-    if (c.gbar)
-      return launch_splitk_reduce_wsum(c.ws.splitk, mn, mn, p.seg_split, c.w, c.gbar + L.w,
-                                       c.sg.count, L.cin, L.cin, c.s);
-    float* outs[MAX_SEG];
-    for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + L.w;
-    return launch_splitk_reduce_seg(c.ws.splitk, mn, mn, p.seg_split, outs, c.sg.count, L.cin,
-                                    L.cin, c.s);
+    for (int part = 0; part < (proj ? 2 : 1); ++part) {
+      const ConvL& T = part ? *proj : L;
+      const float* src = c.ws.splitk + (part ? mn1 : 0);
+      const int64_t count = part ? mnp : mn1;
+      if (c.gbar) {
+        HS_TRY(launch_splitk_reduce_wsum(src, mn, count, p.seg_split, c.w, c.gbar + T.w,
+                                         c.sg.count, T.cin, T.cin, c.s));
+        continue;
+      }
+      float* outs[MAX_SEG];
+      for (int i = 0; i < c.sg.count; ++i) outs[i] = c.g[i] + T.w;
+      HS_TRY(launch_splitk_reduce_seg(src, mn, count, p.seg_split, outs, c.sg.count, T.cin, T.cin,
+                                      c.s));
+    }
+    return hipSuccess;
   }
+  if (proj) return hipErrorInvalidValue;
+  const int64_t mn = mn1;
   const int bm = p.M <= 64 ? 64 : 128, bn = 128;
   const int tiles = ceil_div(p.M, bm) * ceil_div(p.N, bn);
   const int bke = 128 / (c.bf ? 2 : 4);
@@ -1180,12 +1215,14 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     const int64_t rps = (int64_t)b.c1.Ho * b.c1.Wo;
     const int p1 = gi;
     int pz = -1, pz_done = -1;
+    // the projection's weight gradient in conv1's launch where the shapes allow
+    const bool wfuse = b.proj && wgrad_fuses_proj(cs, b.c1, b.cp);
     if (b.proj) {   // dZP on the second stream, needed only by conv1's data gradient
       if (gp.take(pz) != 0) return hipErrorInvalidValue;
       HS_TRY(fork(c));
       HS_TRY(bn_bwd(cs, b.bp, gp[p1], nullptr, ZP, rps, gp[pz]));          // dZP
       pz_done = side_mark(c);
-      HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
+      if (!wfuse) HS_TRY(conv_wgrad(cs, b.cp, gp[pz], in));
       HS_TRY(gp.read_on_side(pz));
       HS_TRY(gp.read_on_side(p1));
     }
@@ -1201,7 +1238,12 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     HS_TRY(bn_bwd(c, b.b1, gp[p3], nullptr, Z1, rps, gp[p4]));              // dZ1
     gp.drop(p3);
     HS_TRY(fork(c));
-    HS_TRY(conv_wgrad(cs, b.c1, gp[p4], in));
+    if (wfuse) {
+      HS_TRY(conv_wgrad(cs, b.c1, gp[p4], in, 0, 0.0, &b.cp, gp[pz]));
+      HS_TRY(gp.read_on_side(pz));
+    } else {
+      HS_TRY(conv_wgrad(cs, b.c1, gp[p4], in));
+    }
     HS_TRY(gp.read_on_side(p4));
     HS_TAKE(gp, out);
     if (b.proj) {

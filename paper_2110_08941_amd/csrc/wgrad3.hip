@@ -45,7 +45,13 @@
 // taps s = 0 and s = 2 are the odd-column plane at shifts 0 and 1 (three
 // reads, one byte-aligned), s = 1 the even-column plane at shift 1 (two
 // reads).  A slice is 64 output pixels (four planes of its input take four
-// times the slots of a stride-1 patch).
+// times the slots of a stride-1 patch).  With a2 set (PROJ) the kernel also
+// takes the weight gradient of the residual block's 1x1 stride-2 projection
+// of the same input: its input pixel (2 o, 2 p) is what tap (1, 1) reads,
+// so the four waves of filter row 1 add one more MFMA per k step, with the
+// projection's dy (a2, staged as dy) against the tap's operand, into a
+// fourth accumulator; that partial follows the 3x3 one in each split's
+// output (out + y split_stride + 9 K C, [K][C]).
 #include "kernels.h"
 
 namespace hs {
@@ -407,7 +413,7 @@ struct Slice2 {
 
 }  // namespace
 
-template <int WO>
+template <int WO, bool PROJ>
 __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
   typedef Slice2<WO> S;
   constexpr int NT = 768;
@@ -423,11 +429,15 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(16))) char sA1[AROWS * ROWB];
   __shared__ __attribute__((aligned(16))) char sB0[BROWS * ROWB];
   __shared__ __attribute__((aligned(16))) char sB1[BROWS * ROWB];
+  // the projection's dy rows (PROJ)
+  __shared__ __attribute__((aligned(16))) char sC0[PROJ ? AROWS * ROWB : 16];
+  __shared__ __attribute__((aligned(16))) char sC1[PROJ ? AROWS * ROWB : 16];
 
   const ConvGeom& g = p.g;
   const int C = g.C, K = g.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 2, wk = (wave >> 1) & 1, wc = wave & 1;
+  const bool sc = PROJ && wr == 1;   // wave-uniform: this wave also takes the projection
   // all tiles of a split on one XCD, as in the stride-1 kernel
   const int nblk = (int)(gridDim.x * gridDim.y), q8 = nblk / 8;
   int lb = (int)(blockIdx.y * gridDim.x + blockIdx.x);
@@ -454,6 +464,7 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
 
   const bf16_t* X = (const bf16_t*)p.b;    // x  [n][2 WO][2 WO][C]
   const bf16_t* DY = (const bf16_t*)p.a;   // dy [n][WO][WO][K]
+  const bf16_t* DY2 = (const bf16_t*)p.a2; // the projection's dy, same layout (PROJ)
   const void* zero16 = &g_zero16;
   __asm__ volatile("" : "+s"(zero16));
 
@@ -484,7 +495,7 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
     bfy[i] = colok ? iy : NEVER;
     bfr[i] = colok ? f : NEVER;
   }
-  auto copy_slice = [&](int j, char* As, char* Bs) {
+  auto copy_slice = [&](int j, char* As, char* Bs, char* Cs) {
     int img0, y0, nfr;
     if (S::ROWS) {
       img0 = s_n0 + j / S::SPI;
@@ -495,13 +506,18 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
       y0 = 0;
       nfr = s_n1 - img0;
     }
-    const bf16_t* dyb = DY + ((int64_t)(img0 * WO + y0) * WO) * K + k0;
+    const int64_t dyo = ((int64_t)(img0 * WO + y0) * WO) * K + k0;
     const bf16_t* xb = X + ((int64_t)(img0 * S::WI + 2 * y0) * S::WI) * C + c0;
 #pragma unroll
     for (int i = 0; i < AIT; ++i) {
       if (NT * i + 64 * wave >= ACH) continue;              // wave-uniform
-      const void* src = afr[i] < nfr || S::ROWS ? (const void*)(dyb + aoff[i]) : zero16;
+      const bool live = afr[i] < nfr || S::ROWS;
+      const void* src = live ? (const void*)(DY + dyo + aoff[i]) : zero16;
       __builtin_amdgcn_global_load_lds((gbl_cptr)src, (lds_ptr)(As + (NT * i + 64 * wave) * 16), 16, 0, 0);
+      if constexpr (PROJ) {
+        const void* src2 = live ? (const void*)(DY2 + dyo + aoff[i]) : zero16;
+        __builtin_amdgcn_global_load_lds((gbl_cptr)src2, (lds_ptr)(Cs + (NT * i + 64 * wave) * 16), 16, 0, 0);
+      }
     }
 #pragma unroll
     for (int i = 0; i < BIT; ++i) {
@@ -514,9 +530,10 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
   auto tr_read = [&](const char* lane_base, int off) -> i16x4 {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(lds_i16p)(short*)(lane_base + off));
   };
-  f32x16 acc[3];
+  constexpr int NACC = PROJ ? 4 : 3;
+  f32x16 acc[NACC];
 #pragma unroll
-  for (int t = 0; t < 3; ++t) acc[t] = (f32x16){};
+  for (int t = 0; t < NACC; ++t) acc[t] = (f32x16){};
 
   const int grp = lane >> 4, q = lane & 15;
   const int colA = wk * 32 + 16 * (grp & 1);
@@ -542,10 +559,15 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
   // half)
   constexpr int NBO = WO >= 8 ? 3 : 4;
   constexpr int NBE = 2;
-  auto read_k = [&](const char* pa_, const char* pb_, int kk, i16x4 (&fa)[2], i16x4 (&fo)[NBO],
-                    i16x4 (&fe)[NBE]) {
+  // (the projection's dy fragment, fc, is read by the filter-row-1 waves)
+  auto read_k = [&](const char* pa_, const char* pb_, const char* pc_, int kk, i16x4 (&fa)[2],
+                    i16x4 (&fo)[NBO], i16x4 (&fe)[NBE], i16x4 (&fc)[2]) {
     fa[0] = rd(pa_, baseA, 16 * kk);
     fa[1] = rd(pa_, baseA, 16 * kk + 4);
+    if (sc) {
+      fc[0] = rd(pc_, baseA, 16 * kk);
+      fc[1] = rd(pc_, baseA, 16 * kk + 4);
+    }
     if constexpr (WO >= 8) {
       const int r0 = S::slot(16 * kk);
       fo[0] = rd(pb_, baseO, r0);
@@ -605,20 +627,27 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
   };
 
   constexpr int KK = S::PIX / 16;
-  i16x4 fa[2], fo[NBO], fe[NBE];
-  auto slice = [&](int i, const char* pa_, const char* pb_, char* na, char* nb) {
+  i16x4 fa[2], fo[NBO], fe[NBE], fc[2];
+  auto slice = [&](int i, const char* pa_, const char* pb_, const char* pc_, char* na, char* nb,
+                   char* nc) {
     const bool more = i + 1 < cnt;
-    if (more) copy_slice(j0 + i + 1, na, nb);
+    if (more) copy_slice(j0 + i + 1, na, nb, nc);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      bf16x8 av, bv[3];
+      bf16x8 av, bv[3], cv;
       prep_k(fa, fo, fe, av, bv);
+      if (sc) {
+        __builtin_memcpy(&cv, &fc[0], 8);
+        __builtin_memcpy((char*)&cv + 8, &fc[1], 8);
+      }
       __builtin_amdgcn_sched_barrier(0);
-      i16x4 ga[2], go[NBO], ge[NBE];
-      if (kk + 1 < KK) read_k(pa_, pb_, kk + 1, ga, go, ge);
+      i16x4 ga[2], go[NBO], ge[NBE], gc[2];
+      if (kk + 1 < KK) read_k(pa_, pb_, pc_, kk + 1, ga, go, ge, gc);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int s = 0; s < 3; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[s], av, acc[s], 0, 0, 0);
+      if constexpr (PROJ)
+        if (sc) acc[NACC - 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[1], cv, acc[NACC - 1], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       if (kk + 1 < KK) {
         fa[0] = ga[0];
@@ -627,24 +656,27 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
         for (int u = 0; u < NBO; ++u) fo[u] = go[u];
 #pragma unroll
         for (int u = 0; u < NBE; ++u) fe[u] = ge[u];
+        fc[0] = gc[0];
+        fc[1] = gc[1];
       }
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (more) read_k(na, nb, 0, fa, fo, fe);
+    if (more) read_k(na, nb, nc, 0, fa, fo, fe, fc);
   };
   if (cnt > 0) {
-    copy_slice(j0, sA0, sB0);
+    copy_slice(j0, sA0, sB0, sC0);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    read_k(sA0, sB0, 0, fa, fo, fe);
+    read_k(sA0, sB0, sC0, 0, fa, fo, fe, fc);
   }
   for (int i = 0; i < cnt; i += 2) {
-    slice(i, sA0, sB0, sA1, sB1);
-    if (i + 1 < cnt) slice(i + 1, sA1, sB1, sA0, sB0);
+    slice(i, sA0, sB0, sC0, sA1, sB1, sC1);
+    if (i + 1 < cnt) slice(i + 1, sA1, sB1, sC1, sA0, sB0, sC0);
   }
 
-  // ---- epilogue as the stride-1 kernel
+  // ---- epilogue as the stride-1 kernel; the projection's partial after
+  // the 3x3 one
   const int co = k0 + wk * 32 + (lane & 31);
   float* out = (float*)p.out + (int64_t)by * p.split_stride;
 #pragma unroll
@@ -655,6 +687,18 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
       *(float4*)(out + ((int64_t)co * 9 + 3 * wr + s) * C + ci) =
           make_float4(acc[s][4 * r4], acc[s][4 * r4 + 1], acc[s][4 * r4 + 2], acc[s][4 * r4 + 3]);
     }
+  if constexpr (PROJ) {
+    if (sc) {
+      float* out2 = out + (int64_t)9 * K * C;
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int ci = c0 + wc * 32 + 8 * r4 + 4 * (lane >> 5);
+        *(float4*)(out2 + (int64_t)co * C + ci) =
+            make_float4(acc[NACC - 1][4 * r4], acc[NACC - 1][4 * r4 + 1], acc[NACC - 1][4 * r4 + 2],
+                        acc[NACC - 1][4 * r4 + 3]);
+      }
+    }
+  }
 }
 
 bool wgrad3_ok(const GemmParams& p) {
@@ -681,13 +725,22 @@ hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s) {
   if (!wgrad3_ok(p) || p.nseg < 1) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((p.g.K / 64) * (p.g.C / 64)), (unsigned)p.seg_split[p.nseg]);
   if (p.g.stride == 2) {
-    switch (p.g.Wo) {
-      case 16: hipLaunchKernelGGL(wgrad3s2_kernel<16>, grid, dim3(768), 0, s, p); break;
-      case 8: hipLaunchKernelGGL(wgrad3s2_kernel<8>, grid, dim3(768), 0, s, p); break;
-      default: hipLaunchKernelGGL(wgrad3s2_kernel<4>, grid, dim3(768), 0, s, p); break;
+    if (p.a2) {
+      switch (p.g.Wo) {
+        case 16: hipLaunchKernelGGL((wgrad3s2_kernel<16, true>), grid, dim3(768), 0, s, p); break;
+        case 8: hipLaunchKernelGGL((wgrad3s2_kernel<8, true>), grid, dim3(768), 0, s, p); break;
+        default: hipLaunchKernelGGL((wgrad3s2_kernel<4, true>), grid, dim3(768), 0, s, p); break;
+      }
+    } else {
+      switch (p.g.Wo) {
+        case 16: hipLaunchKernelGGL((wgrad3s2_kernel<16, false>), grid, dim3(768), 0, s, p); break;
+        case 8: hipLaunchKernelGGL((wgrad3s2_kernel<8, false>), grid, dim3(768), 0, s, p); break;
+        default: hipLaunchKernelGGL((wgrad3s2_kernel<4, false>), grid, dim3(768), 0, s, p); break;
+      }
     }
     return hipGetLastError();
   }
+  if (p.a2) return hipErrorInvalidValue;   // the projection is taken at stride 2 only
   switch (p.g.W) {
     case 32: hipLaunchKernelGGL(wgrad3_kernel<32>, grid, dim3(768), 0, s, p); break;
     case 16: hipLaunchKernelGGL(wgrad3_kernel<16>, grid, dim3(768), 0, s, p); break;
