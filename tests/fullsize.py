@@ -10,7 +10,11 @@ with the tensor's largest exact magnitude (over all its entries) as the
 denominator, as tests/gpu_util.pertensor does for whole tensors.  Inputs
 (He-normal parameters, separated decisions, synthetic images) are drawn here
 from their seeds on every machine; a fingerprint of them is stored with the
-values and checked before any comparison."""
+values and checked before any comparison.  A tensor's stored floor (the
+oracle's own error at the path's precision) is its error over all entries,
+not only the sampled ones: the sampled entries miss a tensor's worst ones,
+and on the tensors where bf16 is most fragile that underestimates what a
+valid bf16 computation is off by."""
 import os
 
 import numpy as np
@@ -101,6 +105,23 @@ def tensor_scales(table, v):
     scales = np.array([float(np.max(np.abs(v[r[3]:r[3] + int(np.prod(r[2]))])))
                        for r in table])
     return scales, float(np.max(np.abs(v)))
+
+
+def full_errors(a, ref, table, scales, vmax):
+    """Per tensor: max over all its entries of |a - ref| divided by the
+    tensor's largest exact magnitude (at least ZERO_FLOOR of the whole
+    vector's), ref the whole exact vector: the per-tensor error of
+    tests/gpu_util.pertensor."""
+    from tests.gpu_util import ZERO_FLOOR
+    a = np.asarray(a, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    out = []
+    for t, r in enumerate(table):
+        off, k = r[3], int(np.prod(r[2]))
+        d = float(np.max(np.abs(a[off:off + k] - ref[off:off + k])))
+        den = max(float(scales[t]), ZERO_FLOOR * vmax)
+        out.append(d / den if den > 0 else d)
+    return out
 
 
 def sampled_errors(a, ref_samples, idx, scales, vmax):

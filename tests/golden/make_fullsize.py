@@ -12,10 +12,10 @@ the worker's own partition):
   w<i>_scale       per tensor, max |g| over all its entries
   w<i>_vmax        max |g| over the whole vector
   w<i>_ref         g at the sampled entries (fullsize.sample_index), float32
-  w<i>_floor       per tensor, the sampled error of the oracle's own
-                   arithmetic at the path's precision (Ctx modes "fp32" /
-                   "bf16"), the largest over the precision's rounding
-                   realizations
+  w<i>_floor       per tensor, the error (over all its entries) of the
+                   oracle's own arithmetic at the path's precision (Ctx
+                   modes "fp32" / "bf16"), the largest over the precision's
+                   rounding realizations
   w<i>_relu        the smallest ReLU margin of the exact pass
 and the configuration's partition, compared workers and input fingerprint.
 The step file holds the same for the update theta' - theta ("d_") and the
@@ -68,7 +68,7 @@ def make_config(name):
         for k in REALIZATIONS[dtype]:
             say("%s worker %d: %s realization %d" % (name, i, dtype, k))
             _, gk = Mo.worker_grad(net, th, x[a:b], y[a:b], storage=dtype, grid=k)
-            floors.append(F.sampled_errors(gk, ref, idx, scales, vmax))
+            floors.append(F.full_errors(gk, g, table, scales, vmax))
         out["w%d_loss" % i] = np.array(loss)
         out["w%d_scale" % i] = scales
         out["w%d_vmax" % i] = np.array(vmax)
@@ -104,7 +104,7 @@ def make_step():
         out[key + "_scale"] = scales
         out[key + "_vmax"] = np.array(vmax)
         out[key + "_ref"] = ref.astype(np.float32)
-        out[key + "_floor"] = np.array(F.sampled_errors(low_v, ref, idx, scales, vmax))
+        out[key + "_floor"] = np.array(F.full_errors(low_v, ref_v, table, scales, vmax))
     out["losses"] = np.array(ex["losses"])
     return out
 

@@ -8,7 +8,8 @@ test_gpu_worker.py: per parameter tensor against the exact float64 oracle,
 1e-4 (fp32) / 2e-2 (bf16), or 3 x the oracle's own error at the path's
 precision on a tensor where that floor exceeds the bar.  The workload
 configurations are checked at their own sizes against stored oracle values
-(tests/fullsize.py) on sampled entries: every worker of the ResNet-18 bf16
+(tests/fullsize.py) on sampled entries, each tensor's floor being the
+oracle's own error over all its entries: every worker of the ResNet-18 bf16
 (N = 2048) and fp32 (N = 1024) workloads, the smallest and the largest worker
 of the VGG-16 workload (N = 4096), every worker of the small-CNN workload
 (N = 512), the two smallest of ResNet-50 (N = 1024).  Every case prints its
@@ -229,8 +230,9 @@ def load_golden(name):
 def check_sampled(a, gold, prefix, table, idx, tol, what, floor_scale=1.0, ref=None):
     """Sampled per-tensor errors of a against the stored values `prefix`
     (or against `ref` sampled the same way, with the stored scales), bound
-    max(tol, 3 x floor_scale x stored floor) on every tensor; returns the
-    worst (error, tensor)."""
+    max(tol, 3 x floor_scale x stored floor) on every tensor (the floor: the
+    oracle's error at the path's precision over all of the tensor's
+    entries); returns the worst (error, tensor)."""
     scales, vmax = gold[prefix + "_scale"], float(gold[prefix + "_vmax"])
     r = gold[prefix + "_ref"] if ref is None else np.concatenate([ref[ix] for ix in idx])
     errs = F.sampled_errors(a, r, idx, scales, vmax)
