@@ -178,6 +178,43 @@ def standalone_wavg(reps=20):
             "frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
+def attainable(reps=5):
+    """What this GPU sustains on the two pipes the rooflines are priced
+    against, event-timed: the MFMA loop of hs_probe_mfma_loop (dense bf16
+    32x32x16 MFMAs on registers, 4 blocks of 8 waves per CU) and the plain
+    1 GiB device copy of hs_probe_copy (2 GiB moved per copy)."""
+    import torch
+    from paper_2110_08941_amd import hs
+    blocks, iters = 1024, 4000
+    out = torch.empty(blocks * 512, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    hs.probe_mfma_loop(blocks, iters, out.data_ptr(), stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        hs.probe_mfma_loop(blocks, iters, out.data_ptr(), stream)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / reps
+    tf = blocks * 8 * iters * 8 * 32768 / (us * 1e-6) / 1e12
+    n = (1 << 30) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    hs.probe_copy(src.data_ptr(), dst.data_ptr(), 4 * n, stream)
+    e0.record()
+    for _ in range(reps):
+        hs.probe_copy(src.data_ptr(), dst.data_ptr(), 4 * n, stream)
+    e1.record()
+    torch.cuda.synchronize()
+    cus = 1e3 * e0.elapsed_time(e1) / reps
+    gbs = 2 * 4 * n / (cus * 1e-6) / 1e9
+    del out, src, dst
+    return {"mfma_bf16_loop": {"achieved": round(tf, 1), "unit": "TFLOP/s", "avg_launch_us": round(us, 1),
+                               "frac_of_peak": round(tf / PEAK_TFLOPS["bf16"], 4)},
+            "copy_1GiB": {"achieved": round(gbs, 1), "unit": "GB/s", "avg_launch_us": round(cus, 1),
+                          "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}}
+
+
 def copy_calibration(mib, reps=4):
     """A plain device-to-device copy of a known size: under rocprofv3 --pmc its
     FETCH_SIZE and WRITE_SIZE per dispatch give the counters' scale."""
@@ -441,6 +478,15 @@ def main():
     result["partitions_last"] = r["partitions_last"]
     result["loss_last"] = r["loss_last"]
     result["wavg_sgd_standalone"] = standalone_wavg()
+    result["attainable"] = attainable()
+    if wl.dtype == "bf16":   # the loop runs bf16 MFMAs
+        mf = result["attainable"]["mfma_bf16_loop"]["achieved"]
+        if "roofline" in result:
+            result["roofline"]["frac_of_attainable"] = round(result["roofline"]["achieved"] / mf, 4)
+        result["step_roofline"]["frac_of_attainable"] = round(
+            result["step_roofline"]["achieved"] / mf, 4)
+    result["hbm_roofline"]["frac_of_attainable"] = round(
+        result["hbm_roofline"]["achieved"] / result["attainable"]["copy_1GiB"]["achieved"], 4)
     if not args.no_extra and not args.streams:
         extra = {}
         for name in EXTRA:

@@ -22,8 +22,8 @@ extern "C" {
  * and 1, 3x3 weight gradient in mode 2; 256 x 256 in mode 1 the stride-2
  * data-gradient patch kernel, in mode 0 the stride-2 forward patch kernel
  * (256 x 128); 32 x 64 the direct bf16 stem, forward in mode 0 and weight
- * gradient in mode 2) on this
- * workspace is
+ * gradient in mode 2; 64 x 256 in mode 2 the stride-2 3x3 weight-gradient
+ * patch kernel) on this workspace is
  * bracketed by two HIP events on the worker's stream, and its algorithmic
  * FLOPs (2 x pixels x c_out x taps x c_in, i.e. dense 3x3 taps, independent of
  * the stride handling) are added up.  At most `capacity` launches are
@@ -35,6 +35,22 @@ hs_status hs_probe_enable(hs_workspace* ws, int32_t mode, int32_t bm, int32_t bn
  * number of timed launches and their summed algorithmic FLOPs, then clears
  * the record (the probe stays enabled). */
 hs_status hs_probe_read(hs_workspace* ws, double* total_ms, int64_t* launches, double* flops);
+
+/* The attainable bf16 MFMA rate, for roofline reports: launches `blocks`
+ * blocks of 512 threads on `stream` (null: the default stream); each of the
+ * 8 waves of a block runs iters x 8 dense 32x32x16 bf16 MFMAs on register
+ * operands (2 x 32 x 32 x 16 FLOPs each), with no memory traffic but one
+ * float per thread written to out (blocks x 512 floats, device): thread t
+ * of a block feeds A elements (t + i) mod 8 and B elements (3 t + i) mod 8,
+ * i = 0..7 of its operand registers, and writes the sum of its accumulator
+ * elements.  Asynchronous; blocks 1..65536, iters 1..2^20. */
+hs_status hs_probe_mfma_loop(int32_t blocks, int32_t iters, float* out, void* stream);
+
+/* The attainable HBM rate, for roofline reports: dst[0, bytes) = src[0,
+ * bytes) on `stream` by a plain copy kernel (16 bytes per lane and access).
+ * bytes a positive multiple of 16, both pointers device, 16-byte aligned, the
+ * ranges disjoint.  Asynchronous. */
+hs_status hs_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
 /* ------------------------------------------------------ layer-level access -- */
 

@@ -25,7 +25,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
 # Host arithmetic of the repartition must not be contracted (bit-exact with the
 # reference arithmetic in the header).
 PER_FILE = {"api.cpp": ["-ffp-contract=off"]}
-SOURCES = ["igemm.hip", "igemm_fast.hip", "conv2.hip", "conv64.hip", "stem.hip", "wgrad3.hip", "layers.hip", "stats.hip", "opt.hip", "static_scratch.hip", "model.cpp", "api.cpp"]
+SOURCES = ["igemm.hip", "igemm_fast.hip", "conv2.hip", "conv64.hip", "stem.hip", "wgrad3.hip", "layers.hip", "stats.hip", "opt.hip", "static_scratch.hip", "probe.hip", "model.cpp", "api.cpp"]
 
 
 def _compile(src):

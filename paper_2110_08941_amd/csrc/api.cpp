@@ -493,6 +493,28 @@ hs_status hs_probe_read(hs_workspace* ws, double* total_ms, int64_t* launches, d
   return ok();
 }
 
+hs_status hs_probe_mfma_loop(int32_t blocks, int32_t iters, float* out, void* stream) {
+  if (blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 20))
+    return fail(HS_ERR_INVALID, "hs_probe_mfma_loop: blocks %d, iters %d", blocks, iters);
+  if (!out) return fail(HS_ERR_INVALID, "hs_probe_mfma_loop: NULL output");
+  hipError_t e = launch_mfma_loop(blocks, iters, out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_probe_mfma_loop");
+  return ok();
+}
+
+hs_status hs_probe_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (!src || !dst) return fail(HS_ERR_INVALID, "hs_probe_copy: NULL pointer");
+  if (bytes < 16 || bytes % 16 != 0 || ((uintptr_t)src | (uintptr_t)dst) % 16 != 0)
+    return fail(HS_ERR_INVALID, "hs_probe_copy: %lld bytes, pointers must be 16-byte aligned",
+                (long long)bytes);
+  const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+  if (s0 < d0 + (uintptr_t)bytes && d0 < s0 + (uintptr_t)bytes)
+    return fail(HS_ERR_INVALID, "hs_probe_copy: overlapping ranges");
+  hipError_t e = launch_copy(src, dst, bytes, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hs_probe_copy");
+  return ok();
+}
+
 hs_status hs_layer_gemm(int32_t mode, int32_t dtype, int32_t n, int32_t H, int32_t W, int32_t C,
                         int32_t K, int32_t R, int32_t stride, int32_t pad, const void* a,
                         const void* b, void* out, const float* bias, int32_t relu,

@@ -196,6 +196,12 @@ hipError_t launch_splitk_reduce_wsum(const float* part, int64_t stride, int64_t 
                                      const int* split0, const float* w, float* out, int nseg,
                                      int c, int cp, hipStream_t s);
 
+// ---- attainable MFMA rate (probe.hip): blocks x 512 threads, each wave
+// iters x 8 dense 32x32x16 bf16 MFMAs; out[blocks * 512]
+hipError_t launch_mfma_loop(int blocks, int iters, float* out, hipStream_t s);
+// plain device copy of `bytes` (a multiple of 16; 16-byte aligned pointers)
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
+
 // ---- elementwise / reduction kernels (layers.hip) ----
 // NCHW fp32 input -> NHWC activation (fp32 or bf16)
 hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int hw, bool bf16,

@@ -74,6 +74,8 @@ def _load():
                                 I32, P, I64, P]),
         "hs_probe_enable": (I32, [P, I32, I32, I32, I32]),
         "hs_probe_read": (I32, [P, PD, PI64, PD]),
+        "hs_probe_mfma_loop": (I32, [I32, I32, P, P]),
+        "hs_probe_copy": (I32, [P, P, I64, P]),
         "hs_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():
@@ -102,7 +104,8 @@ EXPORTED = (
     "hs_repartition", "hs_partitioner_create", "hs_partitioner_destroy",
     "hs_partitioner_partition", "hs_partitioner_set_partition", "hs_partitioner_observe",
     "hs_partitioner_set_estimator",
-    "hs_layer_gemm", "hs_probe_enable", "hs_probe_read", "hs_last_error")
+    "hs_layer_gemm", "hs_probe_enable", "hs_probe_read", "hs_probe_mfma_loop", "hs_probe_copy",
+    "hs_last_error")
 
 
 def lib():
@@ -249,6 +252,17 @@ def probe_read(ws):
     t, n, f = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double()
     _check(_lib.hs_probe_read(ws, ctypes.byref(t), ctypes.byref(n), ctypes.byref(f)))
     return t.value, n.value, f.value
+
+
+def probe_mfma_loop(blocks, iters, out, stream=0):
+    """Asynchronous launch of the MFMA loop (hs_probe_mfma_loop); out: device
+    pointer to blocks x 512 floats.  FLOPs: blocks x 8 x iters x 8 x 32768."""
+    _check(_lib.hs_probe_mfma_loop(int(blocks), int(iters), out, stream or None))
+
+
+def probe_copy(src, dst, nbytes, stream=0):
+    """Asynchronous plain device copy (hs_probe_copy) of nbytes."""
+    _check(_lib.hs_probe_copy(src, dst, int(nbytes), stream or None))
 
 
 def layer_gemm(mode, dtype, n, H, W, C, K, R, stride, pad, a, b, out, bias=0, relu=False,

@@ -207,6 +207,14 @@ def test_error_paths():
         hs.sgd_step(16, 32, 0, 64, 0.1, 0.9, 0.0)         # mu != 0 needs a momentum buffer
     with pytest.raises(hs.HSError):
         hs.wavg_sgd([16 + 4], [1], 64, 0, 64, 0.1, 0.0, 0.0)  # misaligned gradient
+    for args in ((0, 4096, 64), (4096, 8192, 40), (4096, 4100, 64), (4096, 4096 + 32, 64)):
+        with pytest.raises(hs.HSError):           # null, ragged, misaligned, overlapping
+            hs.probe_copy(*args)
+    for blocks, iters in ((0, 1), (1, 0), (65537, 1), (1, (1 << 20) + 1)):
+        with pytest.raises(hs.HSError):
+            hs.probe_mfma_loop(blocks, iters, 4096)
+    with pytest.raises(hs.HSError):
+        hs.probe_mfma_loop(1, 1, 0)
     hs.model_destroy(m)
 
 

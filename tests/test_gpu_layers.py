@@ -144,3 +144,37 @@ def check_layer_gemm(mode, shape, dtype, packed):
     # bf16 outputs (data gradient, packed forward) carry the output rounding
     tol = 1e-5 if dtype == "fp32" else (5e-3 if mode == 1 or packed else 1e-5)
     assert err <= tol
+
+
+def test_mfma_loop_probe():
+    """hs_probe_mfma_loop (the attainable-rate probe the benchmark reports)
+    runs the MFMAs it counts: each wave's outputs add up to 8 x iters x the
+    sum of one 32x32x16 product of its operands, sum_k colsum(A)[k] rowsum(B)[k],
+    with lane l feeding k block l // 32, elements i = 0..7."""
+    hs = require_gpu()
+    blocks, iters = 3, 5
+    out = torch.zeros(blocks * 512, device="cuda")
+    hs.probe_mfma_loop(blocks, iters, out.data_ptr())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64).reshape(blocks, 8, 64).sum(axis=2)
+    for w in range(8):
+        t = 64 * w + np.arange(64)
+        total = 0.0
+        for h in range(2):
+            lanes = t[32 * h:32 * h + 32]
+            for i in range(8):
+                total += float(((lanes + i) % 8).sum()) * float(((3 * lanes + i) % 8).sum())
+        np.testing.assert_array_equal(got[:, w], 8 * iters * total)
+
+
+@pytest.mark.parametrize("nbytes", [16, 4096 + 48, (1 << 24) + 16 * 12345])
+def test_copy_probe(nbytes):
+    """hs_probe_copy (the attainable-bandwidth probe) copies every byte, with
+    a ragged tail past its unrolled loop."""
+    hs = require_gpu()
+    n = nbytes // 4
+    src = torch.arange(n, device="cuda", dtype=torch.int32)
+    dst = torch.full((n + 4,), -1, device="cuda", dtype=torch.int32)
+    hs.probe_copy(src.data_ptr(), dst.data_ptr(), nbytes)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:n], src) and torch.all(dst[n:] == -1)
