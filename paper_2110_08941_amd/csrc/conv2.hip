@@ -1077,7 +1077,17 @@ PackJob pack_job(int64_t woff, int64_t dst, int mode, const GemmParams& p) {
 
 hipError_t launch_pack_batch(const void* W, void* Bp, const PackBatch& b, hipStream_t s) {
   if (b.count < 1 || b.count > PACK_BATCH) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(pack_batch_kernel, dim3(64, (unsigned)b.count), dim3(256), 0, s,
+  // blocks per job from the largest job, about 4 chunks per thread (the
+  // blocks of smaller jobs past their chunks return at once)
+  int64_t most = 0;
+  for (int i = 0; i < b.count; ++i) {
+    const PackJob& j = b.job[i];
+    const int64_t chunks = (int64_t)(j.C / C2_CK) * j.RS * 2 * j.N;
+    most = chunks > most ? chunks : most;
+  }
+  int64_t bx = (most + 1023) / 1024;
+  bx = bx < 1 ? 1 : (bx > 1024 ? 1024 : bx);
+  hipLaunchKernelGGL(pack_batch_kernel, dim3((unsigned)bx, (unsigned)b.count), dim3(256), 0, s,
                      (const bf16_t*)W, (bf16_t*)Bp, b);
   return hipGetLastError();
 }
