@@ -435,7 +435,10 @@ __global__ __launch_bounds__(768) void wgrad3s2_kernel(GemmParams p) {
 
   const ConvGeom& g = p.g;
   const int C = g.C, K = g.K;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index as a scalar: the projection's MFMA is then skipped by a
+  // scalar branch in the other waves, not issued with an empty exec mask
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave >> 2, wk = (wave >> 1) & 1, wc = wave & 1;
   const bool sc = PROJ && wr == 1;   // wave-uniform: this wave also takes the projection
   // all tiles of a split on one XCD, as in the stride-1 kernel
