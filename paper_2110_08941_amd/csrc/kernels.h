@@ -171,10 +171,27 @@ hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8
 // stem_wgrad_splits fills seg_split (blocks of each segment) from the
 // segments' sample counts and returns the split count; launch_stem_wgrad
 // writes split y's partial gW [64][27] (fp32) at part + 1728 y, from x (fp32
-// NCHW) and dy [n][32][32][64] bf16.
+// NCHW) and dy [n][32][32][64] bf16.  With bn set, dy is the gradient of the
+// stem's batch-norm output instead, and the kernel forms the batch-norm
+// backward itself as it reads dy (the stem's dz is used nowhere else):
+//   d = dy [act > 0] (act may be null), xh = (z - mean_s) rstd_s,
+//   dz = gamma rstd_s (d - (sum0_s / rows_s + xh sum1_s / rows_s)), rounded
+//   to bf16, with segment s's statistics and its sums of d and d xh
+//   (sum0_s, sum1_s), rows_s = 1024 x its samples.
+struct StemBnBwd {
+  const void* z;                // [n][32][32][64] bf16, the stem convolution's output
+  const void* act;              // [n][32][32][64] bf16 or null
+  const float* mean;            // segment s at mean + s * mstride
+  const float* rstd;
+  int mstride;
+  const float* gamma;           // [64]
+  const float* sum0[MAX_SEG];   // [64] per segment
+  const float* sum1[MAX_SEG];
+};
 int stem_wgrad_splits(const int* n, int nseg, int* seg_split);
 hipError_t launch_stem_wgrad(const float* x, const void* dy, float* part, const int* seg_n0,
-                             const int* seg_split, int nseg, hipStream_t s);
+                             const int* seg_split, int nseg, hipStream_t s,
+                             const StemBnBwd* bn = nullptr);
 hipError_t launch_nchw_to_nhwc_pad(const float* x, void* y, int n, int c, int cp, int hw, bool bf16,
                                    hipStream_t s);
 // weights [k][rs][c] fp32 -> [k][rs][cp] activation type, zero padded

@@ -925,10 +925,11 @@ hipError_t bn_apply(const Ctx& c, const BNL& b, const void* z, const void* res, 
 
 // dz = batch-norm backward of dy (masked by [act > 0] if act); writes every
 // worker's dbeta, dgamma into its g[s]
-hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
-                  int64_t rps, void* dz) {
-  float *db[MAX_SEG], *dg[MAX_SEG];
-  StatWsum ws{};
+// Where the batch-norm backward's per-worker sums go: the beta and gamma
+// gradients of g[s] (or, forming g_bar, this stream's slots, with their
+// weighted sums into g_bar)
+void bn_sum_targets(const Ctx& c, const BNL& b, float* (&db)[MAX_SEG], float* (&dg)[MAX_SEG],
+                    StatWsum& ws) {
   if (c.gbar) {
     // the workers' sums in this stream's slots (the backward below reads
     // them), their weighted sums into gbar
@@ -945,6 +946,13 @@ hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, c
       dg[i] = c.g[i] + b.g;
     }
   }
+}
+
+hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
+                  int64_t rps, void* dz) {
+  float *db[MAX_SEG], *dg[MAX_SEG];
+  StatWsum ws{};
+  bn_sum_targets(c, b, db, dg, ws);
   HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps, b.c,
                            c.sp(), db, dg, 0.f, c.s, c.gbar ? &ws : nullptr));
   return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
@@ -1074,8 +1082,10 @@ hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void
   return conv_fwd(c, st, X0, y, false, c.ws.stem_w, nullptr, layer_flops(L, c.n));
 }
 
+// With bn (the direct kernel only), dz is the batch-norm output's gradient
+// and the kernel forms the batch-norm backward as it reads it (StemBnBwd).
 hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0,
-                      const float* x) {
+                      const float* x, const StemBnBwd* bn = nullptr) {
   if (c.bf && stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W)) {
     // the direct stem weight gradient (stem.hip): split-K partials per worker
     // from x and dz, then the per-worker reduce
@@ -1085,7 +1095,7 @@ hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* 
     const int64_t mn = (int64_t)L.cout * L.k * L.k * L.cin;
     if ((int64_t)splits * mn > c.ws.splitk_floats) return hipErrorInvalidValue;
     const bool probe = probe_begin(c, MODE_WGRAD, 32, 64);
-    HS_TRY(launch_stem_wgrad(x, dz, c.ws.splitk, c.sg.n0, split, c.sg.count, c.s));
+    HS_TRY(launch_stem_wgrad(x, dz, c.ws.splitk, c.sg.n0, split, c.sg.count, c.s, bn));
     if (probe) HS_TRY(probe_end(c, layer_flops(L, c.n)));
     if (c.gbar)
       return launch_splitk_reduce_wsum(c.ws.splitk, mn, mn, split, c.w, c.gbar + L.w, c.sg.count,
@@ -1095,9 +1105,45 @@ hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* 
     return launch_splitk_reduce_seg(c.ws.splitk, mn, mn, split, outs, c.sg.count, (int)mn,
                                     (int)mn, c.s);
   }
+  if (bn) return hipErrorInvalidValue;
   ConvL st = L;
   st.cin = stem_cpad(c);
   return conv_wgrad(c, st, dz, X0, L.cin, layer_flops(L, c.n));
+}
+
+// The first layer's batch-norm backward and weight gradient, last in the
+// backward pass: the batch-norm sums on the caller's stream (beside the
+// second stream's last weight gradients), the join (the weight gradient
+// shares the split-K buffer), then the weight gradient.  The direct bf16 stem
+// forms dz = BN backward of dy (dy masked by [act > 0] when act is set) as it
+// reads dy and z, since nothing else reads that dz; otherwise dz is written
+// to dz_buf first.
+hipError_t stem_backward(const Ctx& c, const ConvL& L, const BNL& b, const void* dy,
+                         const void* act, const void* z, int64_t rps, void* dz_buf,
+                         const void* X0, const float* x) {
+  if (c.bf && c.theta && stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W)) {
+    float *db[MAX_SEG], *dg[MAX_SEG];
+    StatWsum ws{};
+    bn_sum_targets(c, b, db, dg, ws);
+    HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps,
+                             b.c, c.sp(), db, dg, 0.f, c.s, c.gbar ? &ws : nullptr));
+    HS_TRY(join(c));
+    StemBnBwd bn{};
+    bn.z = z;
+    bn.act = act;
+    bn.mean = c.mean(b);
+    bn.rstd = c.rstd(b);
+    bn.mstride = c.mstride();
+    bn.gamma = c.theta + b.g;
+    for (int i = 0; i < c.sg.count; ++i) {
+      bn.sum0[i] = db[i];
+      bn.sum1[i] = dg[i];
+    }
+    return stem_wgrad(c, L, dy, X0, x, &bn);
+  }
+  HS_TRY(bn_bwd(c, b, dy, act, z, rps, dz_buf));
+  HS_TRY(join(c));
+  return stem_wgrad(c, L, dz_buf, X0, x);
 }
 
 // ---------------------------------------------------------------- MLP ----
@@ -1266,14 +1312,10 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     gp.drop(p1);
     gi = out;
   }
-  // stem (its ReLU mask is already applied): its batch-norm backward beside
-  // the second stream's last weight gradients, then the join; every weight
-  // gradient is done when this returns (the stem's weight gradient shares
-  // the split-K buffer)
+  // stem (its ReLU mask is already applied): batch-norm backward and
+  // weight gradient; every weight gradient is done when this returns
   HS_TAKE(gp, zs);
-  HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
-  HS_TRY(join(c));
-  return stem_wgrad(c, m.stem, gp[zs], S[0], x);
+  return stem_backward(c, m.stem, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs], S[0], x);
 }
 
 // ---------------------------------------------------------- ResNet-50 ----
@@ -1397,13 +1439,10 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
     gp.drop(p1);
     gi = out;
   }
-  // the stem's batch-norm backward beside the second stream's last weight
-  // gradients, then the join; every weight gradient is done when this
-  // returns (the stem's shares the split-K buffer)
+  // the stem's batch-norm backward and weight gradient; every weight
+  // gradient is done when this returns
   HS_TAKE(gp, zs);
-  HS_TRY(bn_bwd(c, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs]));
-  HS_TRY(join(c));
-  return stem_wgrad(c, m.stem, gp[zs], S[0], x);
+  return stem_backward(c, m.stem, m.stem_bn, gp[gi], nullptr, S[1], 1024, gp[zs], S[0], x);
 }
 
 // -------------------------------------------------------------- VGG-16 ----
@@ -1462,13 +1501,13 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       pa = q;
     }
     HS_TAKE(gp, dz);
-    HS_TRY(bn_bwd(c, l.bn, gp[pa], A, Z, rps, gp[dz]));
-    gp.drop(pa);
-    if (i == 0) {   // the first layer's weight gradient shares the split-K buffer
-      HS_TRY(join(c));
-      HS_TRY(stem_wgrad(c, l.c, gp[dz], in, x));
+    if (i == 0) {   // the first layer: batch-norm backward and weight gradient
+      HS_TRY(stem_backward(c, l.c, l.bn, gp[pa], A, Z, rps, gp[dz], in, x));
+      gp.drop(pa);
       break;
     }
+    HS_TRY(bn_bwd(c, l.bn, gp[pa], A, Z, rps, gp[dz]));
+    gp.drop(pa);
     HS_TRY(fork(c));
     HS_TRY(conv_wgrad(cs, l.c, gp[dz], in));
     HS_TRY(gp.read_on_side(dz));

@@ -172,8 +172,12 @@ struct StemWgradArgs {
   int nseg;
   int seg_split[MAX_SEG + 1];
   int seg_n0[MAX_SEG + 1];
+  StemBnBwd bn;       // BN > 0: the batch-norm backward formed on the fly
 };
 
+// BN: 0 dy is the operand; 1 the operand is the batch-norm backward of dy;
+// 2 the same with dy masked by [act > 0]
+template <int BN>
 __global__ __launch_bounds__(256) void stem_wgrad_kernel(StemWgradArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t img[9 * STW_COPY];
   // the transposed dy quarter; after the loop, the waves' accumulators
@@ -194,6 +198,29 @@ __global__ __launch_bounds__(256) void stem_wgrad_kernel(StemWgradArgs a) {
     }
   const int i0 = n0 + (y - sp) * STW_IMG;
   const int i1 = min(n1, i0 + STW_IMG);
+  // batch-norm backward constants of the thread's 8 channels (a thread's
+  // dy chunks all hold channels 8 (tid % 8) .. + 7) for this segment
+  float bgr[BN ? 8 : 1], bmu[BN ? 8 : 1], brs[BN ? 8 : 1], bk1[BN ? 8 : 1], bk2[BN ? 8 : 1];
+  if constexpr (BN > 0) {
+    const float* s0 = a.bn.sum0[0];
+    const float* s1 = a.bn.sum1[0];
+#pragma unroll
+    for (int i = 1; i < MAX_SEG; ++i)
+      if (i == sg) {
+        s0 = a.bn.sum0[i];
+        s1 = a.bn.sum1[i];
+      }
+    const float inv_rows = 1.0f / (float)((n1 - n0) * ST_W * ST_W);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int c = 8 * (tid & 7) + j;
+      brs[j] = a.bn.rstd[(int64_t)sg * a.bn.mstride + c];
+      bgr[j] = a.bn.gamma[c] * brs[j];
+      bmu[j] = a.bn.mean[(int64_t)sg * a.bn.mstride + c];
+      bk1[j] = s0[c] * inv_rows;
+      bk2[j] = s1[c] * inv_rows;
+    }
+  }
   const int nq = i1 > i0 ? 4 * (i1 - i0) : 0;   // quarters of this block
 
   // the lane's tap row k and its offset in the shifted copies (-1: k >= 27)
@@ -204,16 +231,21 @@ __global__ __launch_bounds__(256) void stem_wgrad_kernel(StemWgradArgs a) {
 
   // quarter q's inputs go to registers one quarter ahead
   float4 xv[3];
-  uint4 dv[8];
+  uint4 dv[8], zv[BN ? 8 : 1], mv[BN == 2 ? 8 : 1];
   auto load_x = [&](int im) {
     const float* xb = a.x + (int64_t)im * 3 * ST_W * ST_W;
 #pragma unroll
     for (int it = 0; it < 3; ++it) xv[it] = *(const float4*)(xb + 4 * (tid + 256 * it));
   };
   auto load_dy = [&](int im, int qt) {
-    const bf16_t* db = a.dy + ((int64_t)im * ST_W * ST_W + qt * STW_QPIX) * ST_CO;
+    const int64_t o = ((int64_t)im * ST_W * ST_W + qt * STW_QPIX) * ST_CO;
 #pragma unroll
-    for (int it = 0; it < 8; ++it) dv[it] = *(const uint4*)(db + (int64_t)(tid + 256 * it) * 8);
+    for (int it = 0; it < 8; ++it) {
+      const int64_t e = o + (int64_t)(tid + 256 * it) * 8;
+      dv[it] = *(const uint4*)(a.dy + e);
+      if constexpr (BN > 0) zv[it] = *(const uint4*)((const bf16_t*)a.bn.z + e);
+      if constexpr (BN == 2) mv[it] = *(const uint4*)((const bf16_t*)a.bn.act + e);
+    }
   };
   if (nq > 0) {
     load_x(i0);
@@ -246,6 +278,36 @@ __global__ __launch_bounds__(256) void stem_wgrad_kernel(StemWgradArgs a) {
     for (int it = 0; it < 8; ++it) {
       const int c = tid + 256 * it;               // 16-byte chunk: pixel c / 8, channels 8 (c % 8)
       const int px = c >> 3, co = (c & 7) * 8;
+      if constexpr (BN > 0) {   // dz of the 8 channels, as the batch-norm backward forms it
+        const uint32_t dw[4] = {dv[it].x, dv[it].y, dv[it].z, dv[it].w};
+        const uint32_t zw[4] = {zv[it].x, zv[it].y, zv[it].z, zv[it].w};
+        uint32_t mw[4] = {~0u, ~0u, ~0u, ~0u};
+        if constexpr (BN == 2) {
+          mw[0] = mv[it].x;
+          mw[1] = mv[it].y;
+          mw[2] = mv[it].z;
+          mw[3] = mv[it].w;
+        }
+        uint32_t ow[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float o2[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int j = 2 * e + h;
+            float g = __uint_as_float(h ? (dw[e] & 0xffff0000u) : (dw[e] << 16));
+            if constexpr (BN == 2) {
+              const float m = __uint_as_float(h ? (mw[e] & 0xffff0000u) : (mw[e] << 16));
+              if (!(m > 0.f)) g = 0.f;
+            }
+            const float zf = __uint_as_float(h ? (zw[e] & 0xffff0000u) : (zw[e] << 16));
+            const float xh = (zf - bmu[j]) * brs[j];
+            o2[h] = bgr[j] * (g - (bk1[j] + xh * bk2[j]));
+          }
+          ow[e] = (uint32_t)f2bf(o2[0]) | ((uint32_t)f2bf(o2[1]) << 16);
+        }
+        dv[it] = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+      }
       const uint32_t w[4] = {dv[it].x, dv[it].y, dv[it].z, dv[it].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -325,9 +387,14 @@ int stem_wgrad_splits(const int* n, int nseg, int* seg_split) {
 }
 
 hipError_t launch_stem_wgrad(const float* x, const void* dy, float* part, const int* seg_n0,
-                             const int* seg_split, int nseg, hipStream_t s) {
+                             const int* seg_split, int nseg, hipStream_t s, const StemBnBwd* bn) {
   if (nseg < 1 || nseg > MAX_SEG || seg_split[nseg] < 1) return hipErrorInvalidValue;
+  if (bn && (!bn->z || !bn->mean || !bn->rstd || !bn->gamma)) return hipErrorInvalidValue;
+  if (bn)
+    for (int i = 0; i < nseg; ++i)
+      if (!bn->sum0[i] || !bn->sum1[i]) return hipErrorInvalidValue;
   StemWgradArgs a{};
+  if (bn) a.bn = *bn;
   a.x = x;
   a.dy = (const bf16_t*)dy;
   a.part = part;
@@ -340,7 +407,10 @@ hipError_t launch_stem_wgrad(const float* x, const void* dy, float* part, const 
     a.seg_split[i] = seg_split[nseg];
     a.seg_n0[i] = seg_n0[nseg];
   }
-  hipLaunchKernelGGL(stem_wgrad_kernel, dim3((unsigned)seg_split[nseg]), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)seg_split[nseg]);
+  if (!bn) hipLaunchKernelGGL(stem_wgrad_kernel<0>, grid, dim3(256), 0, s, a);
+  else if (!bn->act) hipLaunchKernelGGL(stem_wgrad_kernel<1>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(stem_wgrad_kernel<2>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
