@@ -478,15 +478,17 @@ def main():
     result["partitions_last"] = r["partitions_last"]
     result["loss_last"] = r["loss_last"]
     result["wavg_sgd_standalone"] = standalone_wavg()
-    result["attainable"] = attainable()
-    if wl.dtype == "bf16":   # the loop runs bf16 MFMAs
+    if not args.no_probe:    # the attainable rates are probes too
+        result["attainable"] = attainable()
+    if "attainable" in result and wl.dtype == "bf16":   # the loop runs bf16 MFMAs
         mf = result["attainable"]["mfma_bf16_loop"]["achieved"]
         if "roofline" in result:
             result["roofline"]["frac_of_attainable"] = round(result["roofline"]["achieved"] / mf, 4)
         result["step_roofline"]["frac_of_attainable"] = round(
             result["step_roofline"]["achieved"] / mf, 4)
-    result["hbm_roofline"]["frac_of_attainable"] = round(
-        result["hbm_roofline"]["achieved"] / result["attainable"]["copy_1GiB"]["achieved"], 4)
+    if "attainable" in result:
+        result["hbm_roofline"]["frac_of_attainable"] = round(
+            result["hbm_roofline"]["achieved"] / result["attainable"]["copy_1GiB"]["achieved"], 4)
     if not args.no_extra and not args.streams:
         extra = {}
         for name in EXTRA:
