@@ -44,6 +44,13 @@ FULL_SIZE = [
 ]
 CONFIGS = {c[0]: c for c in FULL_SIZE}
 
+# rounding realizations behind a configuration's stored floors, where three
+# (tests/gpu_util.REALIZATIONS) are too few: VGG-16's gradients behind its
+# max-pool decisions have heavy-tailed bf16 errors (over 12 realizations of
+# its smallest worker, the largest of the first 8 exceeds the largest of the
+# first 3 by up to 1.9x, median 1.18x over the tensors)
+REALIZATIONS_FULL = {"vgg16_bf16_N4096": (0, 1, 2, 3, 4, 5, 6, 7)}
+
 # the ResNet-18 fp32 workload's step at its own size: partition, seed
 STEP_NAME = "resnet18_fp32_step_N1024"
 STEP_PARTITION = [128, 192, 256, 448]

@@ -15,7 +15,8 @@ the worker's own partition):
   w<i>_floor       per tensor, the error (over all its entries) of the
                    oracle's own arithmetic at the path's precision (Ctx
                    modes "fp32" / "bf16"), the largest over the precision's
-                   rounding realizations
+                   rounding realizations (fullsize.REALIZATIONS_FULL where
+                   a configuration needs more than tests.gpu_util's)
   w<i>_relu        the smallest ReLU margin of the exact pass
 and the configuration's partition, compared workers and input fingerprint.
 The step file holds the same for the update theta' - theta ("d_") and the
@@ -65,7 +66,7 @@ def make_config(name):
         relu = min(m[1][0] for m in ctx.margins if m[0] == "relu" and m[1].size)
         scales, vmax, ref = summarize(table, idx, g)
         floors = []
-        for k in REALIZATIONS[dtype]:
+        for k in F.REALIZATIONS_FULL.get(name, REALIZATIONS[dtype]):
             say("%s worker %d: %s realization %d" % (name, i, dtype, k))
             _, gk = Mo.worker_grad(net, th, x[a:b], y[a:b], storage=dtype, grid=k)
             floors.append(F.full_errors(gk, g, table, scales, vmax))
