@@ -165,8 +165,10 @@ hipError_t launch_wgrad3(const GemmParams& p, hipStream_t s);
 // [64][3][3][3]; writes y [n][32][32][64] bf16 and, when x8 is not null, the
 // input rounded to bf16 in NHWC with 8 channels (3 real, 5 zero).
 bool stem_ok(int cin, int cout, int k, int stride, int pad, int H, int W);
+// stat_part (or null): per image b, the batch-norm sums of its stored output,
+// stat_part[(b * 2 + k) * 64 + c] = sum over its pixels of y[c]^(k + 1)
 hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8, int n,
-                           hipStream_t s);
+                           hipStream_t s, float* stat_part = nullptr);
 // The stem's weight gradient in bf16 (stem.hip), split-K per worker segment:
 // stem_wgrad_splits fills seg_split (blocks of each segment) from the
 // segments' sample counts and returns the split count; launch_stem_wgrad
@@ -254,11 +256,13 @@ hipError_t launch_softmax_ce(const float* logits, const int32_t* labels, const S
 // part: float scratch [STAT_MAX_BLOCKS][2][C].
 constexpr int STAT_MAX_BLOCKS = 1024;
 // The finish alone, on block partials written elsewhere (GemmParams::
-// stat_part): segment s sums partials [s * blocks, (s + 1) * blocks) of
-// unshifted kind-0 sums over rows_per_sample rows per sample.
+// stat_part): segment s sums partials [s * blocks, (s + 1) * blocks) (with
+// seg_blk: [seg_blk[s], seg_blk[s + 1])) of unshifted kind-0 sums over
+// rows_per_sample rows per sample.
 hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, const Segs& sg,
                                    int64_t rows_per_sample, int C, float* const* mean,
-                                   float* const* rstd, float eps, hipStream_t s);
+                                   float* const* rstd, float eps, hipStream_t s,
+                                   const int* seg_blk = nullptr);
 // Optional weighted sum over the segments of kinds 1 and 2 (the partition-
 // weighted gradient): sum0[c] = w[0] out0[0][c] + w[1] out0[1][c] + ... in
 // segment order (sum1 likewise from out1), the per-segment outputs still

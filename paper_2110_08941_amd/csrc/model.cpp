@@ -923,8 +923,6 @@ hipError_t bn_apply(const Ctx& c, const BNL& b, const void* z, const void* res, 
                           c.theta + b.b, res, relu, c.sg, rps, b.c, y, c.s, ybits);
 }
 
-// dz = batch-norm backward of dy (masked by [act > 0] if act); writes every
-// worker's dbeta, dgamma into its g[s]
 // Where the batch-norm backward's per-worker sums go: the beta and gamma
 // gradients of g[s] (or, forming g_bar, this stream's slots, with their
 // weighted sums into g_bar)
@@ -948,6 +946,8 @@ void bn_sum_targets(const Ctx& c, const BNL& b, float* (&db)[MAX_SEG], float* (&
   }
 }
 
+// dz = batch-norm backward of dy (masked by [act > 0] if act); writes every
+// worker's dbeta, dgamma into its g[s]
 hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, const void* z,
                   int64_t rps, void* dz) {
   float *db[MAX_SEG], *dg[MAX_SEG];
@@ -1082,6 +1082,35 @@ hipError_t stem_fwd(const Ctx& c, const ConvL& L, const float* x, void* X0, void
   return conv_fwd(c, st, X0, y, false, c.ws.stem_w, nullptr, layer_flops(L, c.n));
 }
 
+// The first layer and its batch-norm statistics: the direct bf16 stem takes
+// the sums of its stored output per image (one image per block, so one
+// worker per block) and the finish adds each worker's images; otherwise the
+// statistics pass over z follows.
+hipError_t stem_bn_fwd(const Ctx& c, const ConvL& L, const BNL& b, const float* x, void* X0,
+                       void* z) {
+  bool fuse = c.bf && !c.part && b.c == L.cout && L.cout == 64 &&
+              stem_ok(L.cin, L.cout, L.k, L.stride, L.pad, L.H, L.W) &&
+              (int64_t)c.n * 2 * 64 <= (int64_t)STAT_MAX_BLOCKS * 2 * 512 && c.sg.count >= 1 &&
+              c.sg.n0[0] == 0 && c.sg.n0[c.sg.count] == c.n;
+  for (int i = 0; fuse && i < c.sg.count; ++i) fuse = c.sg.n0[i + 1] > c.sg.n0[i];
+  if (!fuse) {
+    HS_TRY(stem_fwd(c, L, x, X0, z));
+    return bn_stats(c, b, z, (int64_t)L.Ho * L.Wo);
+  }
+  const bool probe = probe_begin(c, MODE_FWD, 32, 64);
+  HS_TRY(launch_stem_fwd(x, c.W(L.w), z, nullptr, c.n, c.s, c.sp()));
+  if (probe) HS_TRY(probe_end(c, layer_flops(L, c.n)));
+  float *o0[MAX_SEG], *o1[MAX_SEG];
+  int blk[MAX_SEG + 1];
+  for (int i = 0; i < c.sg.count; ++i) {
+    o0[i] = c.mean(b, i);
+    o1[i] = c.rstd(b, i);
+  }
+  for (int i = 0; i <= c.sg.count; ++i) blk[i] = c.sg.n0[i];
+  return launch_stats_finish_fwd(c.bf, c.sp(), 0, c.sg, (int64_t)L.Ho * L.Wo, b.c, o0, o1, 1e-5f,
+                                 c.s, blk);
+}
+
 // With bn (the direct kernel only), dz is the batch-norm output's gradient
 // and the kernel forms the batch-norm backward as it reads it (StemBnBwd).
 hipError_t stem_wgrad(const Ctx& c, const ConvL& L, const void* dz, const void* X0,
@@ -1203,8 +1232,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   void** G = c.ws.grad;
   const int n = c.n;
   const Ctx cs = side(c);   // second stream: projection shortcuts, weight gradients
-  HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
-  HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
+  HS_TRY(stem_bn_fwd(c, m.stem, m.stem_bn, x, S[0], S[1]));
   HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
   const void* cur = S[2];
   int si = 3;
@@ -1331,8 +1359,7 @@ hipError_t resnet_bottleneck(const Ctx& c, const float* x, const int32_t* y, flo
   const int n = c.n;
   constexpr int SLOTS = 7;
   const Ctx cs = side(c);   // second stream: projection shortcuts, weight gradients
-  HS_TRY(stem_fwd(c, m.stem, x, S[0], S[1]));
-  HS_TRY(bn_stats(c, m.stem_bn, S[1], 1024));
+  HS_TRY(stem_bn_fwd(c, m.stem, m.stem_bn, x, S[0], S[1]));
   HS_TRY(bn_apply(c, m.stem_bn, S[1], nullptr, 1, 1024, S[2], Bt[2]));
   const void* cur = S[2];
   int si = 3;
@@ -1458,8 +1485,7 @@ hipError_t vgg(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     void *Z = S[1 + 3 * i], *A = S[2 + 3 * i], *P = S[3 + 3 * i];
     const int64_t rps = (int64_t)l.c.Ho * l.c.Wo;
     if (i == 0) {
-      HS_TRY(stem_fwd(c, l.c, x, S[0], Z));
-      HS_TRY(bn_stats(c, l.bn, Z, rps));
+      HS_TRY(stem_bn_fwd(c, l.c, l.bn, x, S[0], Z));
     } else {
       HS_TRY(conv_bn_fwd(c, l.c, cur, Z, l.bn, rps));
     }

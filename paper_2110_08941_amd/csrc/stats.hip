@@ -387,8 +387,10 @@ __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
 
 hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, const Segs& sg,
                                    int64_t rows_per_sample, int C, float* const* mean,
-                                   float* const* rstd, float eps, hipStream_t s) {
-  if (C < 1 || sg.count < 1 || sg.count > MAX_SEG || blocks < 1) return hipErrorInvalidValue;
+                                   float* const* rstd, float eps, hipStream_t s,
+                                   const int* seg_blk) {
+  if (C < 1 || sg.count < 1 || sg.count > MAX_SEG || (!seg_blk && blocks < 1))
+    return hipErrorInvalidValue;
   FinishArgs f{};
   f.x = nullptr;
   f.part = part;
@@ -397,7 +399,7 @@ hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, con
   f.sr.count = sg.count;
   for (int i = 0; i <= MAX_SEG; ++i) {
     const int k = i < sg.count ? i : sg.count;
-    f.sr.blk[i] = k * blocks;
+    f.sr.blk[i] = seg_blk ? seg_blk[k] : k * blocks;
     f.sr.row[i] = (int64_t)sg.n0[k] * rows_per_sample;
   }
   for (int i = 0; i < sg.count; ++i) {

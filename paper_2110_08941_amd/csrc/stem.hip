@@ -39,13 +39,21 @@ __device__ inline uint32_t pack2s(float a, float b) {
   return u;
 }
 
+// With part set, the block also writes its image's batch-norm sums of the
+// stored (bf16) output: part[(b * 2 + k) * 64 + c] = sum over the image's
+// pixels of y[c]^(k + 1).  Lane c of each wave adds channel c of every row it
+// stages (a column of the staged row), the waves' sums are then added in
+// order.
 __global__ __launch_bounds__(256) void stem_fwd_kernel(const float* __restrict__ x,
                                                        const bf16_t* __restrict__ w,
                                                        bf16_t* __restrict__ y,
-                                                       bf16_t* __restrict__ x8) {
+                                                       bf16_t* __restrict__ x8,
+                                                       float* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) bf16_t img[3 * ST_PLANE + 4];
   __shared__ __attribute__((aligned(16))) char stage[4][32 * ST_ROWB];
+  __shared__ float sred[4][2][ST_CO];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kh = lane >> 5;
+  float ssum = 0.f, ssq = 0.f;   // channel `lane`: the wave's rows
   const int64_t b = blockIdx.x;
 
   // the framed image: zero, then the interior rounded to bf16
@@ -139,7 +147,24 @@ __global__ __launch_bounds__(256) void stem_fwd_kernel(const float* __restrict__
       const uint4 q = *(const uint4*)(sg + (c >> 3) * ST_ROWB + (c & 7) * 16);
       *(uint4*)(yo + (c >> 3) * ST_CO + (c & 7) * 8) = q;
     }
+    if (part) {   // channel `lane` of the row's 32 pixels, as stored
+#pragma unroll 8
+      for (int px = 0; px < 32; ++px) {
+        const float v = __uint_as_float((uint32_t)*(const uint16_t*)(sg + px * ST_ROWB + lane * 2) << 16);
+        ssum += v;
+        ssq += v * v;
+      }
+    }
     __builtin_amdgcn_wave_barrier();
+  }
+  if (part) {
+    sred[wave][0][lane] = ssum;
+    sred[wave][1][lane] = ssq;
+    __syncthreads();
+    if (tid < 2 * ST_CO) {
+      const int k = tid >> 6, c = tid & (ST_CO - 1);
+      part[(b * 2 + k) * ST_CO + c] = ((sred[0][k][c] + sred[1][k][c]) + sred[2][k][c]) + sred[3][k][c];
+    }
   }
 }
 
@@ -370,10 +395,10 @@ bool stem_ok(int cin, int cout, int k, int stride, int pad, int H, int W) {
 }
 
 hipError_t launch_stem_fwd(const float* x, const void* w_bf16, void* y, void* x8, int n,
-                           hipStream_t s) {
+                           hipStream_t s, float* stat_part) {
   if (n < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stem_fwd_kernel, dim3((unsigned)n), dim3(256), 0, s, x,
-                     (const bf16_t*)w_bf16, (bf16_t*)y, (bf16_t*)x8);
+                     (const bf16_t*)w_bf16, (bf16_t*)y, (bf16_t*)x8, stat_part);
   return hipGetLastError();
 }
 
