@@ -44,7 +44,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void* lds_ptr;          // LDS
 typedef __attribute__((address_space(1))) const void* gbl_cptr;   // global
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32, EPI_STATS = 64 };
 
 constexpr int C2_WAVES = 8;
 constexpr int C2_BM = 64 * C2_WAVES;   // rows per block
@@ -59,6 +59,14 @@ __device__ inline uint32_t pack2(float a, float b) {
 }
 
 __device__ inline float bfl(const bf16_t* p, int64_t i) { return bf2f(p[i]); }
+
+// x plus x of the lane n places over within its row of 16 lanes (DPP row
+// rotate)
+template <int N>
+__device__ inline float add_row_ror(float x) {
+  const int y = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false);
+  return x + __builtin_bit_cast(float, y);
+}
 
 }  // namespace
 
@@ -143,6 +151,7 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
   typedef uint4 BsT[RS][2][BN];
   BsT* Bs = (BsT*)smem;
   float* Ewave = (float*)smem + (threadIdx.x >> 6) * 64 * EROW;   // epilogue staging of this wave
+  float* Qst[2] = {nullptr, nullptr};   // statistics: quarter sums of waves 0-3, 4-7
 
   const ConvGeom& g = p.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -208,6 +217,9 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
     __shared__ __attribute__((aligned(16))) char sP0[2 * PPLANE];
     __shared__ __attribute__((aligned(16))) char sP1[2 * PPLANE];
     Ewave = (float*)(wave < 4 ? sB0 : sB1) + (wave & 3) * 64 * EROW;
+    Qst[0] = (float*)sP0;
+    Qst[1] = (float*)sP1;
+    static_assert(16 * 2 * BN * 4 <= 2 * PPLANE, "quarter sums fit a patch buffer");
 
     // Tile rows are whole images: the image-local pixel of tile row q is
     // q % (H * W); bit t of vm[mb] = tap t of that row lies in the image.
@@ -438,6 +450,102 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
       __syncthreads();
     }
 
+  }
+
+  if constexpr ((EPI & EPI_STATS) != 0) {
+    // Forward with the batch-norm sums of the stored output per worker
+    // segment.  The loop ended with a barrier: B and the patch are no longer
+    // read.  Each wave stages its 64 x 32 fp32 chunks in its own region (as
+    // below); lane l takes the four consecutive rows 4 (l / 4) + i and the 8
+    // channels 8 (l % 4) .. of a chunk, stores them in bf16 and adds the
+    // stored values and their squares (bf16 dot products of row pairs,
+    // accumulated in fp32).  A row of 16 lanes covers 16
+    // consecutive rows (a quarter of the wave's rows, inside one image since
+    // images are whole quarters): DPP row rotates by 4 and 8 add its four
+    // lanes of each channel group, and lanes 0-3 of the row write the
+    // quarter's sums to LDS.  Then one thread per (sum, channel) adds the
+    // tile's 32 quarters in order (those of other segments masked to zero),
+    // one partial per worker segment: row tile
+    // t writes segment s's partial at slot t + s (slots increase with (t, s),
+    // so a segment's partials are consecutive), and where the next tile
+    // starts a new segment, a zero at slot t + s + 1 so that the slot ranges
+    // of consecutive segments meet.
+    static_assert(PATCH && MODE == MODE_FWD && EPI == EPI_STATS, "statistics: plain patch forward");
+    float* E = Ewave;
+    const int c8 = 8 * (lane & 3), r4 = 4 * (lane >> 2);
+    float* Qw = Qst[wave >> 2] + ((wave & 3) * 4 + (lane >> 4)) * 2 * BN;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *(float4*)(E + (32 * mb + (lane & 31)) * EROW + 8 * q + 4 * kh) =
+              make_float4(acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
+                          acc[mb][nb][4 * q + 3]);
+      __builtin_amdgcn_wave_barrier();
+      float rv[4][8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = r4 + i, m = m0 + row;
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        rv[i][0] = lo.x; rv[i][1] = lo.y; rv[i][2] = lo.z; rv[i][3] = lo.w;
+        rv[i][4] = hi.x; rv[i][5] = hi.y; rv[i][6] = hi.z; rv[i][7] = hi.w;
+        const uint4 o = make_uint4(pack2(lo.x, lo.y), pack2(lo.z, lo.w), pack2(hi.x, hi.y),
+                                   pack2(hi.z, hi.w));
+        if (m < p.M) *(uint4*)((bf16_t*)p.out + (int64_t)m * p.N + n0 + nb * 32 + c8) = o;
+      }
+      __builtin_amdgcn_wave_barrier();
+      // per channel: the stored (bf16-rounded) values of rows 0, 1 and 2, 3
+      // as pairs; a bf16 dot product adds a pair (with ones) or its squares
+      float s0[8], s1[8];
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bf16x2 p01 = __builtin_convertvector((f32x2){rv[0][e], rv[1][e]}, bf16x2);
+        const bf16x2 p23 = __builtin_convertvector((f32x2){rv[2][e], rv[3][e]}, bf16x2);
+        s0[e] = __builtin_amdgcn_fdot2_f32_bf16(p23, ones, __builtin_amdgcn_fdot2_f32_bf16(p01, ones, 0.f, false), false);
+        s1[e] = __builtin_amdgcn_fdot2_f32_bf16(p23, p23, __builtin_amdgcn_fdot2_f32_bf16(p01, p01, 0.f, false), false);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        s0[e] = add_row_ror<8>(add_row_ror<4>(s0[e]));
+        s1[e] = add_row_ror<8>(add_row_ror<4>(s1[e]));
+      }
+      if ((lane & 12) == 0) {
+        float* q0 = Qw + nb * 32 + c8;
+        *(float4*)q0 = make_float4(s0[0], s0[1], s0[2], s0[3]);
+        *(float4*)(q0 + 4) = make_float4(s0[4], s0[5], s0[6], s0[7]);
+        *(float4*)(q0 + BN) = make_float4(s1[0], s1[1], s1[2], s1[3]);
+        *(float4*)(q0 + BN + 4) = make_float4(s1[4], s1[5], s1[6], s1[7]);
+      }
+    }
+    __syncthreads();   // every wave's quarter sums are in LDS
+    if (tid < 2 * BN) {
+      const int k = tid / BN, c = tid % BN;
+      const int tile_m0 = tm * C2_BM;
+      const int64_t HW = (int64_t)g.H * g.W;
+      float v[32];
+#pragma unroll
+      for (int gq = 0; gq < 32; ++gq) v[gq] = Qst[gq >> 4][((gq & 15) * 2 + k) * BN + c];
+      // quarters of the tile holding output rows (images are whole quarters)
+      const int nq = (int)((p.M - tile_m0) / 16 < 32 ? (p.M - tile_m0) / 16 : 32);
+      for (int sg = 0; sg < p.nseg; ++sg) {
+        const int64_t r0 = p.seg_n0[sg] * HW - tile_m0, r1 = p.seg_n0[sg + 1] * HW - tile_m0;
+        if (sg > 0 && r0 == C2_BM)   // the next tile starts segment sg: the gap slot
+          p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = 0.f;
+        // segment sg's quarters [lo, hi) of this tile, added in order
+        const int lo = r0 <= 0 ? 0 : (r0 >= 16 * nq ? nq : (int)(r0 / 16));
+        const int hi = r1 <= 0 ? 0 : (r1 >= 16 * nq ? nq : (int)(r1 / 16));
+        if (lo >= hi) continue;
+        float a = 0.f;
+#pragma unroll
+        for (int gq = 0; gq < 32; ++gq) a += (gq >= lo && gq < hi) ? v[gq] : 0.f;
+        p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = a;
+      }
+    }
+    return;
   }
 
   if constexpr (STAGE_EPI) {
@@ -1096,6 +1204,12 @@ template <int MODE, int BN, int RS, bool PATCH>
 static void launch_epi2(const GemmParams& p, dim3 grid, hipStream_t s) {
   if constexpr (MODE == MODE_FWD) {
     const bool bias = p.bias != nullptr, relu = p.relu != 0;
+    if constexpr (PATCH && BN == 128) {
+      if (p.stat_part) {   // launch_conv2 checked conv2_stats_ok
+        hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_STATS, PATCH>), grid, dim3(512), 0, s, p);
+        return;
+      }
+    }
     if (bias && relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS | EPI_RELU, PATCH>), grid, dim3(512), 0, s, p);
     else if (bias) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_BIAS, PATCH>), grid, dim3(512), 0, s, p);
     else if (relu) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_RELU, PATCH>), grid, dim3(512), 0, s, p);
@@ -1200,9 +1314,29 @@ hipError_t launch_conv2s2f(const GemmParams& p0, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool conv2_stats_ok(const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  if (!conv2_ok(MODE_FWD, p) || !conv2_patch(p) || conv2_bn(p.N) != 128 || p.bias || p.relu)
+    return false;
+  if ((g.H * g.W) % 16 != 0 || p.M != (int64_t)g.n * g.H * g.W) return false;
+  if (p.nseg < 1 || p.nseg > MAX_SEG || p.seg_n0[0] != 0 || p.seg_n0[p.nseg] != g.n) return false;
+  for (int i = 0; i < p.nseg; ++i)
+    if (p.seg_n0[i + 1] <= p.seg_n0[i]) return false;
+  return true;
+}
+
+int conv2_stat_slots(const GemmParams& p, int* blk) {
+  const int64_t hw = (int64_t)p.g.H * p.g.W;
+  const int tiles_m = (int)ceil_div(p.M, C2_BM);
+  for (int s = 0; s < p.nseg; ++s) blk[s] = (int)(p.seg_n0[s] * hw / C2_BM) + s;
+  blk[p.nseg] = tiles_m + p.nseg - 1;
+  return blk[p.nseg];
+}
+
 // p.b must point to the packed weights (launch_pack_weights of the same p)
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s) {
   if (!conv2_ok(mode, p)) return hipErrorInvalidValue;
+  if (p.stat_part && (mode != MODE_FWD || !conv2_stats_ok(p))) return hipErrorInvalidValue;
   if (mode == MODE_FWD) return launch_mode2<MODE_FWD>(p, s);
   return launch_mode2<MODE_DGRAD>(p, s);
 }

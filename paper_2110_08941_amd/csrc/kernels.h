@@ -68,11 +68,14 @@ struct GemmParams {
   int seg_split[MAX_SEG + 1];
   int seg_n0[MAX_SEG + 1];
   // Batch-norm forward sums of the output, taken in the epilogue (conv64
-  // forward only; null: none): per segment s (samples seg_n0[s] ..
-  // seg_n0[s + 1] - 1, nseg segments) and block b of the launch,
-  // stat_part[((s * blocks + b) * 2 + k) * N + n] = sum over the block's
-  // output rows of segment s of y^(k + 1), y the stored (rounded) output;
-  // zero where the block has no rows of s.
+  // forward and the conv2 patch-form forward; null: none), per segment s
+  // (samples seg_n0[s] .. seg_n0[s + 1] - 1, nseg segments):
+  // stat_part[(slot * 2 + k) * N + n] = sum over a part of the output rows of
+  // s of y^(k + 1), y the stored (rounded) output, at the slots of s:
+  //   conv64: slot s * blocks + b, block b's rows (zero where b has none);
+  //   conv2: slot t + s, row tile t's rows, and a zero at slot t + s + 1
+  //     when tile t + 1 starts segment s + 1 (conv2_stat_slots).
+  // Either way segment s's partials are the slots [blk[s], blk[s + 1]).
   float* stat_part;
 };
 
@@ -120,6 +123,13 @@ int64_t conv2_packed_elems(const GemmParams& p, int mode);
 hipError_t launch_pack_weights(const void* W, void* Bp, int mode, const GemmParams& p,
                                hipStream_t s);
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
+// Whether the conv2 forward can take the batch-norm sums of its output
+// (p.stat_part with nseg / seg_n0 set): the patch form, 128-channel column
+// tiles, no bias or ReLU, images of a multiple of 16 pixels, nonempty
+// segments covering the batch.  conv2_stat_slots fills blk[0 .. nseg] (the
+// slot range of each segment) and returns the number of slots.
+bool conv2_stats_ok(const GemmParams& p);
+int conv2_stat_slots(const GemmParams& p, int* blk);
 // Up to PACK_BATCH packings (launch_pack_weights of theta_bf16 + woff into
 // Bp + dst, offsets in elements) in one launch, passed by value.
 struct PackJob {

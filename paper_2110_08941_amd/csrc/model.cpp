@@ -521,8 +521,11 @@ hipError_t probe_end(const Ctx& c, double flops) {
 
 // Launch one GEMM (fast kernel when the shape allows, generic otherwise);
 // brackets it with probe events when it is the probed instantiation.
+// With p.stat_part set (a forward), *stats_fused tells whether the kernel
+// took the batch-norm sums and stat_blk[0 .. workers] receives their slot
+// ranges (GemmParams::stat_part).
 hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vecb, int bm, int bn,
-                int splits, double flops, bool* stats_fused = nullptr) {
+                int splits, double flops, bool* stats_fused = nullptr, int* stat_blk = nullptr) {
   Workspace& ws = c.ws;
   if (stats_fused) *stats_fused = false;
   int fbm = 0, fbn = 0;
@@ -554,13 +557,26 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // stream (c.part set) take the other kernels
   if (c.part) mfma32 = w64 = false;
   // epilogue statistics (GemmParams::stat_part) per worker: the 64-channel
-  // forward kernel only (nseg stays 0 for the others, where it means split-K
-  // over worker segments)
-  if (w64 && mode == MODE_FWD && q.stat_part) {
+  // forward kernel and the conv2 patch form (nseg stays 0 for the others,
+  // where it means split-K over worker segments), while the partials fit
+  // the workspace's buffer
+  bool stats = false;
+  if ((w64 || mfma32) && mode == MODE_FWD && q.stat_part && stat_blk) {
     q.nseg = c.sg.count;
     for (int i = 0; i <= MAX_SEG; ++i) q.seg_n0[i] = c.sg.n0[i < c.sg.count ? i : c.sg.count];
-  } else {
+    int64_t slots = -1;
+    if (w64) {
+      const int blocks = conv64_blocks(q);
+      for (int i = 0; i <= q.nseg; ++i) stat_blk[i] = i * blocks;
+      slots = (int64_t)q.nseg * blocks;
+    } else if (conv2_stats_ok(q)) {
+      slots = conv2_stat_slots(q, stat_blk);
+    }
+    stats = slots > 0 && slots * 2 * p.N <= (int64_t)STAT_MAX_BLOCKS * 2 * 512;
+  }
+  if (!stats) {
     q.stat_part = nullptr;
+    q.nseg = p.nseg;
   }
   if (mfma32 || w64) {
     const void* wb = nullptr;
@@ -571,10 +587,7 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   }
   const bool probe = (fast || mfma32 || wg3 || w64) && probe_begin(c, mode, bm, bn);
   if (wg3) HS_TRY(launch_wgrad3(p, c.s));
-  else if (w64) {
-    HS_TRY(launch_conv64(mode, q, c.s));
-    if (stats_fused && q.stat_part) *stats_fused = true;
-  }
+  else if (w64) HS_TRY(launch_conv64(mode, q, c.s));
   else if (mfma32) HS_TRY(launch_conv2(mode, q, c.s));
   else if (fast) HS_TRY(launch_igemm_fast(mode, c.bf, p, bm, bn, splits, c.s));
   else {
@@ -583,6 +596,7 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
     HS_TRY(launch_igemm(mode, c.bf, r, veca, vecb, bm, bn, splits, c.s));
   }
   if (probe) HS_TRY(probe_end(c, flops));
+  if (stats_fused) *stats_fused = stats;
   return hipSuccess;
 }
 
@@ -593,10 +607,12 @@ double layer_flops(const ConvL& L, int n) {
 
 // y = conv(x) (+ bias, ReLU); out_f32 forces an fp32 output
 // stat_part: request the batch-norm sums of y from the epilogue (see
-// GemmParams::stat_part); *stats_fused tells whether the kernel took them
+// GemmParams::stat_part); *stats_fused tells whether the kernel took them,
+// stat_blk receives the workers' slot ranges
 hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool out_f32,
                     const void* wptr = nullptr, const float* bias = nullptr, double flops = 0.0,
-                    float* stat_part = nullptr, bool* stats_fused = nullptr) {
+                    float* stat_part = nullptr, bool* stats_fused = nullptr,
+                    int* stat_blk = nullptr) {
   GemmParams p = base_params(L, c.n);
   p.stat_part = stat_part;
   p.a = x;
@@ -627,7 +643,7 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
   return gemm(c, MODE_FWD, p, vec, vec, bm, bn, 1, flops > 0 ? flops : layer_flops(L, c.n),
-              stats_fused);
+              stats_fused, stat_blk);
 }
 
 // dx = dgrad(dy) (+ addend) (* [mask > 0]); a stride-2 layer is computed by
@@ -893,27 +909,24 @@ hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
 
 // z = conv(x) and the batch-norm statistics of z: summed in the
 // convolution's epilogue where its kernel takes them (the 64-channel 3x3
-// layers on 32-wide maps: partials per block and worker, then the finish),
-// else by a pass over z
+// layers on 32-wide maps and the conv2 patch form: partials per block or
+// row tile and worker, then the finish), else by a pass over z
 hipError_t conv_bn_fwd(const Ctx& c, const ConvL& L, const void* x, void* z, const BNL& b,
                        int64_t rps) {
   bool want = c.bf && !c.part && L.b < 0 && !L.relu && b.c == L.cout && c.sg.count >= 1 &&
               c.sg.n0[0] == 0 && c.sg.n0[c.sg.count] == c.n;
   for (int i = 0; want && i < c.sg.count; ++i) want = c.sg.n0[i + 1] > c.sg.n0[i];
-  int blocks = 0;
-  if (want) {
-    blocks = conv64_blocks(base_params(L, c.n));
-    want = (int64_t)c.sg.count * blocks * 2 * L.cout <= (int64_t)STAT_MAX_BLOCKS * 2 * 512;
-  }
   bool fused = false;
-  HS_TRY(conv_fwd(c, L, x, z, false, nullptr, nullptr, 0.0, want ? c.sp() : nullptr, &fused));
+  int blk[MAX_SEG + 1];
+  HS_TRY(conv_fwd(c, L, x, z, false, nullptr, nullptr, 0.0, want ? c.sp() : nullptr, &fused,
+                  blk));
   if (!fused) return bn_stats(c, b, z, rps);
   float *o0[MAX_SEG], *o1[MAX_SEG];
   for (int i = 0; i < c.sg.count; ++i) {
     o0[i] = c.mean(b, i);
     o1[i] = c.rstd(b, i);
   }
-  return launch_stats_finish_fwd(c.bf, c.sp(), blocks, c.sg, rps, b.c, o0, o1, 1e-5f, c.s);
+  return launch_stats_finish_fwd(c.bf, c.sp(), 0, c.sg, rps, b.c, o0, o1, 1e-5f, c.s, blk);
 }
 
 // y = relu?(batch-norm(z) + res) with every worker's own statistics

@@ -151,7 +151,12 @@ def separated_problem(arch, dtype, n, seed):
     pytest.fail("no data seed with separated decisions in every worker")
 
 
+# resnet18 bf16 [32, 1, 7, 24]: worker boundaries on the edges of the 512-row
+# tiles of the 16x16, 8x8 and 4x4 maps (samples 32, 40, 64) and inside them
+# (33), where the forward epilogue's batch-norm partials of consecutive
+# workers meet
 SEPARATED = [("resnet18", "fp32", [3, 1, 4]), ("resnet18", "bf16", [4, 2, 6, 1, 3]),
+             ("resnet18", "bf16", [32, 1, 7, 24]),
              ("vgg16", "fp32", [2, 3]), ("vgg16", "bf16", [3, 5, 1]),
              ("resnet50", "fp32", [2, 1, 3]), ("resnet50", "bf16", [3, 5, 1, 2]),
              ("small_cnn", "bf16", [3, 4]), ("mlp", "bf16", [6, 17, 2])]
