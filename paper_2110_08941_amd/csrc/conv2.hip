@@ -68,6 +68,40 @@ __device__ inline float add_row_ror(float x) {
   return x + __builtin_bit_cast(float, y);
 }
 
+// The batch-norm partials of one output tile (TILE rows from row tile_m0 =
+// tm * TILE, BN channels from n0) from the sums of its 32 row groups of
+// TILE / 32 rows (group gq's two sums at Q[gq / 16] + ((gq % 16) * 2 + k) * BN,
+// images are whole groups).  Thread (k, c) < 2 BN adds the groups in order,
+// those of other worker segments masked to zero, and writes segment s's
+// partial at slot tm + s; where the next tile starts segment s, a zero at
+// slot tm + s (slots then increase with (tile, segment) and the slots of
+// consecutive segments meet).
+template <int BN, int TILE>
+__device__ inline void flush_tile_stats(const GemmParams& p, float* const (&Q)[2], int tm, int n0,
+                                        int tid) {
+  constexpr int G = TILE / 32;
+  if (tid >= 2 * BN) return;
+  const int k = tid / BN, c = tid % BN;
+  const int64_t tile_m0 = (int64_t)tm * TILE;
+  const int64_t HW = (int64_t)p.g.Ho * p.g.Wo;
+  float v[32];
+#pragma unroll
+  for (int gq = 0; gq < 32; ++gq) v[gq] = Q[gq >> 4][((gq & 15) * 2 + k) * BN + c];
+  // groups of the tile holding output rows
+  const int nq = (int)((p.M - tile_m0) / G < 32 ? (p.M - tile_m0) / G : 32);
+  for (int sg = 0; sg < p.nseg; ++sg) {
+    const int64_t r0 = p.seg_n0[sg] * HW - tile_m0, r1 = p.seg_n0[sg + 1] * HW - tile_m0;
+    if (sg > 0 && r0 == TILE) p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = 0.f;
+    const int lo = r0 <= 0 ? 0 : (r0 >= (int64_t)G * nq ? nq : (int)(r0 / G));
+    const int hi = r1 <= 0 ? 0 : (r1 >= (int64_t)G * nq ? nq : (int)(r1 / G));
+    if (lo >= hi) continue;
+    float a = 0.f;
+#pragma unroll
+    for (int gq = 0; gq < 32; ++gq) a += (gq >= lo && gq < hi) ? v[gq] : 0.f;
+    p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = a;
+  }
+}
+
 }  // namespace
 
 // Bp[((s * RS + tap) * 2 + kh) * N + n][e] = B[n][tap][16 s + 8 kh + e]
@@ -463,13 +497,8 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
     // consecutive rows (a quarter of the wave's rows, inside one image since
     // images are whole quarters): DPP row rotates by 4 and 8 add its four
     // lanes of each channel group, and lanes 0-3 of the row write the
-    // quarter's sums to LDS.  Then one thread per (sum, channel) adds the
-    // tile's 32 quarters in order (those of other segments masked to zero),
-    // one partial per worker segment: row tile
-    // t writes segment s's partial at slot t + s (slots increase with (t, s),
-    // so a segment's partials are consecutive), and where the next tile
-    // starts a new segment, a zero at slot t + s + 1 so that the slot ranges
-    // of consecutive segments meet.
+    // quarter's sums to LDS; flush_tile_stats turns the tile's 32 quarters
+    // into one partial per worker segment.
     static_assert(PATCH && MODE == MODE_FWD && EPI == EPI_STATS, "statistics: plain patch forward");
     float* E = Ewave;
     const int c8 = 8 * (lane & 3), r4 = 4 * (lane >> 2);
@@ -522,29 +551,7 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
       }
     }
     __syncthreads();   // every wave's quarter sums are in LDS
-    if (tid < 2 * BN) {
-      const int k = tid / BN, c = tid % BN;
-      const int tile_m0 = tm * C2_BM;
-      const int64_t HW = (int64_t)g.H * g.W;
-      float v[32];
-#pragma unroll
-      for (int gq = 0; gq < 32; ++gq) v[gq] = Qst[gq >> 4][((gq & 15) * 2 + k) * BN + c];
-      // quarters of the tile holding output rows (images are whole quarters)
-      const int nq = (int)((p.M - tile_m0) / 16 < 32 ? (p.M - tile_m0) / 16 : 32);
-      for (int sg = 0; sg < p.nseg; ++sg) {
-        const int64_t r0 = p.seg_n0[sg] * HW - tile_m0, r1 = p.seg_n0[sg + 1] * HW - tile_m0;
-        if (sg > 0 && r0 == C2_BM)   // the next tile starts segment sg: the gap slot
-          p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = 0.f;
-        // segment sg's quarters [lo, hi) of this tile, added in order
-        const int lo = r0 <= 0 ? 0 : (r0 >= 16 * nq ? nq : (int)(r0 / 16));
-        const int hi = r1 <= 0 ? 0 : (r1 >= 16 * nq ? nq : (int)(r1 / 16));
-        if (lo >= hi) continue;
-        float a = 0.f;
-#pragma unroll
-        for (int gq = 0; gq < 32; ++gq) a += (gq >= lo && gq < hi) ? v[gq] : 0.f;
-        p.stat_part[((int64_t)(tm + sg) * 2 + k) * p.N + n0 + c] = a;
-      }
-    }
+    flush_tile_stats<BN, C2_BM>(p, Qst, tm, n0, tid);
     return;
   }
 
@@ -979,6 +986,7 @@ __global__ __launch_bounds__(512) void conv2s2_kernel(GemmParams p) {
 constexpr int F2_POS = 256;   // output positions per block
 constexpr int F2_BN = 128;    // output channels per block
 
+template <bool STATS>
 __global__ __launch_bounds__(512) void conv2s2f_kernel(GemmParams p) {
   constexpr int BN = F2_BN, NB = BN / 32, RS = 9;
   constexpr int SEG = RS * 2 * BN;              // 16-byte B chunks per slice
@@ -1116,6 +1124,59 @@ __global__ __launch_bounds__(512) void conv2s2f_kernel(GemmParams p) {
   // channels each
   float* E = (float*)sB0 + wave * 32 * EROW;
   const int c8 = 8 * (lane & 3);
+  if constexpr (STATS) {
+    // With the batch-norm sums of the stored output per worker segment: lane
+    // l takes the two consecutive rows 2 (l / 4) + i, so a row of 16 lanes
+    // covers 8 consecutive rows (inside one image: output images are whole
+    // 8-row groups); per channel the stored pair's sum and sum of squares
+    // (bf16 dot products), DPP row rotates by 4 and 8 over the row's lanes,
+    // and lanes 0-3 of each row write the group's sums to a patch buffer
+    // (free after the last barrier) for flush_tile_stats.
+    static_assert(32 * 2 * BN * 4 <= 2 * PPLANE, "group sums fit a patch buffer");
+    float* Qg = (float*)sP0 + (wave * 4 + (lane >> 4)) * 2 * BN;
+    const int r2 = 2 * (lane >> 2);
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        *(float4*)(E + (lane & 31) * EROW + 8 * qq + 4 * kh) =
+            make_float4(acc[nb][4 * qq], acc[nb][4 * qq + 1], acc[nb][4 * qq + 2], acc[nb][4 * qq + 3]);
+      __builtin_amdgcn_wave_barrier();
+      float rv[2][8];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int row = r2 + i;
+        const int64_t m = (int64_t)tile_m0 + wave * 32 + row;
+        const float4 lo = *(const float4*)(E + row * EROW + c8);
+        const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
+        rv[i][0] = lo.x; rv[i][1] = lo.y; rv[i][2] = lo.z; rv[i][3] = lo.w;
+        rv[i][4] = hi.x; rv[i][5] = hi.y; rv[i][6] = hi.z; rv[i][7] = hi.w;
+        if (m < p.M)
+          *(uint4*)((bf16_t*)p.out + m * p.N + n0 + nb * 32 + c8) =
+              make_uint4(pack2(lo.x, lo.y), pack2(lo.z, lo.w), pack2(hi.x, hi.y), pack2(hi.z, hi.w));
+      }
+      __builtin_amdgcn_wave_barrier();
+      float s0[8], s1[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bf16x2 p01 = __builtin_convertvector((f32x2){rv[0][e], rv[1][e]}, bf16x2);
+        s0[e] = add_row_ror<8>(add_row_ror<4>(__builtin_amdgcn_fdot2_f32_bf16(p01, ones, 0.f, false)));
+        s1[e] = add_row_ror<8>(add_row_ror<4>(__builtin_amdgcn_fdot2_f32_bf16(p01, p01, 0.f, false)));
+      }
+      if ((lane & 12) == 0) {
+        float* q0 = Qg + nb * 32 + c8;
+        *(float4*)q0 = make_float4(s0[0], s0[1], s0[2], s0[3]);
+        *(float4*)(q0 + 4) = make_float4(s0[4], s0[5], s0[6], s0[7]);
+        *(float4*)(q0 + BN) = make_float4(s1[0], s1[1], s1[2], s1[3]);
+        *(float4*)(q0 + BN + 4) = make_float4(s1[4], s1[5], s1[6], s1[7]);
+      }
+    }
+    __syncthreads();   // every wave's group sums are in LDS
+    float* const Q[2] = {(float*)sP0, (float*)sP0 + 16 * 2 * BN};
+    flush_tile_stats<BN, F2_POS>(p, Q, tm, n0, tid);
+    return;
+  }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
@@ -1310,28 +1371,46 @@ hipError_t launch_conv2s2f(const GemmParams& p0, hipStream_t s) {
   p.tiles_n = p.N / F2_BN;
   const int64_t tiles_m = ceil_div(p.M, F2_POS);
   const dim3 grid((unsigned)(p.tiles_n > 1 ? ceil_div(tiles_m, 8) * 8 * p.tiles_n : tiles_m));
-  hipLaunchKernelGGL(conv2s2f_kernel, grid, dim3(512), 0, s, p);
+  if (p.stat_part) {
+    if (!conv2s2f_stats_ok(p)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv2s2f_kernel<true>, grid, dim3(512), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(conv2s2f_kernel<false>, grid, dim3(512), 0, s, p);
+  }
   return hipGetLastError();
 }
+
+// the statistics map of a forward whose tiles hold whole output images:
+// row tile t's partial of segment s at slot t + s
+static int stat_slots_by_tile(const GemmParams& p, int64_t tile_rows, int* blk) {
+  const int64_t hw = (int64_t)p.g.Ho * p.g.Wo;
+  const int tiles_m = (int)ceil_div(p.M, tile_rows);
+  for (int s = 0; s < p.nseg; ++s) blk[s] = (int)(p.seg_n0[s] * hw / tile_rows) + s;
+  blk[p.nseg] = tiles_m + p.nseg - 1;
+  return blk[p.nseg];
+}
+
+static bool stat_segments_ok(const GemmParams& p) {
+  if (p.nseg < 1 || p.nseg > MAX_SEG || p.seg_n0[0] != 0 || p.seg_n0[p.nseg] != p.g.n) return false;
+  for (int i = 0; i < p.nseg; ++i)
+    if (p.seg_n0[i + 1] <= p.seg_n0[i]) return false;
+  return p.M == (int64_t)p.g.n * p.g.Ho * p.g.Wo;
+}
+
+bool conv2s2f_stats_ok(const GemmParams& p) {
+  return conv2s2f_ok(p) && ((int64_t)p.g.Ho * p.g.Wo) % (F2_POS / 32) == 0 && stat_segments_ok(p);
+}
+
+int conv2s2f_stat_slots(const GemmParams& p, int* blk) { return stat_slots_by_tile(p, F2_POS, blk); }
 
 bool conv2_stats_ok(const GemmParams& p) {
   const ConvGeom& g = p.g;
   if (!conv2_ok(MODE_FWD, p) || !conv2_patch(p) || conv2_bn(p.N) != 128 || p.bias || p.relu)
     return false;
-  if ((g.H * g.W) % 16 != 0 || p.M != (int64_t)g.n * g.H * g.W) return false;
-  if (p.nseg < 1 || p.nseg > MAX_SEG || p.seg_n0[0] != 0 || p.seg_n0[p.nseg] != g.n) return false;
-  for (int i = 0; i < p.nseg; ++i)
-    if (p.seg_n0[i + 1] <= p.seg_n0[i]) return false;
-  return true;
+  return (g.H * g.W) % (C2_BM / 32) == 0 && stat_segments_ok(p);
 }
 
-int conv2_stat_slots(const GemmParams& p, int* blk) {
-  const int64_t hw = (int64_t)p.g.H * p.g.W;
-  const int tiles_m = (int)ceil_div(p.M, C2_BM);
-  for (int s = 0; s < p.nseg; ++s) blk[s] = (int)(p.seg_n0[s] * hw / C2_BM) + s;
-  blk[p.nseg] = tiles_m + p.nseg - 1;
-  return blk[p.nseg];
-}
+int conv2_stat_slots(const GemmParams& p, int* blk) { return stat_slots_by_tile(p, C2_BM, blk); }
 
 // p.b must point to the packed weights (launch_pack_weights of the same p)
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s) {

@@ -68,13 +68,14 @@ struct GemmParams {
   int seg_split[MAX_SEG + 1];
   int seg_n0[MAX_SEG + 1];
   // Batch-norm forward sums of the output, taken in the epilogue (conv64
-  // forward and the conv2 patch-form forward; null: none), per segment s
-  // (samples seg_n0[s] .. seg_n0[s + 1] - 1, nseg segments):
+  // forward and the conv2 / conv2s2f patch-form forwards; null: none), per
+  // segment s (samples seg_n0[s] .. seg_n0[s + 1] - 1, nseg segments):
   // stat_part[(slot * 2 + k) * N + n] = sum over a part of the output rows of
   // s of y^(k + 1), y the stored (rounded) output, at the slots of s:
   //   conv64: slot s * blocks + b, block b's rows (zero where b has none);
-  //   conv2: slot t + s, row tile t's rows, and a zero at slot t + s + 1
-  //     when tile t + 1 starts segment s + 1 (conv2_stat_slots).
+  //   conv2, conv2s2f: slot t + s, row tile t's rows, and a zero at slot
+  //     t + s + 1 when tile t + 1 starts segment s + 1 (conv2_stat_slots,
+  //     conv2s2f_stat_slots).
   // Either way segment s's partials are the slots [blk[s], blk[s + 1]).
   float* stat_part;
 };
@@ -151,9 +152,14 @@ bool conv2s2_ok(const GemmParams& p);
 hipError_t launch_conv2s2(const GemmParams& p, hipStream_t s);
 // Forward of a 3x3 stride-2 pad-1 convolution in the patch form (conv2.hip):
 // p.a = x [n][2Ho][2Wo][C], p.b = weights packed for MODE_FWD, p.out = y
-// [n][Ho][Wo][K] bf16, no epilogue operations.
+// [n][Ho][Wo][K] bf16, no epilogue operations other than the batch-norm sums
+// (p.stat_part with nseg / seg_n0 set; output images of a multiple of 8
+// pixels, nonempty segments covering the batch: conv2s2f_stats_ok), whose
+// slot ranges conv2s2f_stat_slots gives as conv2_stat_slots does.
 bool conv2s2f_ok(const GemmParams& p);
 hipError_t launch_conv2s2f(const GemmParams& p, hipStream_t s);
+bool conv2s2f_stats_ok(const GemmParams& p);
+int conv2s2f_stat_slots(const GemmParams& p, int* blk);
 // bf16 forward / data gradient of 64 -> 64 channel 3x3 stride-1 layers on
 // 32-wide maps (conv64.hip): packed weights resident in LDS, input patch of 16
 // output rows staged once per tile, taps as shifted LDS reads

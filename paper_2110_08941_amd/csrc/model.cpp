@@ -626,17 +626,28 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
   p.K = L.k * L.k * L.cin;
   const bool vec = (L.cin % c.V) == 0;
   if (c.bf && L.stride == 2 && !c.part && c.ws.packed && !wptr && conv2s2f_ok(p)) {
-    // bf16 3x3 stride 2: the patch form over whole input images (conv2.hip);
-    // it takes no batch-norm sums (*stats_fused stays false)
+    // bf16 3x3 stride 2: the patch form over whole input images (conv2.hip),
+    // with the batch-norm sums per worker when asked and the partials fit
     const void* wb = nullptr;
     HS_TRY(packed_weights(c, p.b, MODE_FWD, p, false, &wb));
     if (wb) {
       GemmParams q = p;
       q.b = wb;
+      bool stats = false;
+      if (q.stat_part && stat_blk) {
+        q.nseg = c.sg.count;
+        for (int i = 0; i <= MAX_SEG; ++i) q.seg_n0[i] = c.sg.n0[i < c.sg.count ? i : c.sg.count];
+        stats = conv2s2f_stats_ok(q) &&
+                (int64_t)conv2s2f_stat_slots(q, stat_blk) * 2 * q.N <= (int64_t)STAT_MAX_BLOCKS * 2 * 512;
+      }
+      if (!stats) {
+        q.stat_part = nullptr;
+        q.nseg = p.nseg;
+      }
       const bool probe = probe_begin(c, MODE_FWD, 256, 128);
       HS_TRY(launch_conv2s2f(q, c.s));
       if (probe) HS_TRY(probe_end(c, flops > 0 ? flops : layer_flops(L, c.n)));
-      if (stats_fused) *stats_fused = false;
+      if (stats_fused) *stats_fused = stats;
       return hipSuccess;
     }
   }
@@ -909,8 +920,9 @@ hipError_t bn_stats(const Ctx& c, const BNL& b, const void* z, int64_t rps) {
 
 // z = conv(x) and the batch-norm statistics of z: summed in the
 // convolution's epilogue where its kernel takes them (the 64-channel 3x3
-// layers on 32-wide maps and the conv2 patch form: partials per block or
-// row tile and worker, then the finish), else by a pass over z
+// layers on 32-wide maps and the stride-1 and stride-2 patch forms:
+// partials per block or row tile and worker, then the finish), else by a
+// pass over z
 hipError_t conv_bn_fwd(const Ctx& c, const ConvL& L, const void* x, void* z, const BNL& b,
                        int64_t rps) {
   bool want = c.bf && !c.part && L.b < 0 && !L.relu && b.c == L.cout && c.sg.count >= 1 &&
