@@ -44,7 +44,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void* lds_ptr;          // LDS
 typedef __attribute__((address_space(1))) const void* gbl_cptr;   // global
 
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32, EPI_STATS = 64 };
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ADD = 8, EPI_MASK = 16, EPI_MBITS = 32, EPI_STATS = 64,
+       EPI_BSUM = 128 };
 
 constexpr int C2_WAVES = 8;
 constexpr int C2_BM = 64 * C2_WAVES;   // rows per block
@@ -561,19 +562,33 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
     // chunks need no block barrier (one wave's LDS operations run in order).
     // The addend / mask rows of chunk nb + 1 are loaded while chunk nb is
     // written; rows past M re-read row M - 1 and are not stored.
+    //
+    // With EPI_BSUM (a data gradient whose stored output d is the output
+    // gradient of a batch norm with input z, p.bz) the epilogue also takes
+    // that batch norm's backward sums, sum d and sum d z per worker, as the
+    // forward statistics epilogue takes its sums: lane l handles the four
+    // consecutive rows 4 (l / 4) + i, so a row of 16 lanes covers a 16-row
+    // quarter inside one image; z is loaded with the addend; per channel the
+    // rounded d and z of row pairs go into bf16 dot products; DPP row
+    // rotates add the quarter, and flush_tile_stats writes the tile's
+    // partials per worker.
     float* E = Ewave;
     constexpr bool EADD = (EPI & EPI_ADD) != 0, EMASK = (EPI & EPI_MASK) != 0;
     constexpr bool EBITS = (EPI & EPI_MBITS) != 0;   // the mask as bits: one byte per lane row
+    constexpr bool EBSUM = (EPI & EPI_BSUM) != 0;
+    static_assert(!EBSUM || (PATCH && MODE == MODE_DGRAD), "backward sums: patch data gradient");
+    auto erow = [&](int i) { return EBSUM ? 4 * (lane >> 2) + i : 16 * i + (lane >> 2); };
     auto epi_off = [&](int nb, int i) -> int64_t {
-      const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+      const int row = erow(i), c8 = 8 * (lane & 3);
       const int m = m0 + row < p.M ? m0 + row : p.M - 1;
       return (int64_t)m * p.N + n0 + nb * 32 + c8;
     };
-    uint4 addv[2][EADD ? 4 : 1], maskv[2][EMASK && !EBITS ? 4 : 1];
+    uint4 addv[2][EADD ? 4 : 1], maskv[2][EMASK && !EBITS ? 4 : 1], zv[2][EBSUM ? 4 : 1];
     uint32_t maskb[2][EBITS ? 4 : 1];
     auto load_epi = [&](int nb, int slot) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
+        if constexpr (EBSUM) zv[slot][i] = *(const uint4*)((const bf16_t*)p.bz + epi_off(nb, i));
         if constexpr (EADD) addv[slot][i] = *(const uint4*)((const bf16_t*)p.addend + epi_off(nb, i));
         if constexpr (EBITS) maskb[slot][i] = p.mbits[epi_off(nb, i) >> 3];
         else if constexpr (EMASK) maskv[slot][i] = *(const uint4*)((const bf16_t*)p.mask + epi_off(nb, i));
@@ -591,9 +606,10 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
               make_float4(acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
                           acc[mb][nb][4 * q + 3]);
       __builtin_amdgcn_wave_barrier();
+      uint4 dst[EBSUM ? 4 : 1];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 16 * i + (lane >> 2), c8 = 8 * (lane & 3);
+        const int row = erow(i), c8 = 8 * (lane & 3);
         const int m = m0 + row;
         const float4 lo = *(const float4*)(E + row * EROW + c8);
         const float4 hi = *(const float4*)(E + row * EROW + c8 + 4);
@@ -621,11 +637,54 @@ __global__ __launch_bounds__(512) void conv2_kernel(GemmParams p) {
             if (!(bf2f((bf16_t)(w[e] >> 16)) > 0.f)) v[2 * e + 1] = 0.f;
           }
         }
-        if (m < p.M)
-          *(uint4*)((bf16_t*)p.out + (int64_t)m * p.N + n0 + nb * 32 + c8) =
-              make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+        const uint4 o = make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+        if (m < p.M) *(uint4*)((bf16_t*)p.out + (int64_t)m * p.N + n0 + nb * 32 + c8) = o;
+        if constexpr (EBSUM) dst[i] = o;
       }
       __builtin_amdgcn_wave_barrier();
+      if constexpr (EBSUM) {
+        // per channel pair w (channels 2w, 2w + 1) and row pair (0, 1), (2, 3):
+        // the two rows' values of one channel as a bf16 pair (byte selects)
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+        float s0[8], s1[8];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t d0 = ((const uint32_t*)&dst[0])[w], d1 = ((const uint32_t*)&dst[1])[w];
+          const uint32_t d2 = ((const uint32_t*)&dst[2])[w], d3 = ((const uint32_t*)&dst[3])[w];
+          const uint32_t z0 = ((const uint32_t*)&zv[nb & 1][0])[w], z1 = ((const uint32_t*)&zv[nb & 1][1])[w];
+          const uint32_t z2 = ((const uint32_t*)&zv[nb & 1][2])[w], z3 = ((const uint32_t*)&zv[nb & 1][3])[w];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint32_t sel = h ? 0x07060302u : 0x05040100u;   // high or low halves of (b, a)
+            bf16x2 pd01, pd23, pz01, pz23;
+            const uint32_t ud01 = __builtin_amdgcn_perm(d1, d0, sel), ud23 = __builtin_amdgcn_perm(d3, d2, sel);
+            const uint32_t uz01 = __builtin_amdgcn_perm(z1, z0, sel), uz23 = __builtin_amdgcn_perm(z3, z2, sel);
+            __builtin_memcpy(&pd01, &ud01, 4);
+            __builtin_memcpy(&pd23, &ud23, 4);
+            __builtin_memcpy(&pz01, &uz01, 4);
+            __builtin_memcpy(&pz23, &uz23, 4);
+            const int e = 2 * w + h;
+            s0[e] = __builtin_amdgcn_fdot2_f32_bf16(pd23, ones, __builtin_amdgcn_fdot2_f32_bf16(pd01, ones, 0.f, false), false);
+            s1[e] = __builtin_amdgcn_fdot2_f32_bf16(pd23, pz23, __builtin_amdgcn_fdot2_f32_bf16(pd01, pz01, 0.f, false), false);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          s0[e] = add_row_ror<8>(add_row_ror<4>(s0[e]));
+          s1[e] = add_row_ror<8>(add_row_ror<4>(s1[e]));
+        }
+        if ((lane & 12) == 0) {
+          float* q0 = Qst[wave >> 2] + ((wave & 3) * 4 + (lane >> 4)) * 2 * BN + nb * 32 + 8 * (lane & 3);
+          *(float4*)q0 = make_float4(s0[0], s0[1], s0[2], s0[3]);
+          *(float4*)(q0 + 4) = make_float4(s0[4], s0[5], s0[6], s0[7]);
+          *(float4*)(q0 + BN) = make_float4(s1[0], s1[1], s1[2], s1[3]);
+          *(float4*)(q0 + BN + 4) = make_float4(s1[4], s1[5], s1[6], s1[7]);
+        }
+      }
+    }
+    if constexpr (EBSUM) {
+      __syncthreads();   // every wave's quarter sums are in LDS
+      flush_tile_stats<BN, C2_BM>(p, Qst, tm, n0, tid);
     }
     return;
   }
@@ -1277,6 +1336,13 @@ static void launch_epi2(const GemmParams& p, dim3 grid, hipStream_t s) {
     else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, 0, PATCH>), grid, dim3(512), 0, s, p);
   } else {
     const bool add = p.addend != nullptr, mask = p.mask != nullptr || p.mbits != nullptr;
+    if constexpr (PATCH && BN == 128) {
+      if (p.bz) {   // launch_conv2 checked conv2_bsum_ok
+        if (add) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK | EPI_MBITS | EPI_BSUM, PATCH>), grid, dim3(512), 0, s, p);
+        else hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK | EPI_MBITS | EPI_BSUM, PATCH>), grid, dim3(512), 0, s, p);
+        return;
+      }
+    }
     if (add && p.mbits) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK | EPI_MBITS, PATCH>), grid, dim3(512), 0, s, p);
     else if (p.mbits) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_MASK | EPI_MBITS, PATCH>), grid, dim3(512), 0, s, p);
     else if (add && mask) hipLaunchKernelGGL((conv2_kernel<MODE, BN, RS, EPI_ADD | EPI_MASK, PATCH>), grid, dim3(512), 0, s, p);
@@ -1412,10 +1478,20 @@ bool conv2_stats_ok(const GemmParams& p) {
 
 int conv2_stat_slots(const GemmParams& p, int* blk) { return stat_slots_by_tile(p, C2_BM, blk); }
 
+bool conv2_bsum_ok(const GemmParams& p) {
+  const ConvGeom& g = p.g;
+  if (!conv2_ok(MODE_DGRAD, p) || !conv2_patch(p) || conv2_bn(p.N) != 128 || !p.stat_part ||
+      !p.bz || !p.mbits || p.out_f32)
+    return false;
+  return (g.H * g.W) % (C2_BM / 32) == 0 && stat_segments_ok(p);
+}
+
 // p.b must point to the packed weights (launch_pack_weights of the same p)
 hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s) {
   if (!conv2_ok(mode, p)) return hipErrorInvalidValue;
-  if (p.stat_part && (mode != MODE_FWD || !conv2_stats_ok(p))) return hipErrorInvalidValue;
+  if (p.bz ? (mode != MODE_DGRAD || !conv2_bsum_ok(p))
+           : (p.stat_part && (mode != MODE_FWD || !conv2_stats_ok(p))))
+    return hipErrorInvalidValue;
   if (mode == MODE_FWD) return launch_mode2<MODE_FWD>(p, s);
   return launch_mode2<MODE_DGRAD>(p, s);
 }

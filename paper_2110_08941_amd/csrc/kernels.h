@@ -77,7 +77,12 @@ struct GemmParams {
   //     t + s + 1 when tile t + 1 starts segment s + 1 (conv2_stat_slots,
   //     conv2s2f_stat_slots).
   // Either way segment s's partials are the slots [blk[s], blk[s + 1]).
+  // A conv2 data gradient with bz set ([M][N] bf16: the input z of the batch
+  // norm whose output gradient this data gradient is) writes instead, at the
+  // same conv2 slots, the backward sums of the stored (rounded) output d:
+  // k = 0 sum d, k = 1 sum d z (conv2_bsum_ok).
   float* stat_part;
+  const void* bz;
 };
 
 // K range of weight-gradient split y (default blockIdx.y) over worker segments: the
@@ -131,6 +136,11 @@ hipError_t launch_conv2(int mode, const GemmParams& p, hipStream_t s);
 // slot range of each segment) and returns the number of slots.
 bool conv2_stats_ok(const GemmParams& p);
 int conv2_stat_slots(const GemmParams& p, int* blk);
+// Whether the conv2 stride-1 data gradient can take the backward sums of a
+// batch norm (p.stat_part, p.bz, nseg / seg_n0 set): the patch form,
+// 128-channel column tiles, bf16, images of a multiple of 16 pixels,
+// nonempty segments covering the batch; slots as conv2_stat_slots.
+bool conv2_bsum_ok(const GemmParams& p);
 // Up to PACK_BATCH packings (launch_pack_weights of theta_bf16 + woff into
 // Bp + dst, offsets in elements) in one launch, passed by value.
 struct PackJob {
@@ -293,6 +303,16 @@ hipError_t launch_chan_stats(int kind, bool bf16, const void* x, const void* dy,
                              int64_t rows_per_sample, int C, float* part, float* const* out0,
                              float* const* out1, float eps, hipStream_t s,
                              const StatWsum* wsum = nullptr);
+// The backward finish alone, on partials of (sum d, sum d z) per segment
+// written elsewhere (GemmParams::bz): segment s sums partials [seg_blk[s],
+// seg_blk[s + 1]) in double and writes out0[s] = sum d, out1[s] = rstd_s
+// (sum d z - mean_s sum d) = sum d (z - mean_s) rstd_s (kind 1's outputs),
+// mean_s = mean + s * mstride (rstd likewise); with wsum, also their
+// weighted sums as launch_chan_stats.
+hipError_t launch_stats_finish_bwd(const float* part, const Segs& sg, int C, const float* mean,
+                                   const float* rstd, int mstride, float* const* out0,
+                                   float* const* out1, hipStream_t s, const int* seg_blk,
+                                   const StatWsum* wsum);
 // vectorised (C % 8 == 0) batch-norm apply / backward by segment: segment s
 // normalises with mean + s * mstride, rstd + s * mstride; the backward takes
 // its sums from sum_dy[s], sum_dyx[s]

@@ -307,6 +307,9 @@ int64_t plan_workspace(const Model& m, int max_n, Workspace* ws, int64_t splitk_
   ws->stem_w = a.take((int64_t)64 * 9 * 8 * es);
   ws->stat_part = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
   ws->stat_part_side = (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4);
+  // (the ResNet-18 backward is the one that takes them)
+  ws->stat_part_bsum = m.arch == HS_RESNET18 ? (float*)a.take((int64_t)STAT_MAX_BLOCKS * 2 * cmax * 4)
+                                             : nullptr;
   // split-K partials: at least one split per worker of the largest weight
   // gradient (first layer counted with its padded channels)
   int64_t max_w = 64 * 9 * 8;
@@ -560,12 +563,17 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   // forward kernel and the conv2 patch form (nseg stays 0 for the others,
   // where it means split-K over worker segments), while the partials fit
   // the workspace's buffer
+  // (the data gradient's backward sums of a batch norm, GemmParams::bz: the
+  // conv2 patch form)
   bool stats = false;
-  if ((w64 || mfma32) && mode == MODE_FWD && q.stat_part && stat_blk) {
+  const bool bsum = mode == MODE_DGRAD && q.bz;
+  if ((w64 || mfma32) && (mode == MODE_FWD || bsum) && q.stat_part && stat_blk) {
     q.nseg = c.sg.count;
     for (int i = 0; i <= MAX_SEG; ++i) q.seg_n0[i] = c.sg.n0[i < c.sg.count ? i : c.sg.count];
     int64_t slots = -1;
-    if (w64) {
+    if (bsum) {
+      if (mfma32 && !w64 && conv2_bsum_ok(q)) slots = conv2_stat_slots(q, stat_blk);
+    } else if (w64) {
       const int blocks = conv64_blocks(q);
       for (int i = 0; i <= q.nseg; ++i) stat_blk[i] = i * blocks;
       slots = (int64_t)q.nseg * blocks;
@@ -576,6 +584,7 @@ hipError_t gemm(const Ctx& c, int mode, const GemmParams& p, bool veca, bool vec
   }
   if (!stats) {
     q.stat_part = nullptr;
+    q.bz = nullptr;
     q.nseg = p.nseg;
   }
   if (mfma32 || w64) {
@@ -665,11 +674,22 @@ hipError_t conv_fwd(const Ctx& c, const ConvL& L, const void* x, void* y, bool o
 // projection's data gradient, summed in the same reduction; that needs the
 // stride-2 parity path, and when it is not available nothing is launched and
 // *fused is false (the caller then runs the two data gradients itself).
+// With bsum set, dx is the output gradient d of a batch norm whose input is
+// bsum->z: the kernel takes that batch norm's backward sums (sum d, sum d z
+// per worker) in its epilogue where it can (the bf16 conv2 patch form),
+// *bsum->fused tells whether it did, bsum->blk receives their slot ranges
+// (the partials are in the workspace's stat_part_bsum).
+struct BsumReq {
+  const void* z;
+  int blk[MAX_SEG + 1];
+  bool fused;
+};
 hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, const void* addend,
                       const void* mask, const uint8_t* mbits = nullptr,
                       const ConvL* proj = nullptr, const void* dproj = nullptr,
-                      bool* fused = nullptr) {
+                      bool* fused = nullptr, BsumReq* bsum = nullptr) {
   if (fused) *fused = false;
+  if (bsum) bsum->fused = false;
   GemmParams p = base_params(L, c.n);
   p.a = dy;
   p.b = c.W(L.w);
@@ -748,7 +768,12 @@ hipError_t conv_dgrad(const Ctx& c, const ConvL& L, const void* dy, void* dx, co
   if (proj) return hipSuccess;   // fusion requested but not possible
   int bm, bn;
   pick_tiles(p.M, p.N, bm, bn);
-  return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n));
+  if (bsum && c.bf && !c.part && c.ws.stat_part_bsum) {
+    p.bz = bsum->z;
+    p.stat_part = c.ws.stat_part_bsum;
+  }
+  return gemm(c, MODE_DGRAD, p, veca, vecb, bm, bn, 1, layer_flops(L, c.n),
+              bsum ? &bsum->fused : nullptr, bsum ? bsum->blk : nullptr);
 }
 
 // Whether the weight gradient of a residual block's 1x1 stride-2 projection
@@ -981,6 +1006,21 @@ hipError_t bn_bwd(const Ctx& c, const BNL& b, const void* dy, const void* act, c
   HS_TRY(launch_chan_stats(1, c.bf, z, dy, act, c.mean(b), c.rstd(b), c.mstride(), c.sg, rps, b.c,
                            c.sp(), db, dg, 0.f, c.s, c.gbar ? &ws : nullptr));
   return launch_bn_backward8(c.bf, dy, act, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
+                             db, dg, c.sg, rps, b.c, dz, c.s);
+}
+
+// The batch-norm backward of b where a data gradient's epilogue took its
+// sums (BsumReq, fused): the finish into every worker's dbeta, dgamma (as
+// bn_bwd), then dz; else bn_bwd itself.
+hipError_t bn_bwd_sums(const Ctx& c, const BNL& b, const BsumReq& r, const void* dy,
+                       const void* z, int64_t rps, void* dz) {
+  if (!r.fused) return bn_bwd(c, b, dy, nullptr, z, rps, dz);
+  float *db[MAX_SEG], *dg[MAX_SEG];
+  StatWsum ws{};
+  bn_sum_targets(c, b, db, dg, ws);
+  HS_TRY(launch_stats_finish_bwd(c.ws.stat_part_bsum, c.sg, b.c, c.mean(b), c.rstd(b), c.mstride(), db, dg, c.s,
+                                 r.blk, c.gbar ? &ws : nullptr));
+  return launch_bn_backward8(c.bf, dy, nullptr, z, c.mean(b), c.rstd(b), c.mstride(), c.theta + b.g,
                              db, dg, c.sg, rps, b.c, dz, c.s);
 }
 
@@ -1304,6 +1344,9 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
   GradPool gp(c.ws, c.s);
   gp.live[1] = true;   // G[1]: gradient of the last block's output
   int gi = 1;
+  // the backward sums of the current block's second batch norm, when the
+  // data gradient that produced its output gradient took them
+  BsumReq carry{};
   for (int bi = (int)m.blocks.size() - 1; bi >= 0; --bi) {
     const BlockL& b = m.blocks[bi];
     const int base = 3 + 5 * bi;
@@ -1326,15 +1369,18 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       HS_TRY(gp.read_on_side(p1));
     }
     HS_TAKE(gp, p2);
-    HS_TRY(bn_bwd(c, b.b2, gp[p1], nullptr, Z2, rps, gp[p2]));              // dZ2
+    HS_TRY(bn_bwd_sums(c, b.b2, carry, gp[p1], Z2, rps, gp[p2]));          // dZ2
     HS_TRY(fork(c));
     HS_TRY(conv_wgrad(cs, b.c2, gp[p2], Hh));
     HS_TRY(gp.read_on_side(p2));
     HS_TAKE(gp, p3);
-    HS_TRY(conv_dgrad(c, b.c2, gp[p2], gp[p3], nullptr, Hh, Bt[base + 1])); // dH * [H > 0]
+    BsumReq r1{};
+    r1.z = Z1;
+    HS_TRY(conv_dgrad(c, b.c2, gp[p2], gp[p3], nullptr, Hh, Bt[base + 1], nullptr, nullptr,
+                      nullptr, &r1));                                       // dH * [H > 0]
     gp.drop(p2);
     HS_TAKE(gp, p4);
-    HS_TRY(bn_bwd(c, b.b1, gp[p3], nullptr, Z1, rps, gp[p4]));              // dZ1
+    HS_TRY(bn_bwd_sums(c, b.b1, r1, gp[p3], Z1, rps, gp[p4]));              // dZ1
     gp.drop(p3);
     HS_TRY(fork(c));
     if (wfuse) {
@@ -1345,6 +1391,7 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
     }
     HS_TRY(gp.read_on_side(p4));
     HS_TAKE(gp, out);
+    carry = BsumReq{};
     if (b.proj) {
       HS_TRY(wait_mark(c, pz_done));
       // dIn * [in > 0], the shortcut's data gradient summed in the same pass
@@ -1359,7 +1406,12 @@ hipError_t resnet(const Ctx& c, const float* x, const int32_t* y, float* loss) {
       }
       gp.drop(pz);
     } else {
-      HS_TRY(conv_dgrad(c, b.c1, gp[p4], gp[out], gp[p1], in, inb));        // dIn * [in > 0]
+      // dIn * [in > 0]: the previous block's output gradient, whose second
+      // batch norm's sums the epilogue takes (they wait in their own buffer
+      // until that block's backward starts)
+      carry.z = bi > 0 ? S[3 + 5 * (bi - 1) + 2] : nullptr;
+      HS_TRY(conv_dgrad(c, b.c1, gp[p4], gp[out], gp[p1], in, inb, nullptr, nullptr, nullptr,
+                        bi > 0 ? &carry : nullptr));
     }
     gp.drop(p4);
     gp.drop(p1);

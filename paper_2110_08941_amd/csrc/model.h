@@ -80,6 +80,9 @@ struct Workspace {
   void* stem_w = nullptr;      // first-layer weights, channel-padded copy
   float* stat_part = nullptr;  // per-channel statistics: block partials
   float* stat_part_side = nullptr;  // the same for statistics on the second stream
+  // the batch-norm backward sums taken in data-gradient epilogues, kept until
+  // their finish (no other launch writes them in between)
+  float* stat_part_bsum = nullptr;
   float* splitk = nullptr;     // split-K partial outputs
   int64_t splitk_floats = 0;
   void* wpack = nullptr;       // bf16 weights packed for the 32x32 MFMA kernel

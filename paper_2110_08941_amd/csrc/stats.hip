@@ -102,6 +102,9 @@ struct FinishArgs {
   float* out0[MAX_SEG];
   float* out1[MAX_SEG];
   StatWsum wsum;               // sum0 null: no weighted sum
+  const float* mean;           // kind 3: segment s's mean and rstd at + s * mstride
+  const float* rstd;
+  int mstride;
 };
 
 // V consecutive channels of one row kept in their storage format until they
@@ -294,9 +297,11 @@ __global__ __launch_bounds__(256) void chan_partial_kernel(StatArgs a) {
 }
 
 // blockIdx.y = segment, blockIdx.x = group of 8 channels; thread = channel
-// (t & 7) x lane (t >> 3).  With a weighted sum (a.wsum, kinds 1 and 2) one
+// (t & 7) x lane (t >> 3).  With a weighted sum (a.wsum, kinds 1 to 3) one
 // block per channel group takes every segment in turn and also adds the
-// segments' results with their weights.
+// segments' results with their weights.  Kind 3 finishes partials of
+// (sum d, sum d z) into kind 1's outputs: sum d (z - mean) rstd = rstd
+// (sum d z - mean sum d).
 template <typename T, int KIND>
 __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
   __shared__ double red[2][256];
@@ -353,7 +358,11 @@ __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
     if (lane == 0 && c < C) {
       float* o0 = pick(a.out0, s);
       float* o1 = pick(a.out1, s);
-      const double t0 = red[0][t], t1 = red[1][t];
+      const double t0 = red[0][t];
+      double t1 = red[1][t];
+      if (KIND == 3)
+        t1 = (double)a.rstd[(int64_t)s * a.mstride + c] *
+             (t1 - (double)a.mean[(int64_t)s * a.mstride + c] * t0);
       if (KIND == 0) {
         const double cnt = (double)(seg1 - seg0);
         const double m1 = t0 / cnt;
@@ -365,7 +374,7 @@ __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
       } else {
         const float v0 = (float)t0, v1 = (float)t1;
         if (o0) o0[c] = v0;
-        if (KIND == 1 && o1) o1[c] = v1;
+        if (KIND != 2 && o1) o1[c] = v1;
         if (wsum) {
           if (s == 0) {
             acc0 = w * v0;
@@ -381,7 +390,7 @@ __global__ __launch_bounds__(256) void chan_finish_kernel(FinishArgs a) {
   }
   if (wsum && lane == 0 && c < C) {
     a.wsum.sum0[c] = acc0;
-    if (KIND == 1 && a.wsum.sum1) a.wsum.sum1[c] = acc1;
+    if (KIND != 2 && a.wsum.sum1) a.wsum.sum1[c] = acc1;
   }
 }
 
@@ -409,6 +418,30 @@ hipError_t launch_stats_finish_fwd(bool bf16, const float* part, int blocks, con
   const dim3 fgrid((C + 7) / 8, sg.count);
   if (bf16) hipLaunchKernelGGL((chan_finish_kernel<bf16_t, 0>), fgrid, dim3(256), 0, s, f);
   else hipLaunchKernelGGL((chan_finish_kernel<float, 0>), fgrid, dim3(256), 0, s, f);
+  return hipGetLastError();
+}
+
+hipError_t launch_stats_finish_bwd(const float* part, const Segs& sg, int C, const float* mean,
+                                   const float* rstd, int mstride, float* const* out0,
+                                   float* const* out1, hipStream_t s, const int* seg_blk,
+                                   const StatWsum* wsum) {
+  if (C < 1 || sg.count < 1 || sg.count > MAX_SEG || !seg_blk || !mean || !rstd)
+    return hipErrorInvalidValue;
+  FinishArgs f{};
+  f.part = part;
+  f.C = C;
+  f.sr.count = sg.count;
+  for (int i = 0; i <= MAX_SEG; ++i) f.sr.blk[i] = seg_blk[i < sg.count ? i : sg.count];
+  for (int i = 0; i < sg.count; ++i) {
+    f.out0[i] = out0 ? out0[i] : nullptr;
+    f.out1[i] = out1 ? out1[i] : nullptr;
+  }
+  if (wsum) f.wsum = *wsum;
+  f.mean = mean;
+  f.rstd = rstd;
+  f.mstride = mstride;
+  const dim3 fgrid((C + 7) / 8, wsum ? 1 : sg.count);
+  hipLaunchKernelGGL((chan_finish_kernel<bf16_t, 3>), fgrid, dim3(256), 0, s, f);
   return hipGetLastError();
 }
 
